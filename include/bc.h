@@ -1,0 +1,346 @@
+/*
+ * bc.h -- C ABI of libbarycache, an MI355X (gfx950) implementation of the hot
+ * path of BaryCache sampling for Diffusion Transformers.
+ *
+ * Paper: "Memory-Efficient Training-Free Acceleration of Diffusion
+ * Transformers with BaryCache".  On a full step the sampler runs the DiT layer
+ * stack (Sec. 3.1, Eqs. 4-5) and stores its output, the stepwise feature, in a
+ * cache context of the H most recent outputs (Sec. 3.2, Eq. 6).  On every other
+ * step it forecasts the feature as a weighted sum of the cached ones
+ * (Sec. 3.3, Eq. 13) with barycentric weights built from the step times alone
+ * (Sec. 3.2, Eqs. 7-12).  Here H is called K.
+ *
+ * Conventions for every call:
+ *   - Return value: a bc_status code; nothing is thrown across the ABI.  On an
+ *     error, bc_last_error() (per thread) holds a message.
+ *   - All arguments are checked before any work is enqueued: a call that
+ *     returns BC_ERR_INVALID_ARG, BC_ERR_DEGENERATE or BC_ERR_STATE has had no
+ *     effect on device memory or on any handle.
+ *   - Device pointers are device addresses in the current HIP device's memory;
+ *     the caller owns and allocates every device buffer (weights, features,
+ *     the ring storage, workspaces).  The library never allocates device
+ *     memory.  Handles own host memory only.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Device work is enqueued on it and the call returns without waiting;
+ *     buffers must stay valid until that work has completed.  Errors that
+ *     arise while kernels run surface at the caller's next synchronisation.
+ *   - Matrices are row-major.  Linear weights are [out, in] with the input
+ *     dimension contiguous; a linear layer computes y = x W^T + b.
+ *   - Node order: t_nodes[0] is the time of the most recent cached feature
+ *     (s_1 of Sec. 3.2), t_nodes[K-1] the oldest; weights follow that order.
+ */
+#ifndef BC_H
+#define BC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    BC_OK = 0,
+    BC_ERR_INVALID_ARG = 1,   /* bad pointer, size, shape, dtype or parameter */
+    BC_ERR_DEGENERATE = 2,    /* Eq. 11's normaliser is zero or not finite */
+    BC_ERR_STATE = 3,         /* e.g. forecasting from an empty cache */
+    BC_ERR_HIP = 4,           /* a HIP runtime call or launch failed */
+    BC_ERR_UNSUPPORTED = 5    /* a shape outside what the kernels handle */
+} bc_status;
+
+typedef enum { BC_F32 = 0, BC_BF16 = 1 } bc_dtype;
+
+const char* bc_status_str(int status);
+/* Message of the last failing call on this thread ("" if none). */
+const char* bc_last_error(void);
+/* ABI version, (major << 16) | minor. */
+int bc_version(void);
+
+/* ------------------------------------------------------------------------ */
+/* Barycentric weights (host, fp64)                                          */
+/* ------------------------------------------------------------------------ */
+
+typedef enum {
+    BC_NODES_TRAPEZOID = 0,   /* numerators (-1)^j c_j, c = (1/2, 1, ..., 1, 1/2): Eqs. 8-9 */
+    BC_NODES_LAGRANGE = 1     /* classical weights 1 / prod_{m!=j}(s_j - s_m) (polynomial interpolation) */
+} bc_node_mode;
+
+typedef enum {
+    BC_BLEND_RECENT = 0,      /* w = (1 - lambda) alpha + lambda e_1 (mix with the most recent feature) */
+    BC_BLEND_LITERAL = 1      /* Eq. 12 as printed: [(1-lambda) alpha_1..alpha_{K-1}, lambda alpha_K] */
+} bc_blend_mode;
+
+typedef struct {
+    int nodes;       /* bc_node_mode */
+    double clip_C;   /* clip bound of Eq. 10 (paper: 10); +inf disables the clip */
+    double eta;      /* the small constant of Eq. 11 (paper: 1e-12) */
+    double delta;    /* exponent of Eq. 11; < 0 selects delta_K: 1 (K<=2), 0.95 (K=3), 0.7 (K>=4) */
+    double lambda;   /* blend factor of Eq. 12, in [0, 1] */
+    int blend;       /* bc_blend_mode */
+} bc_bary_params;
+
+/* Paper defaults: trapezoid nodes, C = 10, eta = 1e-12, delta = delta_K,
+ * lambda = 0, RECENT blend (Sec. 3.2; lambda = 0 is the image setting of
+ * Sec. 4.1). */
+void bc_bary_params_default(bc_bary_params* p);
+
+/* The weight vector W of Eq. 12 for K nodes and query time t_query (Sec. 3.2,
+ * Eqs. 8-12: raw weights u_j = b_j / (t - s_j), clip to [-C, C], signed power
+ * sgn(u)(|u| + eta)^delta, normalisation to unit sum, blend).
+ *   t_nodes: host [K] fp64, newest first; trapezoid mode needs them strictly
+ *            monotone, Lagrange mode distinct.  1 <= K <= 8.
+ *   w_out:   host [K] fp64, same order.
+ * A query equal to a node gives +-inf before the clip in trapezoid mode and
+ * the unit vector of that node in Lagrange mode.
+ * Errors: INVALID_ARG (NULL, K out of range, non-finite or badly ordered
+ * nodes, parameters out of range), DEGENERATE (zero or non-finite normaliser;
+ * w_out untouched). */
+int bc_bary_weights(const double* t_nodes, int K, double t_query, double* w_out);
+int bc_bary_weights_ex(const double* t_nodes, int K, double t_query,
+                       const bc_bary_params* p, double* w_out);
+
+/* Full/forecast mask of the equal-spaced schedule (Sec. 3.3 and the schedule
+ * ablation, Table 5): mask_out[k] = 1 (full) iff k % interval == 0, or
+ * force_last and k == S-1; else 0.  mask_out: host [S]. */
+int bc_make_mask(int S, int interval, int force_last, uint8_t* mask_out);
+
+/* One step of the precomputed plan.  A full step writes the new feature to
+ * ring slot `head` and then holds `count` features; a forecast step combines
+ * the `count` newest features, node j in slot slots[j] with weight w[j]
+ * (newest first).  Unused entries are -1 / 0. */
+typedef struct {
+    int is_full;
+    int count;
+    int head;
+    int slots[8];
+    double w[8];
+} bc_plan_step;
+
+/* The whole plan of a sampling run: the weights depend only on the schedule,
+ * so they are all computed before the loop (the paper's "online decoupling",
+ * Sec. 1 and Sec. 3.2 "Get Key").
+ *   mask:   host [S], mask[0] must be 1.
+ *   coords: host [S] node coordinate of each step, or NULL for coords[k] = k.
+ *   K:      ring slots (history length H), 1..8.
+ *   p:      weight parameters, or NULL for the defaults; delta < 0 uses
+ *           delta of the node count actually available at each step.
+ *   out:    host [S].
+ * Errors: INVALID_ARG, DEGENERATE (names the step in bc_last_error()). */
+int bc_plan(int S, const uint8_t* mask, const double* coords, int K,
+            const bc_bary_params* p, bc_plan_step* out);
+
+/* ------------------------------------------------------------------------ */
+/* Cache context: an in-place ring of K feature tensors (Sec. 3.2, Eq. 6)    */
+/* ------------------------------------------------------------------------ */
+
+typedef struct bc_cache_ring bc_cache_ring;
+
+/* Wrap caller-owned device storage of K * numel elements of `dtype` (slot i
+ * starts at element i * numel) as an empty ring.  The handle holds host
+ * metadata only: head, count and the node time of each slot. */
+int bc_cache_create(int K, int64_t numel, int dtype, void* dev_storage, bc_cache_ring** out);
+int bc_cache_destroy(bc_cache_ring* r);
+/* Forget every cached feature (count = 0); storage is untouched. */
+int bc_cache_reset(bc_cache_ring* r);
+/* Device address of the slot the next push will fill, so a producer can write
+ * the feature there directly and push it without a copy. */
+int bc_cache_next_slot(const bc_cache_ring* r, void** dev_ptr);
+/* Insert a feature computed at node time t as the newest entry, evicting the
+ * oldest once K are held (the sliding window of Sec. 3.2).  `feat` is a device
+ * pointer to numel elements of the ring's dtype, or NULL (or the next slot's
+ * own address) when the producer already wrote the next slot: then no device
+ * work is enqueued; otherwise one copy is enqueued on `stream`. */
+int bc_cache_push(bc_cache_ring* r, const void* feat, double t, void* stream);
+/* Ring state: count, head, and for j < count the node time and slot of node j
+ * (newest first).  Any output pointer may be NULL; arrays need K entries. */
+int bc_cache_state(const bc_cache_ring* r, int* count, int* head, double* t_nodes, int* slots);
+
+/* Forecast x_hat = sum_j w[j] * node_j (Eq. 13) over the `count` newest cached
+ * features: one fused pass that reads each feature once and writes `out`
+ * (numel elements of out_dtype) once, accumulating in fp32 with the weights
+ * rounded to fp32.
+ *   w: host [count] fp64, newest first; 1 <= count <= ring count.
+ * Errors: INVALID_ARG, STATE (count exceeds what the ring holds). */
+int bc_bary_extrapolate(const bc_cache_ring* r, const double* w, int count,
+                        void* out, int out_dtype, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* The layer stack (Sec. 3.1, Eqs. 4-5)                                      */
+/* ------------------------------------------------------------------------ */
+
+typedef enum {
+    BC_BLOCK_DIT = 0,     /* adaLN-Zero DiT block */
+    BC_BLOCK_PIXART = 1,  /* DiT block + cross-attention to a text context; modulation = t6 + table */
+    BC_BLOCK_DUAL = 2,    /* image and text streams, joint attention */
+    BC_BLOCK_SINGLE = 3   /* one stream over [image | text] tokens, fused projections */
+} bc_block_kind;
+
+typedef struct {
+    int kind;       /* bc_block_kind */
+    int B;          /* samples */
+    int T;          /* image tokens per sample */
+    int D;          /* hidden width; D == heads * head_dim */
+    int heads;
+    int head_dim;   /* 16..128, a multiple of 8 */
+    int mlp;        /* MLP hidden width */
+    int T_txt;      /* DUAL / SINGLE: text tokens per sample, else 0 */
+    int T_ctx;      /* PIXART: context tokens per sample, else 0 */
+    int dtype;      /* weights and activations: BC_F32 or BC_BF16 */
+} bc_block_desc;
+
+/* One stream's parameters, device pointers in the block's dtype.
+ *   DIT / DUAL stream: w_mod [6D, D], b_mod [6D], w_qkv [3D, D], b_qkv [3D],
+ *     w_o [D, D], b_o [D], w_fc1 [mlp, D], b_fc1 [mlp], w_fc2 [D, mlp], b_fc2 [D].
+ *   PIXART: w_mod is the per-block table [6, D] (b_mod unused), the rest as DIT.
+ *   SINGLE: w_mod [3D, D], b_mod [3D]; w_qkv is the fused input projection
+ *     [3D + mlp, D] with bias b_qkv; w_o is the fused output projection
+ *     [D, D + mlp] with bias b_o; the fc pointers are unused. */
+typedef struct {
+    const void *w_mod, *b_mod;
+    const void *w_qkv, *b_qkv;
+    const void *w_o, *b_o;
+    const void *w_fc1, *b_fc1;
+    const void *w_fc2, *b_fc2;
+} bc_stream_weights;
+
+typedef struct {
+    bc_stream_weights img;     /* the (image) stream */
+    bc_stream_weights txt;     /* DUAL: the text stream */
+    const void *wx_q, *bx_q;   /* PIXART cross-attention: query [D, D], [D] */
+    const void *wx_kv, *bx_kv; /*   keys|values from the context [2D, D], [2D] */
+    const void *wx_o, *bx_o;   /*   output [D, D], [D] */
+} bc_block_weights;
+
+/* Bytes of workspace bc_dit_block_forward needs for this shape. */
+int bc_block_workspace_size(const bc_block_desc* d, size_t* bytes);
+
+/* One block on the residual stream, in place (Eq. 4 with the running residual
+ * stream as the residual).
+ *   x:    device fp32.  DIT / PIXART / DUAL: [B, T, D] image tokens.
+ *         SINGLE: [B, T + T_txt, D] (each sample's image tokens then its text).
+ *   x_txt: DUAL: device fp32 [B, T_txt, D] text tokens, in place; else NULL.
+ *   c:    device fp32 conditioning.  DIT / DUAL / SINGLE: [B, D], the vector
+ *         the modulation linear reads through SiLU.  PIXART: [B, 6D], the
+ *         shared t6 vector to which the block's table is added.
+ *   ctx:  PIXART: device [B, T_ctx, D] projected text context (block dtype);
+ *         the block derives its keys/values with wx_kv.  Else NULL.
+ *   ws:   device workspace of at least bc_block_workspace_size bytes, 256-byte
+ *         aligned.
+ * Activations between the kernels are in the block dtype; the residual stream,
+ * LayerNorm statistics, softmax and every accumulation are fp32.
+ * Errors: INVALID_ARG, UNSUPPORTED (head_dim or widths the kernels do not
+ * tile), HIP. */
+int bc_dit_block_forward(const bc_block_desc* d, const bc_block_weights* w,
+                         float* x, float* x_txt, const float* c, const void* ctx,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Whole model and the sampling loop (Sec. 3.3)                              */
+/* ------------------------------------------------------------------------ */
+
+typedef enum { BC_MODEL_DIT = 0, BC_MODEL_PIXART = 1, BC_MODEL_MMDIT = 2 } bc_model_kind;
+
+typedef struct {
+    int kind;          /* bc_model_kind */
+    int depth;         /* DIT / PIXART blocks; MMDIT dual-stream blocks */
+    int depth_single;  /* MMDIT single-stream blocks */
+    int D, heads, head_dim, mlp;
+    int in_ch, out_ch, patch;
+    int frames, height, width;  /* latent size; frames = 1 for images (latent [B, C, H, W]) */
+    int n_classes;     /* DIT: class table rows = n_classes + 1 (0: unconditional) */
+    int ctx_tokens, ctx_dim;    /* PIXART text: [B, ctx_tokens, ctx_dim] */
+    int txt_tokens;    /* MMDIT text: [B, txt_tokens, D] */
+    int freq_dim;      /* timestep sinusoid width, even */
+    int dtype;         /* BC_F32 or BC_BF16: weights, activations and the ring */
+} bc_model_desc;
+
+/* Device pointers in the model dtype.  Token features are patches in
+ * (p_h, p_w, channel) order; tokens run over (frame,) row, column. */
+typedef struct {
+    const void *t_w1, *t_b1, *t_w2, *t_b2;        /* timestep MLP: [D, freq_dim], [D], [D, D], [D] */
+    const void *patch_w, *patch_b, *pos;          /* [D, in_ch p p], [D], [T, D] */
+    const void *y_table;                          /* DIT with classes: [n_classes + 1, D] */
+    const void *t6_w, *t6_b;                      /* PIXART: [6D, D], [6D] */
+    const void *cap_w1, *cap_b1, *cap_w2, *cap_b2;/* PIXART caption MLP: [D, ctx_dim], [D], [D, D], [D] */
+    const void *txt_w, *txt_b;                    /* MMDIT pooled-text projection: [D, D], [D] */
+    const void *final_w_mod, *final_b_mod;        /* DIT / MMDIT: [2D, D], [2D]; PIXART: table [2, D] */
+    const void *final_w, *final_b;                /* [out_ch p p, D], [out_ch p p] */
+    const bc_block_weights* blocks;               /* host array: depth (+ depth_single) blocks */
+} bc_model_weights;
+
+typedef struct bc_model bc_model;
+
+/* Validate and copy a model description and its weight pointers (the host
+ * array `blocks` is copied; the device weights are referenced, not copied). */
+int bc_model_create(const bc_model_desc* d, const bc_model_weights* w, bc_model** out);
+int bc_model_destroy(bc_model* m);
+
+typedef enum { BC_SAMPLER_DDIM = 0, BC_SAMPLER_DPMPP2M = 1, BC_SAMPLER_EULER = 2 } bc_sampler;
+
+/* The step schedule: tau_out[k] the integer timestep (999 - floor(1000k/S))
+ * and time_out[k] the value fed to the timestep embedding (tau for the
+ * noise-prediction samplers, 1000 (1 - k/S) for Euler).  Either may be NULL. */
+int bc_make_schedule(int sampler, int S, int32_t* tau_out, double* time_out);
+
+/* Bytes of workspace bc_sample needs for B samples. */
+int bc_sample_workspace_size(const bc_model* m, int B, size_t* bytes);
+
+/* The BaryCache sampling loop (Sec. 3.3): for k = 0..S-1, a full step
+ * (mask[k] = 1) runs the layer stack and its last block writes the stepwise
+ * feature straight into the ring's next slot (Eq. 6's insertion); a forecast
+ * step builds the feature from the ring with the precomputed weights
+ * (Eq. 13).  Both then run the final layer and the sampler update.  The whole
+ * loop is enqueued on `stream` without any host synchronisation.
+ *   mask:    host [S], mask[0] = 1.
+ *   K, p:    ring history length (must equal the ring's K) and weight params
+ *            (NULL = defaults); node coordinate of step k is k.
+ *   ring:    holds K slots of B*T*D elements of the model dtype; reset here.
+ *   latents: device fp32 [B, in_ch, (frames,) height, width]; in: x_T, out: the sample.
+ *   labels:  DIT with classes: device int64 [B]; else NULL.
+ *   text:    PIXART: device [B, ctx_tokens, ctx_dim]; MMDIT: device [B, txt_tokens, D]
+ *            (model dtype); else NULL.
+ *   ws:      device workspace of bc_sample_workspace_size bytes, 256-byte aligned.
+ * Errors: INVALID_ARG, DEGENERATE (a forecast step's weights), UNSUPPORTED, HIP. */
+int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
+              int K, const bc_bary_params* p, bc_cache_ring* ring, float* latents,
+              const int64_t* labels, const void* text, void* ws, size_t ws_bytes,
+              void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Building blocks exposed for measurement and tests                         */
+/* ------------------------------------------------------------------------ */
+
+typedef enum {
+    BC_EPI_BIAS = 0,        /* out = acc + b (out in the dtype) */
+    BC_EPI_BIAS_GELU = 1,   /* out = GELU_tanh(acc + b) */
+    BC_EPI_GATE_RES = 2     /* out(fp32) = res(fp32) + gate[row / rows_per_gate] * (acc + b) */
+} bc_epilogue;
+
+/* y = epilogue(A W^T) for A [M, K] and W [N, K] in `dtype` (MFMA tiles on
+ * gfx950).  out: [M, N] in `dtype`, or fp32 for GATE_RES.  bias: [N] dtype.
+ * res, gate: GATE_RES only: res fp32 [M, N] (may alias out), gate fp32
+ * [M / rows_per_gate, N].  K must be a multiple of 8. */
+int bc_linear(int M, int N, int K, const void* A, const void* W, const void* bias,
+              void* out, int epilogue, const float* res, const float* gate,
+              int rows_per_gate, int dtype, void* stream);
+
+/* Scaled dot-product attention softmax(Q K^T / sqrt(d)) V per (sample, head):
+ * q [B, Tq, H, d], k and v [B, Tk, H, d], out [B, Tq, H, d], all `dtype`. */
+int bc_attention(int B, int H, int Tq, int Tk, int d, const void* q, const void* k,
+                 const void* v, void* out, int dtype, void* ws, size_t ws_bytes, void* stream);
+int bc_attention_workspace_size(int B, int H, int Tq, int Tk, int d, int dtype, size_t* bytes);
+
+/* Per-kernel timing with HIP events on the stream each kernel is launched on.
+ * While enabled for a kernel class, every launch of that class is bracketed by
+ * two events (at most max_launches).  bc_profile_collect waits for them and
+ * returns the summed duration and the number of launches, then disables.
+ * Classes: 0 forecast, 1 GEMM with GELU epilogue, 2 GEMM gated residual,
+ * 3 GEMM bias (QKV), 4 attention, 5 layernorm-modulate. */
+int bc_profile_enable(int kernel_class, int max_launches);
+int bc_profile_collect(int kernel_class, double* total_ms, int* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BC_H */

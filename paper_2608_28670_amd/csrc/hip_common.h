@@ -1,0 +1,79 @@
+// Device-side types and helpers shared by the HIP sources (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "common.h"
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));   // one 16-byte chunk
+
+namespace bc {
+
+// Element access in either storage type, always through fp32.
+__device__ __forceinline__ float ld(const float* p) { return *p; }
+__device__ __forceinline__ float ld(const bf16* p) { return (float)*p; }
+__device__ __forceinline__ void st(float* p, float v) { *p = v; }
+__device__ __forceinline__ void st(bf16* p, float v) { *p = (bf16)v; }   // round to nearest even
+
+// 16-byte chunk <-> 8 (bf16) or 4 (fp32) values.
+__device__ __forceinline__ void unpack(const u32x4& u, float* f, const bf16*) {
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        f[2 * i] = __uint_as_float(w[i] << 16);
+        f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+}
+__device__ __forceinline__ void unpack(const u32x4& u, float* f, const float*) {
+    f[0] = __uint_as_float(u.x); f[1] = __uint_as_float(u.y);
+    f[2] = __uint_as_float(u.z); f[3] = __uint_as_float(u.w);
+}
+
+template <typename T> struct ElemsPer16B { static constexpr int v = 16 / (int)sizeof(T); };
+
+__device__ __forceinline__ float silu(float x) { return x / (1.0f + __expf(-x)); }
+
+// GELU with the tanh approximation, using tanh(y) = 1 - 2 / (1 + e^{2y}).
+__device__ __forceinline__ float gelu_tanh(float x) {
+    const float y = 0.7978845608028654f * (x + 0.044715f * x * x * x);
+    const float t = 1.0f - 2.0f / (1.0f + __expf(2.0f * y));
+    return 0.5f * x * (1.0f + t);
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
+inline int dtype_size(int dt) { return dt == BC_BF16 ? 2 : 4; }
+
+// Check a launch; returns BC_OK or BC_ERR_HIP with the message recorded.
+int check_launch(const char* what);
+
+// Kernel classes timed by bc_profile_*; see bc.h.
+enum ProfClass { PROF_FORECAST = 0, PROF_GEMM_GELU = 1, PROF_GEMM_GATE = 2, PROF_GEMM_BIAS = 3,
+                 PROF_ATTENTION = 4, PROF_LAYERNORM = 5, PROF_NCLASS = 6 };
+void prof_begin(int cls, hipStream_t s);
+void prof_end(int cls, hipStream_t s);
+
+// ---- kernel launchers (each returns a bc_status) ---------------------------
+
+// out[i] = sum_j w[j] * src[j][i] for i < n (Eq. 13), fp32 accumulation.
+int launch_forecast(const void* const* src, const float* w, int K, int64_t n, int in_dt,
+                    void* out, int out_dt, hipStream_t s);
+int launch_copy(const void* src, void* dst, int64_t bytes, hipStream_t s);
+int launch_fill_zero(void* dst, int64_t bytes, hipStream_t s);
+
+}  // namespace bc

@@ -255,10 +255,25 @@ def text(cfg: ModelConfig, seed: int = SEED, batch: Optional[int] = None) -> np.
 FORECAST_SHAPE = (8, 16384, 3072)
 
 
-def forecast_features(K: int, shape=FORECAST_SHAPE, seed: int = SEED, dtype: str = "f32") -> np.ndarray:
-    """[K, *shape] N(0,1) features (bf16-rounded values when dtype == 'bf16')."""
-    a = normal(f"forecast/feat/K{K}/{'x'.join(map(str, shape))}", (K,) + tuple(shape), 1.0, seed)
-    return bf16_round(a) if dtype == "bf16" else a
+def forecast_features(K: int, shape=FORECAST_SHAPE, seed: int = SEED, dtype: str = "f32",
+                      threads: Optional[int] = None) -> np.ndarray:
+    """[K, *shape] N(0,1) features (bf16-rounded values when dtype == 'bf16').
+
+    Slot j, leading index i is drawn from its own stream, so the large
+    microbenchmark tensors are generated in parallel."""
+    tag = f"forecast/feat/{'x'.join(map(str, shape))}"
+    out = np.empty((K,) + tuple(shape), dtype=np.float32)
+    jobs = [(j, i) for j in range(K) for i in range(shape[0])]
+
+    def fill(ji):
+        j, i = ji
+        a = normal(f"{tag}/{j}/{i}", shape[1:], 1.0, seed)
+        out[j, i] = bf16_round(a) if dtype == "bf16" else a
+
+    nt = threads or min(16, os.cpu_count() or 1)
+    with ThreadPoolExecutor(nt) as ex:
+        list(ex.map(fill, jobs))
+    return out
 
 
 def forecast_times(K: int, seed: int = SEED) -> Tuple[np.ndarray, float]:

@@ -17,3 +17,19 @@ def pytest_collection_modifyitems(config, items):
     # GPU tests run in file order, but the allocation-free entry point's test
     # (if present) is kept last so a failure there cannot hide the others.
     items.sort(key=lambda it: 1 if "test_zz_" in it.nodeid else 0)
+
+
+def ensure_built():
+    """Build the library if nothing is built yet (the driver builds first)."""
+    from paper_2608_28670_amd import LIB_PATH
+    if not os.path.exists(LIB_PATH):
+        from paper_2608_28670_amd import build
+        build.build()
+
+
+@pytest.fixture(scope="session")
+def bclib():
+    ensure_built()
+    import paper_2608_28670_amd as bc
+    bc.lib()
+    return bc
