@@ -1,0 +1,313 @@
+// Multi-head attention softmax(Q K^T / sqrt(d)) V, flash style (online
+// softmax, no T x T buffer), on MFMA.
+//
+// A workgroup owns 64 queries of one (sample, head); each of its 4 waves owns
+// 16 of them and keeps their Q fragments in registers.  Keys and values
+// stream through LDS 64 at a time (K row-major, V transposed).  The wave
+// computes the transposed scores S^T = K Q^T, so after the MFMA a lane holds
+// 16 scores of a single query (its lane index mod 16).  That makes the
+// softmax statistics per-lane values (plus two cross-lane reductions), and the
+// probabilities are already laid out as the B operand of O^T = V^T P^T, whose
+// accumulator again holds one query per lane: rescaling O by the running-max
+// correction is one multiply per register.  Scores, max, sum and O are fp32.
+//
+// Rows of Q, K, V and O may come from two segments (the image and text
+// streams of joint attention): position p of sample b is row b*T0 + p of
+// segment 0 if p < T0, else row b*T1 + (p - T0) of segment 1.  Head h of a row
+// is the d consecutive elements starting at column h*d.
+#include "attention.h"
+
+namespace bc {
+
+constexpr int kAttnThreads = 256;
+constexpr int kQTile = 64;   // queries per workgroup
+constexpr int kKTile = 64;   // keys per step
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+template <typename T, int HD> struct AttnShape {
+    // K dimension of Q K^T: bf16 uses 32-wide MFMA steps with a 16-wide tail;
+    // fp32 uses 4-wide steps.
+    static constexpr int n32 = sizeof(T) == 2 ? HD / 32 : 0;
+    static constexpr int rem = sizeof(T) == 2 ? HD - 32 * n32 : 0;
+    static constexpr int DK = sizeof(T) == 2 ? 32 * n32 + (rem > 16 ? 32 : rem > 0 ? 16 : 0) : HD;
+    static constexpr bool tail16 = sizeof(T) == 2 && rem > 0 && rem <= 16;
+    static constexpr int n32x = n32 + (rem > 16 ? 1 : 0);   // 32-wide steps incl. a padded one
+    static constexpr int DV = (HD + 15) / 16 * 16;           // rows of O^T
+    static constexpr int EPC = 16 / (int)sizeof(T);          // elements per 16-byte chunk
+    static constexpr int CPR = HD / EPC;                     // chunks per head row
+    static constexpr int KPAD = EPC;                         // LDS row padding (elements)
+};
+
+template <typename T>
+__device__ __forceinline__ const T* seg_row(const void* p0, const void* p1, int T0, int T1, int64_t ld,
+                                            int b, int p) {
+    return p < T0 ? static_cast<const T*>(p0) + ((int64_t)b * T0 + p) * ld
+                  : static_cast<const T*>(p1) + ((int64_t)b * T1 + (p - T0)) * ld;
+}
+
+template <typename T, int HD>
+__global__ __launch_bounds__(kAttnThreads) void attention_kernel(AttnArgs a) {
+    typedef AttnShape<T, HD> S;
+    constexpr int LDK = S::DK + S::KPAD;
+    constexpr int LDV = kKTile + S::KPAD;
+    __shared__ __attribute__((aligned(16))) T sK[kKTile][LDK];
+    __shared__ __attribute__((aligned(16))) T sVt[S::DV][LDV];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int b = blockIdx.z, h = blockIdx.y;
+    const int Tq = a.Tq0 + a.Tq1, Tk = a.Tk0 + a.Tk1;
+    const int q0 = blockIdx.x * kQTile + wave * 16;
+    const int col0 = h * HD;
+    const int ql = lane & 15, grp = lane >> 4;
+    const int myq = q0 + ql;
+
+    // Zero the padding columns of K and the padding rows of V^T once.
+    for (int i = tid; i < kKTile * (LDK - HD); i += kAttnThreads)
+        sK[i / (LDK - HD)][HD + i % (LDK - HD)] = (T)0.f;
+    for (int i = tid; i < (S::DV - HD) * LDV; i += kAttnThreads)
+        sVt[HD + i / LDV][i % LDV] = (T)0.f;
+
+    // Q fragments (B operand of S^T = K Q^T): lane holds query ql.
+    const T* qrow = myq < Tq ? seg_row<T>(a.q0, a.q1, a.Tq0, a.Tq1, a.ldq, b, myq) + col0 : nullptr;
+    bf16x8 qf[S::n32x > 0 ? S::n32x : 1];
+    s16x4 qt;
+    float qf32[sizeof(T) == 4 ? HD / 4 : 1];
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+        for (int c = 0; c < S::n32x; ++c) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int d = 32 * c + grp * 8 + i;
+                qf[c][i] = (qrow && d < HD) ? (bf16)qrow[d] : (bf16)0.f;
+            }
+        }
+        if constexpr (S::tail16) {
+            const unsigned short* qraw = reinterpret_cast<const unsigned short*>(qrow);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int d = 32 * S::n32 + grp * 4 + i;
+                qt[i] = (qraw && d < HD) ? (short)qraw[d] : (short)0;
+            }
+        }
+    } else {
+#pragma unroll
+        for (int c = 0; c < HD / 4; ++c) qf32[c] = qrow ? (float)qrow[4 * c + grp] : 0.f;
+    }
+
+    f32x4 o[S::DV / 16];
+#pragma unroll
+    for (int i = 0; i < S::DV / 16; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY, l_run = 0.f;
+
+    // Staging of one K/V tile: 64 rows x CPR chunks each.
+    constexpr int NCH = kKTile * S::CPR;
+    constexpr int PER = (NCH + kAttnThreads - 1) / kAttnThreads;
+    u32x4 rk[PER], rv[PER];
+    auto load_tile = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int c = tid + i * kAttnThreads;
+            const int row = c / S::CPR, ch = c % S::CPR;
+            const int p = k0 + row;
+            if (c < NCH && p < Tk) {
+                const T* kr = seg_row<T>(a.k0, a.k1, a.Tk0, a.Tk1, a.ldk, b, p) + col0 + ch * S::EPC;
+                const T* vr = seg_row<T>(a.v0, a.v1, a.Tk0, a.Tk1, a.ldv, b, p) + col0 + ch * S::EPC;
+                rk[i] = *reinterpret_cast<const u32x4*>(kr);
+                rv[i] = *reinterpret_cast<const u32x4*>(vr);
+            } else {
+                rk[i] = u32x4{0, 0, 0, 0};
+                rv[i] = u32x4{0, 0, 0, 0};
+            }
+        }
+    };
+    auto store_tile = [&]() {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int c = tid + i * kAttnThreads;
+            if (c < NCH) {
+                const int row = c / S::CPR, ch = c % S::CPR;
+                *reinterpret_cast<u32x4*>(&sK[row][ch * S::EPC]) = rk[i];
+                const T* vv = reinterpret_cast<const T*>(&rv[i]);
+#pragma unroll
+                for (int e = 0; e < S::EPC; ++e) sVt[ch * S::EPC + e][row] = vv[e];
+            }
+        }
+    };
+
+    const int ntiles = (Tk + kKTile - 1) / kKTile;
+    load_tile(0);
+    __syncthreads();   // padding zeroed before the first tile lands
+    store_tile();
+    __syncthreads();
+
+    for (int t = 0; t < ntiles; ++t) {
+        const int k0 = t * kKTile;
+        if (t + 1 < ntiles) load_tile(k0 + kKTile);
+
+        // S^T tiles: s[j] covers keys k0 + 16j .. +16; lane holds keys 16j + 4grp + r of query ql.
+        f32x4 s[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            s[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+            const int krow = 16 * j + ql;
+            if constexpr (sizeof(T) == 2) {
+#pragma unroll
+                for (int c = 0; c < S::n32x; ++c) {
+                    const bf16x8 kf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sK[krow][32 * c + grp * 8]));
+                    s[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[c], s[j], 0, 0, 0);
+                }
+                if constexpr (S::tail16) {
+                    const s16x4 kt = __builtin_bit_cast(s16x4, *reinterpret_cast<const u32x2*>(&sK[krow][32 * S::n32 + grp * 4]));
+                    s[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(kt, qt, s[j], 0, 0, 0);
+                }
+            } else {
+#pragma unroll
+                for (int c = 0; c < HD / 4; ++c)
+                    s[j] = __builtin_amdgcn_mfma_f32_16x16x4f32((float)sK[krow][4 * c + grp], qf32[c], s[j], 0, 0, 0);
+            }
+        }
+
+        // Online softmax (base 2, scores pre-scaled by log2(e)/sqrt(d)).
+        float mloc = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int key = k0 + 16 * j + 4 * grp + r;
+                const float v = key < Tk ? s[j][r] * a.scale_log2 : -INFINITY;
+                s[j][r] = v;
+                mloc = fmaxf(mloc, v);
+            }
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+        const float m_new = fmaxf(m_run, mloc);
+        const float alpha = exp2f(m_run - m_new);
+        float lsum = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float p = exp2f(s[j][r] - m_new);
+                s[j][r] = p;
+                lsum += p;
+            }
+        lsum += __shfl_xor(lsum, 16, 64);
+        lsum += __shfl_xor(lsum, 32, 64);
+        l_run = l_run * alpha + lsum;
+        m_run = m_new;
+#pragma unroll
+        for (int i = 0; i < S::DV / 16; ++i) o[i] *= alpha;
+
+        // O^T += V^T P^T.
+        if constexpr (sizeof(T) == 2) {
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                bf16x8 pf;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    pf[r] = (bf16)s[2 * u][r];
+                    pf[4 + r] = (bf16)s[2 * u + 1][r];
+                }
+#pragma unroll
+                for (int i = 0; i < S::DV / 16; ++i) {
+                    // keys 32u + 4grp + 0..3 and 32u + 16 + 4grp + 0..3, matching pf
+                    const T* vrow = &sVt[16 * i + ql][32 * u + 4 * grp];
+                    const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow);
+                    const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 16);
+                    const bf16x8 vf = __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, hi.x, hi.y});
+                    o[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[i], 0, 0, 0);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+#pragma unroll
+                    for (int i = 0; i < S::DV / 16; ++i)
+                        o[i] = __builtin_amdgcn_mfma_f32_16x16x4f32((float)sVt[16 * i + ql][16 * j + 4 * grp + r],
+                                                                     s[j][r], o[i], 0, 0, 0);
+        }
+
+        __syncthreads();
+        if (t + 1 < ntiles) {
+            store_tile();
+            __syncthreads();
+        }
+    }
+
+    if (myq < Tq) {
+        const float inv = 1.f / l_run;
+        T* orow = const_cast<T*>(seg_row<T>(a.o0, a.o1, a.Tq0, a.Tq1, a.ldo, b, myq)) + col0;
+#pragma unroll
+        for (int i = 0; i < S::DV / 16; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int d = 16 * i + 4 * grp + r;
+                if (d < HD) st(orow + d, o[i][r] * inv);
+            }
+    }
+}
+
+template <typename T>
+static int run_attention(const AttnArgs& a, int hd, hipStream_t s) {
+    const int Tq = a.Tq0 + a.Tq1;
+    dim3 grid((Tq + kQTile - 1) / kQTile, a.H, a.B), block(kAttnThreads);
+    switch (hd) {
+#define BC_ATT_CASE(HD) case HD: attention_kernel<T, HD><<<grid, block, 0, s>>>(a); break;
+        BC_ATT_CASE(32) BC_ATT_CASE(64) BC_ATT_CASE(72) BC_ATT_CASE(128)
+#undef BC_ATT_CASE
+        default: return fail(BC_ERR_UNSUPPORTED, "head_dim %d (supported: 32, 64, 72, 128)", hd);
+    }
+    return check_launch("attention");
+}
+
+bool attention_supported(int hd) { return hd == 32 || hd == 64 || hd == 72 || hd == 128; }
+
+int launch_attention(int dtype, AttnArgs a, hipStream_t s) {
+    if (a.B <= 0 || a.H <= 0 || a.Tq0 + a.Tq1 <= 0) return BC_OK;
+    if (a.Tk0 + a.Tk1 <= 0) return fail(BC_ERR_INVALID_ARG, "attention over zero keys");
+    if (!attention_supported(a.d)) return fail(BC_ERR_UNSUPPORTED, "head_dim %d (supported: 32, 64, 72, 128)", a.d);
+    if ((a.ldk | a.ldv) % 8 || (reinterpret_cast<uintptr_t>(a.k0) | reinterpret_cast<uintptr_t>(a.v0)) % 16)
+        return fail(BC_ERR_UNSUPPORTED, "attention K/V rows must be 16-byte aligned");
+    if (dtype == BC_F32 && a.d > 64) return fail(BC_ERR_UNSUPPORTED, "fp32 attention supports head_dim <= 64");
+    a.scale_log2 = 1.4426950408889634f / sqrtf((float)a.d);
+    prof_begin(PROF_ATTENTION, s);
+    const int rc = dtype == BC_BF16 ? run_attention<bf16>(a, a.d, s) : run_attention<float>(a, a.d, s);
+    prof_end(PROF_ATTENTION, s);
+    return rc;
+}
+
+}  // namespace bc
+
+using namespace bc;
+
+extern "C" {
+
+int bc_attention_workspace_size(int B, int H, int Tq, int Tk, int d, int dtype, size_t* bytes) {
+    clear_error();
+    if (!bytes) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
+    (void)B; (void)H; (void)Tq; (void)Tk; (void)d; (void)dtype;
+    *bytes = 0;   // the kernel reads the [B, T, H, d] layout directly
+    return BC_OK;
+}
+
+int bc_attention(int B, int H, int Tq, int Tk, int d, const void* q, const void* k, const void* v, void* out,
+                 int dtype, void* ws, size_t ws_bytes, void* stream) {
+    clear_error();
+    (void)ws; (void)ws_bytes;
+    if (!q || !k || !v || !out) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
+    if (B < 1 || H < 1 || Tq < 1 || Tk < 1 || d < 1) return fail(BC_ERR_INVALID_ARG, "empty attention");
+    if (dtype != BC_F32 && dtype != BC_BF16) return fail(BC_ERR_INVALID_ARG, "dtype %d", dtype);
+    AttnArgs a = {};
+    a.q0 = q; a.q1 = q; a.Tq0 = Tq; a.Tq1 = 0; a.ldq = (int64_t)H * d;
+    a.k0 = k; a.k1 = k; a.Tk0 = Tk; a.Tk1 = 0; a.ldk = (int64_t)H * d;
+    a.v0 = v; a.v1 = v; a.ldv = (int64_t)H * d;
+    a.o0 = out; a.o1 = out; a.ldo = (int64_t)H * d;
+    a.B = B; a.H = H; a.d = d;
+    return launch_attention(dtype, a, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

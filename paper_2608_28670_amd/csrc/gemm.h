@@ -1,0 +1,45 @@
+// GEMM launcher interface shared by the block orchestration.
+#pragma once
+
+#include "hip_common.h"
+
+namespace bc {
+
+// Epilogue of y = A W^T.  Column c of row r gets v = acc + bias[c]; then
+//   BIAS kind: v = GELU(v) if c >= gelu_from; stored (in the operand dtype)
+//     to out[r*ldo + c] if c < split, else to out2[r*ldo2 + c - split + off2];
+//   GATE_RES kind: v = res[r*ldr + c] + gate[(r / rows_per_gate)*ldg + c] * v
+//     (gate NULL: a plain residual add),
+//     stored to row (r / seg) * keep + r % seg of out (fp32 if out_f32, else
+//     the operand dtype) when r % seg < keep, dropped otherwise.
+struct GemmEpi {
+    const void* bias;
+    void* out;
+    int64_t ldo;
+    int out_f32;
+    void* out2;
+    int64_t ldo2;
+    int split, off2, gelu_from;
+    const float* res;
+    int64_t ldr;
+    const float* gate;
+    int64_t ldg;
+    int rows_per_gate;
+    int seg, keep;
+};
+
+struct GemmArgs {
+    const void* A;
+    int64_t lda;
+    const void* W;
+    int64_t ldw;
+    int M, N, K;
+    GemmEpi e;
+};
+
+// Defaults: plain bias epilogue writing [M, N] densely to (unset) out.
+GemmArgs gemm_args(const void* A, int64_t lda, const void* W, int64_t ldw, int M, int N, int K);
+// epi: BC_EPI_BIAS (covers GELU via gelu_from) or BC_EPI_GATE_RES.
+int launch_gemm(int dtype, int epi, const GemmArgs& g, hipStream_t s);
+
+}  // namespace bc

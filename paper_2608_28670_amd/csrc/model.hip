@@ -1,0 +1,664 @@
+// Orchestration of the hot path on one HIP stream: the DiT-family blocks
+// (Sec. 3.1, Eq. 4 with the running residual stream), the whole denoiser, and
+// the BaryCache sampling loop (Sec. 3.3).
+//
+// Nothing here computes; it validates, lays out the caller's workspace and
+// enqueues kernels.  The loop needs no device-to-host synchronisation: the
+// full/forecast mask, the ring bookkeeping and every forecast weight are known
+// before the first launch (the weights depend only on the schedule).
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "attention.h"
+#include "gemm.h"
+#include "ops.h"
+
+namespace bc {
+
+// ---------------------------------------------------------------------------
+// Workspace carving (every sub-buffer 256-byte aligned)
+// ---------------------------------------------------------------------------
+struct Carver {
+    char* base;
+    size_t off = 0;
+    explicit Carver(void* b) : base(static_cast<char*>(b)) {}
+    template <typename P> P* take(size_t bytes) {
+        off = (off + 255) & ~size_t(255);
+        P* p = base ? reinterpret_cast<P*>(base + off) : nullptr;
+        off += bytes;
+        return p;
+    }
+};
+
+struct BlockBufs {
+    void* h;        // [R, D]        LayerNorm output / cast of the stream
+    void* qkv;      // [R, 3D]       (image rows, then text rows)
+    void* attn;     // [R, D + F] for single-stream blocks, else [R, D]
+    void* mlp;      // [R, F]
+};
+
+// wide_attn: the attention buffer doubles as the single-stream block's
+// [attention | GELU(mlp)] input (R x (D + F)); need_mlp: a separate MLP hidden
+// buffer for DiT / PixArt / dual-stream blocks.
+static void carve_block(Carver& c, int dt, int64_t R, int D, int F, bool wide_attn, bool need_mlp, BlockBufs& b) {
+    const size_t sz = dtype_size(dt);
+    b.h = c.take<char>(R * D * sz);
+    b.qkv = c.take<char>(R * 3 * D * sz);
+    b.attn = c.take<char>(R * (wide_attn ? D + F : D) * sz);
+    b.mlp = need_mlp ? c.take<char>(R * F * sz) : nullptr;
+}
+
+// Where the last gated residual of a block goes: the stream itself, or the
+// ring slot of the stepwise feature (only the first `keep` of every `seg`
+// rows, in `dt`).
+struct BlockOut {
+    void* ptr = nullptr;
+    int dt = BC_F32;
+    int seg = 0, keep = 0;
+};
+
+static int gated(int dt, const void* A, int64_t lda, const void* W, const void* bias, int M, int N, int K, float* x,
+                 const float* gate, int64_t ldg, int rows_per_gate, const BlockOut* out, hipStream_t s) {
+    GemmArgs g = gemm_args(A, lda, W, K, M, N, K);
+    g.e.bias = bias;
+    g.e.res = x;
+    g.e.ldr = N;
+    g.e.gate = gate;
+    g.e.ldg = ldg;
+    g.e.rows_per_gate = rows_per_gate;
+    if (out && out->ptr) {
+        g.e.out = out->ptr;
+        g.e.out_f32 = out->dt == BC_F32;
+        g.e.seg = out->seg;
+        g.e.keep = out->keep;
+    } else {
+        g.e.out = x;
+        g.e.out_f32 = 1;
+    }
+    g.e.ldo = N;
+    return launch_gemm(dt, BC_EPI_GATE_RES, g, s);
+}
+
+static int plain(int dt, const void* A, int64_t lda, const void* W, const void* bias, int M, int N, int K, void* out,
+                 bool gelu, hipStream_t s) {
+    GemmArgs g = gemm_args(A, lda, W, K, M, N, K);
+    g.e.bias = bias;
+    g.e.out = out;
+    g.e.ldo = N;
+    if (gelu) g.e.gelu_from = 0;
+    return launch_gemm(dt, BC_EPI_BIAS, g, s);
+}
+
+#define BC_TRY(x) do { const int _rc = (x); if (_rc != BC_OK) return _rc; } while (0)
+
+// One DiT or PixArt block on x [B*T, D] (fp32).  mod: [B, >= 6D] fp32 rows
+// ld_mod apart, ordered (shift1, scale1, gate1, shift2, scale2, gate2).
+static int dit_block(const bc_block_desc& d, const bc_block_weights& w, float* x, const float* mod, int64_t ld_mod,
+                     const void* ctx_kv, const BlockBufs& bb, const BlockOut* out, hipStream_t s) {
+    const int dt = d.dtype, D = d.D, F = d.mlp, T = d.T;
+    const int M = d.B * T;
+    const bc_stream_weights& sw = w.img;
+    BC_TRY(launch_ln_mod(BC_F32, x, M, D, mod, mod + D, ld_mod, T, dt, bb.h, s));
+    BC_TRY(plain(dt, bb.h, D, sw.w_qkv, sw.b_qkv, M, 3 * D, D, bb.qkv, false, s));
+    AttnArgs a = {};
+    const size_t esz = dtype_size(dt);
+    a.q0 = a.q1 = bb.qkv; a.Tq0 = T; a.ldq = 3 * D;
+    a.k0 = a.k1 = static_cast<char*>(bb.qkv) + D * esz; a.Tk0 = T; a.ldk = 3 * D;
+    a.v0 = a.v1 = static_cast<char*>(bb.qkv) + 2 * D * esz; a.ldv = 3 * D;
+    a.o0 = a.o1 = bb.attn; a.ldo = D;
+    a.B = d.B; a.H = d.heads; a.d = d.head_dim;
+    BC_TRY(launch_attention(dt, a, s));
+    BC_TRY(gated(dt, bb.attn, D, sw.w_o, sw.b_o, M, D, D, x, mod + 2 * D, ld_mod, T, nullptr, s));
+    if (d.kind == BC_BLOCK_PIXART) {
+        // Cross-attention to the text context: no norm, no gate.
+        BC_TRY(launch_convert(BC_F32, x, dt, bb.h, (int64_t)M * D, s));
+        BC_TRY(plain(dt, bb.h, D, w.wx_q, w.bx_q, M, D, D, bb.qkv, false, s));
+        AttnArgs c = {};
+        c.q0 = c.q1 = bb.qkv; c.Tq0 = T; c.ldq = D;
+        c.k0 = c.k1 = ctx_kv; c.Tk0 = d.T_ctx; c.ldk = 2 * D;
+        c.v0 = c.v1 = static_cast<const char*>(ctx_kv) + D * esz; c.ldv = 2 * D;
+        c.o0 = c.o1 = bb.attn; c.ldo = D;
+        c.B = d.B; c.H = d.heads; c.d = d.head_dim;
+        BC_TRY(launch_attention(dt, c, s));
+        BC_TRY(gated(dt, bb.attn, D, w.wx_o, w.bx_o, M, D, D, x, nullptr, 0, T, nullptr, s));
+    }
+    BC_TRY(launch_ln_mod(BC_F32, x, M, D, mod + 3 * D, mod + 4 * D, ld_mod, T, dt, bb.h, s));
+    BC_TRY(plain(dt, bb.h, D, sw.w_fc1, sw.b_fc1, M, F, D, bb.mlp, true, s));
+    return gated(dt, bb.mlp, F, sw.w_fc2, sw.b_fc2, M, D, F, x, mod + 5 * D, ld_mod, T, out, s);
+}
+
+// Dual-stream block: image x [B*T, D] and text xt [B*Tt, D], each with its own
+// modulation; attention is joint over the image then text tokens of a sample.
+static int dual_block(const bc_block_desc& d, const bc_block_weights& w, float* x, float* xt, const float* mi,
+                      const float* mt, int64_t ld_mod, const BlockBufs& bb, hipStream_t s) {
+    const int dt = d.dtype, D = d.D, F = d.mlp, T = d.T, Tt = d.T_txt;
+    const int Mi = d.B * T, Mt = d.B * Tt;
+    const size_t esz = dtype_size(dt);
+    char* qkv_i = static_cast<char*>(bb.qkv);
+    char* qkv_t = qkv_i + (int64_t)Mi * 3 * D * esz;
+    char* at_i = static_cast<char*>(bb.attn);
+    char* at_t = at_i + (int64_t)Mi * D * esz;
+    BC_TRY(launch_ln_mod(BC_F32, x, Mi, D, mi, mi + D, ld_mod, T, dt, bb.h, s));
+    BC_TRY(plain(dt, bb.h, D, w.img.w_qkv, w.img.b_qkv, Mi, 3 * D, D, qkv_i, false, s));
+    BC_TRY(launch_ln_mod(BC_F32, xt, Mt, D, mt, mt + D, ld_mod, Tt, dt, bb.h, s));
+    BC_TRY(plain(dt, bb.h, D, w.txt.w_qkv, w.txt.b_qkv, Mt, 3 * D, D, qkv_t, false, s));
+    AttnArgs a = {};
+    a.q0 = qkv_i; a.q1 = qkv_t; a.Tq0 = T; a.Tq1 = Tt; a.ldq = 3 * D;
+    a.k0 = qkv_i + D * esz; a.k1 = qkv_t + D * esz; a.Tk0 = T; a.Tk1 = Tt; a.ldk = 3 * D;
+    a.v0 = qkv_i + 2 * D * esz; a.v1 = qkv_t + 2 * D * esz; a.ldv = 3 * D;
+    a.o0 = at_i; a.o1 = at_t; a.ldo = D;
+    a.B = d.B; a.H = d.heads; a.d = d.head_dim;
+    BC_TRY(launch_attention(dt, a, s));
+    BC_TRY(gated(dt, at_i, D, w.img.w_o, w.img.b_o, Mi, D, D, x, mi + 2 * D, ld_mod, T, nullptr, s));
+    BC_TRY(gated(dt, at_t, D, w.txt.w_o, w.txt.b_o, Mt, D, D, xt, mt + 2 * D, ld_mod, Tt, nullptr, s));
+    BC_TRY(launch_ln_mod(BC_F32, x, Mi, D, mi + 3 * D, mi + 4 * D, ld_mod, T, dt, bb.h, s));
+    BC_TRY(plain(dt, bb.h, D, w.img.w_fc1, w.img.b_fc1, Mi, F, D, bb.mlp, true, s));
+    BC_TRY(gated(dt, bb.mlp, F, w.img.w_fc2, w.img.b_fc2, Mi, D, F, x, mi + 5 * D, ld_mod, T, nullptr, s));
+    BC_TRY(launch_ln_mod(BC_F32, xt, Mt, D, mt + 3 * D, mt + 4 * D, ld_mod, Tt, dt, bb.h, s));
+    BC_TRY(plain(dt, bb.h, D, w.txt.w_fc1, w.txt.b_fc1, Mt, F, D, bb.mlp, true, s));
+    return gated(dt, bb.mlp, F, w.txt.w_fc2, w.txt.b_fc2, Mt, D, F, xt, mt + 5 * D, ld_mod, Tt, nullptr, s);
+}
+
+// Single-stream block on x [B*(T+Tt), D]: mod (shift, scale, gate) [B, >= 3D].
+static int single_block(const bc_block_desc& d, const bc_block_weights& w, float* x, const float* mod,
+                        int64_t ld_mod, const BlockBufs& bb, const BlockOut* out, hipStream_t s) {
+    const int dt = d.dtype, D = d.D, F = d.mlp, L = d.T + d.T_txt;
+    const int M = d.B * L;
+    const size_t esz = dtype_size(dt);
+    BC_TRY(launch_ln_mod(BC_F32, x, M, D, mod, mod + D, ld_mod, L, dt, bb.h, s));
+    // [qkv | GELU(mlp)]: the qkv part to its own buffer, the MLP part to
+    // columns D.. of the output projection's input.
+    GemmArgs g = gemm_args(bb.h, D, w.img.w_qkv, D, M, 3 * D + F, D);
+    g.e.bias = w.img.b_qkv;
+    g.e.out = bb.qkv;
+    g.e.ldo = 3 * D;
+    g.e.split = 3 * D;
+    g.e.out2 = bb.attn;
+    g.e.ldo2 = D + F;
+    g.e.off2 = D;
+    g.e.gelu_from = 3 * D;
+    BC_TRY(launch_gemm(dt, BC_EPI_BIAS, g, s));
+    AttnArgs a = {};
+    a.q0 = a.q1 = bb.qkv; a.Tq0 = L; a.ldq = 3 * D;
+    a.k0 = a.k1 = static_cast<char*>(bb.qkv) + D * esz; a.Tk0 = L; a.ldk = 3 * D;
+    a.v0 = a.v1 = static_cast<char*>(bb.qkv) + 2 * D * esz; a.ldv = 3 * D;
+    a.o0 = a.o1 = bb.attn; a.ldo = D + F;
+    a.B = d.B; a.H = d.heads; a.d = d.head_dim;
+    BC_TRY(launch_attention(dt, a, s));
+    return gated(dt, bb.attn, D + F, w.img.w_o, w.img.b_o, M, D, D + F, x, mod + 2 * D, ld_mod, L, out, s);
+}
+
+static int check_block_desc(const bc_block_desc& d) {
+    if (d.kind < BC_BLOCK_DIT || d.kind > BC_BLOCK_SINGLE) return fail(BC_ERR_INVALID_ARG, "block kind %d", d.kind);
+    if (d.dtype != BC_F32 && d.dtype != BC_BF16) return fail(BC_ERR_INVALID_ARG, "dtype %d", d.dtype);
+    if (d.B < 1 || d.T < 1 || d.D < 1 || d.heads < 1 || d.mlp < 1) return fail(BC_ERR_INVALID_ARG, "empty block shape");
+    if (d.heads * d.head_dim != d.D) return fail(BC_ERR_INVALID_ARG, "heads*head_dim != D");
+    if (d.T_txt < 0 || d.T_ctx < 0) return fail(BC_ERR_INVALID_ARG, "negative token count");
+    if ((d.kind == BC_BLOCK_DUAL || d.kind == BC_BLOCK_SINGLE) ? d.T_txt < 1 && d.kind == BC_BLOCK_DUAL : d.T_txt != 0)
+        return fail(BC_ERR_INVALID_ARG, "T_txt=%d does not fit block kind %d", d.T_txt, d.kind);
+    if ((d.kind == BC_BLOCK_PIXART) != (d.T_ctx > 0)) return fail(BC_ERR_INVALID_ARG, "T_ctx only for PIXART");
+    if (!attention_supported(d.head_dim)) return fail(BC_ERR_UNSUPPORTED, "head_dim %d", d.head_dim);
+    if (d.dtype == BC_F32 && d.head_dim > 64) return fail(BC_ERR_UNSUPPORTED, "fp32 blocks need head_dim <= 64");
+    const int epc = d.dtype == BC_BF16 ? 8 : 4;
+    if (d.D % 16 || d.mlp % epc || d.D > 4096) return fail(BC_ERR_UNSUPPORTED, "D=%d mlp=%d", d.D, d.mlp);
+    return BC_OK;
+}
+
+static bool have(const void* p) { return p != nullptr; }
+
+static int check_stream_weights(const bc_stream_weights& w, int kind) {
+    bool ok = have(w.w_mod) && have(w.w_qkv) && have(w.b_qkv) && have(w.w_o) && have(w.b_o);
+    if (kind != BC_BLOCK_PIXART) ok = ok && have(w.b_mod);
+    if (kind != BC_BLOCK_SINGLE) ok = ok && have(w.w_fc1) && have(w.b_fc1) && have(w.w_fc2) && have(w.b_fc2);
+    return ok ? BC_OK : fail(BC_ERR_INVALID_ARG, "missing block weight");
+}
+
+static int check_block_weights(const bc_block_weights& w, int kind) {
+    BC_TRY(check_stream_weights(w.img, kind));
+    if (kind == BC_BLOCK_DUAL) BC_TRY(check_stream_weights(w.txt, kind));
+    if (kind == BC_BLOCK_PIXART && !(have(w.wx_q) && have(w.bx_q) && have(w.wx_kv) && have(w.bx_kv) && have(w.wx_o) && have(w.bx_o)))
+        return fail(BC_ERR_INVALID_ARG, "missing cross-attention weight");
+    return BC_OK;
+}
+
+// Workspace of one standalone block call: block buffers, modulation vectors,
+// and the PixArt context keys/values.
+static size_t block_ws(const bc_block_desc& d, void* base, BlockBufs* bb, float** mod, float** mod_t, void** ctx_kv) {
+    Carver c(base);
+    const int64_t R = (int64_t)d.B * (d.T + d.T_txt);
+    BlockBufs tmp;
+    carve_block(c, d.dtype, R, d.D, d.mlp, d.kind == BC_BLOCK_SINGLE, d.kind != BC_BLOCK_SINGLE, bb ? *bb : tmp);
+    float* m = c.take<float>((size_t)d.B * 6 * d.D * sizeof(float));
+    float* mt = c.take<float>(d.kind == BC_BLOCK_DUAL ? (size_t)d.B * 6 * d.D * sizeof(float) : 0);
+    void* kv = c.take<char>(d.kind == BC_BLOCK_PIXART ? (size_t)d.B * d.T_ctx * 2 * d.D * dtype_size(d.dtype) : 0);
+    if (mod) *mod = m;
+    if (mod_t) *mod_t = mt;
+    if (ctx_kv) *ctx_kv = kv;
+    return c.off + 256;
+}
+
+static SkinnyArgs skinny1(const void* W, const void* b, int N, int K, int B, const float* in, float* out,
+                          int act_in, int act_out) {
+    SkinnyArgs a;
+    std::memset(&a, 0, sizeof a);
+    a.W[0] = W; a.bias[0] = b;
+    a.nseg = 1; a.Nseg = N; a.K = K; a.B = B;
+    a.in = in; a.ld_in = K; a.out = out; a.ld_out = N;
+    a.act_in = act_in; a.act_out = act_out;
+    return a;
+}
+
+}  // namespace bc
+
+// ---------------------------------------------------------------------------
+// Model handle
+// ---------------------------------------------------------------------------
+struct bc_model {
+    bc_model_desc d;
+    bc_model_weights w;
+    std::vector<bc_block_weights> blocks;
+};
+
+namespace bc {
+
+struct SampleWs {
+    BlockBufs bb;
+    float *x, *x_img, *x_txt;                 // residual streams
+    float *e, *t1, *temb, *c, *t6, *fmod, *pooled, *txtp;
+    float *mods, *mods_s;                     // per-block modulation (dual/dit/pixart; single)
+    void *cap_h, *ctx, *ctx_kv;               // pixart text context
+    void* feat;                               // forecast output [B*T, D] (model dtype)
+    float *out, *prev;                        // model output, DPM-Solver++ history
+    size_t bytes;
+};
+
+static int64_t latent_spatial(const bc_model_desc& d) { return (int64_t)d.frames * d.height * d.width; }
+
+static int model_tokens(const bc_model_desc& d) { return d.frames * (d.height / d.patch) * (d.width / d.patch); }
+
+static SampleWs carve_sample(const bc_model_desc& d, int B, void* base) {
+    Carver c(base);
+    SampleWs w;
+    const int T = model_tokens(d), D = d.D, F = d.mlp;
+    const int Tt = d.kind == BC_MODEL_MMDIT ? d.txt_tokens : 0;
+    const int64_t R = (int64_t)B * (T + Tt);
+    const size_t esz = dtype_size(d.dtype);
+    const size_t f4 = sizeof(float);
+    carve_block(c, d.dtype, R, D, F, d.kind == BC_MODEL_MMDIT, true, w.bb);
+    w.x = c.take<float>(R * D * f4);
+    w.x_img = w.x;
+    w.x_txt = nullptr;
+    if (d.kind == BC_MODEL_MMDIT) {
+        if (B == 1) {
+            w.x_txt = w.x + (int64_t)T * D;            // one sample: [img | txt] is already the joint layout
+        } else {
+            w.x_img = c.take<float>((int64_t)B * T * D * f4);
+            w.x_txt = c.take<float>((int64_t)B * Tt * D * f4);
+        }
+    }
+    w.e = c.take<float>((size_t)B * d.freq_dim * f4);
+    w.t1 = c.take<float>((size_t)B * D * f4);
+    w.temb = c.take<float>((size_t)B * D * f4);
+    w.c = c.take<float>((size_t)B * D * f4);
+    w.t6 = c.take<float>(d.kind == BC_MODEL_PIXART ? (size_t)B * 6 * D * f4 : 0);
+    w.fmod = c.take<float>((size_t)B * 2 * D * f4);
+    w.pooled = c.take<float>(d.kind == BC_MODEL_MMDIT ? (size_t)B * D * f4 : 0);
+    w.txtp = c.take<float>(d.kind == BC_MODEL_MMDIT ? (size_t)B * D * f4 : 0);
+    const int nmod = d.kind == BC_MODEL_MMDIT ? 2 * d.depth : d.depth;
+    w.mods = c.take<float>((size_t)B * nmod * 6 * D * f4);
+    w.mods_s = c.take<float>(d.kind == BC_MODEL_MMDIT ? (size_t)B * d.depth_single * 3 * D * f4 : 0);
+    const bool px = d.kind == BC_MODEL_PIXART;
+    w.cap_h = c.take<char>(px ? (size_t)B * d.ctx_tokens * D * esz : 0);
+    w.ctx = c.take<char>(px ? (size_t)B * d.ctx_tokens * D * esz : 0);
+    w.ctx_kv = c.take<char>(px ? (size_t)d.depth * B * d.ctx_tokens * 2 * D * esz : 0);
+    w.feat = c.take<char>((size_t)B * T * D * esz);
+    w.out = c.take<float>((size_t)B * d.out_ch * latent_spatial(d) * f4);
+    w.prev = c.take<float>((size_t)B * d.in_ch * latent_spatial(d) * f4);
+    w.bytes = c.off + 256;
+    return w;
+}
+
+static bc_block_desc block_desc_of(const bc_model_desc& d, int B, int kind) {
+    bc_block_desc b;
+    b.kind = kind;
+    b.B = B;
+    b.T = model_tokens(d);
+    b.D = d.D;
+    b.heads = d.heads;
+    b.head_dim = d.head_dim;
+    b.mlp = d.mlp;
+    b.T_txt = (kind == BC_BLOCK_DUAL || kind == BC_BLOCK_SINGLE) ? d.txt_tokens : 0;
+    b.T_ctx = kind == BC_BLOCK_PIXART ? d.ctx_tokens : 0;
+    b.dtype = d.dtype;
+    return b;
+}
+
+// alpha_bar of the linear beta schedule 1e-4 .. 0.02 over 1000 steps.
+static void alpha_bar(double* ab) {
+    double p = 1.0;
+    for (int i = 0; i < 1000; ++i) {
+        p *= 1.0 - (1e-4 + (0.02 - 1e-4) * (double)i / 999.0);
+        ab[i] = p;
+    }
+}
+
+// Sampler coefficients of step k (see launch_sampler for their meaning).
+static SamplerCoef sampler_coef(int sampler, int k, int S, const int32_t* tau, const double* ab, double* h_prev) {
+    SamplerCoef c;
+    std::memset(&c, 0, sizeof c);
+    if (sampler == BC_SAMPLER_EULER) {
+        c.mode = 0;
+        c.c[0] = 1.f;
+        c.c[1] = (float)((1.0 - (double)(k + 1) / S) - (1.0 - (double)k / S));
+        return c;
+    }
+    const double a = ab[tau[k]];
+    const double a2 = k + 1 < S ? ab[tau[k + 1]] : 1.0;
+    if (sampler == BC_SAMPLER_DDIM) {
+        c.mode = 0;
+        c.c[0] = (float)std::sqrt(a2 / a);
+        c.c[1] = (float)(std::sqrt(1.0 - a2) - std::sqrt(a2 * (1.0 - a) / a));
+        return c;
+    }
+    // DPM-Solver++(2M), data prediction.
+    const double al = std::sqrt(a), sg = std::sqrt(1.0 - a);
+    c.c[2] = (float)sg;
+    c.c[3] = (float)al;
+    if (k == S - 1) {
+        c.mode = 2;
+        return c;
+    }
+    const double al2 = std::sqrt(a2), sg2 = std::sqrt(1.0 - a2);
+    const double h = std::log(al2 / sg2) - std::log(al / sg);
+    c.mode = 1;
+    c.c[0] = (float)(sg2 / sg);
+    c.c[1] = (float)(-al2 * (std::exp(-h) - 1.0));
+    if (k == 0) {
+        c.c[4] = 1.f;
+        c.c[5] = 0.f;
+    } else {
+        const double r = *h_prev / h;
+        c.c[4] = (float)(1.0 + 1.0 / (2.0 * r));
+        c.c[5] = (float)(-1.0 / (2.0 * r));
+    }
+    *h_prev = h;
+    return c;
+}
+
+}  // namespace bc
+
+using namespace bc;
+
+extern "C" {
+
+int bc_block_workspace_size(const bc_block_desc* d, size_t* bytes) {
+    clear_error();
+    if (!d || !bytes) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
+    BC_TRY(check_block_desc(*d));
+    *bytes = block_ws(*d, nullptr, nullptr, nullptr, nullptr, nullptr);
+    return BC_OK;
+}
+
+int bc_dit_block_forward(const bc_block_desc* dp, const bc_block_weights* wp, float* x, float* x_txt, const float* c,
+                         const void* ctx, void* ws, size_t ws_bytes, void* stream) {
+    clear_error();
+    if (!dp || !wp || !x || !c || !ws) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
+    const bc_block_desc& d = *dp;
+    BC_TRY(check_block_desc(d));
+    BC_TRY(check_block_weights(*wp, d.kind));
+    if (d.kind == BC_BLOCK_DUAL && !x_txt) return fail(BC_ERR_INVALID_ARG, "dual-stream block needs x_txt");
+    if (d.kind == BC_BLOCK_PIXART && !ctx) return fail(BC_ERR_INVALID_ARG, "PixArt block needs ctx");
+    if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(BC_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    BlockBufs bb;
+    float *mod, *mod_t;
+    void* kv;
+    const size_t need = block_ws(d, ws, &bb, &mod, &mod_t, &kv);
+    if (ws_bytes < need) return fail(BC_ERR_INVALID_ARG, "workspace %zu < %zu bytes", ws_bytes, need);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const bc_block_weights& w = *wp;
+    const int D = d.D;
+    if (d.kind == BC_BLOCK_PIXART) {
+        const void* tab = w.img.w_mod;
+        BC_TRY(launch_add_tables(d.dtype, c, 6 * D, &tab, 1, 6 * D, d.B, mod, 6 * D, s));
+        GemmArgs g = gemm_args(ctx, D, w.wx_kv, D, d.B * d.T_ctx, 2 * D, D);
+        g.e.bias = w.bx_kv;
+        g.e.out = kv;
+        g.e.ldo = 2 * D;
+        BC_TRY(launch_gemm(d.dtype, BC_EPI_BIAS, g, s));
+        return dit_block(d, w, x, mod, 6 * D, kv, bb, nullptr, s);
+    }
+    const int nm = d.kind == BC_BLOCK_SINGLE ? 3 : 6;
+    BC_TRY(launch_skinny(d.dtype, skinny1(w.img.w_mod, w.img.b_mod, nm * D, D, d.B, c, mod, 1, 0), s));
+    if (d.kind == BC_BLOCK_DIT) return dit_block(d, w, x, mod, 6 * D, nullptr, bb, nullptr, s);
+    if (d.kind == BC_BLOCK_SINGLE) return single_block(d, w, x, mod, 3 * D, bb, nullptr, s);
+    BC_TRY(launch_skinny(d.dtype, skinny1(w.txt.w_mod, w.txt.b_mod, 6 * D, D, d.B, c, mod_t, 1, 0), s));
+    return dual_block(d, w, x, x_txt, mod, mod_t, 6 * D, bb, s);
+}
+
+int bc_model_create(const bc_model_desc* dp, const bc_model_weights* wp, bc_model** out) {
+    clear_error();
+    if (!dp || !wp || !out) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
+    const bc_model_desc& d = *dp;
+    if (d.kind < BC_MODEL_DIT || d.kind > BC_MODEL_MMDIT) return fail(BC_ERR_INVALID_ARG, "model kind %d", d.kind);
+    if (d.dtype != BC_F32 && d.dtype != BC_BF16) return fail(BC_ERR_INVALID_ARG, "dtype %d", d.dtype);
+    if (d.depth < 1 || d.depth_single < 0 || (d.kind != BC_MODEL_MMDIT && d.depth_single != 0))
+        return fail(BC_ERR_INVALID_ARG, "depth %d / %d", d.depth, d.depth_single);
+    if (d.depth > kMaxSeg || d.depth_single > kMaxSeg || (d.kind == BC_MODEL_MMDIT && 2 * d.depth > kMaxSeg))
+        return fail(BC_ERR_UNSUPPORTED, "too many blocks");
+    if (d.in_ch < 1 || d.out_ch < d.in_ch || d.patch < 1 || d.frames < 1 || d.height % d.patch || d.width % d.patch ||
+        d.height < 1 || d.width < 1)
+        return fail(BC_ERR_INVALID_ARG, "latent/patch shape");
+    if (d.freq_dim < 2 || d.freq_dim % 2 || d.freq_dim % (d.dtype == BC_BF16 ? 8 : 4))
+        return fail(BC_ERR_INVALID_ARG, "freq_dim %d", d.freq_dim);
+    if (d.n_classes < 0 || (d.kind != BC_MODEL_DIT && d.n_classes))
+        return fail(BC_ERR_INVALID_ARG, "n_classes only for DIT");
+    if (d.kind == BC_MODEL_PIXART && (d.ctx_tokens < 1 || d.ctx_dim < 1 || d.ctx_dim % 8))
+        return fail(BC_ERR_INVALID_ARG, "PixArt context %d x %d", d.ctx_tokens, d.ctx_dim);
+    if (d.kind == BC_MODEL_MMDIT && d.txt_tokens < 1) return fail(BC_ERR_INVALID_ARG, "MMDiT needs txt_tokens");
+    const int kinds[2] = {d.kind == BC_MODEL_DIT ? BC_BLOCK_DIT : d.kind == BC_MODEL_PIXART ? BC_BLOCK_PIXART : BC_BLOCK_DUAL,
+                          BC_BLOCK_SINGLE};
+    for (int k = 0; k < (d.kind == BC_MODEL_MMDIT ? 2 : 1); ++k) {
+        bc_block_desc bd = block_desc_of(d, 1, kinds[k]);
+        BC_TRY(check_block_desc(bd));
+    }
+    const bc_model_weights& w = *wp;
+    bool ok = have(w.t_w1) && have(w.t_b1) && have(w.t_w2) && have(w.t_b2) && have(w.patch_w) && have(w.patch_b) &&
+              have(w.pos) && have(w.final_w_mod) && have(w.final_w) && have(w.final_b) && have(w.blocks);
+    if (d.kind != BC_MODEL_PIXART) ok = ok && have(w.final_b_mod);
+    if (d.kind == BC_MODEL_DIT && d.n_classes) ok = ok && have(w.y_table);
+    if (d.kind == BC_MODEL_PIXART)
+        ok = ok && have(w.t6_w) && have(w.t6_b) && have(w.cap_w1) && have(w.cap_b1) && have(w.cap_w2) && have(w.cap_b2);
+    if (d.kind == BC_MODEL_MMDIT) ok = ok && have(w.txt_w) && have(w.txt_b);
+    if (!ok) return fail(BC_ERR_INVALID_ARG, "missing model weight");
+    const int nb = d.depth + d.depth_single;
+    for (int l = 0; l < nb; ++l) BC_TRY(check_block_weights(w.blocks[l], l < d.depth ? kinds[0] : BC_BLOCK_SINGLE));
+    bc_model* m = new (std::nothrow) bc_model;
+    if (!m) return fail(BC_ERR_INVALID_ARG, "out of host memory");
+    m->d = d;
+    m->w = w;
+    m->blocks.assign(w.blocks, w.blocks + nb);
+    m->w.blocks = m->blocks.data();
+    *out = m;
+    return BC_OK;
+}
+
+int bc_model_destroy(bc_model* m) {
+    clear_error();
+    delete m;
+    return BC_OK;
+}
+
+int bc_sample_workspace_size(const bc_model* m, int B, size_t* bytes) {
+    clear_error();
+    if (!m || !bytes) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
+    if (B < 1 || B > 64) return fail(BC_ERR_INVALID_ARG, "B=%d outside [1, 64]", B);
+    *bytes = carve_sample(m->d, B, nullptr).bytes;
+    return BC_OK;
+}
+
+int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask, int K, const bc_bary_params* p,
+              bc_cache_ring* ring, float* latents, const int64_t* labels, const void* text, void* ws,
+              size_t ws_bytes, void* stream) {
+    clear_error();
+    if (!m || !mask || !ring || !latents || !ws) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
+    const bc_model_desc& d = m->d;
+    if (B < 1 || B > 64) return fail(BC_ERR_INVALID_ARG, "B=%d outside [1, 64]", B);
+    if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(BC_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    const int T = model_tokens(d), D = d.D;
+    if (K != ring->K) return fail(BC_ERR_INVALID_ARG, "K=%d but the ring has %d slots", K, ring->K);
+    if (ring->dtype != d.dtype || ring->numel != (int64_t)B * T * D)
+        return fail(BC_ERR_INVALID_ARG, "ring must hold %lld elements of the model dtype per slot", (long long)B * T * D);
+    if (d.kind == BC_MODEL_DIT && d.n_classes && !labels) return fail(BC_ERR_INVALID_ARG, "class labels required");
+    if (d.kind != BC_MODEL_DIT && !text) return fail(BC_ERR_INVALID_ARG, "text input required");
+    std::vector<int32_t> tau(S > 0 ? S : 1);
+    std::vector<double> tin(S > 0 ? S : 1);
+    BC_TRY(bc_make_schedule(sampler, S, tau.data(), tin.data()));
+    std::vector<bc_plan_step> plan(S);
+    BC_TRY(bc_plan(S, mask, nullptr, K, p, plan.data()));
+    const SampleWs w = carve_sample(d, B, ws);
+    if (ws_bytes < w.bytes) return fail(BC_ERR_INVALID_ARG, "workspace %zu < %zu bytes", ws_bytes, w.bytes);
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int dt = d.dtype, Tt = d.kind == BC_MODEL_MMDIT ? d.txt_tokens : 0;
+    const size_t esz = dtype_size(dt);
+    const LatentShape ls{d.in_ch, d.frames, d.height, d.width, d.patch};
+    const int64_t spatial = latent_spatial(d);
+    double ab[1000];
+    alpha_bar(ab);
+    double h_prev = 0.0;
+    bc_cache_reset(ring);
+    const bc_block_weights* blk = m->w.blocks;
+    const bc_model_weights& mw = m->w;
+    const bc_block_desc bd_main = block_desc_of(d, B, d.kind == BC_MODEL_DIT ? BC_BLOCK_DIT
+                                                      : d.kind == BC_MODEL_PIXART ? BC_BLOCK_PIXART : BC_BLOCK_DUAL);
+    const bc_block_desc bd_single = block_desc_of(d, B, BC_BLOCK_SINGLE);
+
+    // Per-run text context.
+    if (d.kind == BC_MODEL_PIXART) {
+        const int Mc = B * d.ctx_tokens;
+        BC_TRY(plain(dt, text, d.ctx_dim, mw.cap_w1, mw.cap_b1, Mc, D, d.ctx_dim, w.cap_h, true, s));
+        BC_TRY(plain(dt, w.cap_h, D, mw.cap_w2, mw.cap_b2, Mc, D, D, w.ctx, false, s));
+        for (int l = 0; l < d.depth; ++l)
+            BC_TRY(plain(dt, w.ctx, D, blk[l].wx_kv, blk[l].bx_kv, Mc, 2 * D, D,
+                         static_cast<char*>(w.ctx_kv) + (int64_t)l * Mc * 2 * D * esz, false, s));
+    } else if (d.kind == BC_MODEL_MMDIT) {
+        BC_TRY(launch_token_mean(dt, text, B, Tt, D, w.pooled, s));
+        BC_TRY(launch_skinny(dt, skinny1(mw.txt_w, mw.txt_b, D, D, B, w.pooled, w.txtp, 0, 0), s));
+    }
+
+    for (int k = 0; k < S; ++k) {
+        const bc_plan_step& st = plan[k];
+        // Conditioning: timestep MLP, class / text terms, final-layer modulation.
+        BC_TRY(launch_sinusoid(tin[k], B, d.freq_dim, w.e, s));
+        BC_TRY(launch_skinny(dt, skinny1(mw.t_w1, mw.t_b1, D, d.freq_dim, B, w.e, w.t1, 0, 1), s));
+        SkinnyArgs t2 = skinny1(mw.t_w2, mw.t_b2, D, D, B, w.t1, w.temb, 0, 0);
+        if (d.kind == BC_MODEL_MMDIT) t2.addend = w.txtp;
+        BC_TRY(launch_skinny(dt, t2, s));
+        const float* c = w.temb;
+        if (d.kind == BC_MODEL_DIT && d.n_classes) {
+            BC_TRY(launch_add_label(dt, w.temb, mw.y_table, labels, B, D, d.n_classes + 1, w.c, s));
+            c = w.c;
+        }
+        if (d.kind == BC_MODEL_PIXART) {
+            const void* ft[2] = {mw.final_w_mod, static_cast<const char*>(mw.final_w_mod) + D * esz};
+            BC_TRY(launch_add_tables(dt, w.temb, D, ft, 2, D, B, w.fmod, 2 * D, s));
+        } else {
+            BC_TRY(launch_skinny(dt, skinny1(mw.final_w_mod, mw.final_b_mod, 2 * D, D, B, c, w.fmod, 1, 0), s));
+        }
+
+        const void* feat;
+        if (st.is_full) {
+            void* slot = nullptr;
+            BC_TRY(bc_cache_next_slot(ring, &slot));
+            BlockOut out;
+            out.ptr = slot;
+            out.dt = dt;
+            // Per-block modulation vectors for the whole stack.
+            if (d.kind == BC_MODEL_PIXART) {
+                BC_TRY(launch_skinny(dt, skinny1(mw.t6_w, mw.t6_b, 6 * D, D, B, w.temb, w.t6, 1, 0), s));
+                std::vector<const void*> tabs(d.depth);
+                for (int l = 0; l < d.depth; ++l) tabs[l] = blk[l].img.w_mod;
+                BC_TRY(launch_add_tables(dt, w.t6, 6 * D, tabs.data(), d.depth, 6 * D, B, w.mods, (int64_t)d.depth * 6 * D, s));
+            } else {
+                SkinnyArgs ma;
+                std::memset(&ma, 0, sizeof ma);
+                const int nseg = d.kind == BC_MODEL_MMDIT ? 2 * d.depth : d.depth;
+                for (int l = 0; l < d.depth; ++l) {
+                    if (d.kind == BC_MODEL_MMDIT) {
+                        ma.W[2 * l] = blk[l].img.w_mod; ma.bias[2 * l] = blk[l].img.b_mod;
+                        ma.W[2 * l + 1] = blk[l].txt.w_mod; ma.bias[2 * l + 1] = blk[l].txt.b_mod;
+                    } else {
+                        ma.W[l] = blk[l].img.w_mod; ma.bias[l] = blk[l].img.b_mod;
+                    }
+                }
+                ma.nseg = nseg; ma.Nseg = 6 * D; ma.K = D; ma.B = B;
+                ma.in = c; ma.ld_in = D; ma.out = w.mods; ma.ld_out = (int64_t)nseg * 6 * D;
+                ma.act_in = 1;
+                BC_TRY(launch_skinny(dt, ma, s));
+                if (d.kind == BC_MODEL_MMDIT && d.depth_single) {
+                    SkinnyArgs sa;
+                    std::memset(&sa, 0, sizeof sa);
+                    for (int l = 0; l < d.depth_single; ++l) {
+                        sa.W[l] = blk[d.depth + l].img.w_mod;
+                        sa.bias[l] = blk[d.depth + l].img.b_mod;
+                    }
+                    sa.nseg = d.depth_single; sa.Nseg = 3 * D; sa.K = D; sa.B = B;
+                    sa.in = c; sa.ld_in = D; sa.out = w.mods_s; sa.ld_out = (int64_t)d.depth_single * 3 * D;
+                    sa.act_in = 1;
+                    BC_TRY(launch_skinny(dt, sa, s));
+                }
+            }
+            BC_TRY(launch_patch_embed(dt, latents, ls, B, mw.patch_w, mw.patch_b, mw.pos, D, w.x_img, s));
+            if (d.kind == BC_MODEL_MMDIT) {
+                BC_TRY(launch_convert(dt, text, BC_F32, w.x_txt, (int64_t)B * Tt * D, s));
+                const int64_t ldm = (int64_t)2 * d.depth * 6 * D;
+                for (int l = 0; l < d.depth; ++l)
+                    BC_TRY(dual_block(bd_main, blk[l], w.x_img, w.x_txt, w.mods + (int64_t)2 * l * 6 * D,
+                                      w.mods + (int64_t)(2 * l + 1) * 6 * D, ldm, w.bb, s));
+                if (w.x_img != w.x) {   // regroup [img | txt] per sample for the single-stream blocks
+                    for (int b = 0; b < B; ++b) {
+                        BC_TRY(launch_copy(w.x_img + (int64_t)b * T * D, w.x + (int64_t)b * (T + Tt) * D, (int64_t)T * D * 4, s));
+                        BC_TRY(launch_copy(w.x_txt + (int64_t)b * Tt * D, w.x + ((int64_t)b * (T + Tt) + T) * D, (int64_t)Tt * D * 4, s));
+                    }
+                }
+                out.seg = T + Tt;
+                out.keep = T;
+                const int64_t lds = (int64_t)d.depth_single * 3 * D;
+                for (int l = 0; l < d.depth_single; ++l)
+                    BC_TRY(single_block(bd_single, blk[d.depth + l], w.x, w.mods_s + (int64_t)l * 3 * D, lds, w.bb,
+                                        l + 1 == d.depth_single ? &out : nullptr, s));
+                if (d.depth_single == 0) {   // stack ends with a dual block: cache its image stream
+                    BC_TRY(launch_convert(BC_F32, w.x_img, dt, slot, (int64_t)B * T * D, s));
+                }
+            } else {
+                out.seg = T;
+                out.keep = T;
+                const int64_t ldm = (int64_t)d.depth * 6 * D;
+                for (int l = 0; l < d.depth; ++l)
+                    BC_TRY(dit_block(bd_main, blk[l], w.x, w.mods + (int64_t)l * 6 * D, ldm,
+                                     d.kind == BC_MODEL_PIXART ? static_cast<char*>(w.ctx_kv) + (int64_t)l * B * d.ctx_tokens * 2 * D * esz : nullptr,
+                                     w.bb, l + 1 == d.depth ? &out : nullptr, s));
+            }
+            BC_TRY(bc_cache_push(ring, nullptr, (double)k, stream));
+            feat = slot;
+        } else {
+            const void* src[kMaxK];
+            float wf[kMaxK];
+            for (int j = 0; j < st.count; ++j) {
+                src[j] = ring->storage + (int64_t)st.slots[j] * ring->numel * esz;
+                wf[j] = (float)st.w[j];
+            }
+            BC_TRY(launch_forecast(src, wf, st.count, ring->numel, dt, w.feat, dt, s));
+            feat = w.feat;
+        }
+        BC_TRY(launch_final_layer(dt, feat, dt, w.fmod, w.fmod + D, 2 * D, mw.final_w, mw.final_b, {d.out_ch, d.frames, d.height, d.width, d.patch},
+                                  d.out_ch, B, D, w.out, s));
+        const SamplerCoef sc = sampler_coef(sampler, k, S, tau.data(), ab, &h_prev);
+        BC_TRY(launch_sampler(sc, latents, w.out, w.prev, B, d.in_ch, d.out_ch, spatial, s));
+    }
+    return BC_OK;
+}
+
+}  // extern "C"

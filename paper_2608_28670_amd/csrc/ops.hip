@@ -1,0 +1,442 @@
+// Small kernels around the block GEMMs and attention: LayerNorm + adaLN
+// modulation, the skinny linear layers of the conditioning path, patch
+// embedding, the final layer, sampler updates and element-wise helpers.
+// All statistics and accumulations are fp32.
+#include <cmath>
+
+#include "ops.h"
+
+namespace bc {
+
+constexpr float kLnEps = 1e-6f;
+
+// ---------------------------------------------------------------------------
+// LayerNorm + modulate: one wave per row, the row cached in registers.
+// ---------------------------------------------------------------------------
+template <typename Tin, typename Tout, int NV>
+__global__ __launch_bounds__(256) void ln_mod_kernel(const Tin* __restrict__ x, int64_t rows, int D,
+                                                     const float* __restrict__ shift,
+                                                     const float* __restrict__ scale, int64_t ld_mod, int rps,
+                                                     Tout* __restrict__ h) {
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const Tin* xr = x + row * D;
+    float v[NV];
+    float sum = 0.f;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        const int c = lane + 64 * j;
+        v[j] = c < D ? ld(xr + c) : 0.f;
+        sum += v[j];
+    }
+    const float mean = wave_sum(sum) / (float)D;
+    float sq = 0.f;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        const int c = lane + 64 * j;
+        const float d = c < D ? v[j] - mean : 0.f;
+        sq += d * d;
+    }
+    const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + kLnEps);
+    const int64_t b = row / rps;
+    const float* sh = shift + b * ld_mod;
+    const float* sc = scale + b * ld_mod;
+    Tout* hr = h + row * D;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        const int c = lane + 64 * j;
+        if (c < D) st(hr + c, (v[j] - mean) * rstd * (1.0f + sc[c]) + sh[c]);
+    }
+}
+
+template <typename Tin, typename Tout>
+static int run_ln(const void* x, int64_t rows, int D, const float* shift, const float* scale, int64_t ld_mod, int rps,
+                  void* h, hipStream_t s) {
+    const int nv = (D + 63) / 64;
+    dim3 g((unsigned)((rows + 3) / 4)), b(256);
+    const Tin* xi = static_cast<const Tin*>(x);
+    Tout* ho = static_cast<Tout*>(h);
+    if (nv <= 4) ln_mod_kernel<Tin, Tout, 4><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nv <= 8) ln_mod_kernel<Tin, Tout, 8><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nv <= 18) ln_mod_kernel<Tin, Tout, 18><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nv <= 32) ln_mod_kernel<Tin, Tout, 32><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nv <= 48) ln_mod_kernel<Tin, Tout, 48><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nv <= 64) ln_mod_kernel<Tin, Tout, 64><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else return fail(BC_ERR_UNSUPPORTED, "LayerNorm width %d > 4096", D);
+    return check_launch("ln_mod");
+}
+
+int launch_ln_mod(int in_dt, const void* x, int64_t rows, int D, const float* shift, const float* scale,
+                  int64_t ld_mod, int rows_per_sample, int out_dt, void* h, hipStream_t s) {
+    if (rows <= 0) return BC_OK;
+    prof_begin(PROF_LAYERNORM, s);
+    int rc;
+    if (in_dt == BC_F32 && out_dt == BC_BF16) rc = run_ln<float, bf16>(x, rows, D, shift, scale, ld_mod, rows_per_sample, h, s);
+    else if (in_dt == BC_F32) rc = run_ln<float, float>(x, rows, D, shift, scale, ld_mod, rows_per_sample, h, s);
+    else if (out_dt == BC_BF16) rc = run_ln<bf16, bf16>(x, rows, D, shift, scale, ld_mod, rows_per_sample, h, s);
+    else rc = run_ln<bf16, float>(x, rows, D, shift, scale, ld_mod, rows_per_sample, h, s);
+    prof_end(PROF_LAYERNORM, s);
+    return rc;
+}
+
+// ---------------------------------------------------------------------------
+// Skinny linear on MFMA: a 16 x 16 output tile per wave (16 samples x 16
+// output features); act(in) is staged in LDS in the weight dtype, the weights
+// stream straight from HBM into the B operand.
+// ---------------------------------------------------------------------------
+template <typename T> struct SkMma;
+template <> struct SkMma<bf16> {
+    static constexpr int E = 8, KI = 32, KC = 1024;
+    typedef bf16x8 frag;
+    __device__ static f32x4 mma(const frag& a, const frag& b, const f32x4& c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    }
+    __device__ static frag load(const bf16* p) { return __builtin_bit_cast(frag, *reinterpret_cast<const u32x4*>(p)); }
+    __device__ static frag zero() { return __builtin_bit_cast(frag, u32x4{0, 0, 0, 0}); }
+};
+template <> struct SkMma<float> {
+    static constexpr int E = 1, KI = 4, KC = 512;
+    typedef float frag;
+    __device__ static f32x4 mma(frag a, frag b, const f32x4& c) {
+        return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+    }
+    __device__ static frag load(const float* p) { return *p; }
+    __device__ static frag zero() { return 0.f; }
+};
+
+constexpr int kSkTiles = 4;   // 16-column tiles per wave
+
+template <typename T>
+__global__ __launch_bounds__(256) void skinny_kernel(SkinnyArgs a) {
+    typedef SkMma<T> MM;
+    constexpr int KC = MM::KC;
+    constexpr int PAD = 16 / (int)sizeof(T);
+    __shared__ __attribute__((aligned(16))) T sIn[16][KC + PAD];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int Ntot = a.nseg * a.Nseg;
+    const int nbase = blockIdx.x * (4 * kSkTiles * 16) + wave * kSkTiles * 16;
+    const int r16 = lane & 15, kg = (lane >> 4) * MM::E;
+
+    for (int b0 = 0; b0 < a.B; b0 += 16) {
+        f32x4 acc[kSkTiles];
+#pragma unroll
+        for (int t = 0; t < kSkTiles; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int kc0 = 0; kc0 < a.K; kc0 += KC) {
+            const int kn = min(KC, a.K - kc0);
+            __syncthreads();
+            for (int i = tid; i < 16 * KC; i += 256) {
+                const int bb = i / KC, k = i % KC;
+                float v = 0.f;
+                if (b0 + bb < a.B && k < kn) {
+                    v = a.in[(int64_t)(b0 + bb) * a.ld_in + kc0 + k];
+                    if (a.act_in == 1) v = silu(v);
+                }
+                sIn[bb][k] = (T)v;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int t = 0; t < kSkTiles; ++t) {
+                const int ncol = nbase + t * 16;
+                if (ncol >= Ntot) break;
+                const int seg = ncol / a.Nseg;
+                const int nloc = ncol - seg * a.Nseg + r16;
+                const T* wr = static_cast<const T*>(a.W[seg]) + (int64_t)nloc * a.K + kc0;
+                for (int k = 0; k < kn; k += MM::KI) {
+                    const typename MM::frag bf = (k + kg < kn) ? MM::load(wr + k + kg) : MM::zero();
+                    const typename MM::frag af = MM::load(&sIn[r16][k + kg]);
+                    acc[t] = MM::mma(af, bf, acc[t]);
+                }
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < kSkTiles; ++t) {
+            const int ncol = nbase + t * 16;
+            if (ncol >= Ntot) break;
+            const int seg = ncol / a.Nseg;
+            const int nloc = ncol - seg * a.Nseg + r16;
+            const float bv = a.bias[seg] ? ld(static_cast<const T*>(a.bias[seg]) + nloc) : 0.f;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int bb = b0 + 4 * (lane >> 4) + r;
+                if (bb >= a.B) continue;
+                float v = acc[t][r] + bv;
+                if (a.act_out == 1) v = silu(v);
+                const int64_t o = (int64_t)bb * a.ld_out + ncol + r16;
+                if (a.addend) v += a.addend[o];
+                a.out[o] = v;
+            }
+        }
+    }
+}
+
+int launch_skinny(int dt, const SkinnyArgs& a, hipStream_t s) {
+    if (a.B <= 0 || a.nseg <= 0) return BC_OK;
+    if (a.B > 64) return fail(BC_ERR_UNSUPPORTED, "conditioning batch %d > 64", a.B);
+    if (a.nseg > kMaxSeg || a.Nseg % 16 || a.K % (dt == BC_BF16 ? 8 : 4))
+        return fail(BC_ERR_UNSUPPORTED, "skinny linear segments=%d N=%d K=%d", a.nseg, a.Nseg, a.K);
+    for (int i = 0; i < a.nseg; ++i)
+        if (!a.W[i] || reinterpret_cast<uintptr_t>(a.W[i]) % 16)
+            return fail(BC_ERR_INVALID_ARG, "skinny linear weight %d missing or misaligned", i);
+    const int Ntot = a.nseg * a.Nseg;
+    const unsigned grid = (unsigned)((Ntot + 4 * kSkTiles * 16 - 1) / (4 * kSkTiles * 16));
+    if (dt == BC_BF16) skinny_kernel<bf16><<<grid, 256, 0, s>>>(a);
+    else skinny_kernel<float><<<grid, 256, 0, s>>>(a);
+    return check_launch("skinny linear");
+}
+
+// ---------------------------------------------------------------------------
+// Conditioning helpers
+// ---------------------------------------------------------------------------
+__global__ void sinusoid_kernel(double t, int B, int half, float* e) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= half) return;
+    const double f = exp(-log(10000.0) * (double)i / (double)half);
+    const double ang = t * f;
+    const float c = (float)cos(ang), sn = (float)sin(ang);
+    for (int b = 0; b < B; ++b) {
+        e[(int64_t)b * 2 * half + i] = c;
+        e[(int64_t)b * 2 * half + half + i] = sn;
+    }
+}
+
+int launch_sinusoid(double t, int B, int dim, float* e, hipStream_t s) {
+    const int half = dim / 2;
+    sinusoid_kernel<<<(half + 127) / 128, 128, 0, s>>>(t, B, half, e);
+    return check_launch("sinusoid");
+}
+
+template <typename T>
+__global__ void add_label_kernel(const float* t, const T* table, const int64_t* labels, int B, int D, int n_rows,
+                                 float* c) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (int64_t)B * D) return;
+    const int b = (int)(i / D), n = (int)(i % D);
+    int64_t lab = labels[b];
+    lab = lab < 0 ? 0 : (lab >= n_rows ? n_rows - 1 : lab);   // out-of-range labels are clamped
+    c[i] = t[i] + ld(table + lab * D + n);
+}
+
+int launch_add_label(int dt, const float* t, const void* table, const int64_t* labels, int B, int D, int n_rows,
+                     float* c, hipStream_t s) {
+    const int64_t n = (int64_t)B * D;
+    const unsigned g = (unsigned)((n + 255) / 256);
+    if (dt == BC_BF16) add_label_kernel<bf16><<<g, 256, 0, s>>>(t, static_cast<const bf16*>(table), labels, B, D, n_rows, c);
+    else add_label_kernel<float><<<g, 256, 0, s>>>(t, static_cast<const float*>(table), labels, B, D, n_rows, c);
+    return check_launch("add_label");
+}
+
+struct TableArgs { const void* tab[kMaxSeg]; };
+
+template <typename T>
+__global__ void add_tables_kernel(const float* vec, int64_t ld_vec, TableArgs ta, int nseg, int N, int B, float* out,
+                                  int64_t ld_out) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (int64_t)B * nseg * N) return;
+    const int j = (int)(i % N);
+    const int seg = (int)((i / N) % nseg);
+    const int b = (int)(i / ((int64_t)N * nseg));
+    out[(int64_t)b * ld_out + (int64_t)seg * N + j] = vec[(int64_t)b * ld_vec + j] + ld(static_cast<const T*>(ta.tab[seg]) + j);
+}
+
+int launch_add_tables(int dt, const float* vec, int64_t ld_vec, const void* const* tables, int nseg, int N, int B,
+                      float* out, int64_t ld_out, hipStream_t s) {
+    if (nseg > kMaxSeg) return fail(BC_ERR_UNSUPPORTED, "%d tables", nseg);
+    TableArgs ta;
+    for (int i = 0; i < nseg; ++i) ta.tab[i] = tables[i];
+    const int64_t n = (int64_t)B * nseg * N;
+    const unsigned g = (unsigned)((n + 255) / 256);
+    if (dt == BC_BF16) add_tables_kernel<bf16><<<g, 256, 0, s>>>(vec, ld_vec, ta, nseg, N, B, out, ld_out);
+    else add_tables_kernel<float><<<g, 256, 0, s>>>(vec, ld_vec, ta, nseg, N, B, out, ld_out);
+    return check_launch("add_tables");
+}
+
+template <typename T>
+__global__ void token_mean_kernel(const T* x, int B, int T_, int D, float* out) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (int64_t)B * D) return;
+    const int b = (int)(i / D), n = (int)(i % D);
+    float acc = 0.f;
+    for (int t = 0; t < T_; ++t) acc += ld(x + ((int64_t)b * T_ + t) * D + n);
+    out[i] = acc / (float)T_;
+}
+
+int launch_token_mean(int dt, const void* x, int B, int T, int D, float* out, hipStream_t s) {
+    const int64_t n = (int64_t)B * D;
+    const unsigned g = (unsigned)((n + 255) / 256);
+    if (dt == BC_BF16) token_mean_kernel<bf16><<<g, 256, 0, s>>>(static_cast<const bf16*>(x), B, T, D, out);
+    else token_mean_kernel<float><<<g, 256, 0, s>>>(static_cast<const float*>(x), B, T, D, out);
+    return check_launch("token_mean");
+}
+
+template <typename Tin, typename Tout>
+__global__ void convert_kernel(const Tin* in, Tout* out, int64_t n) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        st(out + i, ld(in + i));
+}
+
+int launch_convert(int in_dt, const void* in, int out_dt, void* out, int64_t n, hipStream_t s) {
+    if (n <= 0) return BC_OK;
+    int64_t blocks = (n + 255) / 256;
+    if (blocks > 16384) blocks = 16384;
+    const unsigned g = (unsigned)blocks;
+    if (in_dt == BC_F32 && out_dt == BC_BF16) convert_kernel<float, bf16><<<g, 256, 0, s>>>(static_cast<const float*>(in), static_cast<bf16*>(out), n);
+    else if (in_dt == BC_BF16 && out_dt == BC_F32) convert_kernel<bf16, float><<<g, 256, 0, s>>>(static_cast<const bf16*>(in), static_cast<float*>(out), n);
+    else return launch_copy(in, out, n * dtype_size(in_dt), s);
+    return check_launch("convert");
+}
+
+// ---------------------------------------------------------------------------
+// Patch embedding and the final layer
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void patch_embed_kernel(const float* __restrict__ lat, LatentShape ls, int B,
+                                                          const T* __restrict__ W, const T* __restrict__ bias,
+                                                          const T* __restrict__ pos, int D, float* __restrict__ x) {
+    const int Tn = ls.tokens();
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (int64_t)B * Tn * D) return;
+    const int c = (int)(i % D);
+    const int tok = (int)((i / D) % Tn);
+    const int b = (int)(i / ((int64_t)D * Tn));
+    const int hp = ls.H / ls.p, wp = ls.W / ls.p;
+    const int f = tok / (hp * wp), ti = (tok / wp) % hp, tj = tok % wp;
+    const int PD = ls.p * ls.p * ls.C;
+    float acc = 0.f;
+    for (int q = 0; q < PD; ++q) {
+        const int ph = q / (ls.p * ls.C), pw = (q / ls.C) % ls.p, ch = q % ls.C;
+        const float v = lat[((((int64_t)b * ls.C + ch) * ls.F + f) * ls.H + ti * ls.p + ph) * ls.W + tj * ls.p + pw];
+        acc = __builtin_fmaf(v, ld(W + (int64_t)c * PD + q), acc);
+    }
+    x[i] = acc + ld(bias + c) + ld(pos + (int64_t)tok * D + c);
+}
+
+int launch_patch_embed(int dt, const float* lat, LatentShape ls, int B, const void* W, const void* bias,
+                       const void* pos, int D, float* x, hipStream_t s) {
+    const int64_t n = (int64_t)B * ls.tokens() * D;
+    const unsigned g = (unsigned)((n + 255) / 256);
+    if (dt == BC_BF16)
+        patch_embed_kernel<bf16><<<g, 256, 0, s>>>(lat, ls, B, static_cast<const bf16*>(W), static_cast<const bf16*>(bias),
+                                                   static_cast<const bf16*>(pos), D, x);
+    else
+        patch_embed_kernel<float><<<g, 256, 0, s>>>(lat, ls, B, static_cast<const float*>(W), static_cast<const float*>(bias),
+                                                    static_cast<const float*>(pos), D, x);
+    return check_launch("patch_embed");
+}
+
+template <typename Tin, typename T, int NV>
+__global__ __launch_bounds__(256) void final_layer_kernel(const Tin* __restrict__ feat, const float* __restrict__ shift,
+                                                          const float* __restrict__ scale, int64_t ld_mod,
+                                                          const T* __restrict__ W, const T* __restrict__ bias,
+                                                          LatentShape ls, int C_out, int B, int D,
+                                                          float* __restrict__ out) {
+    const int lane = threadIdx.x & 63;
+    const int Tn = ls.tokens();
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= (int64_t)B * Tn) return;
+    const int b = (int)(row / Tn), tok = (int)(row % Tn);
+    const Tin* xr = feat + row * D;
+    float v[NV];
+    float sum = 0.f;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        const int c = lane + 64 * j;
+        v[j] = c < D ? ld(xr + c) : 0.f;
+        sum += v[j];
+    }
+    const float mean = wave_sum(sum) / (float)D;
+    float sq = 0.f;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        const int c = lane + 64 * j;
+        const float d = c < D ? v[j] - mean : 0.f;
+        sq += d * d;
+    }
+    const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + kLnEps);
+    const float* sh = shift + (int64_t)b * ld_mod;
+    const float* sc = scale + (int64_t)b * ld_mod;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+        const int c = lane + 64 * j;
+        v[j] = c < D ? (v[j] - mean) * rstd * (1.0f + sc[c]) + sh[c] : 0.f;
+    }
+    const int hp = ls.H / ls.p, wp = ls.W / ls.p;
+    const int f = tok / (hp * wp), ti = (tok / wp) % hp, tj = tok % wp;
+    const int NO = ls.p * ls.p * C_out;
+    for (int n = 0; n < NO; ++n) {
+        const T* wr = W + (int64_t)n * D;
+        float part = 0.f;
+#pragma unroll
+        for (int j = 0; j < NV; ++j) {
+            const int c = lane + 64 * j;
+            if (c < D) part = __builtin_fmaf(v[j], ld(wr + c), part);
+        }
+        const float y = wave_sum(part) + ld(bias + n);
+        if (lane == 0) {
+            const int ph = n / (ls.p * C_out), pw = (n / C_out) % ls.p, ch = n % C_out;
+            out[((((int64_t)b * C_out + ch) * ls.F + f) * ls.H + ti * ls.p + ph) * ls.W + tj * ls.p + pw] = y;
+        }
+    }
+}
+
+template <typename Tin, typename T>
+static int run_final(const void* feat, const float* shift, const float* scale, int64_t ld_mod, const void* W,
+                     const void* bias, LatentShape ls, int C_out, int B, int D, float* out, hipStream_t s) {
+    const int64_t rows = (int64_t)B * ls.tokens();
+    dim3 g((unsigned)((rows + 3) / 4)), blk(256);
+    const Tin* fi = static_cast<const Tin*>(feat);
+    const T* w = static_cast<const T*>(W);
+    const T* bi = static_cast<const T*>(bias);
+    const int nv = (D + 63) / 64;
+    if (nv <= 4) final_layer_kernel<Tin, T, 4><<<g, blk, 0, s>>>(fi, shift, scale, ld_mod, w, bi, ls, C_out, B, D, out);
+    else if (nv <= 18) final_layer_kernel<Tin, T, 18><<<g, blk, 0, s>>>(fi, shift, scale, ld_mod, w, bi, ls, C_out, B, D, out);
+    else if (nv <= 48) final_layer_kernel<Tin, T, 48><<<g, blk, 0, s>>>(fi, shift, scale, ld_mod, w, bi, ls, C_out, B, D, out);
+    else return fail(BC_ERR_UNSUPPORTED, "final layer width %d > 3072", D);
+    return check_launch("final_layer");
+}
+
+int launch_final_layer(int feat_dt, const void* feat, int dt, const float* shift, const float* scale, int64_t ld_mod,
+                       const void* W, const void* bias, LatentShape ls, int C_out, int B, int D, float* out,
+                       hipStream_t s) {
+    if (dt == BC_BF16) {
+        if (feat_dt == BC_BF16) return run_final<bf16, bf16>(feat, shift, scale, ld_mod, W, bias, ls, C_out, B, D, out, s);
+        return run_final<float, bf16>(feat, shift, scale, ld_mod, W, bias, ls, C_out, B, D, out, s);
+    }
+    if (feat_dt == BC_BF16) return run_final<bf16, float>(feat, shift, scale, ld_mod, W, bias, ls, C_out, B, D, out, s);
+    return run_final<float, float>(feat, shift, scale, ld_mod, W, bias, ls, C_out, B, D, out, s);
+}
+
+// ---------------------------------------------------------------------------
+// Sampler update
+// ---------------------------------------------------------------------------
+__global__ void sampler_kernel(SamplerCoef k, float* x, const float* eps, float* prev, int B, int C, int C_out,
+                               int64_t S) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (int64_t)B * C * S) return;
+    const int64_t sp = i % S;
+    const int64_t bc = i / S;
+    const int c = (int)(bc % C), b = (int)(bc / C);
+    const float e = eps[((int64_t)b * C_out + c) * S + sp];
+    const float xv = x[i];
+    if (k.mode == 0) {
+        x[i] = k.c[0] * xv + k.c[1] * e;
+        return;
+    }
+    const float x0 = (xv - k.c[2] * e) / k.c[3];
+    if (k.mode == 2) {
+        x[i] = x0;
+        return;
+    }
+    const float d = k.c[5] != 0.f ? k.c[4] * x0 + k.c[5] * prev[i] : k.c[4] * x0;
+    x[i] = k.c[0] * xv + k.c[1] * d;
+    if (prev) prev[i] = x0;
+}
+
+int launch_sampler(const SamplerCoef& k, float* x, const float* eps, float* prev, int B, int C, int C_out, int64_t S,
+                   hipStream_t s) {
+    const int64_t n = (int64_t)B * C * S;
+    sampler_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(k, x, eps, prev, B, C, C_out, S);
+    return check_launch("sampler");
+}
+
+}  // namespace bc

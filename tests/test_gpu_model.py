@@ -1,0 +1,247 @@
+"""GPU parity of the layer stack and of the whole BaryCache sampling loop,
+through the C ABI (bc_dit_block_forward, bc_sample), against the oracle on the
+same seeded inputs.
+
+Gates: relative L2 error <= 2e-2 for bf16 block outputs and final latents.
+Because random-init blocks are close to the identity, block tests also gate
+the relative L2 error of the block's update (output - input).  The fp32 tiny
+model is expected to agree to ~1e-6 and is gated at 1e-4."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import bary, model as om, sampler as osm
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def rel_l2(g, r):
+    return float(np.linalg.norm(np.asarray(g, np.float64) - r) / max(np.linalg.norm(r), 1e-30))
+
+
+def _f32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV)
+
+
+def _block_call(bc, cfg, P, kind, x, c, x_txt=None, ctx=None, l=0):
+    from paper_2608_28670_amd import loader
+    dP = loader.upload(P, cfg)
+    blocks = loader.block_list(cfg, dP)
+    dtc = bc.BF16 if cfg.dtype == "bf16" else bc.F32
+    B = x.shape[0]
+    desc = bc.block_desc(kind, B, cfg.tokens, cfg.hidden, cfg.heads, cfg.head_dim, cfg.mlp, dtc,
+                         T_txt=cfg.txt_tokens if kind in (bc.BLOCK_DUAL, bc.BLOCK_SINGLE) else 0,
+                         T_ctx=cfg.ctx_tokens if kind == bc.BLOCK_PIXART else 0)
+    ws = torch.empty(bc.block_workspace_size(desc), dtype=torch.uint8, device=DEV)
+    tx = _f32(x)
+    tt = _f32(x_txt) if x_txt is not None else None
+    tctx = torch.from_numpy(ctx).to(DEV).to(loader.torch_dtype(cfg)) if ctx is not None else None
+    bc.dit_block_forward(desc, blocks[l], tx, _f32(c), ws, x_txt=tt, ctx=tctx)
+    torch.cuda.synchronize()
+    return tx.cpu().numpy(), (tt.cpu().numpy() if tt is not None else None)
+
+
+def _check_block(got, x, exp, tol):
+    e_out = rel_l2(got, exp)
+    e_upd = rel_l2(got - x, exp - x)
+    print(f"block rel-L2 out {e_out:.2e} update {e_upd:.2e}")
+    assert e_out <= tol and e_upd <= tol, (e_out, e_upd)
+    return e_upd
+
+
+@pytest.mark.parametrize("name,B", [("tiny", 2), ("dit_xl2", 2), ("dit_xl2", 16)])
+def test_dit_block(bclib, name, B):
+    cfg = synth.scaled(synth.CONFIGS[name], depth=1)
+    P = synth.params(cfg)
+    M = om.Model(cfg, P)
+    x = synth.normal("blk/x", (B, cfg.tokens, cfg.hidden))
+    c = synth.normal("blk/c", (B, cfg.hidden), 0.5)
+    exp = M.dit_block(0, x.astype(np.float64), M.block_mod(0, {"c": c.astype(np.float64)}))
+    got, _ = _block_call(bclib, cfg, P, bclib.BLOCK_DIT, x, c)
+    upd = _check_block(got, x, exp, 1e-4 if cfg.dtype == "f32" else 2e-2)
+    if cfg.dtype == "f32":
+        assert upd < 1e-4
+
+
+def test_pixart_block(bclib):
+    cfg = synth.scaled(synth.CONFIGS["pixart"], depth=1, latent=(4, 32, 32), batch=2)
+    P = synth.params(cfg)
+    M = om.Model(cfg, P)
+    B, D = 2, cfg.hidden
+    x = synth.normal("pblk/x", (B, cfg.tokens, D))
+    t6 = synth.normal("pblk/t6", (B, 6 * D), 0.3)
+    ctx = synth.bf16_round(synth.normal("pblk/ctx", (B, cfg.ctx_tokens, D)))
+    y = om.linear(ctx.astype(np.float64), P["blocks.0.wx_kv"], P["blocks.0.bx_kv"])
+    kv = [(om.split_heads(y[..., :D], cfg.heads), om.split_heads(y[..., D:], cfg.heads))]
+    mod = M.block_mod(0, {"t6": t6.astype(np.float64)})
+    exp = M.dit_block(0, x.astype(np.float64), mod, {"kv": kv})
+    got, _ = _block_call(bclib, cfg, P, bclib.BLOCK_PIXART, x, t6, ctx=ctx)
+    _check_block(got, x, exp, 2e-2)
+
+
+def _mm_cfg(**kw):
+    base = dict(depth=1, depth_single=1, hidden=256, heads=2, head_dim=128, mlp=1024, latent=(16, 3, 20, 20),
+                txt_tokens=40, batch=2)
+    base.update(kw)
+    return synth.scaled(synth.CONFIGS["hunyuan"], **base)
+
+
+def test_dual_block(bclib):
+    cfg = _mm_cfg()
+    P = synth.params(cfg)
+    M = om.Model(cfg, P)
+    B = 2
+    x = synth.normal("dblk/x", (B, cfg.tokens, cfg.hidden))
+    xt = synth.normal("dblk/xt", (B, cfg.txt_tokens, cfg.hidden))
+    c = synth.normal("dblk/c", (B, cfg.hidden), 0.5)
+    ei, et = M.dual_block(0, x.astype(np.float64), xt.astype(np.float64), {"c": c.astype(np.float64)})
+    gi, gt = _block_call(bclib, cfg, P, bclib.BLOCK_DUAL, x, c, x_txt=xt)
+    _check_block(gi, x, ei, 2e-2)
+    _check_block(gt, xt, et, 2e-2)
+
+
+def test_single_block(bclib):
+    cfg = _mm_cfg()
+    P = synth.params(cfg)
+    M = om.Model(cfg, P)
+    B = 2
+    x = synth.normal("sblk/x", (B, cfg.tokens + cfg.txt_tokens, cfg.hidden))
+    c = synth.normal("sblk/c", (B, cfg.hidden), 0.5)
+    exp = M.single_block(0, x.astype(np.float64), {"c": c.astype(np.float64)})
+    got, _ = _block_call(bclib, cfg, P, bclib.BLOCK_SINGLE, x, c, l=1)
+    _check_block(got, x, exp, 2e-2)
+
+
+def test_block_rejects_bad_shapes(bclib):
+    desc = bclib.block_desc(bclib.BLOCK_DIT, 1, 16, 120, 3, 40, 256, bclib.BF16)
+    with pytest.raises(bclib.BCError) as e:
+        bclib.block_workspace_size(desc)
+    assert e.value.code == bclib.ERR_UNSUPPORTED
+    desc = bclib.block_desc(bclib.BLOCK_DIT, 1, 16, 128, 3, 32, 256, bclib.BF16)
+    with pytest.raises(bclib.BCError) as e:
+        bclib.block_workspace_size(desc)
+    assert e.value.code == bclib.ERR_INVALID_ARG
+
+
+# ---------------------------------------------------------------------------
+# the sampling loop
+# ---------------------------------------------------------------------------
+
+def _run_sample(bc, cfg, P, B, mask, labels=None, text=None, sample_idx=None):
+    from paper_2608_28670_amd import loader
+    dm = loader.DeviceModel(cfg, P)
+    xT = synth.latents(cfg, batch=B)
+    x = _f32(xT)
+    tl = torch.from_numpy(labels).to(DEV) if labels is not None else None
+    tt = torch.from_numpy(text).to(DEV).to(loader.torch_dtype(cfg)) if text is not None else None
+    ring = dm.sample(x, mask, labels=tl, text=tt)
+    torch.cuda.synchronize()
+    return xT, x.cpu().numpy(), ring
+
+
+def _oracle_sample(cfg, P, xT, mask, labels=None, text=None, dtype=np.float64):
+    M = om.Model(cfg, P, dtype=dtype)
+    return osm.sample(M, xT.astype(np.float64), mask, cfg.K, labels=labels, text=text)
+
+
+def _check_ring(ring, mask, K):
+    steps = bary.plan(mask, K)
+    cnt, head, tn, slots = ring.state()
+    full = [k for k in range(len(mask)) if mask[k]]
+    assert cnt == min(len(full), K) and head == steps[-1].head
+    assert list(tn) == [float(k) for k in full[::-1][:cnt]]
+
+
+def test_sample_tiny_fp32(bclib):
+    cfg = synth.CONFIGS["tiny"]
+    P = synth.params(cfg)
+    mask = bary.make_mask(cfg.steps, cfg.interval)
+    xT, got, ring = _run_sample(bclib, cfg, P, cfg.batch, mask)
+    exp = _oracle_sample(cfg, P, xT, mask)
+    err = rel_l2(got, exp)
+    print(f"tiny fp32 final latents rel-L2 {err:.2e}")
+    assert err <= 1e-4
+    _check_ring(ring, mask, cfg.K)
+
+
+def test_sample_tiny_all_full_and_k1(bclib):
+    cfg = synth.scaled(synth.CONFIGS["tiny"], K=1)
+    P = synth.params(cfg)
+    mask = np.array([1, 0, 0, 1, 0, 1, 1, 0, 0, 0], np.uint8)
+    xT, got, _ = _run_sample(bclib, cfg, P, cfg.batch, mask)
+    assert rel_l2(got, _oracle_sample(cfg, P, xT, mask)) <= 1e-4
+    ones = np.ones(cfg.steps, np.uint8)
+    xT, got, _ = _run_sample(bclib, cfg, P, cfg.batch, ones)
+    assert rel_l2(got, _oracle_sample(cfg, P, xT, ones)) <= 1e-4
+
+
+def test_sample_dit_xl2_reduced_depth(bclib):
+    cfg = synth.scaled(synth.CONFIGS["dit_xl2"], depth=2, batch=2)
+    P = synth.params(cfg)
+    mask = bary.make_mask(cfg.steps, cfg.interval)
+    labels = synth.labels(cfg, batch=2)
+    xT, got, ring = _run_sample(bclib, cfg, P, 2, mask, labels=labels)
+    exp = _oracle_sample(cfg, P, xT, mask, labels=labels)
+    err = rel_l2(got, exp)
+    print(f"dit_xl2 depth 2 final latents rel-L2 {err:.2e}")
+    assert err <= 2e-2
+    _check_ring(ring, mask, cfg.K)
+
+
+def test_sample_pixart_reduced(bclib):
+    cfg = synth.scaled(synth.CONFIGS["pixart"], depth=2, latent=(4, 32, 32), batch=1)
+    P = synth.params(cfg)
+    mask = bary.make_mask(cfg.steps, cfg.interval)
+    text = synth.text(cfg, batch=1)
+    xT, got, ring = _run_sample(bclib, cfg, P, 1, mask, text=text)
+    exp = _oracle_sample(cfg, P, xT, mask, text=text)
+    err = rel_l2(got, exp)
+    print(f"pixart reduced final latents rel-L2 {err:.2e}")
+    assert err <= 2e-2
+    _check_ring(ring, mask, cfg.K)
+
+
+@pytest.mark.parametrize("B", [1, 2])
+def test_sample_mmdit_reduced(bclib, B):
+    cfg = _mm_cfg(steps=12, batch=B)
+    P = synth.params(cfg)
+    mask = bary.make_mask(cfg.steps, cfg.interval)
+    text = synth.text(cfg, batch=B)
+    xT, got, ring = _run_sample(bclib, cfg, P, B, mask, text=text)
+    exp = _oracle_sample(cfg, P, xT, mask, text=text)
+    err = rel_l2(got, exp)
+    print(f"mmdit reduced B={B} final latents rel-L2 {err:.2e}")
+    assert err <= 2e-2
+    _check_ring(ring, mask, cfg.K)
+
+
+def test_sample_dit_xl2_full_size_sampled(bclib):
+    """The benchmark workload (28 blocks, batch 16, 50 DDIM steps, K=3, one
+    full step in 4): all 16 samples run on the GPU; samples 0 and 15 are
+    recomputed alone by the oracle (in fp32, for time) and compared."""
+    cfg = synth.CONFIGS["dit_xl2"]
+    P = synth.params(cfg)
+    mask = bary.make_mask(cfg.steps, cfg.interval)
+    labels = synth.labels(cfg)
+    xT, got, ring = _run_sample(bclib, cfg, P, cfg.batch, mask, labels=labels)
+    _check_ring(ring, mask, cfg.K)
+    for b in (0, cfg.batch - 1):
+        exp = _oracle_sample(cfg, P, xT[b:b + 1], mask, labels=labels[b:b + 1], dtype=np.float32)
+        err = rel_l2(got[b:b + 1], exp)
+        print(f"dit_xl2 full, sample {b}: final latents rel-L2 {err:.2e}")
+        assert err <= 2e-2
+
+
+def test_sample_rejects_bad_inputs(bclib):
+    cfg = synth.CONFIGS["tiny"]
+    P = synth.params(cfg)
+    from paper_2608_28670_amd import loader
+    dm = loader.DeviceModel(cfg, P)
+    x = _f32(synth.latents(cfg))
+    with pytest.raises(bclib.BCError) as e:
+        dm.sample(x, np.array([0, 1, 1], np.uint8))
+    assert e.value.code == bclib.ERR_INVALID_ARG
+    with pytest.raises(bclib.BCError):
+        dm.sample(x, np.ones(3, np.uint8), K=9)
