@@ -1,0 +1,244 @@
+"""Benchmark of the BaryCache hot path on one MI355X.
+
+One step = one BaryCache sampling run of the whole batch through the full
+schedule (every full step runs the block stack, every other step the K-way
+forecast; all steps run the final layer and the sampler update), starting
+from resident noise.  Default workload: the DiT-XL/2-shaped class-conditional
+model (28 blocks, D 1152, 16 x 72 heads, MLP 4608, 256 tokens), batch 16,
+50 DDIM steps, K = 3, one full step every 4 (14 of 50), bf16, random-init
+weights drawn from seed 2026.
+
+Prints one JSON line: samples/s, the dominant kernel's roofline (the fc1
+GEMM with GELU epilogue, timed with HIP events on its launch stream), the
+forecast kernel's HBM bandwidth on [8, 16384, 3072] features, the speedup over
+the all-full mask, and the oracle's CPU throughput on a bounded sample.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="dit_xl2")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-forecast", action="store_true")
+    ap.add_argument("--cpu-steps", type=int, default=9, help="oracle sample: first N steps of one sample")
+    return ap.parse_args()
+
+
+def source_hash(*names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2608_28670_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def counters_traffic(kernel_tag, src_hash, launches_bytes_ref):
+    """HBM bytes per launch from committed rocprofv3 counter summaries, or None
+    if none exist for the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{kernel_tag}_counters.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        c = json.load(f)
+    if c.get("source_hash") != src_hash:
+        return None
+    return c.get("hbm_bytes_per_launch")
+
+
+def forecast_bench(bc, torch, dev, K=3, dtype="bf16", iters=10):
+    """HBM bandwidth of the forecast kernel on K cached [8, 16384, 3072] features."""
+    import synth
+    from oracle import bary  # noqa: F401  (not used for timing; weights come from the library)
+    shape = synth.FORECAST_SHAPE
+    n = shape[0] * shape[1] * shape[2]
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    g = torch.Generator(device=dev)
+    g.manual_seed(synth.SEED + K)
+    storage = torch.empty((K, n), dtype=tdt, device=dev)
+    for j in range(K):
+        storage[j].normal_(generator=g)
+    ring = bc.CacheRing(K, storage)
+    s, t = synth.forecast_times(K)
+    for j in reversed(range(K)):
+        ring.push(None, float(s[j]))
+    w = bc.bary_weights(s, t)
+    out = torch.empty(n, dtype=tdt, device=dev)
+    for _ in range(2):
+        bc.bary_extrapolate(ring, w, out)
+    torch.cuda.synchronize()
+    bc.profile_enable(bc.PROF_FORECAST, iters)
+    for _ in range(iters):
+        bc.bary_extrapolate(ring, w, out)
+    ms, cnt = bc.profile_collect(bc.PROF_FORECAST)
+    esz = 2 if dtype == "bf16" else 4
+    bytes_alg = (K + 1) * n * esz
+    avg_s = ms / cnt / 1e3
+    gbs = bytes_alg / avg_s / 1e9
+    del storage, out
+    torch.cuda.empty_cache()
+    return {"K": K, "dtype": dtype, "shape": list(shape), "bytes_per_launch": bytes_alg,
+            "avg_us": round(avg_s * 1e6, 2), "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+            "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
+
+
+def cpu_baseline(cfg, params, labels, xT, mask, nsteps):
+    """The oracle on the host cores, on one sample and the first `nsteps` steps
+    of the schedule; per-step times composed to the whole schedule."""
+    import numpy as np
+    from oracle import bary, model as om, sampler as osm
+    M = om.Model(cfg, params)
+    x = xT[:1].astype(np.float64)
+    lab = labels[:1]
+    steps = bary.plan(mask, cfg.K)
+    tin = osm.model_time(cfg.sampler, cfg.steps)
+    smp = osm.Sampler(cfg.sampler, cfg.steps, cfg.in_ch)
+    ring = bary.Ring(cfg.K)
+    t_full, t_fc = [], []
+    for k in range(min(nsteps, cfg.steps)):
+        t0 = time.perf_counter()
+        cond = M.condition(tin[k], 1, lab)
+        if mask[k]:
+            feat = M.stack(M.embed(x), cond, None)
+            ring.push(feat, k)
+        else:
+            st = steps[k]
+            feat = bary.forecast([ring.slots[i] for i in st.slots], st.w)
+        out = M.final(feat, cond)
+        x = smp.step(k, x, out)
+        (t_full if mask[k] else t_fc).append(time.perf_counter() - t0)
+    nfull = int(mask.sum())
+    per_sample = nfull * np.mean(t_full) + (cfg.steps - nfull) * np.mean(t_fc)
+    cores = len(os.sched_getaffinity(0))
+    return {"value": round(1.0 / per_sample, 6), "unit": "samples/s", "cores": cores, "kind": "oracle",
+            "sample": (f"1 sample, steps 0-{nsteps - 1} of the {cfg.steps}-step schedule "
+                       f"({len(t_full)} full at {np.mean(t_full):.2f} s, {len(t_fc)} forecast at "
+                       f"{np.mean(t_fc) * 1e3:.1f} ms), composed to {nfull} full + {cfg.steps - nfull} "
+                       f"forecast steps; numpy fp64 on {cores} host threads")}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
+              file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_2608_28670_amd as bc
+    from paper_2608_28670_amd import loader
+    from oracle import bary
+
+    if not os.path.exists(bc.LIB_PATH):
+        from paper_2608_28670_amd import build
+        build.build()
+    dev = "cuda:0"
+    cfg = synth.CONFIGS[args.workload]
+    t0 = time.time()
+    params = synth.params(cfg)
+    dm = loader.DeviceModel(cfg, params)
+    B = cfg.batch
+    mask = bary.make_mask(cfg.steps, cfg.interval)
+    labels = synth.labels(cfg) if cfg.n_classes else None
+    text = synth.text(cfg) if cfg.kind != "dit" else None
+    xT = synth.latents(cfg)
+    x0 = torch.from_numpy(xT).to(dev)
+    x = torch.empty_like(x0)
+    tl = torch.from_numpy(labels).to(dev) if labels is not None else None
+    tt = torch.from_numpy(text).to(dev).to(loader.torch_dtype(cfg)) if text is not None else None
+    print(f"setup {time.time() - t0:.1f} s", file=sys.stderr)
+
+    def run(m):
+        x.copy_(x0)
+        dm.sample(x, m, labels=tl, text=tt)
+
+    for _ in range(args.warmup):
+        run(mask)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        run(mask)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    ms_per_step = elapsed / args.steps * 1e3
+    value = B * args.steps / elapsed
+
+    # Speedup reference: the same sampler with every step full.
+    full = np.ones(cfg.steps, np.uint8)
+    run(full)
+    torch.cuda.synchronize()
+    tf = time.perf_counter()
+    nref = max(1, min(3, args.steps))
+    for _ in range(nref):
+        run(full)
+    torch.cuda.synchronize()
+    ms_full = (time.perf_counter() - tf) / nref * 1e3
+
+    # Dominant kernel: the fc1 GEMM (bias + GELU epilogue), HIP events on its stream.
+    nfull = int(mask.sum())
+    launches = nfull * cfg.depth
+    bc.profile_enable(bc.PROF_GEMM_GELU, launches)
+    run(mask)
+    gemm_ms, gemm_n = bc.profile_collect(bc.PROF_GEMM_GELU)
+    M_rows = B * cfg.tokens
+    flops = 2.0 * M_rows * cfg.mlp * cfg.hidden
+    avg_s = gemm_ms / gemm_n / 1e3
+    achieved = flops / avg_s / 1e12
+    gemm_hash = source_hash("gemm.hip", "gemm.h", "hip_common.h")
+    roofline = {"bound": "mfma", "kernel": "gemm fc1 (bias+GELU)",
+                "shape": [M_rows, cfg.mlp, cfg.hidden], "flops_per_launch": flops,
+                "avg_us": round(avg_s * 1e6, 2), "launches": gemm_n,
+                "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": counters_traffic("gemm_fc1_dit_xl2", gemm_hash, None),
+                "source_hash": gemm_hash}
+
+    forecast = None
+    if not args.no_forecast:
+        del dm
+        torch.cuda.empty_cache()
+        forecast = forecast_bench(bc, torch, dev, K=3, dtype="bf16")
+        fc_hash = source_hash("forecast.hip", "hip_common.h")
+        forecast["traffic"] = counters_traffic("forecast_k3_bf16", fc_hash, None)
+        forecast["source_hash"] = fc_hash
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, params, labels, xT, mask, args.cpu_steps)
+
+    line = {
+        "metric": "end-to-end samples/s at fixed skip schedule; forecast HBM GB/s; block MFMA util",
+        "value": round(value, 3), "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.depth} blocks, D {cfg.hidden}, {cfg.heads}x{cfg.head_dim} heads, "
+                               f"MLP {cfg.mlp}, {cfg.tokens} tokens, batch {B}, {cfg.steps} {cfg.sampler} steps, "
+                               f"K={cfg.K}, full every {cfg.interval} ({nfull}/{cfg.steps}), random-init weights",
+                   "global_batch": B, "parallelism": "none (1 GPU)"},
+        "speedup_vs_all_full": round(ms_full / ms_per_step, 3),
+        "ms_all_full": round(ms_full, 3),
+        "roofline": roofline,
+        "forecast": forecast,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()
