@@ -282,8 +282,9 @@ typedef enum { BC_SAMPLER_DDIM = 0, BC_SAMPLER_DPMPP2M = 1, BC_SAMPLER_EULER = 2
  * noise-prediction samplers, 1000 (1 - k/S) for Euler).  Either may be NULL. */
 int bc_make_schedule(int sampler, int S, int32_t* tau_out, double* time_out);
 
-/* Bytes of workspace bc_sample needs for B samples. */
-int bc_sample_workspace_size(const bc_model* m, int B, size_t* bytes);
+/* Bytes of workspace bc_sample needs for B samples and an S-step schedule
+ * (the per-step conditioning of the whole schedule is held at once). */
+int bc_sample_workspace_size(const bc_model* m, int B, int S, size_t* bytes);
 
 /* The BaryCache sampling loop (Sec. 3.3): for k = 0..S-1, a full step
  * (mask[k] = 1) runs the layer stack and its last block writes the stepwise
@@ -299,7 +300,10 @@ int bc_sample_workspace_size(const bc_model* m, int B, size_t* bytes);
  *   labels:  DIT with classes: device int64 [B]; else NULL.
  *   text:    PIXART: device [B, ctx_tokens, ctx_dim]; MMDIT: device [B, txt_tokens, D]
  *            (model dtype); else NULL.
- *   ws:      device workspace of bc_sample_workspace_size bytes, 256-byte aligned.
+ *   ws:      device workspace of bc_sample_workspace_size(m, B, S) bytes, 256-byte aligned.
+ * The conditioning of every step (timestep MLP, class or text terms, the
+ * final layer's and the blocks' adaLN vectors) depends only on the schedule,
+ * labels and text, so it is computed up front in batched launches.
  * Errors: INVALID_ARG, DEGENERATE (a forecast step's weights), UNSUPPORTED, HIP. */
 int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
               int K, const bc_bary_params* p, bc_cache_ring* ring, float* latents,

@@ -111,7 +111,7 @@ _SIGS = {
     "bc_model_create": (C.c_int, [C.POINTER(ModelDesc), C.POINTER(ModelWeights), C.POINTER(C.c_void_p)]),
     "bc_model_destroy": (C.c_int, [C.c_void_p]),
     "bc_make_schedule": (C.c_int, [C.c_int, C.c_int, C.c_void_p, C.c_void_p]),
-    "bc_sample_workspace_size": (C.c_int, [C.c_void_p, C.c_int, C.POINTER(C.c_size_t)]),
+    "bc_sample_workspace_size": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.POINTER(C.c_size_t)]),
     "bc_sample": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int,
                             C.POINTER(BaryParams), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
                             C.c_void_p, C.c_size_t, C.c_void_p]),
@@ -370,9 +370,9 @@ class Model:
             _lib.bc_model_destroy(self.h)
             self.h = None
 
-    def workspace_size(self, B: int) -> int:
+    def workspace_size(self, B: int, S: int) -> int:
         n = C.c_size_t()
-        _check(lib().bc_sample_workspace_size(self.h, B, C.byref(n)))
+        _check(lib().bc_sample_workspace_size(self.h, B, S, C.byref(n)))
         return n.value
 
 

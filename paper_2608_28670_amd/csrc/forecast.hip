@@ -112,8 +112,24 @@ __global__ __launch_bounds__(kThreads) void forecast_scalar_kernel(FcArgs a, int
     }
 }
 
+template <typename Tin, typename Tout, int U>
+static void launch_vec(const FcArgs& a, int K, int64_t nv, hipStream_t s) {
+    const int64_t blocks = (nv + kThreads * U - 1) / (kThreads * U);
+    dim3 g((unsigned)blocks), b(kThreads);
+    switch (K) {
+#define BC_FC_CASE(KK) case KK: forecast_vec_kernel<KK, Tin, Tout, U><<<g, b, 0, s>>>(a); break;
+        BC_FC_CASE(1) BC_FC_CASE(2) BC_FC_CASE(3) BC_FC_CASE(4)
+        BC_FC_CASE(5) BC_FC_CASE(6) BC_FC_CASE(7) BC_FC_CASE(8)
+#undef BC_FC_CASE
+        default: break;
+    }
+}
+
 template <typename Tin, typename Tout>
 static int run_forecast(const FcArgs& a, int K, hipStream_t s) {
+    // Large tensors: several 16-byte vectors per thread, all loads issued
+    // first; small ones (below ~32M elements): one per thread, for more
+    // workgroups in flight.
     constexpr int U = sizeof(Tin) == 2 ? 4 : 2;
     bool aligned = (reinterpret_cast<uintptr_t>(a.out) % 16) == 0;
     for (int j = 0; j < K; ++j) aligned = aligned && (reinterpret_cast<uintptr_t>(a.src[j]) % 16) == 0;
@@ -121,16 +137,9 @@ static int run_forecast(const FcArgs& a, int K, hipStream_t s) {
     if (aligned) {
         const int64_t nv = a.n / kEl;
         if (nv > 0) {
-            const int64_t blocks = (nv + kThreads * U - 1) / (kThreads * U);
-            if (blocks > 0x7fffffff) return fail(BC_ERR_UNSUPPORTED, "forecast of %lld elements is too large", (long long)a.n);
-            dim3 g((unsigned)blocks), b(kThreads);
-            switch (K) {
-#define BC_FC_CASE(KK) case KK: forecast_vec_kernel<KK, Tin, Tout, U><<<g, b, 0, s>>>(a); break;
-                BC_FC_CASE(1) BC_FC_CASE(2) BC_FC_CASE(3) BC_FC_CASE(4)
-                BC_FC_CASE(5) BC_FC_CASE(6) BC_FC_CASE(7) BC_FC_CASE(8)
-#undef BC_FC_CASE
-                default: return fail(BC_ERR_INVALID_ARG, "K=%d", K);
-            }
+            if (nv / kThreads > 0x7fffffff) return fail(BC_ERR_UNSUPPORTED, "forecast of %lld elements is too large", (long long)a.n);
+            if (a.n >= ((int64_t)32 << 20)) launch_vec<Tin, Tout, U>(a, K, nv, s);
+            else launch_vec<Tin, Tout, 1>(a, K, nv, s);
             done = nv * kEl;
         }
     }

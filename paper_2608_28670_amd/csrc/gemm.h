@@ -6,8 +6,9 @@
 namespace bc {
 
 // Epilogue of y = A W^T.  Column c of row r gets v = acc + bias[c]; then
-//   BIAS kind: v = GELU(v) if c >= gelu_from; stored (in the operand dtype)
-//     to out[r*ldo + c] if c < split, else to out2[r*ldo2 + c - split + off2];
+//   BIAS kind: v = GELU(v) if c >= gelu_from; stored to out[r*ldo + c] (fp32
+//     if out_f32, else the operand dtype) if c < split, else (operand dtype)
+//     to out2[r*ldo2 + c - split + off2];
 //   GATE_RES kind: v = res[r*ldr + c] + gate[(r / rows_per_gate)*ldg + c] * v
 //     (gate NULL: a plain residual add),
 //     stored to row (r / seg) * keep + r % seg of out (fp32 if out_f32, else
@@ -37,9 +38,21 @@ struct GemmArgs {
     GemmEpi e;
 };
 
+// Grouped weights: output columns [i*Nseg, (i+1)*Nseg) use W[i] ([Nseg, K],
+// row stride ldw) and bias[i] (may be NULL).
+constexpr int kMaxGemmSeg = 64;
+struct GemmSeg {
+    const void* W[kMaxGemmSeg];
+    const void* bias[kMaxGemmSeg];
+    int Nseg;
+};
+
 // Defaults: plain bias epilogue writing [M, N] densely to (unset) out.
 GemmArgs gemm_args(const void* A, int64_t lda, const void* W, int64_t ldw, int M, int N, int K);
 // epi: BC_EPI_BIAS (covers GELU via gelu_from) or BC_EPI_GATE_RES.
 int launch_gemm(int dtype, int epi, const GemmArgs& g, hipStream_t s);
+// Bias epilogue over nseg column segments (g.N is ignored; g.e.out / ldo
+// describe the whole [M, nseg*Nseg] output).
+int launch_gemm_grouped(int dtype, const GemmArgs& g, const GemmSeg& sg, int nseg, hipStream_t s);
 
 }  // namespace bc

@@ -38,17 +38,57 @@ template <> struct Mma<float> {
     __device__ static __forceinline__ frag load(const float* p) { return *p; }
 };
 
-constexpr int kGemmThreads = 256;
+// Bias + GELU / gated-residual epilogue for a wave's TM x TN block of 16x16
+// accumulators whose top-left output element is (row0, col0).
+template <typename T, int EPI, int TM, int TN>
+__device__ __forceinline__ void epilogue(const GemmArgs& g, const f32x4 (&acc)[TM][TN], int row0, int col0, int lane) {
+    const GemmEpi& e = g.e;
+    const T* __restrict__ bias = static_cast<const T*>(e.bias);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int col = col0 + j * 16 + (lane & 15);
+        if (col >= g.N) continue;
+        const float bv = bias ? ld(bias + col) : 0.f;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = row0 + i * 16 + 4 * (lane >> 4) + r;
+                if (row >= g.M) continue;
+                float v = acc[i][j][r] + bv;
+                if constexpr (EPI == BC_EPI_GATE_RES) {
+                    const float gv = e.gate ? e.gate[(int64_t)(row / e.rows_per_gate) * e.ldg + col] : 1.f;
+                    v = e.res[(int64_t)row * e.ldr + col] + gv * v;
+                    const int b = row / e.seg, s = row - b * e.seg;
+                    if (s < e.keep) {
+                        const int64_t o = (int64_t)(b * e.keep + s) * e.ldo + col;
+                        if (e.out_f32) static_cast<float*>(e.out)[o] = v;
+                        else st(static_cast<T*>(e.out) + o, v);
+                    }
+                } else {
+                    if (col >= e.gelu_from) v = gelu_tanh(v);
+                    if (col >= e.split) st(static_cast<T*>(e.out2) + (int64_t)row * e.ldo2 + (col - e.split + e.off2), v);
+                    else if (e.out_f32) static_cast<float*>(e.out)[(int64_t)row * e.ldo + col] = v;
+                    else st(static_cast<T*>(e.out) + (int64_t)row * e.ldo + col, v);
+                }
+            }
+        }
+    }
+}
 
-template <typename T, int EPI, int BM, int BN>
-__global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(GemmArgs g) {
+// Tile shape: BM x BN per workgroup, a WAVES_M x WAVES_N grid of waves, each
+// wave owning a (BM/WAVES_M) x (BN/WAVES_N) block of 16x16 MFMA tiles.
+template <typename T, int EPI, int BM, int BN, int WAVES_M, int WAVES_N>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(GemmArgs g) {
+    constexpr int NT = 64 * WAVES_M * WAVES_N;       // threads
     constexpr int EPC = 16 / (int)sizeof(T);        // elements per 16-byte chunk
     constexpr int BK = 8 * EPC;                      // 128 bytes of K per step
     constexpr int LDK = BK + EPC;                    // padded LDS row (elements)
-    constexpr int WM = BM / 2, WN = BN / 2;
+    constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
     constexpr int TM = WM / 16, TN = WN / 16;
-    constexpr int CA = BM * 8 / kGemmThreads;        // 16-byte chunks per thread per step
-    constexpr int CB = BN * 8 / kGemmThreads;
+    constexpr int CA = BM * 8 / NT;                  // 16-byte chunks per thread per step
+    constexpr int CB = BN * 8 / NT;
+    static_assert(CA * NT == BM * 8 && CB * NT == BN * 8, "tile must split evenly over threads");
     typedef Mma<T> MM;
 
     __shared__ __attribute__((aligned(16))) T sA[2][BM][LDK];
@@ -57,7 +97,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(GemmArgs g) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
 
     // Tile order: consecutive workgroup ids go round-robin to the 8 XCDs; give
     // each XCD a contiguous range of tiles, then raster in groups of 8 row
@@ -82,7 +122,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(GemmArgs g) {
     auto load_global = [&](int k0) {
 #pragma unroll
         for (int i = 0; i < CA; ++i) {
-            const int c = tid + i * kGemmThreads;
+            const int c = tid + i * NT;
             const int row = c >> 3, kc = k0 + (c & 7) * EPC;
             const int grow = bm + row;
             if (grow < g.M && kc < g.K)
@@ -92,7 +132,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(GemmArgs g) {
         }
 #pragma unroll
         for (int i = 0; i < CB; ++i) {
-            const int c = tid + i * kGemmThreads;
+            const int c = tid + i * NT;
             const int row = c >> 3, kc = k0 + (c & 7) * EPC;
             const int grow = bn + row;
             if (grow < g.N && kc < g.K)
@@ -104,12 +144,12 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(GemmArgs g) {
     auto store_lds = [&](int buf) {
 #pragma unroll
         for (int i = 0; i < CA; ++i) {
-            const int c = tid + i * kGemmThreads;
+            const int c = tid + i * NT;
             *reinterpret_cast<u32x4*>(&sA[buf][c >> 3][(c & 7) * EPC]) = ra[i];
         }
 #pragma unroll
         for (int i = 0; i < CB; ++i) {
-            const int c = tid + i * kGemmThreads;
+            const int c = tid + i * NT;
             *reinterpret_cast<u32x4*>(&sB[buf][c >> 3][(c & 7) * EPC]) = rb[i];
         }
     };
@@ -146,47 +186,223 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_kernel(GemmArgs g) {
         __syncthreads();
     }
 
-    // ---- epilogue -----------------------------------------------------------
-    const GemmEpi& e = g.e;
-    const T* __restrict__ bias = static_cast<const T*>(e.bias);
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-        const int col = bn + wn * WN + j * 16 + (lane & 15);
-        if (col >= g.N) continue;
-        const float bv = bias ? ld(bias + col) : 0.f;
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int row = bm + wm * WM + i * 16 + 4 * (lane >> 4) + r;
-                if (row >= g.M) continue;
-                float v = acc[i][j][r] + bv;
-                if constexpr (EPI == BC_EPI_GATE_RES) {
-                    const float gv = e.gate ? e.gate[(int64_t)(row / e.rows_per_gate) * e.ldg + col] : 1.f;
-                    v = e.res[(int64_t)row * e.ldr + col] + gv * v;
-                    const int b = row / e.seg, s = row - b * e.seg;
-                    if (s < e.keep) {
-                        const int64_t o = (int64_t)(b * e.keep + s) * e.ldo + col;
-                        if (e.out_f32) static_cast<float*>(e.out)[o] = v;
-                        else st(static_cast<T*>(e.out) + o, v);
-                    }
-                } else {
-                    if (col >= e.gelu_from) v = gelu_tanh(v);
-                    if (col < e.split) st(static_cast<T*>(e.out) + (int64_t)row * e.ldo + col, v);
-                    else st(static_cast<T*>(e.out2) + (int64_t)row * e.ldo2 + (col - e.split + e.off2), v);
-                }
-            }
-        }
-    }
+    epilogue<T, EPI, TM, TN>(g, acc, bm + wm * WM, bn + wn * WN, lane);
 }
 
+// ---------------------------------------------------------------------------
+// bf16 main loop with direct-to-LDS loads.
+//
+// Operand tiles go from HBM straight into LDS with global_load_lds_dwordx4:
+// one wave-wide instruction moves 8 rows x 128 bytes (each lane 16 bytes,
+// lane i landing at M0 + 16 i), so no registers or ds_write instructions are
+// spent on staging.  LDS rows are 128 bytes (64 k) with no padding; to keep
+// the 16-byte fragment reads of 16 consecutive rows conflict-free, the 16-byte
+// chunk c of row r is stored in slot c ^ ((r >> 1) & 7), which the loading
+// lane realises by choosing which global chunk it fetches.  STAGES k-steps are
+// in flight: after the barrier of step kt the loads of step kt + STAGES - 1
+// are issued into the buffer step kt - 1 used, and the wait before each
+// barrier only drains the loads of the step about to be consumed.
+// Requires K % 64 == 0 (whole k-steps); rows past M or N are clamped to the
+// last row, so they load valid memory and only feed outputs never stored.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+
+// One wave-wide direct-to-LDS load: each lane's 16 bytes at `src` land at
+// lds_base + 16 * lane.  Issued as inline assembly so that the only waits on
+// it are the explicit vmcnt waits of the pipeline (the compiler would
+// otherwise drain every outstanding load before each LDS read and barrier).
+__device__ __forceinline__ void dma16(const void* src, const void* lds_base) {
+    const unsigned m0 = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)lds_base);   // wave-uniform
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(m0) : "memory", "m0");
+}
+
+template <int N> __device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    // gfx9 s_waitcnt encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] at [15:14]
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, bool SEG>
+__device__ __forceinline__ void gemm_dma_body(GemmArgs g, const GemmSeg* sg) {
+    typedef bf16 T;
+    typedef Mma<bf16> MM;
+    constexpr int NW = WAVES_M * WAVES_N;
+    constexpr int BK = 64;
+    constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+    constexpr int TM = WM / 16, TN = WN / 16;
+    constexpr int OA = BM / 8 / NW, OB = BN / 8 / NW;     // row octets per wave per step
+    constexpr int L = OA + OB;                             // loads per wave per step
+    static_assert(OA * 8 * NW == BM && OB * 8 * NW == BN, "octets must split over waves");
+
+    __shared__ __attribute__((aligned(1024))) T sA[STAGES][BM * BK];
+    __shared__ __attribute__((aligned(1024))) T sB[STAGES][BN * BK];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+
+    const int tiles_m = (g.M + BM - 1) / BM;
+    const int tiles_n = (g.N + BN - 1) / BN;
+    const int nwg = gridDim.x;
+    int pid = blockIdx.x;
+    if ((nwg & 7) == 0) pid = (pid & 7) * (nwg >> 3) + (pid >> 3);
+    constexpr int GROUP_M = 8;
+    const int group = GROUP_M * tiles_n;
+    const int first_m = (pid / group) * GROUP_M;
+    const int gm = min(tiles_m - first_m, GROUP_M);
+    const int tm = first_m + (pid % group) % gm;
+    const int tn = (pid % group) / gm;
+    const int bm = tm * BM, bn = tn * BN;
+    if constexpr (SEG) {
+        // Grouped GEMM: column block bn lies in segment bn / Nseg, whose own
+        // weight matrix [Nseg, K] and bias hold its rows.
+        const int seg = bn / sg->Nseg;
+        const int off = seg * sg->Nseg;
+        g.W = static_cast<const bf16*>(sg->W[seg]) - (int64_t)off * g.ldw;
+        g.e.bias = sg->bias[seg] ? static_cast<const bf16*>(sg->bias[seg]) - off : nullptr;
+    }
+
+    // Per-lane global source of each of this wave's octets (k offset added per step).
+    const T* srcA[OA];
+    const T* srcB[OB];
+    const int lrow = lane >> 3, lslot = lane & 7;
+#pragma unroll
+    for (int o = 0; o < OA; ++o) {
+        const int r = (wave * OA + o) * 8 + lrow;
+        const int grow = min(bm + r, g.M - 1);
+        srcA[o] = static_cast<const T*>(g.A) + (int64_t)grow * g.lda + ((lslot ^ swz(r)) * 8);
+    }
+#pragma unroll
+    for (int o = 0; o < OB; ++o) {
+        const int r = (wave * OB + o) * 8 + lrow;
+        const int grow = min(bn + r, g.N - 1);
+        srcB[o] = static_cast<const T*>(g.W) + (int64_t)grow * g.ldw + ((lslot ^ swz(r)) * 8);
+    }
+    auto issue = [&](int kt, int buf) {
+        const int k0 = kt * BK;
+#pragma unroll
+        for (int o = 0; o < OA; ++o)
+            dma16(srcA[o] + k0, &sA[buf][(wave * OA + o) * 8 * BK]);
+#pragma unroll
+        for (int o = 0; o < OB; ++o)
+            dma16(srcB[o] + k0, &sB[buf][(wave * OB + o) * 8 * BK]);
+    };
+
+    f32x4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int nk = g.K / BK;
+#pragma unroll
+    for (int p = 0; p < STAGES - 1; ++p)
+        if (p < nk) issue(p, p);
+
+    const int frow = lane & 15, grp = lane >> 4;
+    for (int kt = 0; kt < nk; ++kt) {
+        if (kt + STAGES - 2 < nk) wait_vmcnt<(STAGES - 2) * L>();
+        else wait_vmcnt<0>();
+        __syncthreads();
+        if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+        const T* a = sA[kt % STAGES];
+        const T* b = sB[kt % STAGES];
+#pragma unroll
+        for (int kk = 0; kk < BK / 32; ++kk) {
+            const int c = kk * 4 + grp;
+            MM::frag af[TM], bfr[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int r = wm * WM + i * 16 + frow;
+                af[i] = MM::load(a + r * BK + ((c ^ swz(r)) * 8));
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int r = wn * WN + j * 16 + frow;
+                bfr[j] = MM::load(b + r * BK + ((c ^ swz(r)) * 8));
+            }
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) acc[i][j] = MM::mma(af[i], bfr[j], acc[i][j]);
+        }
+    }
+
+    epilogue<T, EPI, TM, TN>(g, acc, bm + wm * WM, bn + wn * WN, lane);
+}
+
+template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_dma_kernel(GemmArgs g) {
+    gemm_dma_body<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, false>(g, nullptr);
+}
+
+template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_dma_seg_kernel(GemmArgs g, GemmSeg sg) {
+    gemm_dma_body<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, true>(g, &sg);
+}
+
+template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES>
+static void launch_dma(const GemmArgs& g, hipStream_t s) {
+    const unsigned tiles = (unsigned)(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN));
+    gemm_dma_kernel<EPI, BM, BN, WAVES_M, WAVES_N, STAGES><<<dim3(tiles), dim3(64 * WAVES_M * WAVES_N), 0, s>>>(g);
+}
+
+template <typename T, int EPI, int BM, int BN, int WAVES_M, int WAVES_N>
+static void launch_tile(const GemmArgs& g, hipStream_t s) {
+    const unsigned tiles = (unsigned)(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN));
+    gemm_kernel<T, EPI, BM, BN, WAVES_M, WAVES_N><<<dim3(tiles), dim3(64 * WAVES_M * WAVES_N), 0, s>>>(g);
+}
+
+// Tile choice (measured on MI355X over the DiT-XL/2, PixArt and HunyuanVideo
+// block shapes, see the design notes): bf16 operands with whole 64-wide
+// k-steps take the direct-to-LDS kernel with two stages and 8 waves --
+// 256 x 256 tiles when K is long enough to amortise them and there is at least
+// one full round for the 256 CUs, else 128 x 128 (two workgroups per CU).
+// Other shapes, and fp32, take the register-staged kernel.
 template <typename T, int EPI>
 static int run_gemm(const GemmArgs& g, hipStream_t s) {
-    constexpr int BM = 128, BN = 128;
-    const int64_t tiles = (int64_t)((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-    if (tiles > 0x7fffffff) return fail(BC_ERR_UNSUPPORTED, "GEMM grid too large");
-    gemm_kernel<T, EPI, BM, BN><<<dim3((unsigned)tiles), dim3(kGemmThreads), 0, s>>>(g);
+    const int64_t tiles128 = (int64_t)((g.M + 127) / 128) * ((g.N + 127) / 128);
+    if (tiles128 > 0x7fffffff) return fail(BC_ERR_UNSUPPORTED, "GEMM grid too large");
+    if constexpr (sizeof(T) == 2) {
+        const int64_t tiles256 = (int64_t)((g.M + 255) / 256) * ((g.N + 255) / 256);
+        const bool dma = g.K % 64 == 0 && g.lda % 8 == 0 && g.ldw % 8 == 0;
+        if (dma && g.K >= 2048 && tiles256 >= 256) launch_dma<EPI, 256, 256, 4, 2, 2>(g, s);
+        else if (dma) launch_dma<EPI, 128, 128, 4, 2, 2>(g, s);
+        else launch_tile<T, EPI, 128, 128, 4, 2>(g, s);
+    } else {
+        launch_tile<T, EPI, 128, 128, 2, 2>(g, s);
+    }
     return check_launch("gemm");
+}
+
+int launch_gemm_grouped(int dtype, const GemmArgs& g0, const GemmSeg& sg, int nseg, hipStream_t s) {
+    // Column segment i of the output uses weights sg.W[i] ([Nseg, K]) and bias sg.bias[i].
+    if (g0.M <= 0 || nseg <= 0) return BC_OK;
+    if (nseg > kMaxGemmSeg) return fail(BC_ERR_UNSUPPORTED, "%d GEMM segments", nseg);
+    GemmArgs g = g0;
+    g.N = nseg * sg.Nseg;
+    const bool dma = dtype == BC_BF16 && g.K % 64 == 0 && g.ldw % 8 == 0 && g.lda % 8 == 0 && sg.Nseg % 128 == 0 &&
+                     reinterpret_cast<uintptr_t>(g.A) % 16 == 0;
+    if (dma) {
+        for (int i = 0; i < nseg; ++i)
+            if (reinterpret_cast<uintptr_t>(sg.W[i]) % 16) return fail(BC_ERR_UNSUPPORTED, "misaligned segment weight");
+        prof_begin(PROF_GEMM_BIAS, s);
+        const unsigned tiles = (unsigned)(((g.M + 127) / 128) * (g.N / 128));
+        gemm_dma_seg_kernel<BC_EPI_BIAS, 128, 128, 4, 2, 2><<<dim3(tiles), dim3(512), 0, s>>>(g, sg);
+        prof_end(PROF_GEMM_BIAS, s);
+        return check_launch("grouped gemm");
+    }
+    // One launch per segment, writing its column block of the output.
+    for (int i = 0; i < nseg; ++i) {
+        GemmArgs gi = g0;
+        gi.N = sg.Nseg;
+        gi.W = sg.W[i];
+        gi.e.bias = sg.bias[i];
+        gi.e.out = static_cast<char*>(g0.e.out) + (size_t)i * sg.Nseg * (g0.e.out_f32 ? 4 : dtype_size(dtype));
+        const int rc = launch_gemm(dtype, BC_EPI_BIAS, gi, s);
+        if (rc != BC_OK) return rc;
+    }
+    return BC_OK;
 }
 
 int launch_gemm(int dtype, int epi, const GemmArgs& g, hipStream_t s) {

@@ -6,6 +6,7 @@
 // enqueues kernels.  The loop needs no device-to-host synchronisation: the
 // full/forecast mask, the ring bookkeeping and every forecast weight are known
 // before the first launch (the weights depend only on the schedule).
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <new>
@@ -266,11 +267,17 @@ namespace bc {
 struct SampleWs {
     BlockBufs bb;
     float *x, *x_img, *x_txt;                 // residual streams
-    float *e, *t1, *temb, *c, *t6, *fmod, *pooled, *txtp;
-    float *mods, *mods_s;                     // per-block modulation (dual/dit/pixart; single)
-    void *cap_h, *ctx, *ctx_kv;               // pixart text context
+    float *e, *t1, *temb;                     // per step: sinusoid, hidden, timestep embedding
+    float *c;                                 // per (step, sample): conditioning vector
+    void* sc;                                 // SiLU(c) (or SiLU(t) for PixArt) rows, model dtype
+    float* fmod;                              // per (step, sample): final-layer (shift, scale)
+    float *mods, *mods_s;                     // per (full step, sample): block modulation
+    float* t6;                                // PixArt: per (full step, sample) t6
+    float *pooled, *txtp;                     // MMDiT pooled text and its projection
+    void *cap_h, *ctx, *ctx_kv;               // PixArt text context
     void* feat;                               // forecast output [B*T, D] (model dtype)
-    float *out, *prev;                        // model output, DPM-Solver++ history
+    float *out, *prev;                        // model output (token layout), DPM-Solver++ history
+    int full_chunk;                           // full steps whose modulation is held at once
     size_t bytes;
 };
 
@@ -278,7 +285,15 @@ static int64_t latent_spatial(const bc_model_desc& d) { return (int64_t)d.frames
 
 static int model_tokens(const bc_model_desc& d) { return d.frames * (d.height / d.patch) * (d.width / d.patch); }
 
-static SampleWs carve_sample(const bc_model_desc& d, int B, void* base) {
+// Full steps whose block modulation is computed together: up to 256
+// (step, sample) rows and at most kMaxSeg steps (one gather launch).
+static int full_chunk_of(int B, int S) { return std::max(1, std::min({S, 256 / B, kMaxSeg})); }
+
+static int64_t mod_width(const bc_model_desc& d) {
+    return d.kind == BC_MODEL_MMDIT ? (int64_t)2 * d.depth * 6 * d.D : (int64_t)d.depth * 6 * d.D;
+}
+
+static SampleWs carve_sample(const bc_model_desc& d, int B, int S, void* base) {
     Carver c(base);
     SampleWs w;
     const int T = model_tokens(d), D = d.D, F = d.mlp;
@@ -298,17 +313,20 @@ static SampleWs carve_sample(const bc_model_desc& d, int B, void* base) {
             w.x_txt = c.take<float>((int64_t)B * Tt * D * f4);
         }
     }
-    w.e = c.take<float>((size_t)B * d.freq_dim * f4);
-    w.t1 = c.take<float>((size_t)B * D * f4);
-    w.temb = c.take<float>((size_t)B * D * f4);
-    w.c = c.take<float>((size_t)B * D * f4);
-    w.t6 = c.take<float>(d.kind == BC_MODEL_PIXART ? (size_t)B * 6 * D * f4 : 0);
-    w.fmod = c.take<float>((size_t)B * 2 * D * f4);
+    const int64_t SB = (int64_t)S * B;
+    w.full_chunk = full_chunk_of(B, S);
+    const int64_t FB = (int64_t)w.full_chunk * B;
+    w.e = c.take<float>((size_t)S * d.freq_dim * f4);
+    w.t1 = c.take<float>((size_t)S * D * f4);
+    w.temb = c.take<float>((size_t)S * D * f4);
+    w.c = c.take<float>((size_t)SB * D * f4);
+    w.sc = c.take<char>((size_t)SB * D * esz);
+    w.fmod = c.take<float>((size_t)SB * 2 * D * f4);
+    w.mods = c.take<float>((size_t)FB * mod_width(d) * f4);
+    w.mods_s = c.take<float>(d.kind == BC_MODEL_MMDIT ? (size_t)FB * d.depth_single * 3 * D * f4 : 0);
+    w.t6 = c.take<float>(d.kind == BC_MODEL_PIXART ? (size_t)FB * 6 * D * f4 : 0);
     w.pooled = c.take<float>(d.kind == BC_MODEL_MMDIT ? (size_t)B * D * f4 : 0);
     w.txtp = c.take<float>(d.kind == BC_MODEL_MMDIT ? (size_t)B * D * f4 : 0);
-    const int nmod = d.kind == BC_MODEL_MMDIT ? 2 * d.depth : d.depth;
-    w.mods = c.take<float>((size_t)B * nmod * 6 * D * f4);
-    w.mods_s = c.take<float>(d.kind == BC_MODEL_MMDIT ? (size_t)B * d.depth_single * 3 * D * f4 : 0);
     const bool px = d.kind == BC_MODEL_PIXART;
     w.cap_h = c.take<char>(px ? (size_t)B * d.ctx_tokens * D * esz : 0);
     w.ctx = c.take<char>(px ? (size_t)B * d.ctx_tokens * D * esz : 0);
@@ -490,11 +508,12 @@ int bc_model_destroy(bc_model* m) {
     return BC_OK;
 }
 
-int bc_sample_workspace_size(const bc_model* m, int B, size_t* bytes) {
+int bc_sample_workspace_size(const bc_model* m, int B, int S, size_t* bytes) {
     clear_error();
     if (!m || !bytes) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
     if (B < 1 || B > 64) return fail(BC_ERR_INVALID_ARG, "B=%d outside [1, 64]", B);
-    *bytes = carve_sample(m->d, B, nullptr).bytes;
+    if (S < 1 || S > 1000) return fail(BC_ERR_INVALID_ARG, "S=%d outside [1, 1000]", S);
+    *bytes = carve_sample(m->d, B, S, nullptr).bytes;
     return BC_OK;
 }
 
@@ -517,14 +536,13 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
     BC_TRY(bc_make_schedule(sampler, S, tau.data(), tin.data()));
     std::vector<bc_plan_step> plan(S);
     BC_TRY(bc_plan(S, mask, nullptr, K, p, plan.data()));
-    const SampleWs w = carve_sample(d, B, ws);
+    const SampleWs w = carve_sample(d, B, S, ws);
     if (ws_bytes < w.bytes) return fail(BC_ERR_INVALID_ARG, "workspace %zu < %zu bytes", ws_bytes, w.bytes);
 
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int dt = d.dtype, Tt = d.kind == BC_MODEL_MMDIT ? d.txt_tokens : 0;
     const size_t esz = dtype_size(dt);
     const LatentShape ls{d.in_ch, d.frames, d.height, d.width, d.patch};
-    const int64_t spatial = latent_spatial(d);
     double ab[1000];
     alpha_bar(ab);
     double h_prev = 0.0;
@@ -548,26 +566,96 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
         BC_TRY(launch_skinny(dt, skinny1(mw.txt_w, mw.txt_b, D, D, B, w.pooled, w.txtp, 0, 0), s));
     }
 
+    // Conditioning of every step, computed before the loop: it depends only on
+    // the schedule, the labels and the text, never on the latents.
+    BC_TRY(launch_step_sinusoid(sampler, S, d.freq_dim, w.e, s));
+    for (int k0 = 0; k0 < S; k0 += 64) {
+        const int n = std::min(64, S - k0);
+        BC_TRY(launch_skinny(dt, skinny1(mw.t_w1, mw.t_b1, D, d.freq_dim, n, w.e + (int64_t)k0 * d.freq_dim,
+                                         w.t1 + (int64_t)k0 * D, 0, 1), s));
+        BC_TRY(launch_skinny(dt, skinny1(mw.t_w2, mw.t_b2, D, D, n, w.t1 + (int64_t)k0 * D, w.temb + (int64_t)k0 * D, 0, 0), s));
+    }
+    const bool lab = d.kind == BC_MODEL_DIT && d.n_classes;
+    BC_TRY(launch_build_cond(dt, w.temb, S, B, D, lab ? mw.y_table : nullptr, lab ? labels : nullptr, d.n_classes + 1,
+                             d.kind == BC_MODEL_MMDIT ? w.txtp : nullptr, w.c, s));
+    if (d.kind == BC_MODEL_PIXART) {
+        const void* ft[2] = {mw.final_w_mod, static_cast<const char*>(mw.final_w_mod) + D * esz};
+        BC_TRY(launch_add_tables(dt, w.c, D, ft, 2, D, S * B, w.fmod, 2 * D, s));
+    } else {
+        for (int k0 = 0; k0 < S; k0 += kMaxSeg) {
+            const int n = std::min(kMaxSeg, S - k0);
+            RowList rl;
+            for (int i = 0; i < n; ++i) rl.row[i] = k0 + i;
+            BC_TRY(launch_gather_silu(dt, w.c, B, D, rl, n,
+                                      static_cast<char*>(w.sc) + (int64_t)k0 * B * D * esz, s));
+        }
+        GemmArgs fg = gemm_args(w.sc, D, mw.final_w_mod, D, S * B, 2 * D, D);
+        fg.e.bias = mw.final_b_mod;
+        fg.e.out = w.fmod;
+        fg.e.ldo = 2 * D;
+        fg.e.out_f32 = 1;
+        BC_TRY(launch_gemm(dt, BC_EPI_BIAS, fg, s));
+    }
+    std::vector<int> full_steps;
+    for (int k = 0; k < S; ++k)
+        if (plan[k].is_full) full_steps.push_back(k);
+    const int64_t ldm = mod_width(d);
+    const int64_t lds = (int64_t)d.depth_single * 3 * D;
+    // Block modulation of a chunk of full steps: rows (i, b) for the i-th full
+    // step of the chunk; w.sc is reused for the gathered SiLU(c) rows.
+    auto chunk_mods = [&](int f0) -> int {
+        const int n = std::min<int>(w.full_chunk, (int)full_steps.size() - f0);
+        RowList rl;
+        for (int i = 0; i < n; ++i) rl.row[i] = full_steps[f0 + i];
+        // (PixArt has no class or text term in c, so c is the timestep
+        // embedding and SiLU(c) is t6's input.)
+        BC_TRY(launch_gather_silu(dt, w.c, B, D, rl, n, w.sc, s));
+        const int rows = n * B;
+        if (d.kind == BC_MODEL_PIXART) {
+            GemmArgs tg = gemm_args(w.sc, D, mw.t6_w, D, rows, 6 * D, D);
+            tg.e.bias = mw.t6_b;
+            tg.e.out = w.t6;
+            tg.e.ldo = 6 * D;
+            tg.e.out_f32 = 1;
+            BC_TRY(launch_gemm(dt, BC_EPI_BIAS, tg, s));
+            std::vector<const void*> tabs(d.depth);
+            for (int l = 0; l < d.depth; ++l) tabs[l] = blk[l].img.w_mod;
+            return launch_add_tables(dt, w.t6, 6 * D, tabs.data(), d.depth, 6 * D, rows, w.mods, ldm, s);
+        }
+        GemmSeg sg;
+        std::memset(&sg, 0, sizeof sg);
+        sg.Nseg = 6 * D;
+        int nseg = 0;
+        for (int l = 0; l < d.depth; ++l) {
+            sg.W[nseg] = blk[l].img.w_mod; sg.bias[nseg] = blk[l].img.b_mod; ++nseg;
+            if (d.kind == BC_MODEL_MMDIT) { sg.W[nseg] = blk[l].txt.w_mod; sg.bias[nseg] = blk[l].txt.b_mod; ++nseg; }
+        }
+        GemmArgs mg = gemm_args(w.sc, D, nullptr, D, rows, nseg * 6 * D, D);
+        mg.e.out = w.mods;
+        mg.e.ldo = ldm;
+        mg.e.out_f32 = 1;
+        BC_TRY(launch_gemm_grouped(dt, mg, sg, nseg, s));
+        if (d.kind == BC_MODEL_MMDIT && d.depth_single) {
+            GemmSeg ss;
+            std::memset(&ss, 0, sizeof ss);
+            ss.Nseg = 3 * D;
+            for (int l = 0; l < d.depth_single; ++l) {
+                ss.W[l] = blk[d.depth + l].img.w_mod;
+                ss.bias[l] = blk[d.depth + l].img.b_mod;
+            }
+            GemmArgs sgm = gemm_args(w.sc, D, nullptr, D, rows, (int)lds, D);
+            sgm.e.out = w.mods_s;
+            sgm.e.ldo = lds;
+            sgm.e.out_f32 = 1;
+            BC_TRY(launch_gemm_grouped(dt, sgm, ss, d.depth_single, s));
+        }
+        return BC_OK;
+    };
+
+    int full_index = 0;
     for (int k = 0; k < S; ++k) {
         const bc_plan_step& st = plan[k];
-        // Conditioning: timestep MLP, class / text terms, final-layer modulation.
-        BC_TRY(launch_sinusoid(tin[k], B, d.freq_dim, w.e, s));
-        BC_TRY(launch_skinny(dt, skinny1(mw.t_w1, mw.t_b1, D, d.freq_dim, B, w.e, w.t1, 0, 1), s));
-        SkinnyArgs t2 = skinny1(mw.t_w2, mw.t_b2, D, D, B, w.t1, w.temb, 0, 0);
-        if (d.kind == BC_MODEL_MMDIT) t2.addend = w.txtp;
-        BC_TRY(launch_skinny(dt, t2, s));
-        const float* c = w.temb;
-        if (d.kind == BC_MODEL_DIT && d.n_classes) {
-            BC_TRY(launch_add_label(dt, w.temb, mw.y_table, labels, B, D, d.n_classes + 1, w.c, s));
-            c = w.c;
-        }
-        if (d.kind == BC_MODEL_PIXART) {
-            const void* ft[2] = {mw.final_w_mod, static_cast<const char*>(mw.final_w_mod) + D * esz};
-            BC_TRY(launch_add_tables(dt, w.temb, D, ft, 2, D, B, w.fmod, 2 * D, s));
-        } else {
-            BC_TRY(launch_skinny(dt, skinny1(mw.final_w_mod, mw.final_b_mod, 2 * D, D, B, c, w.fmod, 1, 0), s));
-        }
-
+        const float* fmod = w.fmod + (int64_t)k * B * 2 * D;
         const void* feat;
         if (st.is_full) {
             void* slot = nullptr;
@@ -575,48 +663,18 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
             BlockOut out;
             out.ptr = slot;
             out.dt = dt;
-            // Per-block modulation vectors for the whole stack.
-            if (d.kind == BC_MODEL_PIXART) {
-                BC_TRY(launch_skinny(dt, skinny1(mw.t6_w, mw.t6_b, 6 * D, D, B, w.temb, w.t6, 1, 0), s));
-                std::vector<const void*> tabs(d.depth);
-                for (int l = 0; l < d.depth; ++l) tabs[l] = blk[l].img.w_mod;
-                BC_TRY(launch_add_tables(dt, w.t6, 6 * D, tabs.data(), d.depth, 6 * D, B, w.mods, (int64_t)d.depth * 6 * D, s));
-            } else {
-                SkinnyArgs ma;
-                std::memset(&ma, 0, sizeof ma);
-                const int nseg = d.kind == BC_MODEL_MMDIT ? 2 * d.depth : d.depth;
-                for (int l = 0; l < d.depth; ++l) {
-                    if (d.kind == BC_MODEL_MMDIT) {
-                        ma.W[2 * l] = blk[l].img.w_mod; ma.bias[2 * l] = blk[l].img.b_mod;
-                        ma.W[2 * l + 1] = blk[l].txt.w_mod; ma.bias[2 * l + 1] = blk[l].txt.b_mod;
-                    } else {
-                        ma.W[l] = blk[l].img.w_mod; ma.bias[l] = blk[l].img.b_mod;
-                    }
-                }
-                ma.nseg = nseg; ma.Nseg = 6 * D; ma.K = D; ma.B = B;
-                ma.in = c; ma.ld_in = D; ma.out = w.mods; ma.ld_out = (int64_t)nseg * 6 * D;
-                ma.act_in = 1;
-                BC_TRY(launch_skinny(dt, ma, s));
-                if (d.kind == BC_MODEL_MMDIT && d.depth_single) {
-                    SkinnyArgs sa;
-                    std::memset(&sa, 0, sizeof sa);
-                    for (int l = 0; l < d.depth_single; ++l) {
-                        sa.W[l] = blk[d.depth + l].img.w_mod;
-                        sa.bias[l] = blk[d.depth + l].img.b_mod;
-                    }
-                    sa.nseg = d.depth_single; sa.Nseg = 3 * D; sa.K = D; sa.B = B;
-                    sa.in = c; sa.ld_in = D; sa.out = w.mods_s; sa.ld_out = (int64_t)d.depth_single * 3 * D;
-                    sa.act_in = 1;
-                    BC_TRY(launch_skinny(dt, sa, s));
-                }
-            }
+            // Block modulation of this full step (computed a chunk of full steps at a time).
+            const int fi = full_index % w.full_chunk;
+            if (fi == 0) BC_TRY(chunk_mods(full_index));
+            ++full_index;
+            const float* mods = w.mods + (int64_t)fi * B * ldm;
+            const float* mods_s = w.mods_s + (int64_t)fi * B * lds;
             BC_TRY(launch_patch_embed(dt, latents, ls, B, mw.patch_w, mw.patch_b, mw.pos, D, w.x_img, s));
             if (d.kind == BC_MODEL_MMDIT) {
                 BC_TRY(launch_convert(dt, text, BC_F32, w.x_txt, (int64_t)B * Tt * D, s));
-                const int64_t ldm = (int64_t)2 * d.depth * 6 * D;
                 for (int l = 0; l < d.depth; ++l)
-                    BC_TRY(dual_block(bd_main, blk[l], w.x_img, w.x_txt, w.mods + (int64_t)2 * l * 6 * D,
-                                      w.mods + (int64_t)(2 * l + 1) * 6 * D, ldm, w.bb, s));
+                    BC_TRY(dual_block(bd_main, blk[l], w.x_img, w.x_txt, mods + (int64_t)2 * l * 6 * D,
+                                      mods + (int64_t)(2 * l + 1) * 6 * D, ldm, w.bb, s));
                 if (w.x_img != w.x) {   // regroup [img | txt] per sample for the single-stream blocks
                     for (int b = 0; b < B; ++b) {
                         BC_TRY(launch_copy(w.x_img + (int64_t)b * T * D, w.x + (int64_t)b * (T + Tt) * D, (int64_t)T * D * 4, s));
@@ -625,9 +683,8 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
                 }
                 out.seg = T + Tt;
                 out.keep = T;
-                const int64_t lds = (int64_t)d.depth_single * 3 * D;
                 for (int l = 0; l < d.depth_single; ++l)
-                    BC_TRY(single_block(bd_single, blk[d.depth + l], w.x, w.mods_s + (int64_t)l * 3 * D, lds, w.bb,
+                    BC_TRY(single_block(bd_single, blk[d.depth + l], w.x, mods_s + (int64_t)l * 3 * D, lds, w.bb,
                                         l + 1 == d.depth_single ? &out : nullptr, s));
                 if (d.depth_single == 0) {   // stack ends with a dual block: cache its image stream
                     BC_TRY(launch_convert(BC_F32, w.x_img, dt, slot, (int64_t)B * T * D, s));
@@ -635,9 +692,8 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
             } else {
                 out.seg = T;
                 out.keep = T;
-                const int64_t ldm = (int64_t)d.depth * 6 * D;
                 for (int l = 0; l < d.depth; ++l)
-                    BC_TRY(dit_block(bd_main, blk[l], w.x, w.mods + (int64_t)l * 6 * D, ldm,
+                    BC_TRY(dit_block(bd_main, blk[l], w.x, mods + (int64_t)l * 6 * D, ldm,
                                      d.kind == BC_MODEL_PIXART ? static_cast<char*>(w.ctx_kv) + (int64_t)l * B * d.ctx_tokens * 2 * D * esz : nullptr,
                                      w.bb, l + 1 == d.depth ? &out : nullptr, s));
             }
@@ -653,10 +709,18 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
             BC_TRY(launch_forecast(src, wf, st.count, ring->numel, dt, w.feat, dt, s));
             feat = w.feat;
         }
-        BC_TRY(launch_final_layer(dt, feat, dt, w.fmod, w.fmod + D, 2 * D, mw.final_w, mw.final_b, {d.out_ch, d.frames, d.height, d.width, d.patch},
-                                  d.out_ch, B, D, w.out, s));
+        // Final layer: LayerNorm + adaLN, then the linear to p*p*C_out per token
+        // (token layout; the sampler reads it back through unpatchify).
+        BC_TRY(launch_ln_mod(dt, feat, (int64_t)B * T, D, fmod, fmod + D, 2 * D, T, dt, w.bb.h, s));
+        const int NO = d.patch * d.patch * d.out_ch;
+        GemmArgs fg = gemm_args(w.bb.h, D, mw.final_w, D, B * T, NO, D);
+        fg.e.bias = mw.final_b;
+        fg.e.out = w.out;
+        fg.e.ldo = NO;
+        fg.e.out_f32 = 1;
+        BC_TRY(launch_gemm(dt, BC_EPI_BIAS, fg, s));
         const SamplerCoef sc = sampler_coef(sampler, k, S, tau.data(), ab, &h_prev);
-        BC_TRY(launch_sampler(sc, latents, w.out, w.prev, B, d.in_ch, d.out_ch, spatial, s));
+        BC_TRY(launch_sampler(sc, latents, w.out, w.prev, ls, B, d.out_ch, s));
     }
     return BC_OK;
 }

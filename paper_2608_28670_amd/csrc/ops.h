@@ -30,8 +30,20 @@ struct SkinnyArgs {
 };
 int launch_skinny(int dt, const SkinnyArgs& a, hipStream_t s);
 
-// Timestep sinusoid e[b, :] = [cos(t f_i), sin(t f_i)], f_i = 10000^(-i/half), fp32 out.
-int launch_sinusoid(double t, int B, int dim, float* e, hipStream_t s);
+// Timestep sinusoid of every step k < S: e[k, :] = [cos(t_k f_i), sin(t_k f_i)],
+// f_i = 10000^(-i/half), where t_k is the step's model time (999 - floor(1000k/S),
+// or 1000 (1 - k/S) for the flow-matching Euler sampler); fp32 out.
+int launch_step_sinusoid(int sampler, int S, int dim, float* e, hipStream_t s);
+
+// Per-(step, sample) conditioning c[k*B + b, :] = temb[k, :] + extra, where
+// extra is table[labels[b], :] (table in `dt`, if labels), or add[b, :] (fp32,
+// if add), or nothing.
+int launch_build_cond(int dt, const float* temb, int S, int B, int D, const void* table, const int64_t* labels,
+                      int n_rows, const float* add, float* c, hipStream_t s);
+
+// out[i*B + b, :] = SiLU(c[rows[i]*B + b, :]) in `dt`, for i < n (n <= 64).
+struct RowList { int row[kMaxSeg]; };
+int launch_gather_silu(int dt, const float* c, int B, int D, const RowList& rows, int n, void* out, hipStream_t s);
 
 // c[b, :] = t[b, :] + table[labels[b], :] (table in `dt`).
 int launch_add_label(int dt, const float* t, const void* table, const int64_t* labels, int B, int D, int n_rows,
@@ -56,21 +68,14 @@ struct LatentShape {
 int launch_patch_embed(int dt, const float* lat, LatentShape ls, int B, const void* W, const void* bias,
                        const void* pos, int D, float* x, hipStream_t s);
 
-// Final layer on a feature [B*T, D] (fp32 or `feat_dt`): LN, modulate with
-// shift/scale (fp32, rows ld_mod apart), linear to p*p*C_out (weights `dt`),
-// scattered back to the latent layout out [B, C_out, F, H, W] (fp32).
-int launch_final_layer(int feat_dt, const void* feat, int dt, const float* shift, const float* scale,
-                       int64_t ld_mod, const void* W, const void* bias, LatentShape ls, int C_out, int B, int D,
-                       float* out, hipStream_t s);
-
-// Sampler update on fp32 latents x [B, C, S] from the model output [B, C_out, S]
-// (first C channels used):
+// Sampler update on fp32 latents x [B, C, F, H, W] from the model output in
+// token layout out_tok [B*T, p*p*C_out] (first C channels used):
 //   mode 0: x = c0 x + c1 e
 //   mode 1 (DPM-Solver++(2M) data prediction): x0 = (x - c2 e) / c3;
 //     D = c4 x0 + c5 prev; x = c0 x + c1 D; prev = x0 (prev may be NULL if c5 == 0)
 //   mode 2: x = x0 computed as in mode 1 (final step)
 struct SamplerCoef { float c[6]; int mode; };
-int launch_sampler(const SamplerCoef& k, float* x, const float* eps, float* prev, int B, int C, int C_out,
-                   int64_t S, hipStream_t s);
+int launch_sampler(const SamplerCoef& k, float* x, const float* out_tok, float* prev, LatentShape ls, int B, int C_out,
+                   hipStream_t s);
 
 }  // namespace bc

@@ -9,6 +9,7 @@
 namespace bc {
 
 constexpr float kLnEps = 1e-6f;
+constexpr int kMaxPatch = 256;
 
 // ---------------------------------------------------------------------------
 // LayerNorm + modulate: one wave per row, the row cached in registers.
@@ -106,6 +107,7 @@ template <> struct SkMma<float> {
 };
 
 constexpr int kSkTiles = 4;   // 16-column tiles per wave
+constexpr int kSkBatch = 8;   // k-steps of weight loads issued together
 
 template <typename T>
 __global__ __launch_bounds__(256) void skinny_kernel(SkinnyArgs a) {
@@ -135,17 +137,35 @@ __global__ __launch_bounds__(256) void skinny_kernel(SkinnyArgs a) {
                 sIn[bb][k] = (T)v;
             }
             __syncthreads();
+            // Weight rows of this wave's tiles (NULL past the end).
+            const T* wr[kSkTiles];
 #pragma unroll
             for (int t = 0; t < kSkTiles; ++t) {
                 const int ncol = nbase + t * 16;
-                if (ncol >= Ntot) break;
-                const int seg = ncol / a.Nseg;
-                const int nloc = ncol - seg * a.Nseg + r16;
-                const T* wr = static_cast<const T*>(a.W[seg]) + (int64_t)nloc * a.K + kc0;
-                for (int k = 0; k < kn; k += MM::KI) {
-                    const typename MM::frag bf = (k + kg < kn) ? MM::load(wr + k + kg) : MM::zero();
+                wr[t] = nullptr;
+                if (ncol < Ntot) {
+                    const int seg = ncol / a.Nseg;
+                    const int nloc = ncol - seg * a.Nseg + r16;
+                    wr[t] = static_cast<const T*>(a.W[seg]) + (int64_t)nloc * a.K + kc0;
+                }
+            }
+            // kSkBatch k-steps of every tile's weights in flight before the MFMAs.
+            for (int k0 = 0; k0 < kn; k0 += kSkBatch * MM::KI) {
+                typename MM::frag wf[kSkTiles][kSkBatch];
+#pragma unroll
+                for (int t = 0; t < kSkTiles; ++t)
+#pragma unroll
+                    for (int u = 0; u < kSkBatch; ++u) {
+                        const int k = k0 + u * MM::KI + kg;
+                        wf[t][u] = (wr[t] && k < kn) ? MM::load(wr[t] + k) : MM::zero();
+                    }
+#pragma unroll
+                for (int u = 0; u < kSkBatch; ++u) {
+                    const int k = k0 + u * MM::KI;
+                    if (k >= kn) break;
                     const typename MM::frag af = MM::load(&sIn[r16][k + kg]);
-                    acc[t] = MM::mma(af, bf, acc[t]);
+#pragma unroll
+                    for (int t = 0; t < kSkTiles; ++t) acc[t] = MM::mma(af, wf[t][u], acc[t]);
                 }
             }
         }
@@ -188,22 +208,69 @@ int launch_skinny(int dt, const SkinnyArgs& a, hipStream_t s) {
 // ---------------------------------------------------------------------------
 // Conditioning helpers
 // ---------------------------------------------------------------------------
-__global__ void sinusoid_kernel(double t, int B, int half, float* e) {
+__global__ void step_sinusoid_kernel(int sampler, int S, int half, float* e) {
+    const int k = blockIdx.y;
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= half) return;
+    if (i >= half || k >= S) return;
+    const double t = sampler == BC_SAMPLER_EULER ? 1000.0 * (1.0 - (double)k / S) : (double)(999 - (1000 * k) / S);
     const double f = exp(-log(10000.0) * (double)i / (double)half);
     const double ang = t * f;
-    const float c = (float)cos(ang), sn = (float)sin(ang);
-    for (int b = 0; b < B; ++b) {
-        e[(int64_t)b * 2 * half + i] = c;
-        e[(int64_t)b * 2 * half + half + i] = sn;
-    }
+    e[(int64_t)k * 2 * half + i] = (float)cos(ang);
+    e[(int64_t)k * 2 * half + half + i] = (float)sin(ang);
 }
 
-int launch_sinusoid(double t, int B, int dim, float* e, hipStream_t s) {
+int launch_step_sinusoid(int sampler, int S, int dim, float* e, hipStream_t s) {
     const int half = dim / 2;
-    sinusoid_kernel<<<(half + 127) / 128, 128, 0, s>>>(t, B, half, e);
+    step_sinusoid_kernel<<<dim3((half + 127) / 128, S), 128, 0, s>>>(sampler, S, half, e);
     return check_launch("sinusoid");
+}
+
+template <typename T>
+__global__ void build_cond_kernel(const float* temb, int S, int B, int D, const T* table, const int64_t* labels,
+                                  int n_rows, const float* add, float* c) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (int64_t)S * B * D) return;
+    const int n = (int)(i % D);
+    const int64_t kb = i / D;
+    const int b = (int)(kb % B), k = (int)(kb / B);
+    float v = temb[(int64_t)k * D + n];
+    if (labels) {
+        int64_t lab = labels[b];
+        lab = lab < 0 ? 0 : (lab >= n_rows ? n_rows - 1 : lab);   // out-of-range labels are clamped
+        v += ld(table + lab * D + n);
+    } else if (add) {
+        v += add[(int64_t)b * D + n];
+    }
+    c[i] = v;
+}
+
+int launch_build_cond(int dt, const float* temb, int S, int B, int D, const void* table, const int64_t* labels,
+                      int n_rows, const float* add, float* c, hipStream_t s) {
+    const int64_t n = (int64_t)S * B * D;
+    const unsigned g = (unsigned)((n + 255) / 256);
+    if (dt == BC_BF16) build_cond_kernel<bf16><<<g, 256, 0, s>>>(temb, S, B, D, static_cast<const bf16*>(table), labels, n_rows, add, c);
+    else build_cond_kernel<float><<<g, 256, 0, s>>>(temb, S, B, D, static_cast<const float*>(table), labels, n_rows, add, c);
+    return check_launch("build_cond");
+}
+
+template <typename T>
+__global__ void gather_silu_kernel(const float* c, int B, int D, RowList rows, int n, T* out) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (int64_t)n * B * D) return;
+    const int d = (int)(i % D);
+    const int64_t ib = i / D;
+    const int b = (int)(ib % B), r = (int)(ib / B);
+    st(out + i, silu(c[((int64_t)rows.row[r] * B + b) * D + d]));
+}
+
+int launch_gather_silu(int dt, const float* c, int B, int D, const RowList& rows, int n, void* out, hipStream_t s) {
+    if (n <= 0) return BC_OK;
+    if (n > kMaxSeg) return fail(BC_ERR_UNSUPPORTED, "gather of %d rows", n);
+    const int64_t total = (int64_t)n * B * D;
+    const unsigned g = (unsigned)((total + 255) / 256);
+    if (dt == BC_BF16) gather_silu_kernel<bf16><<<g, 256, 0, s>>>(c, B, D, rows, n, static_cast<bf16*>(out));
+    else gather_silu_kernel<float><<<g, 256, 0, s>>>(c, B, D, rows, n, static_cast<float*>(out));
+    return check_launch("gather_silu");
 }
 
 template <typename T>
@@ -289,134 +356,65 @@ int launch_convert(int in_dt, const void* in, int out_dt, void* out, int64_t n, 
 // ---------------------------------------------------------------------------
 // Patch embedding and the final layer
 // ---------------------------------------------------------------------------
+// One workgroup per token: gather its p*p*C patch values once (LDS), then
+// each thread produces output features of the row.
 template <typename T>
-__global__ __launch_bounds__(256) void patch_embed_kernel(const float* __restrict__ lat, LatentShape ls, int B,
+__global__ __launch_bounds__(256) void patch_embed_kernel(const float* __restrict__ lat, LatentShape ls,
                                                           const T* __restrict__ W, const T* __restrict__ bias,
                                                           const T* __restrict__ pos, int D, float* __restrict__ x) {
+    __shared__ float patch[kMaxPatch];
     const int Tn = ls.tokens();
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= (int64_t)B * Tn * D) return;
-    const int c = (int)(i % D);
-    const int tok = (int)((i / D) % Tn);
-    const int b = (int)(i / ((int64_t)D * Tn));
+    const int row = blockIdx.x;
+    const int b = row / Tn, tok = row - b * Tn;
     const int hp = ls.H / ls.p, wp = ls.W / ls.p;
     const int f = tok / (hp * wp), ti = (tok / wp) % hp, tj = tok % wp;
     const int PD = ls.p * ls.p * ls.C;
-    float acc = 0.f;
-    for (int q = 0; q < PD; ++q) {
+    for (int q = threadIdx.x; q < PD; q += blockDim.x) {
         const int ph = q / (ls.p * ls.C), pw = (q / ls.C) % ls.p, ch = q % ls.C;
-        const float v = lat[((((int64_t)b * ls.C + ch) * ls.F + f) * ls.H + ti * ls.p + ph) * ls.W + tj * ls.p + pw];
-        acc = __builtin_fmaf(v, ld(W + (int64_t)c * PD + q), acc);
+        patch[q] = lat[((((int64_t)b * ls.C + ch) * ls.F + f) * ls.H + ti * ls.p + ph) * ls.W + tj * ls.p + pw];
     }
-    x[i] = acc + ld(bias + c) + ld(pos + (int64_t)tok * D + c);
+    __syncthreads();
+    for (int c = threadIdx.x; c < D; c += blockDim.x) {
+        const T* wr = W + (int64_t)c * PD;
+        float acc = 0.f;
+        for (int q = 0; q < PD; ++q) acc = __builtin_fmaf(patch[q], ld(wr + q), acc);
+        x[(int64_t)row * D + c] = acc + ld(bias + c) + ld(pos + (int64_t)tok * D + c);
+    }
 }
 
 int launch_patch_embed(int dt, const float* lat, LatentShape ls, int B, const void* W, const void* bias,
                        const void* pos, int D, float* x, hipStream_t s) {
-    const int64_t n = (int64_t)B * ls.tokens() * D;
-    const unsigned g = (unsigned)((n + 255) / 256);
+    if (ls.p * ls.p * ls.C > kMaxPatch) return fail(BC_ERR_UNSUPPORTED, "patch of %d values", ls.p * ls.p * ls.C);
+    const unsigned rows = (unsigned)(B * ls.tokens());
     if (dt == BC_BF16)
-        patch_embed_kernel<bf16><<<g, 256, 0, s>>>(lat, ls, B, static_cast<const bf16*>(W), static_cast<const bf16*>(bias),
-                                                   static_cast<const bf16*>(pos), D, x);
+        patch_embed_kernel<bf16><<<rows, 256, 0, s>>>(lat, ls, static_cast<const bf16*>(W), static_cast<const bf16*>(bias),
+                                                      static_cast<const bf16*>(pos), D, x);
     else
-        patch_embed_kernel<float><<<g, 256, 0, s>>>(lat, ls, B, static_cast<const float*>(W), static_cast<const float*>(bias),
-                                                    static_cast<const float*>(pos), D, x);
+        patch_embed_kernel<float><<<rows, 256, 0, s>>>(lat, ls, static_cast<const float*>(W), static_cast<const float*>(bias),
+                                                       static_cast<const float*>(pos), D, x);
     return check_launch("patch_embed");
-}
-
-template <typename Tin, typename T, int NV>
-__global__ __launch_bounds__(256) void final_layer_kernel(const Tin* __restrict__ feat, const float* __restrict__ shift,
-                                                          const float* __restrict__ scale, int64_t ld_mod,
-                                                          const T* __restrict__ W, const T* __restrict__ bias,
-                                                          LatentShape ls, int C_out, int B, int D,
-                                                          float* __restrict__ out) {
-    const int lane = threadIdx.x & 63;
-    const int Tn = ls.tokens();
-    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (row >= (int64_t)B * Tn) return;
-    const int b = (int)(row / Tn), tok = (int)(row % Tn);
-    const Tin* xr = feat + row * D;
-    float v[NV];
-    float sum = 0.f;
-#pragma unroll
-    for (int j = 0; j < NV; ++j) {
-        const int c = lane + 64 * j;
-        v[j] = c < D ? ld(xr + c) : 0.f;
-        sum += v[j];
-    }
-    const float mean = wave_sum(sum) / (float)D;
-    float sq = 0.f;
-#pragma unroll
-    for (int j = 0; j < NV; ++j) {
-        const int c = lane + 64 * j;
-        const float d = c < D ? v[j] - mean : 0.f;
-        sq += d * d;
-    }
-    const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + kLnEps);
-    const float* sh = shift + (int64_t)b * ld_mod;
-    const float* sc = scale + (int64_t)b * ld_mod;
-#pragma unroll
-    for (int j = 0; j < NV; ++j) {
-        const int c = lane + 64 * j;
-        v[j] = c < D ? (v[j] - mean) * rstd * (1.0f + sc[c]) + sh[c] : 0.f;
-    }
-    const int hp = ls.H / ls.p, wp = ls.W / ls.p;
-    const int f = tok / (hp * wp), ti = (tok / wp) % hp, tj = tok % wp;
-    const int NO = ls.p * ls.p * C_out;
-    for (int n = 0; n < NO; ++n) {
-        const T* wr = W + (int64_t)n * D;
-        float part = 0.f;
-#pragma unroll
-        for (int j = 0; j < NV; ++j) {
-            const int c = lane + 64 * j;
-            if (c < D) part = __builtin_fmaf(v[j], ld(wr + c), part);
-        }
-        const float y = wave_sum(part) + ld(bias + n);
-        if (lane == 0) {
-            const int ph = n / (ls.p * C_out), pw = (n / C_out) % ls.p, ch = n % C_out;
-            out[((((int64_t)b * C_out + ch) * ls.F + f) * ls.H + ti * ls.p + ph) * ls.W + tj * ls.p + pw] = y;
-        }
-    }
-}
-
-template <typename Tin, typename T>
-static int run_final(const void* feat, const float* shift, const float* scale, int64_t ld_mod, const void* W,
-                     const void* bias, LatentShape ls, int C_out, int B, int D, float* out, hipStream_t s) {
-    const int64_t rows = (int64_t)B * ls.tokens();
-    dim3 g((unsigned)((rows + 3) / 4)), blk(256);
-    const Tin* fi = static_cast<const Tin*>(feat);
-    const T* w = static_cast<const T*>(W);
-    const T* bi = static_cast<const T*>(bias);
-    const int nv = (D + 63) / 64;
-    if (nv <= 4) final_layer_kernel<Tin, T, 4><<<g, blk, 0, s>>>(fi, shift, scale, ld_mod, w, bi, ls, C_out, B, D, out);
-    else if (nv <= 18) final_layer_kernel<Tin, T, 18><<<g, blk, 0, s>>>(fi, shift, scale, ld_mod, w, bi, ls, C_out, B, D, out);
-    else if (nv <= 48) final_layer_kernel<Tin, T, 48><<<g, blk, 0, s>>>(fi, shift, scale, ld_mod, w, bi, ls, C_out, B, D, out);
-    else return fail(BC_ERR_UNSUPPORTED, "final layer width %d > 3072", D);
-    return check_launch("final_layer");
-}
-
-int launch_final_layer(int feat_dt, const void* feat, int dt, const float* shift, const float* scale, int64_t ld_mod,
-                       const void* W, const void* bias, LatentShape ls, int C_out, int B, int D, float* out,
-                       hipStream_t s) {
-    if (dt == BC_BF16) {
-        if (feat_dt == BC_BF16) return run_final<bf16, bf16>(feat, shift, scale, ld_mod, W, bias, ls, C_out, B, D, out, s);
-        return run_final<float, bf16>(feat, shift, scale, ld_mod, W, bias, ls, C_out, B, D, out, s);
-    }
-    if (feat_dt == BC_BF16) return run_final<bf16, float>(feat, shift, scale, ld_mod, W, bias, ls, C_out, B, D, out, s);
-    return run_final<float, float>(feat, shift, scale, ld_mod, W, bias, ls, C_out, B, D, out, s);
 }
 
 // ---------------------------------------------------------------------------
 // Sampler update
 // ---------------------------------------------------------------------------
-__global__ void sampler_kernel(SamplerCoef k, float* x, const float* eps, float* prev, int B, int C, int C_out,
-                               int64_t S) {
+// Model output arrives in token layout [B*T, p*p*C_out] (the final linear's
+// output); element (b, c, f, y, x) of the latent is read from token
+// (f, y/p, x/p), feature ((y%p)*p + x%p)*C_out + c, which is unpatchify.
+__global__ void sampler_kernel(SamplerCoef k, float* x, const float* out_tok, float* prev, LatentShape ls, int B,
+                               int C_out) {
+    const int64_t S = (int64_t)ls.F * ls.H * ls.W;
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= (int64_t)B * C * S) return;
-    const int64_t sp = i % S;
+    if (i >= (int64_t)B * ls.C * S) return;
+    const int xs = (int)(i % ls.W);
+    const int ys = (int)((i / ls.W) % ls.H);
+    const int f = (int)((i / ((int64_t)ls.W * ls.H)) % ls.F);
     const int64_t bc = i / S;
-    const int c = (int)(bc % C), b = (int)(bc / C);
-    const float e = eps[((int64_t)b * C_out + c) * S + sp];
+    const int c = (int)(bc % ls.C), b = (int)(bc / ls.C);
+    const int hp = ls.H / ls.p, wp = ls.W / ls.p;
+    const int tok = (f * hp + ys / ls.p) * wp + xs / ls.p;
+    const int feat = ((ys % ls.p) * ls.p + xs % ls.p) * C_out + c;
+    const float e = out_tok[((int64_t)b * ls.tokens() + tok) * (ls.p * ls.p * C_out) + feat];
     const float xv = x[i];
     if (k.mode == 0) {
         x[i] = k.c[0] * xv + k.c[1] * e;
@@ -432,10 +430,10 @@ __global__ void sampler_kernel(SamplerCoef k, float* x, const float* eps, float*
     if (prev) prev[i] = x0;
 }
 
-int launch_sampler(const SamplerCoef& k, float* x, const float* eps, float* prev, int B, int C, int C_out, int64_t S,
+int launch_sampler(const SamplerCoef& k, float* x, const float* out_tok, float* prev, LatentShape ls, int B, int C_out,
                    hipStream_t s) {
-    const int64_t n = (int64_t)B * C * S;
-    sampler_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(k, x, eps, prev, B, C, C_out, S);
+    const int64_t n = (int64_t)B * ls.C * ls.F * ls.H * ls.W;
+    sampler_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(k, x, out_tok, prev, ls, B, C_out);
     return check_launch("sampler");
 }
 

@@ -96,24 +96,24 @@ class DeviceModel:
         self._ws = {}
         self._ring = {}
 
-    def buffers(self, B: int, K: int):
-        """Workspace and ring storage for batch B (allocated once, reused)."""
+    def buffers(self, B: int, K: int, S: int):
+        """Workspace and ring storage for batch B and S steps (allocated once, reused)."""
         import torch
-        if B not in self._ws:
-            n = self.model.workspace_size(B)
-            self._ws[B] = torch.empty(n, dtype=torch.uint8, device=self.device)
+        if (B, S) not in self._ws:
+            n = self.model.workspace_size(B, S)
+            self._ws[(B, S)] = torch.empty(n, dtype=torch.uint8, device=self.device)
         key = (B, K)
         if key not in self._ring:
             numel = B * self.cfg.tokens * self.cfg.hidden
             storage = torch.empty((K, numel), dtype=torch_dtype(self.cfg), device=self.device)
             self._ring[key] = CacheRing(K, storage)
-        return self._ws[B], self._ring[key]
+        return self._ws[(B, S)], self._ring[key]
 
     def sample(self, x, mask, K: Optional[int] = None, labels=None, text=None, p=None, stream=None):
         """BaryCache sampling in place on x (fp32 device latents [B, ...])."""
         K = K or self.cfg.K
         B = x.shape[0]
-        ws, ring = self.buffers(B, K)
+        ws, ring = self.buffers(B, K, len(mask))
         sample(self.model, B, self.cfg.sampler, mask, K, ring, x, ws, labels=labels, text=text, p=p,
                stream=stream)
         return ring
