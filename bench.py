@@ -36,6 +36,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-forecast", action="store_true")
     ap.add_argument("--cpu-steps", type=int, default=9, help="oracle sample: first N steps of one sample")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run one 1 GiB device copy through the library (counter calibration)")
     return ap.parse_args()
 
 
@@ -217,6 +219,17 @@ def main():
         fc_hash = source_hash("forecast.hip", "hip_common.h")
         forecast["traffic"] = counters_traffic("forecast_k3_bf16", fc_hash, None)
         forecast["source_hash"] = fc_hash
+
+    if args.calib_copy:
+        # A plain copy of known size through the library's 16-byte copy kernel:
+        # the reference for scaling HBM byte counters.
+        n = 1 << 29
+        src = torch.ones(n, dtype=torch.bfloat16, device=dev)
+        store = torch.empty((1, n), dtype=torch.bfloat16, device=dev)
+        ring = bc.CacheRing(1, store)
+        ring.push(src, 0.0)
+        torch.cuda.synchronize()
+        del src, store, ring
 
     cpu = None
     if not args.no_cpu_baseline:
