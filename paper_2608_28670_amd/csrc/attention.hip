@@ -1,8 +1,8 @@
 // Multi-head attention softmax(Q K^T / sqrt(d)) V, flash style (online
 // softmax, no T x T buffer), on MFMA.
 //
-// A workgroup owns 64 queries of one (sample, head); each of its 4 waves owns
-// 16 of them and keeps their Q fragments in registers.  Keys and values
+// A workgroup owns 64*QG queries of one (sample, head); each of its 4 waves
+// owns QG groups of 16 and keeps their Q fragments in registers.  Keys and values
 // stream through LDS 64 at a time (K row-major, V transposed).  The wave
 // computes the transposed scores S^T = K Q^T, so after the MFMA a lane holds
 // 16 scores of a single query (its lane index mod 16).  That makes the
@@ -20,7 +20,6 @@
 namespace bc {
 
 constexpr int kAttnThreads = 256;
-constexpr int kQTile = 64;   // queries per workgroup
 constexpr int kKTile = 64;   // keys per step
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -47,21 +46,31 @@ __device__ __forceinline__ const T* seg_row(const void* p0, const void* p1, int 
                   : static_cast<const T*>(p1) + ((int64_t)b * T1 + (p - T0)) * ld;
 }
 
-template <typename T, int HD>
+// QG groups of 16 queries per wave (64 * QG per workgroup): every K and V
+// fragment read from LDS feeds QG MFMAs.
+template <typename T, int HD, int QG>
 __global__ __launch_bounds__(kAttnThreads) void attention_kernel(AttnArgs a) {
     typedef AttnShape<T, HD> S;
+    constexpr int QT = 64 * QG;                  // queries per workgroup
     constexpr int LDK = S::DK + S::KPAD;
     constexpr int LDV = kKTile + S::KPAD;
     __shared__ __attribute__((aligned(16))) T sK[kKTile][LDK];
     __shared__ __attribute__((aligned(16))) T sVt[S::DV][LDV];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int b = blockIdx.z, h = blockIdx.y;
     const int Tq = a.Tq0 + a.Tq1, Tk = a.Tk0 + a.Tk1;
-    const int q0 = blockIdx.x * kQTile + wave * 16;
+    // Workgroup order: consecutive ids go round-robin to the 8 XCDs; remap so
+    // each XCD holds a contiguous range, i.e. all query tiles of a (sample,
+    // head) share one L2 and its keys and values are fetched once per XCD.
+    const int nqt = (Tq + QT - 1) / QT;
+    const int nwg = gridDim.x;
+    int pid = blockIdx.x;
+    if ((nwg & 7) == 0) pid = (pid & 7) * (nwg >> 3) + (pid >> 3);
+    const int qt = pid % nqt;
+    const int h = (pid / nqt) % a.H;
+    const int b = pid / (nqt * a.H);
     const int col0 = h * HD;
     const int ql = lane & 15, grp = lane >> 4;
-    const int myq = q0 + ql;
 
     // Zero the padding columns of K and the padding rows of V^T once.
     for (int i = tid; i < kKTile * (LDK - HD); i += kAttnThreads)
@@ -69,39 +78,52 @@ __global__ __launch_bounds__(kAttnThreads) void attention_kernel(AttnArgs a) {
     for (int i = tid; i < (S::DV - HD) * LDV; i += kAttnThreads)
         sVt[HD + i / LDV][i % LDV] = (T)0.f;
 
-    // Q fragments (B operand of S^T = K Q^T): lane holds query ql.
-    const T* qrow = myq < Tq ? seg_row<T>(a.q0, a.q1, a.Tq0, a.Tq1, a.ldq, b, myq) + col0 : nullptr;
-    bf16x8 qf[S::n32x > 0 ? S::n32x : 1];
-    s16x4 qt;
-    float qf32[sizeof(T) == 4 ? HD / 4 : 1];
-    if constexpr (sizeof(T) == 2) {
+    // Q fragments (B operand of S^T = K Q^T): in group g, lane holds query
+    // qt*QT + wave*16*QG + 16g + ql.
+    bf16x8 qf[QG][S::n32x > 0 ? S::n32x : 1];
+    s16x4 qt16[QG];
+    float qf32[QG][sizeof(T) == 4 ? HD / 4 : 1];
+    int myq[QG];
 #pragma unroll
-        for (int c = 0; c < S::n32x; ++c) {
+    for (int g = 0; g < QG; ++g) {
+        myq[g] = qt * QT + wave * 16 * QG + 16 * g + ql;
+        const T* qrow = myq[g] < Tq ? seg_row<T>(a.q0, a.q1, a.Tq0, a.Tq1, a.ldq, b, myq[g]) + col0 : nullptr;
+        if constexpr (sizeof(T) == 2) {
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const int d = 32 * c + grp * 8 + i;
-                qf[c][i] = (qrow && d < HD) ? (bf16)qrow[d] : (bf16)0.f;
+            for (int c = 0; c < S::n32x; ++c)
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const int d = 32 * c + grp * 8 + i;
+                    qf[g][c][i] = (qrow && d < HD) ? (bf16)qrow[d] : (bf16)0.f;
+                }
+            if constexpr (S::tail16) {
+                const unsigned short* qraw = reinterpret_cast<const unsigned short*>(qrow);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int d = 32 * S::n32 + grp * 4 + i;
+                    qt16[g][i] = (qraw && d < HD) ? (short)qraw[d] : (short)0;
+                }
             }
-        }
-        if constexpr (S::tail16) {
-            const unsigned short* qraw = reinterpret_cast<const unsigned short*>(qrow);
+        } else {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int d = 32 * S::n32 + grp * 4 + i;
-                qt[i] = (qraw && d < HD) ? (short)qraw[d] : (short)0;
-            }
+            for (int c = 0; c < HD / 4; ++c) qf32[g][c] = qrow ? (float)qrow[4 * c + grp] : 0.f;
         }
-    } else {
-#pragma unroll
-        for (int c = 0; c < HD / 4; ++c) qf32[c] = qrow ? (float)qrow[4 * c + grp] : 0.f;
     }
 
-    f32x4 o[S::DV / 16];
+    f32x4 o[QG][S::DV / 16];
+    float m_run[QG], l_run[QG];
 #pragma unroll
-    for (int i = 0; i < S::DV / 16; ++i) o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float m_run = -INFINITY, l_run = 0.f;
+    for (int g = 0; g < QG; ++g) {
+        m_run[g] = -INFINITY;
+        l_run[g] = 0.f;
+#pragma unroll
+        for (int i = 0; i < S::DV / 16; ++i) o[g][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
 
-    // Staging of one K/V tile: 64 rows x CPR chunks each.
+    // Staging of one K/V tile (64 keys x CPR 16-byte chunks).  K chunks are
+    // assigned row-major (coalesced global reads, 16-byte LDS stores); V chunks
+    // key-major, so a wave's transposed 2-byte LDS stores cover 64 consecutive
+    // keys of one row of V^T.
     constexpr int NCH = kKTile * S::CPR;
     constexpr int PER = (NCH + kAttnThreads - 1) / kAttnThreads;
     u32x4 rk[PER], rv[PER];
@@ -109,16 +131,17 @@ __global__ __launch_bounds__(kAttnThreads) void attention_kernel(AttnArgs a) {
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
             const int c = tid + i * kAttnThreads;
-            const int row = c / S::CPR, ch = c % S::CPR;
-            const int p = k0 + row;
-            if (c < NCH && p < Tk) {
-                const T* kr = seg_row<T>(a.k0, a.k1, a.Tk0, a.Tk1, a.ldk, b, p) + col0 + ch * S::EPC;
-                const T* vr = seg_row<T>(a.v0, a.v1, a.Tk0, a.Tk1, a.ldv, b, p) + col0 + ch * S::EPC;
-                rk[i] = *reinterpret_cast<const u32x4*>(kr);
-                rv[i] = *reinterpret_cast<const u32x4*>(vr);
-            } else {
-                rk[i] = u32x4{0, 0, 0, 0};
-                rv[i] = u32x4{0, 0, 0, 0};
+            rk[i] = u32x4{0, 0, 0, 0};
+            rv[i] = u32x4{0, 0, 0, 0};
+            if (c < NCH) {
+                const int krow = c / S::CPR, kch = c % S::CPR;
+                if (k0 + krow < Tk)
+                    rk[i] = *reinterpret_cast<const u32x4*>(
+                        seg_row<T>(a.k0, a.k1, a.Tk0, a.Tk1, a.ldk, b, k0 + krow) + col0 + kch * S::EPC);
+                const int vrow = c % kKTile, vch = c / kKTile;
+                if (k0 + vrow < Tk)
+                    rv[i] = *reinterpret_cast<const u32x4*>(
+                        seg_row<T>(a.v0, a.v1, a.Tk0, a.Tk1, a.ldv, b, k0 + vrow) + col0 + vch * S::EPC);
             }
         }
     };
@@ -127,11 +150,21 @@ __global__ __launch_bounds__(kAttnThreads) void attention_kernel(AttnArgs a) {
         for (int i = 0; i < PER; ++i) {
             const int c = tid + i * kAttnThreads;
             if (c < NCH) {
-                const int row = c / S::CPR, ch = c % S::CPR;
-                *reinterpret_cast<u32x4*>(&sK[row][ch * S::EPC]) = rk[i];
-                const T* vv = reinterpret_cast<const T*>(&rv[i]);
+                *reinterpret_cast<u32x4*>(&sK[c / S::CPR][(c % S::CPR) * S::EPC]) = rk[i];
+                const int vrow = c % kKTile, vch = c / kKTile;
+                if constexpr (sizeof(T) == 2) {
+                    const uint32_t w4[4] = {rv[i].x, rv[i].y, rv[i].z, rv[i].w};
 #pragma unroll
-                for (int e = 0; e < S::EPC; ++e) sVt[ch * S::EPC + e][row] = vv[e];
+                    for (int e = 0; e < 4; ++e) {
+                        sVt[vch * 8 + 2 * e][vrow] = __builtin_bit_cast(bf16, (unsigned short)(w4[e] & 0xffffu));
+                        sVt[vch * 8 + 2 * e + 1][vrow] = __builtin_bit_cast(bf16, (unsigned short)(w4[e] >> 16));
+                    }
+                } else {
+                    sVt[vch * 4 + 0][vrow] = __uint_as_float(rv[i].x);
+                    sVt[vch * 4 + 1][vrow] = __uint_as_float(rv[i].y);
+                    sVt[vch * 4 + 2][vrow] = __uint_as_float(rv[i].z);
+                    sVt[vch * 4 + 3][vrow] = __uint_as_float(rv[i].w);
+                }
             }
         }
     };
@@ -146,70 +179,82 @@ __global__ __launch_bounds__(kAttnThreads) void attention_kernel(AttnArgs a) {
         const int k0 = t * kKTile;
         if (t + 1 < ntiles) load_tile(k0 + kKTile);
 
-        // S^T tiles: s[j] covers keys k0 + 16j .. +16; lane holds keys 16j + 4grp + r of query ql.
-        f32x4 s[4];
+        // S^T tiles: s[g][j] covers keys k0 + 16j .. +16; lane holds keys
+        // 16j + 4grp + r of its query in group g.
+        f32x4 s[QG][4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            s[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int g = 0; g < QG; ++g) s[g][j] = f32x4{0.f, 0.f, 0.f, 0.f};
             const int krow = 16 * j + ql;
             if constexpr (sizeof(T) == 2) {
 #pragma unroll
                 for (int c = 0; c < S::n32x; ++c) {
                     const bf16x8 kf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sK[krow][32 * c + grp * 8]));
-                    s[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[c], s[j], 0, 0, 0);
+#pragma unroll
+                    for (int g = 0; g < QG; ++g) s[g][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[g][c], s[g][j], 0, 0, 0);
                 }
                 if constexpr (S::tail16) {
                     const s16x4 kt = __builtin_bit_cast(s16x4, *reinterpret_cast<const u32x2*>(&sK[krow][32 * S::n32 + grp * 4]));
-                    s[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(kt, qt, s[j], 0, 0, 0);
+#pragma unroll
+                    for (int g = 0; g < QG; ++g) s[g][j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(kt, qt16[g], s[g][j], 0, 0, 0);
                 }
             } else {
 #pragma unroll
-                for (int c = 0; c < HD / 4; ++c)
-                    s[j] = __builtin_amdgcn_mfma_f32_16x16x4f32((float)sK[krow][4 * c + grp], qf32[c], s[j], 0, 0, 0);
+                for (int c = 0; c < HD / 4; ++c) {
+                    const float kv = (float)sK[krow][4 * c + grp];
+#pragma unroll
+                    for (int g = 0; g < QG; ++g) s[g][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(kv, qf32[g][c], s[g][j], 0, 0, 0);
+                }
             }
         }
 
         // Online softmax (base 2, scores pre-scaled by log2(e)/sqrt(d)).
-        float mloc = -INFINITY;
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int g = 0; g < QG; ++g) {
+            float mloc = -INFINITY;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int key = k0 + 16 * j + 4 * grp + r;
-                const float v = key < Tk ? s[j][r] * a.scale_log2 : -INFINITY;
-                s[j][r] = v;
-                mloc = fmaxf(mloc, v);
-            }
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-        const float m_new = fmaxf(m_run, mloc);
-        const float alpha = exp2f(m_run - m_new);
-        float lsum = 0.f;
+            for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+                for (int r = 0; r < 4; ++r) {
+                    const int key = k0 + 16 * j + 4 * grp + r;
+                    const float v = key < Tk ? s[g][j][r] * a.scale_log2 : -INFINITY;
+                    s[g][j][r] = v;
+                    mloc = fmaxf(mloc, v);
+                }
+            mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+            mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+            const float m_new = fmaxf(m_run[g], mloc);
+            const float alpha = exp2f(m_run[g] - m_new);
+            float lsum = 0.f;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float p = exp2f(s[j][r] - m_new);
-                s[j][r] = p;
-                lsum += p;
-            }
-        lsum += __shfl_xor(lsum, 16, 64);
-        lsum += __shfl_xor(lsum, 32, 64);
-        l_run = l_run * alpha + lsum;
-        m_run = m_new;
+            for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int i = 0; i < S::DV / 16; ++i) o[i] *= alpha;
+                for (int r = 0; r < 4; ++r) {
+                    const float p = exp2f(s[g][j][r] - m_new);
+                    s[g][j][r] = p;
+                    lsum += p;
+                }
+            lsum += __shfl_xor(lsum, 16, 64);
+            lsum += __shfl_xor(lsum, 32, 64);
+            l_run[g] = l_run[g] * alpha + lsum;
+            m_run[g] = m_new;
+#pragma unroll
+            for (int i = 0; i < S::DV / 16; ++i) o[g][i] *= alpha;
+        }
 
         // O^T += V^T P^T.
         if constexpr (sizeof(T) == 2) {
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
-                bf16x8 pf;
+                bf16x8 pf[QG];
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    pf[r] = (bf16)s[2 * u][r];
-                    pf[4 + r] = (bf16)s[2 * u + 1][r];
-                }
+                for (int g = 0; g < QG; ++g)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        pf[g][r] = (bf16)s[g][2 * u][r];
+                        pf[g][4 + r] = (bf16)s[g][2 * u + 1][r];
+                    }
 #pragma unroll
                 for (int i = 0; i < S::DV / 16; ++i) {
                     // keys 32u + 4grp + 0..3 and 32u + 16 + 4grp + 0..3, matching pf
@@ -217,7 +262,8 @@ __global__ __launch_bounds__(kAttnThreads) void attention_kernel(AttnArgs a) {
                     const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow);
                     const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 16);
                     const bf16x8 vf = __builtin_bit_cast(bf16x8, u32x4{lo.x, lo.y, hi.x, hi.y});
-                    o[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[i], 0, 0, 0);
+#pragma unroll
+                    for (int g = 0; g < QG; ++g) o[g][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[g], o[g][i], 0, 0, 0);
                 }
             }
         } else {
@@ -226,9 +272,11 @@ __global__ __launch_bounds__(kAttnThreads) void attention_kernel(AttnArgs a) {
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
 #pragma unroll
-                    for (int i = 0; i < S::DV / 16; ++i)
-                        o[i] = __builtin_amdgcn_mfma_f32_16x16x4f32((float)sVt[16 * i + ql][16 * j + 4 * grp + r],
-                                                                     s[j][r], o[i], 0, 0, 0);
+                    for (int i = 0; i < S::DV / 16; ++i) {
+                        const float vv = (float)sVt[16 * i + ql][16 * j + 4 * grp + r];
+#pragma unroll
+                        for (int g = 0; g < QG; ++g) o[g][i] = __builtin_amdgcn_mfma_f32_16x16x4f32(vv, s[g][j][r], o[g][i], 0, 0, 0);
+                    }
         }
 
         __syncthreads();
@@ -238,25 +286,30 @@ __global__ __launch_bounds__(kAttnThreads) void attention_kernel(AttnArgs a) {
         }
     }
 
-    if (myq < Tq) {
-        const float inv = 1.f / l_run;
-        T* orow = const_cast<T*>(seg_row<T>(a.o0, a.o1, a.Tq0, a.Tq1, a.ldo, b, myq)) + col0;
 #pragma unroll
-        for (int i = 0; i < S::DV / 16; ++i)
+    for (int g = 0; g < QG; ++g) {
+        if (myq[g] < Tq) {
+            const float inv = 1.f / l_run[g];
+            T* orow = const_cast<T*>(seg_row<T>(a.o0, a.o1, a.Tq0, a.Tq1, a.ldo, b, myq[g])) + col0;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int d = 16 * i + 4 * grp + r;
-                if (d < HD) st(orow + d, o[i][r] * inv);
-            }
+            for (int i = 0; i < S::DV / 16; ++i)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int d = 16 * i + 4 * grp + r;
+                    if (d < HD) st(orow + d, o[g][i][r] * inv);
+                }
+        }
     }
 }
 
-template <typename T>
+template <typename T, int QG>
 static int run_attention(const AttnArgs& a, int hd, hipStream_t s) {
     const int Tq = a.Tq0 + a.Tq1;
-    dim3 grid((Tq + kQTile - 1) / kQTile, a.H, a.B), block(kAttnThreads);
+    const int64_t nwg = (int64_t)((Tq + 64 * QG - 1) / (64 * QG)) * a.H * a.B;
+    if (nwg > 0x7fffffff) return fail(BC_ERR_UNSUPPORTED, "attention grid too large");
+    dim3 grid((unsigned)nwg), block(kAttnThreads);
     switch (hd) {
-#define BC_ATT_CASE(HD) case HD: attention_kernel<T, HD><<<grid, block, 0, s>>>(a); break;
+#define BC_ATT_CASE(HD) case HD: attention_kernel<T, HD, QG><<<grid, block, 0, s>>>(a); break;
         BC_ATT_CASE(32) BC_ATT_CASE(64) BC_ATT_CASE(72) BC_ATT_CASE(128)
 #undef BC_ATT_CASE
         default: return fail(BC_ERR_UNSUPPORTED, "head_dim %d (supported: 32, 64, 72, 128)", hd);
@@ -275,7 +328,7 @@ int launch_attention(int dtype, AttnArgs a, hipStream_t s) {
     if (dtype == BC_F32 && a.d > 64) return fail(BC_ERR_UNSUPPORTED, "fp32 attention supports head_dim <= 64");
     a.scale_log2 = 1.4426950408889634f / sqrtf((float)a.d);
     prof_begin(PROF_ATTENTION, s);
-    const int rc = dtype == BC_BF16 ? run_attention<bf16>(a, a.d, s) : run_attention<float>(a, a.d, s);
+    const int rc = dtype == BC_BF16 ? run_attention<bf16, 2>(a, a.d, s) : run_attention<float, 1>(a, a.d, s);
     prof_end(PROF_ATTENTION, s);
     return rc;
 }

@@ -205,7 +205,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(GemmArgs g
 // Requires K % 64 == 0 (whole k-steps); rows past M or N are clamped to the
 // last row, so they load valid memory and only feed outputs never stored.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+// LDS slot permutation of row r (see above); SW selects among candidate maps.
+template <int SW> __device__ __forceinline__ int swz_of(int row) {
+    if constexpr (SW == 0) return (row >> 1) & 7;
+    else if constexpr (SW == 1) return row & 7;
+    else return 0;
+}
+__device__ __forceinline__ int swz(int row) { return swz_of<0>(row); }
 
 // One wave-wide direct-to-LDS load: each lane's 16 bytes at `src` land at
 // lds_base + 16 * lane.  Issued as inline assembly so that the only waits on
@@ -222,7 +228,7 @@ template <int N> __device__ __forceinline__ void wait_vmcnt() {
     __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
-template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, bool SEG>
+template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, bool SEG, int SW = 0>
 __device__ __forceinline__ void gemm_dma_body(GemmArgs g, const GemmSeg* sg) {
     typedef bf16 T;
     typedef Mma<bf16> MM;
@@ -270,13 +276,13 @@ __device__ __forceinline__ void gemm_dma_body(GemmArgs g, const GemmSeg* sg) {
     for (int o = 0; o < OA; ++o) {
         const int r = (wave * OA + o) * 8 + lrow;
         const int grow = min(bm + r, g.M - 1);
-        srcA[o] = static_cast<const T*>(g.A) + (int64_t)grow * g.lda + ((lslot ^ swz(r)) * 8);
+        srcA[o] = static_cast<const T*>(g.A) + (int64_t)grow * g.lda + ((lslot ^ swz_of<SW>(r)) * 8);
     }
 #pragma unroll
     for (int o = 0; o < OB; ++o) {
         const int r = (wave * OB + o) * 8 + lrow;
         const int grow = min(bn + r, g.N - 1);
-        srcB[o] = static_cast<const T*>(g.W) + (int64_t)grow * g.ldw + ((lslot ^ swz(r)) * 8);
+        srcB[o] = static_cast<const T*>(g.W) + (int64_t)grow * g.ldw + ((lslot ^ swz_of<SW>(r)) * 8);
     }
     auto issue = [&](int kt, int buf) {
         const int k0 = kt * BK;
@@ -314,12 +320,12 @@ __device__ __forceinline__ void gemm_dma_body(GemmArgs g, const GemmSeg* sg) {
 #pragma unroll
             for (int i = 0; i < TM; ++i) {
                 const int r = wm * WM + i * 16 + frow;
-                af[i] = MM::load(a + r * BK + ((c ^ swz(r)) * 8));
+                af[i] = MM::load(a + r * BK + ((c ^ swz_of<SW>(r)) * 8));
             }
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
                 const int r = wn * WN + j * 16 + frow;
-                bfr[j] = MM::load(b + r * BK + ((c ^ swz(r)) * 8));
+                bfr[j] = MM::load(b + r * BK + ((c ^ swz_of<SW>(r)) * 8));
             }
 #pragma unroll
             for (int i = 0; i < TM; ++i)
@@ -331,9 +337,9 @@ __device__ __forceinline__ void gemm_dma_body(GemmArgs g, const GemmSeg* sg) {
     epilogue<T, EPI, TM, TN>(g, acc, bm + wm * WM, bn + wn * WN, lane);
 }
 
-template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES>
+template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int SW = 0>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_dma_kernel(GemmArgs g) {
-    gemm_dma_body<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, false>(g, nullptr);
+    gemm_dma_body<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, false, SW>(g, nullptr);
 }
 
 template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES>
@@ -341,10 +347,10 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_dma_seg_kernel(Ge
     gemm_dma_body<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, true>(g, &sg);
 }
 
-template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES>
+template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int SW = 0>
 static void launch_dma(const GemmArgs& g, hipStream_t s) {
     const unsigned tiles = (unsigned)(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN));
-    gemm_dma_kernel<EPI, BM, BN, WAVES_M, WAVES_N, STAGES><<<dim3(tiles), dim3(64 * WAVES_M * WAVES_N), 0, s>>>(g);
+    gemm_dma_kernel<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, SW><<<dim3(tiles), dim3(64 * WAVES_M * WAVES_N), 0, s>>>(g);
 }
 
 template <typename T, int EPI, int BM, int BN, int WAVES_M, int WAVES_N>

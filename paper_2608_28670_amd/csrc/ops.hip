@@ -12,9 +12,41 @@ constexpr float kLnEps = 1e-6f;
 constexpr int kMaxPatch = 256;
 
 // ---------------------------------------------------------------------------
-// LayerNorm + modulate: one wave per row, the row cached in registers.
+// LayerNorm + modulate: one wave per row, the row cached in registers as
+// 4-element chunks (lane l holds chunks l, l + 64, ...), so every load is 16
+// (fp32) or 8 (bf16) bytes and every store 8 (bf16) or 16 (fp32) bytes.
+// Requires D % 4 == 0.
 // ---------------------------------------------------------------------------
-template <typename Tin, typename Tout, int NV>
+template <typename T> struct Vec4;
+template <> struct Vec4<float> {
+    __device__ static void load(const float* p, float* v) {
+        const f32x4 x = *reinterpret_cast<const f32x4*>(p);
+        v[0] = x[0]; v[1] = x[1]; v[2] = x[2]; v[3] = x[3];
+    }
+    __device__ static void store(float* p, const float* v) {
+        *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
+    }
+};
+template <> struct Vec4<bf16> {
+    __device__ static void load(const bf16* p, float* v) {
+        typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+        const u32x2_t w = *reinterpret_cast<const u32x2_t*>(p);
+        v[0] = __uint_as_float(w[0] << 16); v[1] = __uint_as_float(w[0] & 0xffff0000u);
+        v[2] = __uint_as_float(w[1] << 16); v[3] = __uint_as_float(w[1] & 0xffff0000u);
+    }
+    __device__ static void store(bf16* p, const float* v) {
+        typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+        uint32_t w[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const bf16 lo = (bf16)v[2 * i], hi = (bf16)v[2 * i + 1];
+            w[i] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+        }
+        *reinterpret_cast<u32x2_t*>(p) = u32x2_t{w[0], w[1]};
+    }
+};
+
+template <typename Tin, typename Tout, int NC>
 __global__ __launch_bounds__(256) void ln_mod_kernel(const Tin* __restrict__ x, int64_t rows, int D,
                                                      const float* __restrict__ shift,
                                                      const float* __restrict__ scale, int64_t ld_mod, int rps,
@@ -22,22 +54,31 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const Tin* __restrict__ x, 
     const int lane = threadIdx.x & 63;
     const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (row >= rows) return;
+    const int nch = D >> 2;
     const Tin* xr = x + row * D;
-    float v[NV];
+    float v[NC][4];
     float sum = 0.f;
 #pragma unroll
-    for (int j = 0; j < NV; ++j) {
+    for (int j = 0; j < NC; ++j) {
         const int c = lane + 64 * j;
-        v[j] = c < D ? ld(xr + c) : 0.f;
-        sum += v[j];
+        if (c < nch) {
+            Vec4<Tin>::load(xr + 4 * c, v[j]);
+        } else {
+            v[j][0] = v[j][1] = v[j][2] = v[j][3] = 0.f;
+        }
+        sum += (v[j][0] + v[j][1]) + (v[j][2] + v[j][3]);
     }
     const float mean = wave_sum(sum) / (float)D;
     float sq = 0.f;
 #pragma unroll
-    for (int j = 0; j < NV; ++j) {
-        const int c = lane + 64 * j;
-        const float d = c < D ? v[j] - mean : 0.f;
-        sq += d * d;
+    for (int j = 0; j < NC; ++j) {
+        if (lane + 64 * j < nch) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float d = v[j][e] - mean;
+                sq += d * d;
+            }
+        }
     }
     const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + kLnEps);
     const int64_t b = row / rps;
@@ -45,25 +86,32 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const Tin* __restrict__ x, 
     const float* sc = scale + b * ld_mod;
     Tout* hr = h + row * D;
 #pragma unroll
-    for (int j = 0; j < NV; ++j) {
+    for (int j = 0; j < NC; ++j) {
         const int c = lane + 64 * j;
-        if (c < D) st(hr + c, (v[j] - mean) * rstd * (1.0f + sc[c]) + sh[c]);
+        if (c < nch) {
+            float s4[4], c4[4], o[4];
+            Vec4<float>::load(sh + 4 * c, s4);
+            Vec4<float>::load(sc + 4 * c, c4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[e] = (v[j][e] - mean) * rstd * (1.0f + c4[e]) + s4[e];
+            Vec4<Tout>::store(hr + 4 * c, o);
+        }
     }
 }
 
 template <typename Tin, typename Tout>
 static int run_ln(const void* x, int64_t rows, int D, const float* shift, const float* scale, int64_t ld_mod, int rps,
                   void* h, hipStream_t s) {
-    const int nv = (D + 63) / 64;
+    const int nc = (D / 4 + 63) / 64;
     dim3 g((unsigned)((rows + 3) / 4)), b(256);
     const Tin* xi = static_cast<const Tin*>(x);
     Tout* ho = static_cast<Tout*>(h);
-    if (nv <= 4) ln_mod_kernel<Tin, Tout, 4><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nv <= 8) ln_mod_kernel<Tin, Tout, 8><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nv <= 18) ln_mod_kernel<Tin, Tout, 18><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nv <= 32) ln_mod_kernel<Tin, Tout, 32><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nv <= 48) ln_mod_kernel<Tin, Tout, 48><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nv <= 64) ln_mod_kernel<Tin, Tout, 64><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
+    if (nc <= 1) ln_mod_kernel<Tin, Tout, 1><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 2) ln_mod_kernel<Tin, Tout, 2><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 5) ln_mod_kernel<Tin, Tout, 5><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 8) ln_mod_kernel<Tin, Tout, 8><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 12) ln_mod_kernel<Tin, Tout, 12><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 16) ln_mod_kernel<Tin, Tout, 16><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
     else return fail(BC_ERR_UNSUPPORTED, "LayerNorm width %d > 4096", D);
     return check_launch("ln_mod");
 }
@@ -71,6 +119,8 @@ static int run_ln(const void* x, int64_t rows, int D, const float* shift, const 
 int launch_ln_mod(int in_dt, const void* x, int64_t rows, int D, const float* shift, const float* scale,
                   int64_t ld_mod, int rows_per_sample, int out_dt, void* h, hipStream_t s) {
     if (rows <= 0) return BC_OK;
+    if (D % 4 || ld_mod % 4 || (reinterpret_cast<uintptr_t>(shift) | reinterpret_cast<uintptr_t>(scale)) % 16)
+        return fail(BC_ERR_UNSUPPORTED, "LayerNorm needs D and the modulation rows in 16-byte units");
     prof_begin(PROF_LAYERNORM, s);
     int rc;
     if (in_dt == BC_F32 && out_dt == BC_BF16) rc = run_ln<float, bf16>(x, rows, D, shift, scale, ld_mod, rows_per_sample, h, s);
