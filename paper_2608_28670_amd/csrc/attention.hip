@@ -26,13 +26,12 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 template <typename T, int HD> struct AttnShape {
-    // K dimension of Q K^T: bf16 uses 32-wide MFMA steps with a 16-wide tail;
-    // fp32 uses 4-wide steps.
-    static constexpr int n32 = sizeof(T) == 2 ? HD / 32 : 0;
-    static constexpr int rem = sizeof(T) == 2 ? HD - 32 * n32 : 0;
-    static constexpr int DK = sizeof(T) == 2 ? 32 * n32 + (rem > 16 ? 32 : rem > 0 ? 16 : 0) : HD;
-    static constexpr bool tail16 = sizeof(T) == 2 && rem > 0 && rem <= 16;
-    static constexpr int n32x = n32 + (rem > 16 ? 1 : 0);   // 32-wide steps incl. a padded one
+    // K dimension of Q K^T: bf16 uses 32-wide MFMA steps, the last one padded
+    // with zero Q columns (a 16-wide 16x16x16 tail step was dropped: in one
+    // schedule its accumulator was read back before the MFMA had written
+    // it); fp32 uses 4-wide steps.
+    static constexpr int n32x = sizeof(T) == 2 ? (HD + 31) / 32 : 0;   // 32-wide steps
+    static constexpr int DK = sizeof(T) == 2 ? 32 * n32x : HD;
     static constexpr int DV = (HD + 15) / 16 * 16;           // rows of O^T
     static constexpr int EPC = 16 / (int)sizeof(T);          // elements per 16-byte chunk
     static constexpr int CPR = HD / EPC;                     // chunks per head row
@@ -81,7 +80,6 @@ __global__ __launch_bounds__(kAttnThreads) void attention_kernel(AttnArgs a) {
     // Q fragments (B operand of S^T = K Q^T): in group g, lane holds query
     // qt*QT + wave*16*QG + 16g + ql.
     bf16x8 qf[QG][S::n32x > 0 ? S::n32x : 1];
-    s16x4 qt16[QG];
     float qf32[QG][sizeof(T) == 4 ? HD / 4 : 1];
     int myq[QG];
 #pragma unroll
@@ -96,14 +94,6 @@ __global__ __launch_bounds__(kAttnThreads) void attention_kernel(AttnArgs a) {
                     const int d = 32 * c + grp * 8 + i;
                     qf[g][c][i] = (qrow && d < HD) ? (bf16)qrow[d] : (bf16)0.f;
                 }
-            if constexpr (S::tail16) {
-                const unsigned short* qraw = reinterpret_cast<const unsigned short*>(qrow);
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int d = 32 * S::n32 + grp * 4 + i;
-                    qt16[g][i] = (qraw && d < HD) ? (short)qraw[d] : (short)0;
-                }
-            }
         } else {
 #pragma unroll
             for (int c = 0; c < HD / 4; ++c) qf32[g][c] = qrow ? (float)qrow[4 * c + grp] : 0.f;
@@ -193,11 +183,6 @@ __global__ __launch_bounds__(kAttnThreads) void attention_kernel(AttnArgs a) {
                     const bf16x8 kf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sK[krow][32 * c + grp * 8]));
 #pragma unroll
                     for (int g = 0; g < QG; ++g) s[g][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[g][c], s[g][j], 0, 0, 0);
-                }
-                if constexpr (S::tail16) {
-                    const s16x4 kt = __builtin_bit_cast(s16x4, *reinterpret_cast<const u32x2*>(&sK[krow][32 * S::n32 + grp * 4]));
-#pragma unroll
-                    for (int g = 0; g < QG; ++g) s[g][j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(kt, qt16[g], s[g][j], 0, 0, 0);
                 }
             } else {
 #pragma unroll
@@ -302,6 +287,221 @@ __global__ __launch_bounds__(kAttnThreads) void attention_kernel(AttnArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 kernel with direct-to-LDS K/V tiles.
+//
+// K and V tiles are both kept row-major (key rows, head_dim contiguous) and
+// stream HBM -> LDS with global_load_lds_dwordx4 (no register staging), double
+// buffered with one barrier per 64-key step.  The V^T operand of O^T = V^T P^T
+// is read with ds_read_b64_tr_b16: within a 16-lane group, lane L receives
+// element L % 4 of the 8-byte reads of lanes L/4 + 4i (i = 0..3), so if lane s
+// reads V[k0 + s/4][d0 + 4 (s % 4)], lane L gets V[k0 + i][d0 + L], i = 0..3:
+// four consecutive keys of one head-dim column, the operand layout.  Rows of
+// 128 or 256 bytes are XOR-swizzled by 16-byte chunk so the 16-row fragment
+// reads hit distinct banks (a 144-byte row of d = 72 already does).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void dma16a(const void* src, const void* lds_base) {
+    const unsigned m0 = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)lds_base);
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(m0) : "memory", "m0");
+}
+
+template <int HD> struct KvLayout {
+    static constexpr int CPR = HD / 8;                       // 16-byte chunks per row
+    static constexpr int RPB = (HD * 2) >= 256 ? 1 : 256 / (HD * 2);   // rows per 256 bytes
+    static constexpr bool SWZ = (CPR & (CPR - 1)) == 0;      // power-of-two rows are swizzled
+    __device__ static int slot(int row, int chunk) { return SWZ ? chunk ^ ((row / RPB) % CPR) : chunk; }
+    // element offset of (row, column d) in a tile
+    __device__ static int at(int row, int d) { return row * HD + slot(row, d >> 3) * 8 + (d & 7); }
+};
+
+template <int HD, int QG>
+__global__ __launch_bounds__(kAttnThreads) void attention_dma_kernel(AttnArgs a) {
+    typedef AttnShape<bf16, HD> S;
+    typedef KvLayout<HD> LY;
+    constexpr int QT = 64 * QG;
+    constexpr int TILE = kKTile * HD + 32;     // elements per K or V tile (+ slack for d >= HD operand reads)
+    __shared__ __attribute__((aligned(1024))) bf16 sK[2][TILE];
+    __shared__ __attribute__((aligned(1024))) bf16 sV[2][TILE];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int Tq = a.Tq0 + a.Tq1, Tk = a.Tk0 + a.Tk1;
+    const int nqt = (Tq + QT - 1) / QT;
+    const int nwg = gridDim.x;
+    int pid = blockIdx.x;
+    if ((nwg & 7) == 0) pid = (pid & 7) * (nwg >> 3) + (pid >> 3);
+    const int qt = pid % nqt;
+    const int h = (pid / nqt) % a.H;
+    const int b = pid / (nqt * a.H);
+    const int col0 = h * HD;
+    const int ql = lane & 15, grp = lane >> 4;
+
+    // The slack past the last row is read (for d >= HD operand rows, whose
+    // outputs are discarded) but never loaded: keep it finite.
+    if (tid < 32) {
+        sK[0][kKTile * HD + tid] = (bf16)0.f; sK[1][kKTile * HD + tid] = (bf16)0.f;
+        sV[0][kKTile * HD + tid] = (bf16)0.f; sV[1][kKTile * HD + tid] = (bf16)0.f;
+    }
+
+    bf16x8 qf[QG][S::n32x > 0 ? S::n32x : 1];
+    int myq[QG];
+#pragma unroll
+    for (int g = 0; g < QG; ++g) {
+        myq[g] = qt * QT + wave * 16 * QG + 16 * g + ql;
+        const bf16* qrow = myq[g] < Tq ? seg_row<bf16>(a.q0, a.q1, a.Tq0, a.Tq1, a.ldq, b, myq[g]) + col0 : nullptr;
+#pragma unroll
+        for (int c = 0; c < S::n32x; ++c)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int d = 32 * c + grp * 8 + i;
+                qf[g][c][i] = (qrow && d < HD) ? qrow[d] : (bf16)0.f;
+            }
+    }
+
+    f32x4 o[QG][S::DV / 16];
+    float m_run[QG], l_run[QG];
+#pragma unroll
+    for (int g = 0; g < QG; ++g) {
+        m_run[g] = -INFINITY;
+        l_run[g] = 0.f;
+#pragma unroll
+        for (int i = 0; i < S::DV / 16; ++i) o[g][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+
+    // One tile = 64 keys x CPR chunks = CPR wave-wide DMA instructions per
+    // operand; wave w issues instructions w, w + 4, ...  Lane L of instruction j
+    // fills LDS chunk 64 j + L = (row, slot) and fetches the global chunk that
+    // belongs there.  Keys past the end are clamped to the last key (finite
+    // data; their scores are masked).
+    auto issue = [&](int k0, int buf) {
+        for (int j = wave; j < LY::CPR; j += 4) {
+            const int c = 64 * j + lane;
+            const int row = c / LY::CPR, slot = c % LY::CPR;
+            const int chunk = LY::SWZ ? slot ^ ((row / LY::RPB) % LY::CPR) : slot;
+            const int key = min(k0 + row, Tk - 1);
+            const bf16* kr = seg_row<bf16>(a.k0, a.k1, a.Tk0, a.Tk1, a.ldk, b, key) + col0 + chunk * 8;
+            const bf16* vr = seg_row<bf16>(a.v0, a.v1, a.Tk0, a.Tk1, a.ldv, b, key) + col0 + chunk * 8;
+            dma16a(kr, &sK[buf][64 * j * 8]);
+            dma16a(vr, &sV[buf][64 * j * 8]);
+        }
+    };
+
+    const int ntiles = (Tk + kKTile - 1) / kKTile;
+    issue(0, 0);
+    for (int t = 0; t < ntiles; ++t) {
+        const int k0 = t * kKTile;
+        const int buf = t & 1;
+        __builtin_amdgcn_s_waitcnt((0 & 15) | (7 << 4) | (15 << 8));   // vmcnt(0): this wave's loads of tile t
+        __syncthreads();
+        if (t + 1 < ntiles) issue(k0 + kKTile, buf ^ 1);
+        const bf16* K = sK[buf];
+        const bf16* V = sV[buf];
+
+        f32x4 s[QG][4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+#pragma unroll
+            for (int g = 0; g < QG; ++g) s[g][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+            const int krow = 16 * j + ql;
+#pragma unroll
+            for (int c = 0; c < S::n32x; ++c) {
+                const bf16x8 kf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(K + LY::at(krow, 32 * c + grp * 8)));
+#pragma unroll
+                for (int g = 0; g < QG; ++g) s[g][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[g][c], s[g][j], 0, 0, 0);
+            }
+        }
+
+#pragma unroll
+        for (int g = 0; g < QG; ++g) {
+            float mloc = -INFINITY;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int key = k0 + 16 * j + 4 * grp + r;
+                    const float v = key < Tk ? s[g][j][r] * a.scale_log2 : -INFINITY;
+                    s[g][j][r] = v;
+                    mloc = fmaxf(mloc, v);
+                }
+            mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+            mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+            const float m_new = fmaxf(m_run[g], mloc);
+            const float alpha = exp2f(m_run[g] - m_new);
+            float lsum = 0.f;
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const float p = exp2f(s[g][j][r] - m_new);
+                    s[g][j][r] = p;
+                    lsum += p;
+                }
+            lsum += __shfl_xor(lsum, 16, 64);
+            lsum += __shfl_xor(lsum, 32, 64);
+            l_run[g] = l_run[g] * alpha + lsum;
+            m_run[g] = m_new;
+#pragma unroll
+            for (int i = 0; i < S::DV / 16; ++i) o[g][i] *= alpha;
+        }
+
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            bf16x8 pf[QG];
+#pragma unroll
+            for (int g = 0; g < QG; ++g)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    pf[g][r] = (bf16)s[g][2 * u][r];
+                    pf[g][4 + r] = (bf16)s[g][2 * u + 1][r];
+                }
+            const int kb0 = 32 * u + 4 * grp + (ql >> 2);      // this lane's source key, first half
+            const int dsub = 4 * (ql & 3);
+#pragma unroll
+            for (int i = 0; i < S::DV / 16; ++i) {
+                const int d0 = 16 * i + dsub;
+                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) s16x4*)(V + LY::at(kb0, d0)));
+                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) s16x4*)(V + LY::at(kb0 + 16, d0)));
+                const bf16x8 vf = __builtin_bit_cast(bf16x8, u32x4{__builtin_bit_cast(u32x2, lo).x, __builtin_bit_cast(u32x2, lo).y,
+                                                                  __builtin_bit_cast(u32x2, hi).x, __builtin_bit_cast(u32x2, hi).y});
+#pragma unroll
+                for (int g = 0; g < QG; ++g) o[g][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[g], o[g][i], 0, 0, 0);
+            }
+        }
+    }
+
+#pragma unroll
+    for (int g = 0; g < QG; ++g) {
+        if (myq[g] < Tq) {
+            const float inv = 1.f / l_run[g];
+            bf16* orow = const_cast<bf16*>(seg_row<bf16>(a.o0, a.o1, a.Tq0, a.Tq1, a.ldo, b, myq[g])) + col0;
+#pragma unroll
+            for (int i = 0; i < S::DV / 16; ++i)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int d = 16 * i + 4 * grp + r;
+                    if (d < HD) st(orow + d, o[g][i][r] * inv);
+                }
+        }
+    }
+}
+
+template <int QG>
+static int run_attention_dma(const AttnArgs& a, int hd, hipStream_t s) {
+    const int Tq = a.Tq0 + a.Tq1;
+    const int64_t nwg = (int64_t)((Tq + 64 * QG - 1) / (64 * QG)) * a.H * a.B;
+    if (nwg > 0x7fffffff) return fail(BC_ERR_UNSUPPORTED, "attention grid too large");
+    dim3 grid((unsigned)nwg), block(kAttnThreads);
+    switch (hd) {
+#define BC_ATT_CASE(HD) case HD: attention_dma_kernel<HD, QG><<<grid, block, 0, s>>>(a); break;
+        BC_ATT_CASE(32) BC_ATT_CASE(64) BC_ATT_CASE(72) BC_ATT_CASE(128)
+#undef BC_ATT_CASE
+        default: return fail(BC_ERR_UNSUPPORTED, "head_dim %d (supported: 32, 64, 72, 128)", hd);
+    }
+    return check_launch("attention");
+}
+
 template <typename T, int QG>
 static int run_attention(const AttnArgs& a, int hd, hipStream_t s) {
     const int Tq = a.Tq0 + a.Tq1;
@@ -328,7 +528,8 @@ int launch_attention(int dtype, AttnArgs a, hipStream_t s) {
     if (dtype == BC_F32 && a.d > 64) return fail(BC_ERR_UNSUPPORTED, "fp32 attention supports head_dim <= 64");
     a.scale_log2 = 1.4426950408889634f / sqrtf((float)a.d);
     prof_begin(PROF_ATTENTION, s);
-    const int rc = dtype == BC_BF16 ? run_attention<bf16, 2>(a, a.d, s) : run_attention<float, 1>(a, a.d, s);
+    // The direct-to-LDS kernel needs 16-byte aligned K/V rows (checked above).
+    const int rc = dtype == BC_BF16 ? run_attention_dma<2>(a, a.d, s) : run_attention<float, 1>(a, a.d, s);
     prof_end(PROF_ATTENTION, s);
     return rc;
 }

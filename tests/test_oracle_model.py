@@ -16,7 +16,6 @@ import torch.nn.functional as F
 import synth
 from oracle import bary, model as om, sampler as osm
 
-torch.set_default_dtype(torch.float64)
 
 
 def tiny(**kw):
