@@ -337,6 +337,197 @@ __device__ __forceinline__ void gemm_dma_body(GemmArgs g, const GemmSeg* sg) {
     epilogue<T, EPI, TM, TN>(g, acc, bm + wm * WM, bn + wn * WN, lane);
 }
 
+// ---------------------------------------------------------------------------
+// Wide-tile bf16 kernel for one-round grids.
+//
+// Same direct-to-LDS staging and swizzle as above, with three changes:
+//  * tiles need not be powers of two (e.g. 256 x 288 or 128 x 432, so that
+//    the DiT-XL/2 and PixArt block GEMMs split into exactly 256 tiles or a
+//    whole number of rounds over the 256 CUs); the (BM + BN) / 8 row octets
+//    of a k-step are dealt round-robin to the waves, which need not get equal
+//    counts (the pipeline waits count each wave's own loads);
+//  * a wave owns a 64 x 144 (or 64 x 128) block, halving the LDS bytes read
+//    per MFMA flop relative to 32 x 64;
+//  * the MFMA operands are swapped (W rows as the instruction's A), so lane l
+//    accumulates out[row][col..col+3] with row = l % 16 and
+//    col = 4 (l / 16): the epilogue reads and writes four consecutive
+//    columns per lane with one vector access.
+// Host-side conditions: K % 64 == 0; lda, ldw % 8 == 0; every epilogue
+// column index, stride and boundary (N, split, gelu_from, off2, ldo, ldo2,
+// ldr, ldg) a multiple of 4 and the epilogue pointers 16-byte aligned.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void st4(bf16* p, const float (&v)[4]) {
+    bf16x4 q;
+    q[0] = (bf16)v[0]; q[1] = (bf16)v[1]; q[2] = (bf16)v[2]; q[3] = (bf16)v[3];
+    *reinterpret_cast<bf16x4*>(p) = q;
+}
+__device__ __forceinline__ void st4(float* p, const float (&v)[4]) {
+    *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
+}
+
+template <int EPI, int TM, int TN>
+__device__ __forceinline__ void epilogue_t(const GemmArgs& g, const f32x4 (&acc)[TM][TN], int row0, int col0, int lane) {
+    const GemmEpi& e = g.e;
+    const bf16* __restrict__ bias = static_cast<const bf16*>(e.bias);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int col = col0 + j * 16 + 4 * (lane >> 4);
+        if (col >= g.N) continue;
+        float bv[4] = {0.f, 0.f, 0.f, 0.f};
+        if (bias) {
+            const bf16x4 b4 = *reinterpret_cast<const bf16x4*>(bias + col);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) bv[r] = (float)b4[r];
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const int row = row0 + i * 16 + (lane & 15);
+            if (row >= g.M) continue;
+            float v[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = acc[i][j][r] + bv[r];
+            if constexpr (EPI == BC_EPI_GATE_RES) {
+                const f32x4 rv = *reinterpret_cast<const f32x4*>(e.res + (int64_t)row * e.ldr + col);
+                f32x4 gv = f32x4{1.f, 1.f, 1.f, 1.f};
+                if (e.gate) gv = *reinterpret_cast<const f32x4*>(e.gate + (int64_t)(row / e.rows_per_gate) * e.ldg + col);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] = rv[r] + gv[r] * v[r];
+                const int b = row / e.seg, s = row - b * e.seg;
+                if (s < e.keep) {
+                    const int64_t o = (int64_t)(b * e.keep + s) * e.ldo + col;
+                    if (e.out_f32) st4(static_cast<float*>(e.out) + o, v);
+                    else st4(static_cast<bf16*>(e.out) + o, v);
+                }
+            } else {
+                if (col >= e.gelu_from) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) v[r] = gelu_tanh(v[r]);
+                }
+                if (col >= e.split) st4(static_cast<bf16*>(e.out2) + (int64_t)row * e.ldo2 + (col - e.split + e.off2), v);
+                else if (e.out_f32) st4(static_cast<float*>(e.out) + (int64_t)row * e.ldo + col, v);
+                else st4(static_cast<bf16*>(e.out) + (int64_t)row * e.ldo + col, v);
+            }
+        }
+    }
+}
+
+// LDS slot of 16-byte chunk c in row r for k-steps of BK = 64 (128-byte rows,
+// 8 chunks) or BK = 32 (64-byte rows, 4 chunks): the 16 rows read by one
+// fragment load fall on 16 distinct 16-byte bank groups.
+template <int BK> __device__ __forceinline__ int wslot(int c, int r) {
+    if constexpr (BK == 64) return c ^ ((r >> 1) & 7);
+    else return c ^ ((r >> 2) & 3);
+}
+
+template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int BK>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_wide_kernel(GemmArgs g) {
+    typedef bf16 T;
+    typedef Mma<bf16> MM;
+    constexpr int NW = WAVES_M * WAVES_N;
+    static_assert(BK == 64 || BK == 32, "k-step");
+    constexpr int CPR = BK / 8;                            // 16-byte chunks per LDS row
+    constexpr int RPI = 64 / CPR;                          // rows per wave-wide load
+    constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+    constexpr int TM = WM / 16, TN = WN / 16;
+    constexpr int NOCT = (BM + BN) / RPI;                  // wave-wide loads per k-step
+    constexpr int QMAX = (NOCT + NW - 1) / NW;             // octets per wave (at most)
+    static_assert(TM * 16 * WAVES_M == BM && TN * 16 * WAVES_N == BN && BM % 16 == 0 && BN % 16 == 0, "tile shape");
+    constexpr int STAGE = (BM + BN) * BK;                  // elements per stage: BM rows of A, then BN rows of W
+    __shared__ __attribute__((aligned(1024))) T sm[STAGES * STAGE];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+
+    const int tiles_m = (g.M + BM - 1) / BM;
+    const int tiles_n = (g.N + BN - 1) / BN;
+    const int nwg = gridDim.x;
+    int pid = blockIdx.x;
+    if ((nwg & 7) == 0) pid = (pid & 7) * (nwg >> 3) + (pid >> 3);
+    constexpr int GROUP_M = 8;
+    const int group = GROUP_M * tiles_n;
+    const int first_m = (pid / group) * GROUP_M;
+    const int gm = min(tiles_m - first_m, GROUP_M);
+    const int tm = first_m + (pid % group) % gm;
+    const int tn = (pid % group) / gm;
+    const int bm = tm * BM, bn = tn * BN;
+
+    // Load o = wave + NW q of a k-step fills rows RPI o .. RPI o + RPI - 1 of
+    // the stage (A rows first, then W rows); lane L loads row RPI o + L / CPR
+    // into slot L % CPR, fetching the global chunk that the swizzle puts there.
+    const T* src[QMAX];
+    const int lrow = lane / CPR, lslot = lane % CPR;
+#pragma unroll
+    for (int q = 0; q < QMAX; ++q) {
+        const int o = wave + NW * q;
+        const int r = RPI * o + lrow;
+        const T* p;
+        if (r < BM) p = static_cast<const T*>(g.A) + (int64_t)min(bm + r, g.M - 1) * g.lda;
+        else p = static_cast<const T*>(g.W) + (int64_t)min(bn + r - BM, g.N - 1) * g.ldw;
+        src[q] = p + wslot<BK>(lslot, r) * 8;
+    }
+    auto issue = [&](int kt, int buf) {
+        const int k0 = kt * BK;
+#pragma unroll
+        for (int q = 0; q < QMAX; ++q) {
+            const int o = wave + NW * q;
+            if (NOCT % NW == 0 || o < NOCT) dma16(src[q] + k0, &sm[buf * STAGE + o * RPI * BK]);
+        }
+    };
+
+    f32x4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int nk = g.K / BK;
+#pragma unroll
+    for (int p = 0; p < STAGES - 1; ++p)
+        if (p < nk) issue(p, p);
+    // Loads this wave issues per k-step (waves below NOCT % NW get one more).
+    const bool more = NOCT % NW == 0 || wave < NOCT % NW;
+    const int frow = lane & 15, grp = lane >> 4;
+    for (int kt = 0; kt < nk; ++kt) {
+        if (STAGES > 2 && kt + STAGES - 2 < nk) {
+            if (more) wait_vmcnt<(STAGES - 2) * QMAX>();
+            else wait_vmcnt<(STAGES - 2) * (QMAX - 1)>();
+        } else {
+            wait_vmcnt<0>();
+        }
+        __syncthreads();
+        if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+        const T* st = sm + (kt % STAGES) * STAGE;
+#pragma unroll
+        for (int kk = 0; kk < BK / 32; ++kk) {
+            const int c = kk * 4 + grp;
+            MM::frag af[TM], bfr[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int r = wm * WM + i * 16 + frow;
+                af[i] = MM::load(st + r * BK + wslot<BK>(c, r) * 8);
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int r = BM + wn * WN + j * 16 + frow;
+                bfr[j] = MM::load(st + r * BK + wslot<BK>(c, r) * 8);
+            }
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) acc[i][j] = MM::mma(bfr[j], af[i], acc[i][j]);
+        }
+    }
+
+    epilogue_t<EPI, TM, TN>(g, acc, bm + wm * WM, bn + wn * WN, lane);
+}
+
+template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES = 2, int BK = 64>
+static void launch_wide(const GemmArgs& g, hipStream_t s) {
+    const unsigned tiles = (unsigned)(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN));
+    gemm_wide_kernel<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, BK><<<dim3(tiles), dim3(64 * WAVES_M * WAVES_N), 0, s>>>(g);
+}
+
 template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int SW = 0>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_dma_kernel(GemmArgs g) {
     gemm_dma_body<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, false, SW>(g, nullptr);
@@ -359,22 +550,41 @@ static void launch_tile(const GemmArgs& g, hipStream_t s) {
     gemm_kernel<T, EPI, BM, BN, WAVES_M, WAVES_N><<<dim3(tiles), dim3(64 * WAVES_M * WAVES_N), 0, s>>>(g);
 }
 
+// The wide kernel's vector epilogue needs every column index and stride it
+// touches to be a multiple of 4 and its pointers 16-byte aligned.
+static bool wide_ok(const GemmArgs& g, int epi) {
+    const GemmEpi& e = g.e;
+    auto al = [](const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; };
+    if (g.K % 64 || g.lda % 8 || g.ldw % 8 || g.N % 4 || e.ldo % 4 || !al(e.out)) return false;
+    if (e.bias && reinterpret_cast<uintptr_t>(e.bias) % 8) return false;
+    if (epi == BC_EPI_GATE_RES) return e.ldr % 4 == 0 && al(e.res) && (!e.gate || (e.ldg % 4 == 0 && al(e.gate)));
+    if (e.gelu_from < g.N && e.gelu_from % 4) return false;
+    if (e.split < g.N && (e.split % 4 || e.off2 % 4 || e.ldo2 % 4 || !al(e.out2))) return false;
+    return true;
+}
+
 // Tile choice (measured on MI355X over the DiT-XL/2, PixArt and HunyuanVideo
 // block shapes, see the design notes): bf16 operands with whole 64-wide
-// k-steps take the direct-to-LDS kernel with two stages and 8 waves --
-// 256 x 256 tiles when K is long enough to amortise them and there is at least
-// one full round for the 256 CUs, else 128 x 128 (two workgroups per CU).
-// Other shapes, and fp32, take the register-staged kernel.
+// k-steps take the wide kernel -- 256 x 288 tiles (8 waves of 64 x 144) when
+// they make at least one full round over the 256 CUs, else 128 x 128 (8 waves
+// of 32 x 64, two workgroups per CU).  Operands the wide epilogue cannot
+// vectorise take the direct-to-LDS kernel with the scalar epilogue; other
+// shapes, and fp32, the register-staged kernel.
 template <typename T, int EPI>
 static int run_gemm(const GemmArgs& g, hipStream_t s) {
     const int64_t tiles128 = (int64_t)((g.M + 127) / 128) * ((g.N + 127) / 128);
     if (tiles128 > 0x7fffffff) return fail(BC_ERR_UNSUPPORTED, "GEMM grid too large");
     if constexpr (sizeof(T) == 2) {
-        const int64_t tiles256 = (int64_t)((g.M + 255) / 256) * ((g.N + 255) / 256);
+        const int64_t tiles288 = (int64_t)((g.M + 255) / 256) * ((g.N + 287) / 288);
         const bool dma = g.K % 64 == 0 && g.lda % 8 == 0 && g.ldw % 8 == 0;
-        if (dma && g.K >= 2048 && tiles256 >= 256) launch_dma<EPI, 256, 256, 4, 2, 2>(g, s);
-        else if (dma) launch_dma<EPI, 128, 128, 4, 2, 2>(g, s);
-        else launch_tile<T, EPI, 128, 128, 4, 2>(g, s);
+        if (dma && wide_ok(g, EPI)) {
+            if (tiles288 >= 256) launch_wide<EPI, 256, 288, 4, 2>(g, s);
+            else launch_wide<EPI, 128, 128, 4, 2>(g, s);
+        } else if (dma) {
+            launch_dma<EPI, 128, 128, 4, 2, 2>(g, s);
+        } else {
+            launch_tile<T, EPI, 128, 128, 4, 2>(g, s);
+        }
     } else {
         launch_tile<T, EPI, 128, 128, 2, 2>(g, s);
     }
