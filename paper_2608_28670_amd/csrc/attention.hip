@@ -314,14 +314,36 @@ template <int HD> struct KvLayout {
     __device__ static int at(int row, int d) { return row * HD + slot(row, d >> 3) * 8 + (d & 7); }
 };
 
-template <int HD, int QG>
-__global__ __launch_bounds__(kAttnThreads) void attention_dma_kernel(AttnArgs a) {
+// NWV waves of 16 QG queries each per workgroup; NB K/V tile buffers.  When
+// all key tiles fit in the NB buffers they are loaded once, up front, and the
+// key loop runs without further barriers; otherwise two of the buffers are
+// used as a double buffer.
+// Reductions over the four lanes l, l ^ 16, l ^ 32, l ^ 48 that hold one
+// query's scores: with both operands equal, v_permlane16_swap returns the
+// value of lane l in one result and of lane l ^ 16 in the other (likewise
+// v_permlane32_swap for l ^ 32), so no LDS round trip is needed.
+__device__ __forceinline__ float group_max(float v) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float group_sum(float v) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+template <int HD, int QG, int NWV, int NB>
+__global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
     typedef AttnShape<bf16, HD> S;
     typedef KvLayout<HD> LY;
-    constexpr int QT = 64 * QG;
+    constexpr int QT = 16 * QG * NWV;
+    static_assert(NB >= 2, "buffers");
     constexpr int TILE = kKTile * HD + 32;     // elements per K or V tile (+ slack for d >= HD operand reads)
-    __shared__ __attribute__((aligned(1024))) bf16 sK[2][TILE];
-    __shared__ __attribute__((aligned(1024))) bf16 sV[2][TILE];
+    __shared__ __attribute__((aligned(1024))) bf16 sK[NB][TILE];
+    __shared__ __attribute__((aligned(1024))) bf16 sV[NB][TILE];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -339,8 +361,37 @@ __global__ __launch_bounds__(kAttnThreads) void attention_dma_kernel(AttnArgs a)
     // The slack past the last row is read (for d >= HD operand rows, whose
     // outputs are discarded) but never loaded: keep it finite.
     if (tid < 32) {
-        sK[0][kKTile * HD + tid] = (bf16)0.f; sK[1][kKTile * HD + tid] = (bf16)0.f;
-        sV[0][kKTile * HD + tid] = (bf16)0.f; sV[1][kKTile * HD + tid] = (bf16)0.f;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            sK[nb][kKTile * HD + tid] = (bf16)0.f;
+            sV[nb][kKTile * HD + tid] = (bf16)0.f;
+        }
+    }
+
+    // One tile = 64 keys x CPR chunks = CPR wave-wide DMA instructions per
+    // operand; wave w issues instructions w, w + 4, ...  Lane L of instruction j
+    // fills LDS chunk 64 j + L = (row, slot) and fetches the global chunk that
+    // belongs there.  Keys past the end are clamped to the last key (finite
+    // data; their scores are masked).
+    auto issue = [&](int k0, int buf) {
+        for (int j = wave; j < LY::CPR; j += NWV) {
+            const int c = 64 * j + lane;
+            const int row = c / LY::CPR, slot = c % LY::CPR;
+            const int chunk = LY::SWZ ? slot ^ ((row / LY::RPB) % LY::CPR) : slot;
+            const int key = min(k0 + row, Tk - 1);
+            const bf16* kr = seg_row<bf16>(a.k0, a.k1, a.Tk0, a.Tk1, a.ldk, b, key) + col0 + chunk * 8;
+            const bf16* vr = seg_row<bf16>(a.v0, a.v1, a.Tk0, a.Tk1, a.ldv, b, key) + col0 + chunk * 8;
+            dma16a(kr, &sK[buf][64 * j * 8]);
+            dma16a(vr, &sV[buf][64 * j * 8]);
+        }
+    };
+    const int ntiles = (Tk + kKTile - 1) / kKTile;
+    const bool resident = ntiles <= NB;
+    // K/V loads go out first so that their latency overlaps the Q loads.
+    if (resident) {
+        for (int t = 0; t < ntiles; ++t) issue(t * kKTile, t);
+    } else {
+        issue(0, 0);
     }
 
     bf16x8 qf[QG][S::n32x > 0 ? S::n32x : 1];
@@ -350,12 +401,11 @@ __global__ __launch_bounds__(kAttnThreads) void attention_dma_kernel(AttnArgs a)
         myq[g] = qt * QT + wave * 16 * QG + 16 * g + ql;
         const bf16* qrow = myq[g] < Tq ? seg_row<bf16>(a.q0, a.q1, a.Tq0, a.Tq1, a.ldq, b, myq[g]) + col0 : nullptr;
 #pragma unroll
-        for (int c = 0; c < S::n32x; ++c)
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const int d = 32 * c + grp * 8 + i;
-                qf[g][c][i] = (qrow && d < HD) ? qrow[d] : (bf16)0.f;
-            }
+        for (int c = 0; c < S::n32x; ++c) {
+            const int d = 32 * c + grp * 8;       // HD % 8 == 0: a chunk is wholly in or out
+            qf[g][c] = (qrow && d < HD) ? __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qrow + d))
+                                        : __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+        }
     }
 
     f32x4 o[QG][S::DV / 16];
@@ -368,34 +418,9 @@ __global__ __launch_bounds__(kAttnThreads) void attention_dma_kernel(AttnArgs a)
         for (int i = 0; i < S::DV / 16; ++i) o[g][i] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
 
-    // One tile = 64 keys x CPR chunks = CPR wave-wide DMA instructions per
-    // operand; wave w issues instructions w, w + 4, ...  Lane L of instruction j
-    // fills LDS chunk 64 j + L = (row, slot) and fetches the global chunk that
-    // belongs there.  Keys past the end are clamped to the last key (finite
-    // data; their scores are masked).
-    auto issue = [&](int k0, int buf) {
-        for (int j = wave; j < LY::CPR; j += 4) {
-            const int c = 64 * j + lane;
-            const int row = c / LY::CPR, slot = c % LY::CPR;
-            const int chunk = LY::SWZ ? slot ^ ((row / LY::RPB) % LY::CPR) : slot;
-            const int key = min(k0 + row, Tk - 1);
-            const bf16* kr = seg_row<bf16>(a.k0, a.k1, a.Tk0, a.Tk1, a.ldk, b, key) + col0 + chunk * 8;
-            const bf16* vr = seg_row<bf16>(a.v0, a.v1, a.Tk0, a.Tk1, a.ldv, b, key) + col0 + chunk * 8;
-            dma16a(kr, &sK[buf][64 * j * 8]);
-            dma16a(vr, &sV[buf][64 * j * 8]);
-        }
-    };
 
-    const int ntiles = (Tk + kKTile - 1) / kKTile;
-    issue(0, 0);
-    for (int t = 0; t < ntiles; ++t) {
-        const int k0 = t * kKTile;
-        const int buf = t & 1;
-        __builtin_amdgcn_s_waitcnt((0 & 15) | (7 << 4) | (15 << 8));   // vmcnt(0): this wave's loads of tile t
-        __syncthreads();
-        if (t + 1 < ntiles) issue(k0 + kKTile, buf ^ 1);
-        const bf16* K = sK[buf];
-        const bf16* V = sV[buf];
+    // Scores, online softmax and the P V update of one 64-key tile at k0.
+    auto tile = [&](int k0, const bf16* K, const bf16* V) {
 
         f32x4 s[QG][4];
 #pragma unroll
@@ -423,22 +448,19 @@ __global__ __launch_bounds__(kAttnThreads) void attention_dma_kernel(AttnArgs a)
                     s[g][j][r] = v;
                     mloc = fmaxf(mloc, v);
                 }
-            mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-            mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+            mloc = group_max(mloc);
             const float m_new = fmaxf(m_run[g], mloc);
-            const float alpha = exp2f(m_run[g] - m_new);
+            const float alpha = __builtin_amdgcn_exp2f(m_run[g] - m_new);
             float lsum = 0.f;
 #pragma unroll
             for (int j = 0; j < 4; ++j)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const float p = exp2f(s[g][j][r] - m_new);
+                    const float p = __builtin_amdgcn_exp2f(s[g][j][r] - m_new);
                     s[g][j][r] = p;
                     lsum += p;
                 }
-            lsum += __shfl_xor(lsum, 16, 64);
-            lsum += __shfl_xor(lsum, 32, 64);
-            l_run[g] = l_run[g] * alpha + lsum;
+            l_run[g] = l_run[g] * alpha + lsum;   // this lane's keys only; summed over the group at the end
             m_run[g] = m_new;
 #pragma unroll
             for (int i = 0; i < S::DV / 16; ++i) o[g][i] *= alpha;
@@ -469,12 +491,26 @@ __global__ __launch_bounds__(kAttnThreads) void attention_dma_kernel(AttnArgs a)
                 for (int g = 0; g < QG; ++g) o[g][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[g], o[g][i], 0, 0, 0);
             }
         }
+    };
+
+    if (resident) {
+        __builtin_amdgcn_s_waitcnt((0 & 15) | (7 << 4) | (15 << 8));   // vmcnt(0): this wave's loads
+        __syncthreads();
+        for (int t = 0; t < ntiles; ++t) tile(t * kKTile, sK[t], sV[t]);
+    } else {
+        for (int t = 0; t < ntiles; ++t) {
+            const int buf = t & 1;
+            __builtin_amdgcn_s_waitcnt((0 & 15) | (7 << 4) | (15 << 8));   // vmcnt(0): this wave's loads of tile t
+            __syncthreads();
+            if (t + 1 < ntiles) issue((t + 1) * kKTile, buf ^ 1);
+            tile(t * kKTile, sK[buf], sV[buf]);
+        }
     }
 
 #pragma unroll
     for (int g = 0; g < QG; ++g) {
+        const float inv = 1.f / group_sum(l_run[g]);   // all lanes take part in the exchange
         if (myq[g] < Tq) {
-            const float inv = 1.f / l_run[g];
             bf16* orow = const_cast<bf16*>(seg_row<bf16>(a.o0, a.o1, a.Tq0, a.Tq1, a.ldo, b, myq[g])) + col0;
 #pragma unroll
             for (int i = 0; i < S::DV / 16; ++i)
@@ -487,14 +523,14 @@ __global__ __launch_bounds__(kAttnThreads) void attention_dma_kernel(AttnArgs a)
     }
 }
 
-template <int QG>
+template <int QG, int NWV, int NB>
 static int run_attention_dma(const AttnArgs& a, int hd, hipStream_t s) {
     const int Tq = a.Tq0 + a.Tq1;
-    const int64_t nwg = (int64_t)((Tq + 64 * QG - 1) / (64 * QG)) * a.H * a.B;
+    const int64_t nwg = (int64_t)((Tq + 16 * QG * NWV - 1) / (16 * QG * NWV)) * a.H * a.B;
     if (nwg > 0x7fffffff) return fail(BC_ERR_UNSUPPORTED, "attention grid too large");
-    dim3 grid((unsigned)nwg), block(kAttnThreads);
+    dim3 grid((unsigned)nwg), block(64 * NWV);
     switch (hd) {
-#define BC_ATT_CASE(HD) case HD: attention_dma_kernel<HD, QG><<<grid, block, 0, s>>>(a); break;
+#define BC_ATT_CASE(HD) case HD: attention_dma_kernel<HD, QG, NWV, NB><<<grid, block, 0, s>>>(a); break;
         BC_ATT_CASE(32) BC_ATT_CASE(64) BC_ATT_CASE(72) BC_ATT_CASE(128)
 #undef BC_ATT_CASE
         default: return fail(BC_ERR_UNSUPPORTED, "head_dim %d (supported: 32, 64, 72, 128)", hd);
@@ -523,13 +559,25 @@ int launch_attention(int dtype, AttnArgs a, hipStream_t s) {
     if (a.B <= 0 || a.H <= 0 || a.Tq0 + a.Tq1 <= 0) return BC_OK;
     if (a.Tk0 + a.Tk1 <= 0) return fail(BC_ERR_INVALID_ARG, "attention over zero keys");
     if (!attention_supported(a.d)) return fail(BC_ERR_UNSUPPORTED, "head_dim %d (supported: 32, 64, 72, 128)", a.d);
-    if ((a.ldk | a.ldv) % 8 || (reinterpret_cast<uintptr_t>(a.k0) | reinterpret_cast<uintptr_t>(a.v0)) % 16)
-        return fail(BC_ERR_UNSUPPORTED, "attention K/V rows must be 16-byte aligned");
+    const uintptr_t kv = reinterpret_cast<uintptr_t>(a.k0) | reinterpret_cast<uintptr_t>(a.v0) |
+                         reinterpret_cast<uintptr_t>(a.k1) | reinterpret_cast<uintptr_t>(a.v1);
+    const uintptr_t qa = reinterpret_cast<uintptr_t>(a.q0) | reinterpret_cast<uintptr_t>(a.q1);
+    if ((a.ldk | a.ldv) % 8 || kv % 16 || (dtype == BC_BF16 && (a.ldq % 8 || qa % 16)))
+        return fail(BC_ERR_UNSUPPORTED, "attention rows must be 16-byte aligned");
     if (dtype == BC_F32 && a.d > 64) return fail(BC_ERR_UNSUPPORTED, "fp32 attention supports head_dim <= 64");
     a.scale_log2 = 1.4426950408889634f / sqrtf((float)a.d);
     prof_begin(PROF_ATTENTION, s);
-    // The direct-to-LDS kernel needs 16-byte aligned K/V rows (checked above).
-    const int rc = dtype == BC_BF16 ? run_attention_dma<2>(a, a.d, s) : run_attention<float, 1>(a, a.d, s);
+    // The direct-to-LDS kernel needs 16-byte aligned Q/K/V rows (checked above).
+    // Up to 256 keys: 8 waves of 16 queries with every key tile resident in
+    // LDS (one load, no barriers in the key loop); longer sequences: 8 waves
+    // of 32 queries over a double buffer.
+    int rc;
+    if (dtype == BC_BF16) {
+        const int Tk = a.Tk0 + a.Tk1;
+        rc = Tk <= 4 * kKTile ? run_attention_dma<1, 8, 4>(a, a.d, s) : run_attention_dma<2, 8, 2>(a, a.d, s);
+    } else {
+        rc = run_attention<float, 1>(a, a.d, s);
+    }
     prof_end(PROF_ATTENTION, s);
     return rc;
 }
