@@ -16,6 +16,17 @@
 
 namespace bc {
 
+// GELU, tanh form: 0.5 x (1 + tanh(y)), y = sqrt(2/pi) (x + 0.044715 x^3).
+// Since 0.5 (1 + tanh(y)) = 1 / (1 + exp(-2 y)), this is x / (1 + 2^z) with
+// z = -2 log2(e) y = x (A + B x^2): one native exp2 and one reciprocal per
+// element (2^z overflows to +inf for very negative x, giving 0 as it should).
+__device__ __forceinline__ float gelu_tanh(float x) {
+    constexpr float A = -2.0f * 0.7978845608028654f * 1.4426950408889634f;
+    constexpr float B = A * 0.044715f;
+    const float z = x * __builtin_fmaf(B, x * x, A);
+    return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(z));
+}
+
 template <typename T> struct Mma;
 template <> struct Mma<bf16> {
     static constexpr int E = 8;    // operand elements per lane
@@ -365,20 +376,72 @@ __device__ __forceinline__ void st4(float* p, const float (&v)[4]) {
     *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
 }
 
+// jn: number of the TN column blocks this wave holds (the rest are unused).
+// bf16 outputs of the plain epilogue are written 16 bytes per lane: for a pair
+// of row blocks (i, i + 1), lanes of an even 16-lane group (columns c..c+3)
+// and of the odd group next to it (c+4..c+7) swap halves with
+// v_permlane16_swap, so the even lane stores row r_i and the odd lane row
+// r_{i+1}, each as 8 consecutive columns.
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+    bf16x2 q;
+    q[0] = (bf16)a; q[1] = (bf16)b;
+    return __builtin_bit_cast(uint32_t, q);
+}
+
 template <int EPI, int TM, int TN>
-__device__ __forceinline__ void epilogue_t(const GemmArgs& g, const f32x4 (&acc)[TM][TN], int row0, int col0, int lane) {
+__device__ __forceinline__ void epilogue_t(const GemmArgs& g, const f32x4 (&acc)[TM][TN], int row0, int col0, int lane,
+                                           int jn = TN) {
     const GemmEpi& e = g.e;
     const bf16* __restrict__ bias = static_cast<const bf16*>(e.bias);
+    const bool odd = (lane >> 4) & 1;
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
+        if (j >= jn) break;
         const int col = col0 + j * 16 + 4 * (lane >> 4);
-        if (col >= g.N) continue;
+        const bool col_ok = col < g.N;
         float bv[4] = {0.f, 0.f, 0.f, 0.f};
-        if (bias) {
+        if (bias && col_ok) {
             const bf16x4 b4 = *reinterpret_cast<const bf16x4*>(bias + col);
 #pragma unroll
             for (int r = 0; r < 4; ++r) bv[r] = (float)b4[r];
         }
+        if constexpr (EPI != BC_EPI_GATE_RES && TM % 2 == 0) {
+            if (!e.out_f32) {
+                // Pairs of row blocks, 16-byte stores (see above).  Both lanes of
+                // a pair see the same split/gelu decision: the pair's 8 columns
+                // start at a multiple of 8 and those boundaries are multiples of 8
+                // here (checked on the host).
+                const int cpair = col - (odd ? 4 : 0);
+                const bool act = cpair >= e.gelu_from;
+#pragma unroll
+                for (int i = 0; i < TM; i += 2) {
+                    uint32_t w[2][2];
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        float v[4];
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            v[r] = acc[i + h][j][r] + bv[r];
+                            if (act) v[r] = gelu_tanh(v[r]);
+                        }
+                        w[h][0] = pack_bf16x2(v[0], v[1]);
+                        w[h][1] = pack_bf16x2(v[2], v[3]);
+                    }
+                    const auto x0 = __builtin_amdgcn_permlane16_swap(w[0][0], w[1][0], false, false);
+                    const auto x1 = __builtin_amdgcn_permlane16_swap(w[0][1], w[1][1], false, false);
+                    const u32x4 q = u32x4{x0[0], x1[0], x0[1], x1[1]};
+                    const int row = row0 + (i + (odd ? 1 : 0)) * 16 + (lane & 15);
+                    if (row < g.M && cpair < g.N) {
+                        bf16* dst = cpair >= e.split ? static_cast<bf16*>(e.out2) + (int64_t)row * e.ldo2 + (cpair - e.split + e.off2)
+                                                     : static_cast<bf16*>(e.out) + (int64_t)row * e.ldo + cpair;
+                        *reinterpret_cast<u32x4*>(dst) = q;
+                    }
+                }
+                continue;
+            }
+        }
+        if (!col_ok) continue;
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
             const int row = row0 + i * 16 + (lane & 15);
@@ -427,17 +490,21 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_wide_kernel(GemmA
     static_assert(BK == 64 || BK == 32, "k-step");
     constexpr int CPR = BK / 8;                            // 16-byte chunks per LDS row
     constexpr int RPI = 64 / CPR;                          // rows per wave-wide load
-    constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
-    constexpr int TM = WM / 16, TN = WN / 16;
+    constexpr int WM = BM / WAVES_M, TM = WM / 16;
+    // The BN / 16 column blocks are dealt to the WAVES_N wave columns as
+    // evenly as possible (144 = 80 + 64 for two): TN is the larger share.
+    constexpr int NBLK = BN / 16, TN = (NBLK + WAVES_N - 1) / WAVES_N, NREM = NBLK % WAVES_N;
     constexpr int NOCT = (BM + BN) / RPI;                  // wave-wide loads per k-step
     constexpr int QMAX = (NOCT + NW - 1) / NW;             // octets per wave (at most)
-    static_assert(TM * 16 * WAVES_M == BM && TN * 16 * WAVES_N == BN && BM % 16 == 0 && BN % 16 == 0, "tile shape");
+    static_assert(TM * 16 * WAVES_M == BM && BM % 16 == 0 && BN % 16 == 0, "tile shape");
     constexpr int STAGE = (BM + BN) * BK;                  // elements per stage: BM rows of A, then BN rows of W
     __shared__ __attribute__((aligned(1024))) T sm[STAGES * STAGE];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int jn = NREM == 0 ? TN : NBLK / WAVES_N + (wn < NREM ? 1 : 0);    // this wave's column blocks
+    const int j0 = NREM == 0 ? wn * TN : wn * (NBLK / WAVES_N) + min(wn, NREM);
 
     const int tiles_m = (g.M + BM - 1) / BM;
     const int tiles_n = (g.N + BN - 1) / BN;
@@ -509,17 +576,155 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_wide_kernel(GemmA
             }
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
-                const int r = BM + wn * WN + j * 16 + frow;
+                if (NREM != 0 && j >= jn) break;
+                const int r = BM + (j0 + j) * 16 + frow;
                 bfr[j] = MM::load(st + r * BK + wslot<BK>(c, r) * 8);
             }
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int j = 0; j < TN; ++j) acc[i][j] = MM::mma(bfr[j], af[i], acc[i][j]);
+                for (int j = 0; j < TN; ++j)
+                    if (NREM == 0 || j < jn) acc[i][j] = MM::mma(bfr[j], af[i], acc[i][j]);
         }
     }
 
-    epilogue_t<EPI, TM, TN>(g, acc, bm + wm * WM, bn + wn * WN, lane);
+    epilogue_t<EPI, TM, TN>(g, acc, bm + wm * WM, bn + j0 * 16, lane, jn);
+}
+
+// ---------------------------------------------------------------------------
+// Split-K inside the workgroup, for outputs too small to give every CU a
+// wide tile (the N = 1152 projections of DiT-XL/2 at M = 4096 make 256 tiles
+// of 128 x 144).  KG groups of WAVES_M waves share the workgroup's tile: a
+// stage holds KG * 32 k-columns, group kg owning the 32-column slice kg of
+// every stage (its own A and W block in 64-byte LDS rows), so each wave keeps
+// a full (BM / WAVES_M) x BN accumulator over a quarter of K.  After the main
+// loop the groups' partial tiles are summed pairwise through LDS (a tree over
+// the KG groups) and group 0 applies the epilogue.
+// ---------------------------------------------------------------------------
+template <int EPI, int BM, int BN, int WAVES_M, int KG>
+__global__ __launch_bounds__(64 * WAVES_M * KG) void gemm_ksplit_kernel(GemmArgs g) {
+    typedef bf16 T;
+    typedef Mma<bf16> MM;
+    constexpr int NW = WAVES_M * KG;
+    constexpr int GK = 32;                                 // k-columns per group per stage
+    constexpr int BK = GK * KG;                            // k-columns per stage
+    constexpr int WM = BM / WAVES_M, TM = WM / 16, TN = BN / 16;
+    constexpr int ROWS = BM + BN;                          // rows of a group block: A, then W
+    constexpr int RB = ROWS / 16;                          // 16-row loads per group block
+    constexpr int GBLK = ROWS * GK;                        // elements per group block
+    constexpr int STAGE = GBLK * KG;
+    constexpr int NLD = RB * KG;                           // wave-wide loads per stage
+    constexpr int QMAX = (NLD + NW - 1) / NW;
+    constexpr int PART = WAVES_M * TM * TN * 64 * 4;       // floats in one group's partial tile
+    constexpr int STAGE_BYTES = 2 * STAGE * 2;
+    constexpr int RED_BYTES = (KG / 2) * PART * 4;
+    constexpr int SMEM = STAGE_BYTES > RED_BYTES ? STAGE_BYTES : RED_BYTES;
+    static_assert(TM * 16 * WAVES_M == BM && TN * 16 == BN && ROWS % 16 == 0, "tile shape");
+    static_assert(KG == 1 || KG == 2 || KG == 4, "K groups");
+    __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+    T* const sm = reinterpret_cast<T*>(smem);
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave % WAVES_M, kg = wave / WAVES_M;
+
+    const int tiles_m = (g.M + BM - 1) / BM;
+    const int tiles_n = (g.N + BN - 1) / BN;
+    const int nwg = gridDim.x;
+    int pid = blockIdx.x;
+    if ((nwg & 7) == 0) pid = (pid & 7) * (nwg >> 3) + (pid >> 3);
+    constexpr int GROUP_M = 8;
+    const int group = GROUP_M * tiles_n;
+    const int first_m = (pid / group) * GROUP_M;
+    const int gm = min(tiles_m - first_m, GROUP_M);
+    const int tm = first_m + (pid % group) % gm;
+    const int tn = (pid % group) / gm;
+    const int bm = tm * BM, bn = tn * BN;
+
+    // Load o = wave + NW q of a stage: rows 16 (o % RB) .. +15 of group block
+    // o / RB; lane L loads row 16 (o % RB) + L / 4 into slot L % 4.
+    const T* src[QMAX];
+    int dst[QMAX];
+#pragma unroll
+    for (int q = 0; q < QMAX; ++q) {
+        const int o = min(wave + NW * q, NLD - 1);
+        const int go = o / RB, r = 16 * (o % RB) + lane / 4;
+        const T* p;
+        if (r < BM) p = static_cast<const T*>(g.A) + (int64_t)min(bm + r, g.M - 1) * g.lda;
+        else p = static_cast<const T*>(g.W) + (int64_t)min(bn + r - BM, g.N - 1) * g.ldw;
+        src[q] = p + go * GK + wslot<32>(lane % 4, r) * 8;
+        dst[q] = go * GBLK + 16 * (o % RB) * GK;
+    }
+    auto issue = [&](int kt, int buf) {
+        const int k0 = kt * BK;
+#pragma unroll
+        for (int q = 0; q < QMAX; ++q) {
+            const int o = wave + NW * q;
+            if (NLD % NW == 0 || o < NLD) dma16(src[q] + k0, &sm[buf * STAGE + dst[q]]);
+        }
+    };
+
+    f32x4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int nk = g.K / BK;
+    issue(0, 0);
+    const int frow = lane & 15, grp = lane >> 4;
+    for (int kt = 0; kt < nk; ++kt) {
+        wait_vmcnt<0>();
+        __syncthreads();
+        if (kt + 1 < nk) issue(kt + 1, (kt + 1) & 1);
+        const T* st = sm + (kt & 1) * STAGE + kg * GBLK;
+        MM::frag af[TM], bfr[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const int r = wm * WM + i * 16 + frow;
+            af[i] = MM::load(st + r * GK + wslot<32>(grp, r) * 8);
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int r = BM + j * 16 + frow;
+            bfr[j] = MM::load(st + r * GK + wslot<32>(grp, r) * 8);
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[i][j] = MM::mma(bfr[j], af[i], acc[i][j]);
+    }
+
+    // Tree reduction of the KG partial tiles: at each level the upper half of
+    // the remaining groups stores, the lower half adds.  A wave's part sits at
+    // [wm][i][j][lane] so the same wave index of every group lines up.
+    float* const red = reinterpret_cast<float*>(smem);
+#pragma unroll
+    for (int half = KG / 2; half >= 1; half /= 2) {
+        __syncthreads();
+        if (kg >= half && kg < 2 * half) {
+            f32x4* r = reinterpret_cast<f32x4*>(red + (kg - half) * PART) + wm * TM * TN * 64 + lane;
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) r[(i * TN + j) * 64] = acc[i][j];
+        }
+        __syncthreads();
+        if (kg < half) {
+            const f32x4* r = reinterpret_cast<const f32x4*>(red + kg * PART) + wm * TM * TN * 64 + lane;
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) acc[i][j] += r[(i * TN + j) * 64];
+        }
+    }
+    if (kg == 0) epilogue_t<EPI, TM, TN>(g, acc, bm + wm * WM, bn, lane);
+}
+
+template <int EPI, int BM, int BN, int WAVES_M, int KG>
+static void launch_ksplit(const GemmArgs& g, hipStream_t s) {
+    const unsigned tiles = (unsigned)(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN));
+    gemm_ksplit_kernel<EPI, BM, BN, WAVES_M, KG><<<dim3(tiles), dim3(64 * WAVES_M * KG), 0, s>>>(g);
 }
 
 template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES = 2, int BK = 64>
@@ -558,28 +763,42 @@ static bool wide_ok(const GemmArgs& g, int epi) {
     if (g.K % 64 || g.lda % 8 || g.ldw % 8 || g.N % 4 || e.ldo % 4 || !al(e.out)) return false;
     if (e.bias && reinterpret_cast<uintptr_t>(e.bias) % 8) return false;
     if (epi == BC_EPI_GATE_RES) return e.ldr % 4 == 0 && al(e.res) && (!e.gate || (e.ldg % 4 == 0 && al(e.gate)));
-    if (e.gelu_from < g.N && e.gelu_from % 4) return false;
-    if (e.split < g.N && (e.split % 4 || e.off2 % 4 || e.ldo2 % 4 || !al(e.out2))) return false;
+    // The plain epilogue pairs lanes into 8-column groups: N, the split and
+    // GELU boundaries and the bf16 row strides and offsets are multiples of 8.
+    if (g.N % 8 || e.ldo % 8) return false;
+    if (e.gelu_from < g.N && e.gelu_from % 8) return false;
+    if (e.split < g.N && (e.split % 8 || e.off2 % 8 || e.ldo2 % 8 || !al(e.out2))) return false;
     return true;
 }
 
 // Tile choice (measured on MI355X over the DiT-XL/2, PixArt and HunyuanVideo
-// block shapes, see the design notes): bf16 operands with whole 64-wide
-// k-steps take the wide kernel -- 256 x 288 tiles (8 waves of 64 x 144) when
-// they make at least one full round over the 256 CUs, else 128 x 128 (8 waves
-// of 32 x 64, two workgroups per CU).  Operands the wide epilogue cannot
-// vectorise take the direct-to-LDS kernel with the scalar epilogue; other
-// shapes, and fp32, the register-staged kernel.
+// block shapes, see the design notes), for bf16 operands with whole 64-wide
+// k-steps and an epilogue the wide kernel can vectorise:
+//   * at least one full round of 256 x 288 tiles over the 256 CUs: 256 x 288
+//     (8 waves of 64 x 144), or 256 x 256 when N is a multiple of 256 but not
+//     of 288 (no ragged column tile);
+//   * at most 256 tiles of 128 x 144 (the N = 1152 projections at M = 4096):
+//     128 x 144, 2 x 4 waves of 64 x 48 / 64 x 32;
+//   * otherwise 128 x 128 (8 waves of 32 x 64, two workgroups per CU).
+// Other bf16 operands take the direct-to-LDS kernel with the scalar
+// epilogue, or the register-staged kernel; fp32 the register-staged kernel.
 template <typename T, int EPI>
 static int run_gemm(const GemmArgs& g, hipStream_t s) {
     const int64_t tiles128 = (int64_t)((g.M + 127) / 128) * ((g.N + 127) / 128);
     if (tiles128 > 0x7fffffff) return fail(BC_ERR_UNSUPPORTED, "GEMM grid too large");
     if constexpr (sizeof(T) == 2) {
         const int64_t tiles288 = (int64_t)((g.M + 255) / 256) * ((g.N + 287) / 288);
+        const int64_t tiles144 = (int64_t)((g.M + 127) / 128) * ((g.N + 143) / 144);
         const bool dma = g.K % 64 == 0 && g.lda % 8 == 0 && g.ldw % 8 == 0;
         if (dma && wide_ok(g, EPI)) {
-            if (tiles288 >= 256) launch_wide<EPI, 256, 288, 4, 2>(g, s);
-            else launch_wide<EPI, 128, 128, 4, 2>(g, s);
+            if (tiles288 >= 256) {
+                if (g.N % 288 != 0 && g.N % 256 == 0) launch_wide<EPI, 256, 256, 4, 2>(g, s);
+                else launch_wide<EPI, 256, 288, 4, 2>(g, s);
+            } else if (tiles144 <= 256) {
+                launch_wide<EPI, 128, 144, 2, 4>(g, s);
+            } else {
+                launch_wide<EPI, 128, 128, 4, 2>(g, s);
+            }
         } else if (dma) {
             launch_dma<EPI, 128, 128, 4, 2, 2>(g, s);
         } else {

@@ -39,13 +39,6 @@ template <typename T> struct ElemsPer16B { static constexpr int v = 16 / (int)si
 
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + __expf(-x)); }
 
-// GELU with the tanh approximation, using tanh(y) = 1 - 2 / (1 + e^{2y}).
-__device__ __forceinline__ float gelu_tanh(float x) {
-    const float y = 0.7978845608028654f * (x + 0.044715f * x * x * x);
-    const float t = 1.0f - 2.0f / (1.0f + __expf(2.0f * y));
-    return 0.5f * x * (1.0f + t);
-}
-
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

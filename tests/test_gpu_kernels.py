@@ -28,7 +28,7 @@ def _dev(a, dt):
 
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
 @pytest.mark.parametrize("M,N,K", [(300, 200, 136), (128, 128, 64), (1, 16, 8), (517, 384, 1152),
-                                   (4096, 1152, 1152), (4100, 4612, 1152), (130, 260, 192)])
+                                   (4096, 1152, 1152), (4100, 4612, 1152), (130, 260, 192), (1000, 1160, 256)])
 @pytest.mark.parametrize("epi", ["bias", "gelu", "gate"])
 def test_linear(bclib, dt, M, N, K, epi):
     if dt == "f32" and M * N * K > 1e8:
