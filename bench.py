@@ -98,6 +98,24 @@ def forecast_bench(bc, torch, dev, K=3, dtype="bf16", iters=10):
             "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
 
 
+def device_params(cfg, torch, dev):
+    """Random-init weights drawn on the GPU (N(0, 1) * param_scale, seeded):
+    the multi-billion-parameter video workload would take minutes and tens of
+    GB of host memory to draw on the host, and throughput does not depend on
+    the values."""
+    import synth
+    g = torch.Generator(device=dev)
+    g.manual_seed(synth.SEED)
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    out = {}
+    for name, shape in synth.param_shapes(cfg):
+        t = torch.empty(shape, dtype=torch.float32, device=dev)
+        t.normal_(0.0, cfg.param_scale, generator=g)
+        out[name] = t.to(dt)
+        del t
+    return out
+
+
 def cpu_baseline(cfg, params, labels, xT, mask, nsteps):
     """The oracle on the host cores, on one sample and the first `nsteps` steps
     of the schedule; per-step times composed to the whole schedule."""
@@ -153,8 +171,11 @@ def main():
     dev = "cuda:0"
     cfg = synth.CONFIGS[args.workload]
     t0 = time.time()
-    params = synth.params(cfg)
-    dm = loader.DeviceModel(cfg, params)
+    # Host weights (shared with the oracle's CPU baseline) for the default
+    # image workload; GPU-drawn weights for the others.
+    host_weights = args.workload == "dit_xl2"
+    params = synth.params(cfg) if host_weights else None
+    dm = loader.DeviceModel(cfg, params, dev_params=None if host_weights else device_params(cfg, torch, dev))
     B = cfg.batch
     mask = bary.make_mask(cfg.steps, cfg.interval)
     labels = synth.labels(cfg) if cfg.n_classes else None
@@ -192,24 +213,27 @@ def main():
     torch.cuda.synchronize()
     ms_full = (time.perf_counter() - tf) / nref * 1e3
 
-    # Dominant kernel: the fc1 GEMM (bias + GELU epilogue), HIP events on its stream.
+    # Dominant kernel: the fc1 GEMM (bias + GELU epilogue), HIP events on its
+    # stream.  Defined for the DiT / PixArt block (one fc1 shape per block).
     nfull = int(mask.sum())
-    launches = nfull * cfg.depth
-    bc.profile_enable(bc.PROF_GEMM_GELU, launches)
-    run(mask)
-    gemm_ms, gemm_n = bc.profile_collect(bc.PROF_GEMM_GELU)
-    M_rows = B * cfg.tokens
-    flops = 2.0 * M_rows * cfg.mlp * cfg.hidden
-    avg_s = gemm_ms / gemm_n / 1e3
-    achieved = flops / avg_s / 1e12
-    gemm_hash = source_hash("gemm.hip", "gemm.h", "hip_common.h")
-    roofline = {"bound": "mfma", "kernel": "gemm fc1 (bias+GELU)",
-                "shape": [M_rows, cfg.mlp, cfg.hidden], "flops_per_launch": flops,
-                "avg_us": round(avg_s * 1e6, 2), "launches": gemm_n,
-                "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": counters_traffic("gemm_fc1_dit_xl2", gemm_hash, None),
-                "source_hash": gemm_hash}
+    roofline = None
+    if cfg.kind in ("dit", "pixart"):
+        launches = nfull * cfg.depth
+        bc.profile_enable(bc.PROF_GEMM_GELU, launches)
+        run(mask)
+        gemm_ms, gemm_n = bc.profile_collect(bc.PROF_GEMM_GELU)
+        M_rows = B * cfg.tokens
+        flops = 2.0 * M_rows * cfg.mlp * cfg.hidden
+        avg_s = gemm_ms / gemm_n / 1e3
+        achieved = flops / avg_s / 1e12
+        gemm_hash = source_hash("gemm.hip", "gemm.h", "hip_common.h")
+        roofline = {"bound": "mfma", "kernel": "gemm fc1 (bias+GELU)",
+                    "shape": [M_rows, cfg.mlp, cfg.hidden], "flops_per_launch": flops,
+                    "avg_us": round(avg_s * 1e6, 2), "launches": gemm_n,
+                    "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                    "traffic": counters_traffic(f"gemm_fc1_{cfg.name}", gemm_hash, None) if cfg.name == "dit_xl2" else None,
+                    "source_hash": gemm_hash}
 
     forecast = None
     if not args.no_forecast:
@@ -232,15 +256,17 @@ def main():
         del src, store, ring
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and host_weights:
         cpu = cpu_baseline(cfg, params, labels, xT, mask, args.cpu_steps)
 
+    blocks = (f"{cfg.depth} dual-stream + {cfg.depth_single} single-stream blocks" if cfg.kind == "mmdit"
+              else f"{cfg.depth} blocks")
     line = {
         "metric": "end-to-end samples/s at fixed skip schedule; forecast HBM GB/s; block MFMA util",
         "value": round(value, 3), "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: {cfg.depth} blocks, D {cfg.hidden}, {cfg.heads}x{cfg.head_dim} heads, "
+        "config": {"workload": f"{cfg.name}: {blocks}, D {cfg.hidden}, {cfg.heads}x{cfg.head_dim} heads, "
                                f"MLP {cfg.mlp}, {cfg.tokens} tokens, batch {B}, {cfg.steps} {cfg.sampler} steps, "
                                f"K={cfg.K}, full every {cfg.interval} ({nfull}/{cfg.steps}), random-init weights",
                    "global_batch": B, "parallelism": "none (1 GPU)"},
