@@ -591,142 +591,6 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_wide_kernel(GemmA
     epilogue_t<EPI, TM, TN>(g, acc, bm + wm * WM, bn + j0 * 16, lane, jn);
 }
 
-// ---------------------------------------------------------------------------
-// Split-K inside the workgroup, for outputs too small to give every CU a
-// wide tile (the N = 1152 projections of DiT-XL/2 at M = 4096 make 256 tiles
-// of 128 x 144).  KG groups of WAVES_M waves share the workgroup's tile: a
-// stage holds KG * 32 k-columns, group kg owning the 32-column slice kg of
-// every stage (its own A and W block in 64-byte LDS rows), so each wave keeps
-// a full (BM / WAVES_M) x BN accumulator over a quarter of K.  After the main
-// loop the groups' partial tiles are summed pairwise through LDS (a tree over
-// the KG groups) and group 0 applies the epilogue.
-// ---------------------------------------------------------------------------
-template <int EPI, int BM, int BN, int WAVES_M, int KG>
-__global__ __launch_bounds__(64 * WAVES_M * KG) void gemm_ksplit_kernel(GemmArgs g) {
-    typedef bf16 T;
-    typedef Mma<bf16> MM;
-    constexpr int NW = WAVES_M * KG;
-    constexpr int GK = 32;                                 // k-columns per group per stage
-    constexpr int BK = GK * KG;                            // k-columns per stage
-    constexpr int WM = BM / WAVES_M, TM = WM / 16, TN = BN / 16;
-    constexpr int ROWS = BM + BN;                          // rows of a group block: A, then W
-    constexpr int RB = ROWS / 16;                          // 16-row loads per group block
-    constexpr int GBLK = ROWS * GK;                        // elements per group block
-    constexpr int STAGE = GBLK * KG;
-    constexpr int NLD = RB * KG;                           // wave-wide loads per stage
-    constexpr int QMAX = (NLD + NW - 1) / NW;
-    constexpr int PART = WAVES_M * TM * TN * 64 * 4;       // floats in one group's partial tile
-    constexpr int STAGE_BYTES = 2 * STAGE * 2;
-    constexpr int RED_BYTES = (KG / 2) * PART * 4;
-    constexpr int SMEM = STAGE_BYTES > RED_BYTES ? STAGE_BYTES : RED_BYTES;
-    static_assert(TM * 16 * WAVES_M == BM && TN * 16 == BN && ROWS % 16 == 0, "tile shape");
-    static_assert(KG == 1 || KG == 2 || KG == 4, "K groups");
-    __shared__ __attribute__((aligned(1024))) char smem[SMEM];
-    T* const sm = reinterpret_cast<T*>(smem);
-
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave % WAVES_M, kg = wave / WAVES_M;
-
-    const int tiles_m = (g.M + BM - 1) / BM;
-    const int tiles_n = (g.N + BN - 1) / BN;
-    const int nwg = gridDim.x;
-    int pid = blockIdx.x;
-    if ((nwg & 7) == 0) pid = (pid & 7) * (nwg >> 3) + (pid >> 3);
-    constexpr int GROUP_M = 8;
-    const int group = GROUP_M * tiles_n;
-    const int first_m = (pid / group) * GROUP_M;
-    const int gm = min(tiles_m - first_m, GROUP_M);
-    const int tm = first_m + (pid % group) % gm;
-    const int tn = (pid % group) / gm;
-    const int bm = tm * BM, bn = tn * BN;
-
-    // Load o = wave + NW q of a stage: rows 16 (o % RB) .. +15 of group block
-    // o / RB; lane L loads row 16 (o % RB) + L / 4 into slot L % 4.
-    const T* src[QMAX];
-    int dst[QMAX];
-#pragma unroll
-    for (int q = 0; q < QMAX; ++q) {
-        const int o = min(wave + NW * q, NLD - 1);
-        const int go = o / RB, r = 16 * (o % RB) + lane / 4;
-        const T* p;
-        if (r < BM) p = static_cast<const T*>(g.A) + (int64_t)min(bm + r, g.M - 1) * g.lda;
-        else p = static_cast<const T*>(g.W) + (int64_t)min(bn + r - BM, g.N - 1) * g.ldw;
-        src[q] = p + go * GK + wslot<32>(lane % 4, r) * 8;
-        dst[q] = go * GBLK + 16 * (o % RB) * GK;
-    }
-    auto issue = [&](int kt, int buf) {
-        const int k0 = kt * BK;
-#pragma unroll
-        for (int q = 0; q < QMAX; ++q) {
-            const int o = wave + NW * q;
-            if (NLD % NW == 0 || o < NLD) dma16(src[q] + k0, &sm[buf * STAGE + dst[q]]);
-        }
-    };
-
-    f32x4 acc[TM][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    const int nk = g.K / BK;
-    issue(0, 0);
-    const int frow = lane & 15, grp = lane >> 4;
-    for (int kt = 0; kt < nk; ++kt) {
-        wait_vmcnt<0>();
-        __syncthreads();
-        if (kt + 1 < nk) issue(kt + 1, (kt + 1) & 1);
-        const T* st = sm + (kt & 1) * STAGE + kg * GBLK;
-        MM::frag af[TM], bfr[TN];
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-            const int r = wm * WM + i * 16 + frow;
-            af[i] = MM::load(st + r * GK + wslot<32>(grp, r) * 8);
-        }
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int r = BM + j * 16 + frow;
-            bfr[j] = MM::load(st + r * GK + wslot<32>(grp, r) * 8);
-        }
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j) acc[i][j] = MM::mma(bfr[j], af[i], acc[i][j]);
-    }
-
-    // Tree reduction of the KG partial tiles: at each level the upper half of
-    // the remaining groups stores, the lower half adds.  A wave's part sits at
-    // [wm][i][j][lane] so the same wave index of every group lines up.
-    float* const red = reinterpret_cast<float*>(smem);
-#pragma unroll
-    for (int half = KG / 2; half >= 1; half /= 2) {
-        __syncthreads();
-        if (kg >= half && kg < 2 * half) {
-            f32x4* r = reinterpret_cast<f32x4*>(red + (kg - half) * PART) + wm * TM * TN * 64 + lane;
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j) r[(i * TN + j) * 64] = acc[i][j];
-        }
-        __syncthreads();
-        if (kg < half) {
-            const f32x4* r = reinterpret_cast<const f32x4*>(red + kg * PART) + wm * TM * TN * 64 + lane;
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int j = 0; j < TN; ++j) acc[i][j] += r[(i * TN + j) * 64];
-        }
-    }
-    if (kg == 0) epilogue_t<EPI, TM, TN>(g, acc, bm + wm * WM, bn, lane);
-}
-
-template <int EPI, int BM, int BN, int WAVES_M, int KG>
-static void launch_ksplit(const GemmArgs& g, hipStream_t s) {
-    const unsigned tiles = (unsigned)(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN));
-    gemm_ksplit_kernel<EPI, BM, BN, WAVES_M, KG><<<dim3(tiles), dim3(64 * WAVES_M * KG), 0, s>>>(g);
-}
-
 template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES = 2, int BK = 64>
 static void launch_wide(const GemmArgs& g, hipStream_t s) {
     const unsigned tiles = (unsigned)(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN));
