@@ -530,7 +530,7 @@ static int run_attention_dma(const AttnArgs& a, int hd, hipStream_t s) {
     if (nwg > 0x7fffffff) return fail(BC_ERR_UNSUPPORTED, "attention grid too large");
     dim3 grid((unsigned)nwg), block(64 * NWV);
     switch (hd) {
-#define BC_ATT_CASE(HD) case HD: attention_dma_kernel<HD, QG, NWV, NB><<<grid, block, 0, s>>>(a); break;
+#define BC_ATT_CASE(HD) case HD: launch_k(attention_dma_kernel<HD, QG, NWV, NB>, grid, block, s, a); break;
         BC_ATT_CASE(32) BC_ATT_CASE(64) BC_ATT_CASE(72) BC_ATT_CASE(128)
 #undef BC_ATT_CASE
         default: return fail(BC_ERR_UNSUPPORTED, "head_dim %d (supported: 32, 64, 72, 128)", hd);
@@ -545,7 +545,7 @@ static int run_attention(const AttnArgs& a, int hd, hipStream_t s) {
     if (nwg > 0x7fffffff) return fail(BC_ERR_UNSUPPORTED, "attention grid too large");
     dim3 grid((unsigned)nwg), block(kAttnThreads);
     switch (hd) {
-#define BC_ATT_CASE(HD) case HD: attention_kernel<T, HD, QG><<<grid, block, 0, s>>>(a); break;
+#define BC_ATT_CASE(HD) case HD: launch_k(attention_kernel<T, HD, QG>, grid, block, s, a); break;
         BC_ATT_CASE(32) BC_ATT_CASE(64) BC_ATT_CASE(72) BC_ATT_CASE(128)
 #undef BC_ATT_CASE
         default: return fail(BC_ERR_UNSUPPORTED, "head_dim %d (supported: 32, 64, 72, 128)", hd);

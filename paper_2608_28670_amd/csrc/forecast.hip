@@ -117,7 +117,7 @@ static void launch_vec(const FcArgs& a, int K, int64_t nv, hipStream_t s) {
     const int64_t blocks = (nv + kThreads * U - 1) / (kThreads * U);
     dim3 g((unsigned)blocks), b(kThreads);
     switch (K) {
-#define BC_FC_CASE(KK) case KK: forecast_vec_kernel<KK, Tin, Tout, U><<<g, b, 0, s>>>(a); break;
+#define BC_FC_CASE(KK) case KK: launch_k(forecast_vec_kernel<KK, Tin, Tout, U>, g, b, s, a); break;
         BC_FC_CASE(1) BC_FC_CASE(2) BC_FC_CASE(3) BC_FC_CASE(4)
         BC_FC_CASE(5) BC_FC_CASE(6) BC_FC_CASE(7) BC_FC_CASE(8)
 #undef BC_FC_CASE
@@ -147,7 +147,7 @@ static int run_forecast(const FcArgs& a, int K, hipStream_t s) {
         const int64_t rest = a.n - done;
         int64_t blocks = (rest + kThreads - 1) / kThreads;
         if (blocks > 65536) blocks = 65536;
-        forecast_scalar_kernel<Tin, Tout><<<dim3((unsigned)blocks), dim3(kThreads), 0, s>>>(a, K, done);
+        launch_k(forecast_scalar_kernel<Tin, Tout>, dim3((unsigned)blocks), dim3(kThreads), s, a, K, done);
     }
     return check_launch("forecast");
 }

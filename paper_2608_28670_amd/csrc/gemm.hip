@@ -594,7 +594,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_wide_kernel(GemmA
 template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES = 2, int BK = 64>
 static void launch_wide(const GemmArgs& g, hipStream_t s) {
     const unsigned tiles = (unsigned)(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN));
-    gemm_wide_kernel<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, BK><<<dim3(tiles), dim3(64 * WAVES_M * WAVES_N), 0, s>>>(g);
+    launch_k(gemm_wide_kernel<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, BK>, dim3(tiles), dim3(64 * WAVES_M * WAVES_N), s, g);
 }
 
 template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int SW = 0>
@@ -610,13 +610,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_dma_seg_kernel(Ge
 template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int SW = 0>
 static void launch_dma(const GemmArgs& g, hipStream_t s) {
     const unsigned tiles = (unsigned)(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN));
-    gemm_dma_kernel<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, SW><<<dim3(tiles), dim3(64 * WAVES_M * WAVES_N), 0, s>>>(g);
+    launch_k(gemm_dma_kernel<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, SW>, dim3(tiles), dim3(64 * WAVES_M * WAVES_N), s, g);
 }
 
 template <typename T, int EPI, int BM, int BN, int WAVES_M, int WAVES_N>
 static void launch_tile(const GemmArgs& g, hipStream_t s) {
     const unsigned tiles = (unsigned)(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN));
-    gemm_kernel<T, EPI, BM, BN, WAVES_M, WAVES_N><<<dim3(tiles), dim3(64 * WAVES_M * WAVES_N), 0, s>>>(g);
+    launch_k(gemm_kernel<T, EPI, BM, BN, WAVES_M, WAVES_N>, dim3(tiles), dim3(64 * WAVES_M * WAVES_N), s, g);
 }
 
 // The wide kernel's vector epilogue needs every column index and stride it
@@ -687,7 +687,7 @@ int launch_gemm_grouped(int dtype, const GemmArgs& g0, const GemmSeg& sg, int ns
             if (reinterpret_cast<uintptr_t>(sg.W[i]) % 16) return fail(BC_ERR_UNSUPPORTED, "misaligned segment weight");
         prof_begin(PROF_GEMM_BIAS, s);
         const unsigned tiles = (unsigned)(((g.M + 127) / 128) * (g.N / 128));
-        gemm_dma_seg_kernel<BC_EPI_BIAS, 128, 128, 4, 2, 2><<<dim3(tiles), dim3(512), 0, s>>>(g, sg);
+        launch_k(gemm_dma_seg_kernel<BC_EPI_BIAS, 128, 128, 4, 2, 2>, dim3(tiles), dim3(512), s, g, sg);
         prof_end(PROF_GEMM_BIAS, s);
         return check_launch("grouped gemm");
     }

@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 
 #include <cstdint>
 
@@ -60,6 +61,19 @@ enum ProfClass { PROF_FORECAST = 0, PROF_GEMM_GELU = 1, PROF_GEMM_GATE = 2, PROF
                  PROF_ATTENTION = 4, PROF_LAYERNORM = 5, PROF_NCLASS = 6 };
 void prof_begin(int cls, hipStream_t s);
 void prof_end(int cls, hipStream_t s);
+// Next start/stop event pair of the class bracketed by prof_begin/prof_end on
+// this thread, if that class is being timed.
+bool prof_take(hipEvent_t* start, hipEvent_t* stop);
+
+// Kernel launch that, inside a timed bracket, has the runtime stamp the
+// kernel's own start and end into the class's events (the same interval a
+// kernel trace reports), and is a plain launch otherwise.
+template <typename... KArgs, typename... Args>
+inline void launch_k(void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t s, Args... args) {
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (!prof_take(&e0, &e1)) e0 = e1 = nullptr;
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, s, e0, e1, 0, args...);
+}
 
 // ---- kernel launchers (each returns a bc_status) ---------------------------
 

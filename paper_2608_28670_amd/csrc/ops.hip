@@ -106,12 +106,12 @@ static int run_ln(const void* x, int64_t rows, int D, const float* shift, const 
     dim3 g((unsigned)((rows + 3) / 4)), b(256);
     const Tin* xi = static_cast<const Tin*>(x);
     Tout* ho = static_cast<Tout*>(h);
-    if (nc <= 1) ln_mod_kernel<Tin, Tout, 1><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nc <= 2) ln_mod_kernel<Tin, Tout, 2><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nc <= 5) ln_mod_kernel<Tin, Tout, 5><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nc <= 8) ln_mod_kernel<Tin, Tout, 8><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nc <= 12) ln_mod_kernel<Tin, Tout, 12><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nc <= 16) ln_mod_kernel<Tin, Tout, 16><<<g, b, 0, s>>>(xi, rows, D, shift, scale, ld_mod, rps, ho);
+    if (nc <= 1) launch_k(ln_mod_kernel<Tin, Tout, 1>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 2) launch_k(ln_mod_kernel<Tin, Tout, 2>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 5) launch_k(ln_mod_kernel<Tin, Tout, 5>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 8) launch_k(ln_mod_kernel<Tin, Tout, 8>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 12) launch_k(ln_mod_kernel<Tin, Tout, 12>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 16) launch_k(ln_mod_kernel<Tin, Tout, 16>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
     else return fail(BC_ERR_UNSUPPORTED, "LayerNorm width %d > 4096", D);
     return check_launch("ln_mod");
 }

@@ -1,6 +1,8 @@
-// Per-kernel-class timing with HIP events recorded on the launch stream.
-// Enabled classes bracket each launch with a start/stop event pair drawn from
-// a pool created at enable time; collect waits on the events and sums them.
+// Per-kernel-class timing with HIP events on the launch stream.  Inside a
+// prof_begin/prof_end bracket of an enabled class, each kernel launch takes
+// the next start/stop pair of a pool created at enable time and is launched
+// with hipExtLaunchKernelGGL, which records the kernel's own start and end
+// into them; collect waits on the events and sums the intervals.
 #include <vector>
 
 #include "hip_common.h"
@@ -25,17 +27,20 @@ void release(ClassTimer& t) {
 }
 }  // namespace
 
-void prof_begin(int cls, hipStream_t s) {
-    ClassTimer& t = g_timer[cls];
-    if (!t.on || t.used >= (int)t.start.size()) return;
-    (void)hipEventRecord(t.start[t.used], s);
-}
+thread_local int g_pending = -1;   // class of the open bracket on this thread, -1 if none
 
-void prof_end(int cls, hipStream_t s) {
-    ClassTimer& t = g_timer[cls];
-    if (!t.on || t.used >= (int)t.start.size()) return;
-    (void)hipEventRecord(t.stop[t.used], s);
+void prof_begin(int cls, hipStream_t) { g_pending = g_timer[cls].on ? cls : -1; }
+
+void prof_end(int, hipStream_t) { g_pending = -1; }
+
+bool prof_take(hipEvent_t* start, hipEvent_t* stop) {
+    if (g_pending < 0) return false;
+    ClassTimer& t = g_timer[g_pending];
+    if (!t.on || t.used >= (int)t.start.size()) return false;
+    *start = t.start[t.used];
+    *stop = t.stop[t.used];
     ++t.used;
+    return true;
 }
 
 }  // namespace bc
