@@ -376,23 +376,67 @@ __device__ __forceinline__ void st4(float* p, const float (&v)[4]) {
     *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
 }
 
-// jn: number of the TN column blocks this wave holds (the rest are unused).
-// bf16 outputs of the plain epilogue are written 16 bytes per lane: for a pair
-// of row blocks (i, i + 1), lanes of an even 16-lane group (columns c..c+3)
-// and of the odd group next to it (c+4..c+7) swap halves with
-// v_permlane16_swap, so the even lane stores row r_i and the odd lane row
-// r_{i+1}, each as 8 consecutive columns.
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-    bf16x2 q;
-    q[0] = (bf16)a; q[1] = (bf16)b;
-    return __builtin_bit_cast(uint32_t, q);
-}
+// Residual and gate of the gated-residual epilogue, loaded into registers at
+// the start of the last k-step so that their latency hides behind its MFMAs.
+template <int EPI, int TM, int TN> struct EpiPrefetch {
+    f32x4 res[TM][TN], gate[TM][TN];
+    __device__ __forceinline__ void load(const GemmArgs& g, int row0, int col0, int lane, int jn) {
+        if constexpr (EPI == BC_EPI_GATE_RES) {
+            const GemmEpi& e = g.e;
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int row = min(row0 + i * 16 + (lane & 15), g.M - 1);
+                const float* rrow = e.res + (int64_t)row * e.ldr;
+                const float* grow = e.gate ? e.gate + (int64_t)(row / e.rows_per_gate) * e.ldg : nullptr;
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    if (j >= jn) break;
+                    const int col = min(col0 + j * 16 + 4 * (lane >> 4), g.N - 4);
+                    res[i][j] = *reinterpret_cast<const f32x4*>(rrow + col);
+                    gate[i][j] = grow ? *reinterpret_cast<const f32x4*>(grow + col) : f32x4{1.f, 1.f, 1.f, 1.f};
+                }
+            }
+        }
+    }
+};
+
+// Epilogue straight from the accumulators (gated residual; fp32 outputs of
+// the plain epilogue).  jn: number of the TN column blocks this wave holds.
 
 template <int EPI, int TM, int TN>
 __device__ __forceinline__ void epilogue_t(const GemmArgs& g, const f32x4 (&acc)[TM][TN], int row0, int col0, int lane,
-                                           int jn = TN) {
+                                           int jn, const EpiPrefetch<EPI, TM, TN>& pf) {
     const GemmEpi& e = g.e;
+    if constexpr (EPI == BC_EPI_GATE_RES) {
+        // Rows outer: the row's destination (ring-slot remap) is worked out once.
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const int row = row0 + i * 16 + (lane & 15);
+            if (row >= g.M) continue;
+            const int b = row / e.seg, sidx = row - b * e.seg;
+            if (sidx >= e.keep) continue;
+            const int64_t orow = (int64_t)(b * e.keep + sidx) * e.ldo;
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                if (j >= jn) break;
+                const int col = col0 + j * 16 + 4 * (lane >> 4);
+                if (col >= g.N) continue;
+                float v[4];
+                const bf16* __restrict__ bias = static_cast<const bf16*>(e.bias);
+                float bv[4] = {0.f, 0.f, 0.f, 0.f};
+                if (bias) {
+                    const bf16x4 b4 = *reinterpret_cast<const bf16x4*>(bias + col);
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) bv[r] = (float)b4[r];
+                }
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] = pf.res[i][j][r] + pf.gate[i][j][r] * (acc[i][j][r] + bv[r]);
+                if (e.out_f32) st4(static_cast<float*>(e.out) + orow + col, v);
+                else st4(static_cast<bf16*>(e.out) + orow + col, v);
+            }
+        }
+        return;
+    }
     const bf16* __restrict__ bias = static_cast<const bf16*>(e.bias);
     const bool odd = (lane >> 4) & 1;
 #pragma unroll
@@ -406,41 +450,6 @@ __device__ __forceinline__ void epilogue_t(const GemmArgs& g, const f32x4 (&acc)
 #pragma unroll
             for (int r = 0; r < 4; ++r) bv[r] = (float)b4[r];
         }
-        if constexpr (EPI != BC_EPI_GATE_RES && TM % 2 == 0) {
-            if (!e.out_f32) {
-                // Pairs of row blocks, 16-byte stores (see above).  Both lanes of
-                // a pair see the same split/gelu decision: the pair's 8 columns
-                // start at a multiple of 8 and those boundaries are multiples of 8
-                // here (checked on the host).
-                const int cpair = col - (odd ? 4 : 0);
-                const bool act = cpair >= e.gelu_from;
-#pragma unroll
-                for (int i = 0; i < TM; i += 2) {
-                    uint32_t w[2][2];
-#pragma unroll
-                    for (int h = 0; h < 2; ++h) {
-                        float v[4];
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            v[r] = acc[i + h][j][r] + bv[r];
-                            if (act) v[r] = gelu_tanh(v[r]);
-                        }
-                        w[h][0] = pack_bf16x2(v[0], v[1]);
-                        w[h][1] = pack_bf16x2(v[2], v[3]);
-                    }
-                    const auto x0 = __builtin_amdgcn_permlane16_swap(w[0][0], w[1][0], false, false);
-                    const auto x1 = __builtin_amdgcn_permlane16_swap(w[0][1], w[1][1], false, false);
-                    const u32x4 q = u32x4{x0[0], x1[0], x0[1], x1[1]};
-                    const int row = row0 + (i + (odd ? 1 : 0)) * 16 + (lane & 15);
-                    if (row < g.M && cpair < g.N) {
-                        bf16* dst = cpair >= e.split ? static_cast<bf16*>(e.out2) + (int64_t)row * e.ldo2 + (cpair - e.split + e.off2)
-                                                     : static_cast<bf16*>(e.out) + (int64_t)row * e.ldo + cpair;
-                        *reinterpret_cast<u32x4*>(dst) = q;
-                    }
-                }
-                continue;
-            }
-        }
         if (!col_ok) continue;
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
@@ -449,27 +458,13 @@ __device__ __forceinline__ void epilogue_t(const GemmArgs& g, const f32x4 (&acc)
             float v[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) v[r] = acc[i][j][r] + bv[r];
-            if constexpr (EPI == BC_EPI_GATE_RES) {
-                const f32x4 rv = *reinterpret_cast<const f32x4*>(e.res + (int64_t)row * e.ldr + col);
-                f32x4 gv = f32x4{1.f, 1.f, 1.f, 1.f};
-                if (e.gate) gv = *reinterpret_cast<const f32x4*>(e.gate + (int64_t)(row / e.rows_per_gate) * e.ldg + col);
+            if (col >= e.gelu_from) {
 #pragma unroll
-                for (int r = 0; r < 4; ++r) v[r] = rv[r] + gv[r] * v[r];
-                const int b = row / e.seg, s = row - b * e.seg;
-                if (s < e.keep) {
-                    const int64_t o = (int64_t)(b * e.keep + s) * e.ldo + col;
-                    if (e.out_f32) st4(static_cast<float*>(e.out) + o, v);
-                    else st4(static_cast<bf16*>(e.out) + o, v);
-                }
-            } else {
-                if (col >= e.gelu_from) {
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) v[r] = gelu_tanh(v[r]);
-                }
-                if (col >= e.split) st4(static_cast<bf16*>(e.out2) + (int64_t)row * e.ldo2 + (col - e.split + e.off2), v);
-                else if (e.out_f32) st4(static_cast<float*>(e.out) + (int64_t)row * e.ldo + col, v);
-                else st4(static_cast<bf16*>(e.out) + (int64_t)row * e.ldo + col, v);
+                for (int r = 0; r < 4; ++r) v[r] = gelu_tanh(v[r]);
             }
+            if (col >= e.split) st4(static_cast<bf16*>(e.out2) + (int64_t)row * e.ldo2 + (col - e.split + e.off2), v);
+            else if (e.out_f32) st4(static_cast<float*>(e.out) + (int64_t)row * e.ldo + col, v);
+            else st4(static_cast<bf16*>(e.out) + (int64_t)row * e.ldo + col, v);
         }
     }
 }
@@ -498,7 +493,9 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_wide_kernel(GemmA
     constexpr int QMAX = (NOCT + NW - 1) / NW;             // octets per wave (at most)
     static_assert(TM * 16 * WAVES_M == BM && BM % 16 == 0 && BN % 16 == 0, "tile shape");
     constexpr int STAGE = (BM + BN) * BK;                  // elements per stage: BM rows of A, then BN rows of W
-    __shared__ __attribute__((aligned(1024))) T sm[STAGES * STAGE];
+    constexpr int OPITCH = BN + 8;                         // staged bf16 output row (16-byte pad)
+    constexpr int SMEM = STAGES * STAGE > BM * OPITCH ? STAGES * STAGE : BM * OPITCH;
+    __shared__ __attribute__((aligned(1024))) T sm[SMEM];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -548,6 +545,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_wide_kernel(GemmA
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    EpiPrefetch<EPI, TM, TN> pf;
     const int nk = g.K / BK;
 #pragma unroll
     for (int p = 0; p < STAGES - 1; ++p)
@@ -564,6 +562,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_wide_kernel(GemmA
         }
         __syncthreads();
         if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+        if (EPI == BC_EPI_GATE_RES && kt == nk - 1) pf.load(g, bm + wm * WM, bn + j0 * 16, lane, jn);
         const T* st = sm + (kt % STAGES) * STAGE;
 #pragma unroll
         for (int kk = 0; kk < BK / 32; ++kk) {
@@ -588,7 +587,57 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_wide_kernel(GemmA
         }
     }
 
-    epilogue_t<EPI, TM, TN>(g, acc, bm + wm * WM, bn + j0 * 16, lane, jn);
+    if constexpr (EPI == BC_EPI_BIAS) {
+        if (!g.e.out_f32) {
+            // bf16 outputs leave through LDS: the waves write their finished
+            // values into a row-major copy of the tile, then the workgroup stores
+            // it as consecutive 16-byte chunks of each row, so every store
+            // instruction covers whole cache lines.  (Written straight from the
+            // accumulators, 32-byte pieces of lines from all 256 one-round tiles
+            // at once came back as about 1.5x the output bytes in HBM writes.)
+            const GemmEpi& e = g.e;
+            const bf16* __restrict__ bias = static_cast<const bf16*>(e.bias);
+            __syncthreads();   // every wave is done with the stage buffers
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                if (j >= jn) break;
+                const int lc = (j0 + j) * 16 + 4 * (lane >> 4);
+                const int col = bn + lc;
+                float bv[4] = {0.f, 0.f, 0.f, 0.f};
+                if (bias && col < g.N) {
+                    const bf16x4 b4 = *reinterpret_cast<const bf16x4*>(bias + col);
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) bv[r] = (float)b4[r];
+                }
+                const bool act = col >= e.gelu_from;
+#pragma unroll
+                for (int i = 0; i < TM; ++i) {
+                    bf16x4 q;
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        float v = acc[i][j][r] + bv[r];
+                        if (act) v = gelu_tanh(v);
+                        q[r] = (bf16)v;
+                    }
+                    const int lr = wm * WM + i * 16 + (lane & 15);
+                    *reinterpret_cast<bf16x4*>(sm + lr * OPITCH + lc) = q;
+                }
+            }
+            __syncthreads();
+            constexpr int NT = 64 * NW, CPRO = BN / 8;    // threads; 16-byte chunks per tile row
+            for (int q = tid; q < BM * CPRO; q += NT) {
+                const int lr = q / CPRO, c8 = q - lr * CPRO;
+                const int row = bm + lr, col = bn + c8 * 8;
+                if (row >= g.M || col >= g.N) continue;
+                const u32x4 val = *reinterpret_cast<const u32x4*>(sm + lr * OPITCH + c8 * 8);
+                bf16* dst = col >= e.split ? static_cast<bf16*>(e.out2) + (int64_t)row * e.ldo2 + (col - e.split + e.off2)
+                                           : static_cast<bf16*>(e.out) + (int64_t)row * e.ldo + col;
+                *reinterpret_cast<u32x4*>(dst) = val;
+            }
+            return;
+        }
+    }
+    epilogue_t<EPI, TM, TN>(g, acc, bm + wm * WM, bn + j0 * 16, lane, jn, pf);
 }
 
 template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES = 2, int BK = 64>

@@ -56,15 +56,23 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const Tin* __restrict__ x, 
     if (row >= rows) return;
     const int nch = D >> 2;
     const Tin* xr = x + row * D;
-    float v[NC][4];
+    const int64_t b = row / rps;
+    const float* sh = shift + b * ld_mod;
+    const float* sc = scale + b * ld_mod;
+    // The row and its modulation vectors are all loaded up front, so the two
+    // reductions overlap the modulation loads.
+    float v[NC][4], s4[NC][4], c4[NC][4];
     float sum = 0.f;
 #pragma unroll
     for (int j = 0; j < NC; ++j) {
         const int c = lane + 64 * j;
         if (c < nch) {
             Vec4<Tin>::load(xr + 4 * c, v[j]);
+            Vec4<float>::load(sh + 4 * c, s4[j]);
+            Vec4<float>::load(sc + 4 * c, c4[j]);
         } else {
-            v[j][0] = v[j][1] = v[j][2] = v[j][3] = 0.f;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[j][e] = s4[j][e] = c4[j][e] = 0.f;
         }
         sum += (v[j][0] + v[j][1]) + (v[j][2] + v[j][3]);
     }
@@ -81,19 +89,14 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const Tin* __restrict__ x, 
         }
     }
     const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + kLnEps);
-    const int64_t b = row / rps;
-    const float* sh = shift + b * ld_mod;
-    const float* sc = scale + b * ld_mod;
     Tout* hr = h + row * D;
 #pragma unroll
     for (int j = 0; j < NC; ++j) {
         const int c = lane + 64 * j;
         if (c < nch) {
-            float s4[4], c4[4], o[4];
-            Vec4<float>::load(sh + 4 * c, s4);
-            Vec4<float>::load(sc + 4 * c, c4);
+            float o[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) o[e] = (v[j][e] - mean) * rstd * (1.0f + c4[e]) + s4[e];
+            for (int e = 0; e < 4; ++e) o[e] = (v[j][e] - mean) * rstd * (1.0f + c4[j][e]) + s4[j][e];
             Vec4<Tout>::store(hr + 4 * c, o);
         }
     }
