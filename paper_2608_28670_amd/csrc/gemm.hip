@@ -376,27 +376,33 @@ __device__ __forceinline__ void st4(float* p, const float (&v)[4]) {
     *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
 }
 
-// Residual and gate of the gated-residual epilogue, loaded into registers at
-// the start of the last k-step so that their latency hides behind its MFMAs.
+// Residual of the gated-residual epilogue, loaded into registers at the start
+// of the last k-step so that its latency hides behind the MFMAs, when a wave's
+// share is small enough to sit beside the accumulators (at most 12 MFMA tiles);
+// larger tiles read it in the epilogue.  The gate (one row per sample) is read
+// in the epilogue from cache.
 template <int EPI, int TM, int TN> struct EpiPrefetch {
-    f32x4 res[TM][TN], gate[TM][TN];
+    static constexpr bool early = EPI == BC_EPI_GATE_RES && TM * TN <= 12;
+    f32x4 res[early ? TM : 1][early ? TN : 1];
     __device__ __forceinline__ void load(const GemmArgs& g, int row0, int col0, int lane, int jn) {
-        if constexpr (EPI == BC_EPI_GATE_RES) {
+        if constexpr (early) {
             const GemmEpi& e = g.e;
 #pragma unroll
             for (int i = 0; i < TM; ++i) {
                 const int row = min(row0 + i * 16 + (lane & 15), g.M - 1);
                 const float* rrow = e.res + (int64_t)row * e.ldr;
-                const float* grow = e.gate ? e.gate + (int64_t)(row / e.rows_per_gate) * e.ldg : nullptr;
 #pragma unroll
                 for (int j = 0; j < TN; ++j) {
                     if (j >= jn) break;
                     const int col = min(col0 + j * 16 + 4 * (lane >> 4), g.N - 4);
                     res[i][j] = *reinterpret_cast<const f32x4*>(rrow + col);
-                    gate[i][j] = grow ? *reinterpret_cast<const f32x4*>(grow + col) : f32x4{1.f, 1.f, 1.f, 1.f};
                 }
             }
         }
+    }
+    __device__ __forceinline__ f32x4 get(const GemmArgs& g, int i, int j, int row, int col) const {
+        if constexpr (early) return res[i][j];
+        else return *reinterpret_cast<const f32x4*>(g.e.res + (int64_t)row * g.e.ldr + col);
     }
 };
 
@@ -416,6 +422,7 @@ __device__ __forceinline__ void epilogue_t(const GemmArgs& g, const f32x4 (&acc)
             const int b = row / e.seg, sidx = row - b * e.seg;
             if (sidx >= e.keep) continue;
             const int64_t orow = (int64_t)(b * e.keep + sidx) * e.ldo;
+            const float* grow = e.gate ? e.gate + (int64_t)(row / e.rows_per_gate) * e.ldg : nullptr;
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
                 if (j >= jn) break;
@@ -429,8 +436,10 @@ __device__ __forceinline__ void epilogue_t(const GemmArgs& g, const f32x4 (&acc)
 #pragma unroll
                     for (int r = 0; r < 4; ++r) bv[r] = (float)b4[r];
                 }
+                const f32x4 gv = grow ? *reinterpret_cast<const f32x4*>(grow + col) : f32x4{1.f, 1.f, 1.f, 1.f};
+                const f32x4 rv = pf.get(g, i, j, row, col);
 #pragma unroll
-                for (int r = 0; r < 4; ++r) v[r] = pf.res[i][j][r] + pf.gate[i][j][r] * (acc[i][j][r] + bv[r]);
+                for (int r = 0; r < 4; ++r) v[r] = rv[r] + gv[r] * (acc[i][j][r] + bv[r]);
                 if (e.out_f32) st4(static_cast<float*>(e.out) + orow + col, v);
                 else st4(static_cast<bf16*>(e.out) + orow + col, v);
             }
@@ -477,29 +486,47 @@ template <int BK> __device__ __forceinline__ int wslot(int c, int r) {
     else return c ^ ((r >> 2) & 3);
 }
 
-template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int BK>
-__global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_wide_kernel(GemmArgs g) {
+// KG > 1: split K inside the workgroup.  KG groups of WAVES_M x WAVES_N waves
+// share the tile; a stage holds KG consecutive 64-wide k-blocks (one per
+// group, each laid out as above), so every wave keeps a full accumulator over
+// 1/KG of K.  The groups' partial tiles are then summed through LDS and group
+// 0 applies the epilogue.  (For small outputs: 128 x 144 tiles of 2 x 2 waves
+// of 64 x 80 / 64 x 64 in two groups keep eight waves per CU with large wave
+// tiles where a one-round grid has only 256 tiles.)
+template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int BK, int KG>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KG) void gemm_wide_kernel(GemmArgs g) {
     typedef bf16 T;
     typedef Mma<bf16> MM;
-    constexpr int NW = WAVES_M * WAVES_N;
+    constexpr int NWG = WAVES_M * WAVES_N;                // waves per K group
+    constexpr int NW = NWG * KG;
     static_assert(BK == 64 || BK == 32, "k-step");
+    static_assert(KG == 1 || KG == 2, "K groups");
     constexpr int CPR = BK / 8;                            // 16-byte chunks per LDS row
     constexpr int RPI = 64 / CPR;                          // rows per wave-wide load
     constexpr int WM = BM / WAVES_M, TM = WM / 16;
     // The BN / 16 column blocks are dealt to the WAVES_N wave columns as
     // evenly as possible (144 = 80 + 64 for two): TN is the larger share.
     constexpr int NBLK = BN / 16, TN = (NBLK + WAVES_N - 1) / WAVES_N, NREM = NBLK % WAVES_N;
-    constexpr int NOCT = (BM + BN) / RPI;                  // wave-wide loads per k-step
+    constexpr int GOCT = (BM + BN) / RPI;                  // wave-wide loads per group block
+    constexpr int NOCT = GOCT * KG;                        // wave-wide loads per stage
     constexpr int QMAX = (NOCT + NW - 1) / NW;             // octets per wave (at most)
     static_assert(TM * 16 * WAVES_M == BM && BM % 16 == 0 && BN % 16 == 0, "tile shape");
-    constexpr int STAGE = (BM + BN) * BK;                  // elements per stage: BM rows of A, then BN rows of W
+    constexpr int GBLK = (BM + BN) * BK;                   // elements per group block: BM rows of A, then BN rows of W
+    constexpr int STAGE = GBLK * KG;
     constexpr int OPITCH = BN + 8;                         // staged bf16 output row (16-byte pad)
-    constexpr int SMEM = STAGES * STAGE > BM * OPITCH ? STAGES * STAGE : BM * OPITCH;
+    constexpr int SMEM0 = STAGES * STAGE > BM * OPITCH ? STAGES * STAGE : BM * OPITCH;
+    // Gated epilogue through LDS (small tiles): an fp32 row-major copy of the
+    // tile, FPITCH floats per row.
+    constexpr int FPITCH = BN + 4;
+    constexpr bool STAGE_GATED = EPI == BC_EPI_GATE_RES && BM * FPITCH * 4 <= 96 * 1024;
+    constexpr int RED = STAGE_GATED ? BM * FPITCH * 2 : KG > 1 ? NWG * TM * TN * 64 * 4 * 2 : 0;   // in bf16 units
+    constexpr int SMEM = SMEM0 > RED ? SMEM0 : RED;
     __shared__ __attribute__((aligned(1024))) T sm[SMEM];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int kg = wave / NWG, wig = wave % NWG;
+    const int wm = wig / WAVES_N, wn = wig % WAVES_N;
     const int jn = NREM == 0 ? TN : NBLK / WAVES_N + (wn < NREM ? 1 : 0);    // this wave's column blocks
     const int j0 = NREM == 0 ? wn * TN : wn * (NBLK / WAVES_N) + min(wn, NREM);
 
@@ -508,34 +535,37 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_wide_kernel(GemmA
     const int nwg = gridDim.x;
     int pid = blockIdx.x;
     if ((nwg & 7) == 0) pid = (pid & 7) * (nwg >> 3) + (pid >> 3);
+    const int tile = pid;
     constexpr int GROUP_M = 8;
     const int group = GROUP_M * tiles_n;
-    const int first_m = (pid / group) * GROUP_M;
+    const int first_m = (tile / group) * GROUP_M;
     const int gm = min(tiles_m - first_m, GROUP_M);
-    const int tm = first_m + (pid % group) % gm;
-    const int tn = (pid % group) / gm;
+    const int tm = first_m + (tile % group) % gm;
+    const int tn = (tile % group) / gm;
     const int bm = tm * BM, bn = tn * BN;
 
-    // Load o = wave + NW q of a k-step fills rows RPI o .. RPI o + RPI - 1 of
-    // the stage (A rows first, then W rows); lane L loads row RPI o + L / CPR
-    // into slot L % CPR, fetching the global chunk that the swizzle puts there.
+    // Load o = wave + NW q of a stage fills rows RPI (o % GOCT) .. + RPI - 1 of
+    // group block o / GOCT (A rows first, then W rows); lane L loads row
+    // RPI (o % GOCT) + L / CPR into slot L % CPR, fetching the global chunk
+    // that the swizzle puts there.
     const T* src[QMAX];
     const int lrow = lane / CPR, lslot = lane % CPR;
 #pragma unroll
     for (int q = 0; q < QMAX; ++q) {
-        const int o = wave + NW * q;
-        const int r = RPI * o + lrow;
+        const int o = min(wave + NW * q, NOCT - 1);
+        const int og = o / GOCT, r = RPI * (o % GOCT) + lrow;
         const T* p;
         if (r < BM) p = static_cast<const T*>(g.A) + (int64_t)min(bm + r, g.M - 1) * g.lda;
         else p = static_cast<const T*>(g.W) + (int64_t)min(bn + r - BM, g.N - 1) * g.ldw;
-        src[q] = p + wslot<BK>(lslot, r) * 8;
+        src[q] = p + og * BK + wslot<BK>(lslot, r) * 8;
     }
+    const int nk = g.K / (BK * KG);                        // stages
     auto issue = [&](int kt, int buf) {
-        const int k0 = kt * BK;
+        const int k0 = kt * BK * KG;
 #pragma unroll
         for (int q = 0; q < QMAX; ++q) {
             const int o = wave + NW * q;
-            if (NOCT % NW == 0 || o < NOCT) dma16(src[q] + k0, &sm[buf * STAGE + o * RPI * BK]);
+            if (NOCT % NW == 0 || o < NOCT) dma16(src[q] + k0, &sm[buf * STAGE + (o / GOCT) * GBLK + (o % GOCT) * RPI * BK]);
         }
     };
 
@@ -546,7 +576,6 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_wide_kernel(GemmA
         for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     EpiPrefetch<EPI, TM, TN> pf;
-    const int nk = g.K / BK;
 #pragma unroll
     for (int p = 0; p < STAGES - 1; ++p)
         if (p < nk) issue(p, p);
@@ -562,8 +591,8 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_wide_kernel(GemmA
         }
         __syncthreads();
         if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
-        if (EPI == BC_EPI_GATE_RES && kt == nk - 1) pf.load(g, bm + wm * WM, bn + j0 * 16, lane, jn);
-        const T* st = sm + (kt % STAGES) * STAGE;
+        if (EPI == BC_EPI_GATE_RES && !STAGE_GATED && kg == 0 && kt == nk - 1) pf.load(g, bm + wm * WM, bn + j0 * 16, lane, jn);
+        const T* st = sm + (kt % STAGES) * STAGE + kg * GBLK;
 #pragma unroll
         for (int kk = 0; kk < BK / 32; ++kk) {
             const int c = kk * 4 + grp;
@@ -587,6 +616,74 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_wide_kernel(GemmA
         }
     }
 
+    if constexpr (STAGE_GATED) {
+        // The tile goes through LDS as fp32 rows (group 1's partial first, then
+        // group 0 adds its own: a fixed order), and all waves then apply the
+        // gated residual to whole rows, reading the residual and gate and
+        // writing the stream as consecutive 16-byte chunks.
+        const GemmEpi& e = g.e;
+        float* ft = reinterpret_cast<float*>(sm);
+        __syncthreads();   // every wave is done with the stage buffers
+        for (int pass = KG - 1; pass >= 0; --pass) {
+            if (kg == pass) {
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    if (j >= jn) break;
+                    const int lc = (j0 + j) * 16 + 4 * (lane >> 4);
+#pragma unroll
+                    for (int i = 0; i < TM; ++i) {
+                        f32x4* dst = reinterpret_cast<f32x4*>(ft + (wm * WM + i * 16 + (lane & 15)) * FPITCH + lc);
+                        *dst = pass == KG - 1 ? acc[i][j] : *dst + acc[i][j];
+                    }
+                }
+            }
+            __syncthreads();
+        }
+        const bf16* __restrict__ bias = static_cast<const bf16*>(e.bias);
+        constexpr int NT = 64 * NW, C4 = BN / 4;              // threads; 4-column chunks per tile row
+        for (int q = tid; q < BM * C4; q += NT) {
+            const int lr = q / C4, c4 = q - lr * C4;
+            const int row = bm + lr, col = bn + c4 * 4;
+            if (row >= g.M || col >= g.N) continue;
+            const int b = row / e.seg, sidx = row - b * e.seg;
+            if (sidx >= e.keep) continue;
+            const f32x4 y = *reinterpret_cast<const f32x4*>(ft + lr * FPITCH + c4 * 4);
+            const f32x4 rv = *reinterpret_cast<const f32x4*>(e.res + (int64_t)row * e.ldr + col);
+            const f32x4 gv = e.gate ? *reinterpret_cast<const f32x4*>(e.gate + (int64_t)(row / e.rows_per_gate) * e.ldg + col)
+                                    : f32x4{1.f, 1.f, 1.f, 1.f};
+            float bv[4] = {0.f, 0.f, 0.f, 0.f};
+            if (bias) {
+                const bf16x4 b4 = *reinterpret_cast<const bf16x4*>(bias + col);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) bv[r] = (float)b4[r];
+            }
+            float v[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = rv[r] + gv[r] * (y[r] + bv[r]);
+            const int64_t o = (int64_t)(b * e.keep + sidx) * e.ldo + col;
+            if (e.out_f32) st4(static_cast<float*>(e.out) + o, v);
+            else st4(static_cast<bf16*>(e.out) + o, v);
+        }
+        return;
+    }
+    if constexpr (KG == 2) {
+        // Group 1 hands its partial tile to group 0 through LDS.
+        __syncthreads();   // every wave is done with the stage buffers
+        f32x4* red = reinterpret_cast<f32x4*>(sm) + wig * TM * TN * 64 + lane;
+        if (kg == 1) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) red[(i * TN + j) * 64] = acc[i][j];
+        }
+        __syncthreads();
+        if (kg == 0) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) acc[i][j] += red[(i * TN + j) * 64];
+        }
+    }
     if constexpr (EPI == BC_EPI_BIAS) {
         if (!g.e.out_f32) {
             // bf16 outputs leave through LDS: the waves write their finished
@@ -597,10 +694,10 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_wide_kernel(GemmA
             // at once came back as about 1.5x the output bytes in HBM writes.)
             const GemmEpi& e = g.e;
             const bf16* __restrict__ bias = static_cast<const bf16*>(e.bias);
-            __syncthreads();   // every wave is done with the stage buffers
+            __syncthreads();   // every wave is done with the stage buffers (and the reduction)
 #pragma unroll
             for (int j = 0; j < TN; ++j) {
-                if (j >= jn) break;
+                if (j >= jn || kg != 0) break;
                 const int lc = (j0 + j) * 16 + 4 * (lane >> 4);
                 const int col = bn + lc;
                 float bv[4] = {0.f, 0.f, 0.f, 0.f};
@@ -637,13 +734,15 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_wide_kernel(GemmA
             return;
         }
     }
+    if (kg != 0) return;
     epilogue_t<EPI, TM, TN>(g, acc, bm + wm * WM, bn + j0 * 16, lane, jn, pf);
 }
 
-template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES = 2, int BK = 64>
+template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES = 2, int BK = 64, int KG = 1>
 static void launch_wide(const GemmArgs& g, hipStream_t s) {
     const unsigned tiles = (unsigned)(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN));
-    launch_k(gemm_wide_kernel<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, BK>, dim3(tiles), dim3(64 * WAVES_M * WAVES_N), s, g);
+    launch_k(gemm_wide_kernel<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, BK, KG>, dim3(tiles),
+             dim3(64 * WAVES_M * WAVES_N * KG), s, g);
 }
 
 template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int SW = 0>
@@ -690,8 +789,12 @@ static bool wide_ok(const GemmArgs& g, int epi) {
 //   * at least one full round of 256 x 288 tiles over the 256 CUs: 256 x 288
 //     (8 waves of 64 x 144), or 256 x 256 when N is a multiple of 256 but not
 //     of 288 (no ragged column tile);
+//   * N a multiple of 432 with at least one round of 128 x 432 tiles (the
+//     DiT-XL/2 QKV projection: exactly 256): 2 x 4 waves of 64 x 112 / 64 x 96;
 //   * at most 256 tiles of 128 x 144 (the N = 1152 projections at M = 4096):
-//     128 x 144, 2 x 4 waves of 64 x 48 / 64 x 32;
+//     2 x 4 waves of 64 x 48 / 64 x 32, with the gated epilogue staged
+//     through LDS; for the plain epilogue with K % 128 == 0, K split over two
+//     groups of 2 x 2 waves (64 x 80 / 64 x 64) instead;
 //   * otherwise 128 x 128 (8 waves of 32 x 64, two workgroups per CU).
 // Other bf16 operands take the direct-to-LDS kernel with the scalar
 // epilogue, or the register-staged kernel; fp32 the register-staged kernel.
@@ -707,8 +810,11 @@ static int run_gemm(const GemmArgs& g, hipStream_t s) {
             if (tiles288 >= 256) {
                 if (g.N % 288 != 0 && g.N % 256 == 0) launch_wide<EPI, 256, 256, 4, 2>(g, s);
                 else launch_wide<EPI, 256, 288, 4, 2>(g, s);
+            } else if (g.N % 432 == 0 && (int64_t)((g.M + 127) / 128) * (g.N / 432) >= 256) {
+                launch_wide<EPI, 128, 432, 2, 4>(g, s);
             } else if (tiles144 <= 256) {
-                launch_wide<EPI, 128, 144, 2, 4>(g, s);
+                if (EPI == BC_EPI_BIAS && g.K % 128 == 0) launch_wide<EPI, 128, 144, 2, 2, 2, 64, 2>(g, s);
+                else launch_wide<EPI, 128, 144, 2, 4>(g, s);
             } else {
                 launch_wide<EPI, 128, 128, 4, 2>(g, s);
             }

@@ -51,9 +51,11 @@ def _check_block(got, x, exp, tol):
     return e_upd
 
 
-@pytest.mark.parametrize("name,B", [("tiny", 2), ("dit_xl2", 2), ("dit_xl2", 16)])
-def test_dit_block(bclib, name, B):
-    cfg = synth.scaled(synth.CONFIGS[name], depth=1)
+@pytest.mark.parametrize("name,B,latent", [("tiny", 2, None), ("dit_xl2", 2, None), ("dit_xl2", 16, None),
+                                           ("dit_xl2", 3, (4, 16, 16))])
+def test_dit_block(bclib, name, B, latent):
+    # (dit_xl2, B 3, 16x16 latent): 192 rows, a ragged row tile for the split-K projections.
+    cfg = synth.scaled(synth.CONFIGS[name], depth=1, **({"latent": latent} if latent else {}))
     P = synth.params(cfg)
     M = om.Model(cfg, P)
     x = synth.normal("blk/x", (B, cfg.tokens, cfg.hidden))
