@@ -116,6 +116,57 @@ def test_single_block(bclib):
     _check_block(got, x, exp, 2e-2)
 
 
+# Full token shapes of the PixArt (4096 tokens) and HunyuanVideo (14 310 + 256
+# tokens) workloads.  The oracle computes these in fp32 (fp64 would take
+# minutes on the host); the hunyuan-shaped blocks keep the full token count and
+# head_dim 128 with the width reduced to 2 heads (D 256).
+
+def test_pixart_block_full_tokens(bclib):
+    cfg = synth.scaled(synth.CONFIGS["pixart"], depth=1, batch=1)
+    P = synth.params(cfg)
+    M = om.Model(cfg, P, dtype=np.float32)
+    B, D = 1, cfg.hidden
+    x = synth.normal("pfull/x", (B, cfg.tokens, D))
+    t6 = synth.normal("pfull/t6", (B, 6 * D), 0.3)
+    ctx = synth.bf16_round(synth.normal("pfull/ctx", (B, cfg.ctx_tokens, D)))
+    y = om.linear(ctx.astype(np.float32), M.P["blocks.0.wx_kv"], M.P["blocks.0.bx_kv"])
+    kv = [(om.split_heads(y[..., :D], cfg.heads), om.split_heads(y[..., D:], cfg.heads))]
+    mod = M.block_mod(0, {"t6": t6.astype(np.float32)})
+    exp = M.dit_block(0, x.astype(np.float32), mod, {"kv": kv}).astype(np.float64)
+    got, _ = _block_call(bclib, cfg, P, bclib.BLOCK_PIXART, x, t6, ctx=ctx)
+    _check_block(got, x, exp, 2e-2)
+
+
+def _mm_full_tokens_cfg():
+    return synth.scaled(synth.CONFIGS["hunyuan"], depth=1, depth_single=1, hidden=256, heads=2, head_dim=128,
+                        mlp=1024, batch=1)
+
+
+def test_dual_block_full_tokens(bclib):
+    cfg = _mm_full_tokens_cfg()
+    assert cfg.tokens == 14310 and cfg.txt_tokens == 256
+    P = synth.params(cfg)
+    M = om.Model(cfg, P, dtype=np.float32)
+    x = synth.normal("dfull/x", (1, cfg.tokens, cfg.hidden))
+    xt = synth.normal("dfull/xt", (1, cfg.txt_tokens, cfg.hidden))
+    c = synth.normal("dfull/c", (1, cfg.hidden), 0.5)
+    ei, et = M.dual_block(0, x.astype(np.float32), xt.astype(np.float32), {"c": c.astype(np.float32)})
+    gi, gt = _block_call(bclib, cfg, P, bclib.BLOCK_DUAL, x, c, x_txt=xt)
+    _check_block(gi, x, ei.astype(np.float64), 2e-2)
+    _check_block(gt, xt, et.astype(np.float64), 2e-2)
+
+
+def test_single_block_full_tokens(bclib):
+    cfg = _mm_full_tokens_cfg()
+    P = synth.params(cfg)
+    M = om.Model(cfg, P, dtype=np.float32)
+    x = synth.normal("sfull/x", (1, cfg.tokens + cfg.txt_tokens, cfg.hidden))
+    c = synth.normal("sfull/c", (1, cfg.hidden), 0.5)
+    exp = M.single_block(0, x.astype(np.float32), {"c": c.astype(np.float32)}).astype(np.float64)
+    got, _ = _block_call(bclib, cfg, P, bclib.BLOCK_SINGLE, x, c, l=1)
+    _check_block(got, x, exp, 2e-2)
+
+
 def test_block_rejects_bad_shapes(bclib):
     desc = bclib.block_desc(bclib.BLOCK_DIT, 1, 16, 120, 3, 40, 256, bclib.BF16)
     with pytest.raises(bclib.BCError) as e:
@@ -215,6 +266,41 @@ def test_sample_mmdit_reduced(bclib, B):
     exp = _oracle_sample(cfg, P, xT, mask, text=text)
     err = rel_l2(got, exp)
     print(f"mmdit reduced B={B} final latents rel-L2 {err:.2e}")
+    assert err <= 2e-2
+    _check_ring(ring, mask, cfg.K)
+
+
+def test_sample_mmdit_full_schedule(bclib):
+    """The hunyuan schedule as configured (50 Euler steps, K = 3, a full step
+    every 5th: 11 of 50) on the reduced-size dual/single-stream model."""
+    cfg = _mm_cfg(batch=1)
+    assert cfg.steps == 50
+    P = synth.params(cfg)
+    mask = bary.make_mask(cfg.steps, cfg.interval)
+    assert int(mask.sum()) == 11
+    text = synth.text(cfg, batch=1)
+    xT, got, ring = _run_sample(bclib, cfg, P, 1, mask, text=text)
+    exp = _oracle_sample(cfg, P, xT, mask, text=text)
+    err = rel_l2(got, exp)
+    print(f"mmdit full schedule final latents rel-L2 {err:.2e}")
+    assert err <= 2e-2
+    _check_ring(ring, mask, cfg.K)
+
+
+def test_sample_pixart_full_tokens(bclib):
+    """The PixArt workload at its full token shape (128 x 128 x 4 latent: 4096
+    tokens, cross-attention to 120 text tokens of width 4096) and its full
+    schedule (20 DPM-Solver++(2M) steps, K = 4, 6 full), with the depth reduced
+    to 2 blocks and one sample; oracle in fp32."""
+    cfg = synth.scaled(synth.CONFIGS["pixart"], depth=2, batch=1)
+    assert cfg.tokens == 4096 and cfg.steps == 20
+    P = synth.params(cfg)
+    mask = bary.make_mask(cfg.steps, cfg.interval)
+    text = synth.text(cfg, batch=1)
+    xT, got, ring = _run_sample(bclib, cfg, P, 1, mask, text=text)
+    exp = _oracle_sample(cfg, P, xT, mask, text=text, dtype=np.float32)
+    err = rel_l2(got, exp)
+    print(f"pixart full tokens, depth 2, final latents rel-L2 {err:.2e}")
     assert err <= 2e-2
     _check_ring(ring, mask, cfg.K)
 
