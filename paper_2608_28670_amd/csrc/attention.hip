@@ -436,34 +436,47 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
             }
         }
 
+        // Softmax in the log2 domain on raw scores (the scale is positive, so
+        // the row max can be taken before scaling and folded into one FMA).
+        // The reference max m_run moves only when some lane's row max exceeds
+        // it by more than 8 (log2 units), so the rescale of O and l is rare
+        // after the first tiles; until then p = 2^(s c - m c) stays below 2^8.
+        // Keys past Tk exist only in the last tile.
+        const bool tail = k0 + kKTile > Tk;
+        const float c = a.scale_log2;
 #pragma unroll
         for (int g = 0; g < QG; ++g) {
+            if (tail) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (k0 + 16 * j + 4 * grp + r >= Tk) s[g][j][r] = -INFINITY;
+            }
             float mloc = -INFINITY;
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int key = k0 + 16 * j + 4 * grp + r;
-                    const float v = key < Tk ? s[g][j][r] * a.scale_log2 : -INFINITY;
-                    s[g][j][r] = v;
-                    mloc = fmaxf(mloc, v);
-                }
+                mloc = fmaxf(fmaxf(mloc, fmaxf(s[g][j][0], s[g][j][1])), fmaxf(s[g][j][2], s[g][j][3]));
             mloc = group_max(mloc);
-            const float m_new = fmaxf(m_run[g], mloc);
-            const float alpha = __builtin_amdgcn_exp2f(m_run[g] - m_new);
+            const float m_cand = fmaxf(m_run[g], mloc);
+            if (__any((m_cand - m_run[g]) * c > 8.0f)) {     // true on the first tile (m_run = -inf)
+                const float alpha = __builtin_amdgcn_exp2f((m_run[g] - m_cand) * c);
+                l_run[g] *= alpha;
+#pragma unroll
+                for (int i = 0; i < S::DV / 16; ++i) o[g][i] *= alpha;
+                m_run[g] = m_cand;
+            }
+            const float mc = m_run[g] * c;
             float lsum = 0.f;
 #pragma unroll
             for (int j = 0; j < 4; ++j)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const float p = __builtin_amdgcn_exp2f(s[g][j][r] - m_new);
+                    const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[g][j][r], c, -mc));
                     s[g][j][r] = p;
                     lsum += p;
                 }
-            l_run[g] = l_run[g] * alpha + lsum;   // this lane's keys only; summed over the group at the end
-            m_run[g] = m_new;
-#pragma unroll
-            for (int i = 0; i < S::DV / 16; ++i) o[g][i] *= alpha;
+            l_run[g] += lsum;   // this lane's keys only; summed over the group at the end
         }
 
 #pragma unroll
