@@ -652,6 +652,12 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
         return BC_OK;
     };
 
+    // The fused final step needs 16-byte aligned ring slots and weights (checked
+    // here once) and an instantiated (D, p*p*C_out).
+    const bool fused_final = final_step_supported(dt, D, d.patch * d.patch * d.out_ch, T) &&
+                             reinterpret_cast<uintptr_t>(ring->storage) % 16 == 0 && (ring->numel * esz) % 16 == 0 &&
+                             reinterpret_cast<uintptr_t>(mw.final_w) % 16 == 0;
+
     int full_index = 0;
     for (int k = 0; k < S; ++k) {
         const bc_plan_step& st = plan[k];
@@ -699,7 +705,36 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
             }
             BC_TRY(bc_cache_push(ring, nullptr, (double)k, stream));
             feat = slot;
-        } else {
+        }
+        const int NO = d.patch * d.patch * d.out_ch;
+        const SamplerCoef sc = sampler_coef(sampler, k, S, tau.data(), ab, &h_prev);
+        if (fused_final && (st.is_full || st.count <= kFinalMaxK)) {
+            // Stepwise feature (the new slot, or the forecast from the ring), final
+            // layer and sampler update in one pass over the tokens.
+            FinalStepArgs fa;
+            if (st.is_full) {
+                fa.K = 1;
+                fa.src[0] = feat;
+                fa.w[0] = 1.f;
+            } else {
+                fa.K = st.count;
+                for (int j = 0; j < st.count; ++j) {
+                    fa.src[j] = ring->storage + (int64_t)st.slots[j] * ring->numel * esz;
+                    fa.w[j] = (float)st.w[j];
+                }
+            }
+            fa.B = B; fa.T = T; fa.D = D; fa.NO = NO; fa.C_out = d.out_ch;
+            fa.fmod = fmod;
+            fa.W = mw.final_w;
+            fa.bias = mw.final_b;
+            fa.sc = sc;
+            fa.x = latents;
+            fa.prev = w.prev;
+            fa.ls = ls;
+            BC_TRY(launch_final_step(fa, s));
+            continue;
+        }
+        if (!st.is_full) {
             const void* src[kMaxK];
             float wf[kMaxK];
             for (int j = 0; j < st.count; ++j) {
@@ -712,14 +747,12 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
         // Final layer: LayerNorm + adaLN, then the linear to p*p*C_out per token
         // (token layout; the sampler reads it back through unpatchify).
         BC_TRY(launch_ln_mod(dt, feat, (int64_t)B * T, D, fmod, fmod + D, 2 * D, T, dt, w.bb.h, s));
-        const int NO = d.patch * d.patch * d.out_ch;
         GemmArgs fg = gemm_args(w.bb.h, D, mw.final_w, D, B * T, NO, D);
         fg.e.bias = mw.final_b;
         fg.e.out = w.out;
         fg.e.ldo = NO;
         fg.e.out_f32 = 1;
         BC_TRY(launch_gemm(dt, BC_EPI_BIAS, fg, s));
-        const SamplerCoef sc = sampler_coef(sampler, k, S, tau.data(), ab, &h_prev);
         BC_TRY(launch_sampler(sc, latents, w.out, w.prev, ls, B, d.out_ch, s));
     }
     return BC_OK;

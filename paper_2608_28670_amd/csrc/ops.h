@@ -78,4 +78,45 @@ struct SamplerCoef { float c[6]; int mode; };
 int launch_sampler(const SamplerCoef& k, float* x, const float* out_tok, float* prev, LatentShape ls, int B, int C_out,
                    hipStream_t s);
 
+// The update of one latent element from its model output e (the modes above).
+__device__ __forceinline__ void sampler_update(const SamplerCoef& k, float* x, float e, float* prev) {
+    const float xv = *x;
+    if (k.mode == 0) {
+        *x = k.c[0] * xv + k.c[1] * e;
+        return;
+    }
+    const float x0 = (xv - k.c[2] * e) / k.c[3];
+    if (k.mode == 2) {
+        *x = x0;
+        return;
+    }
+    const float d = k.c[5] != 0.f ? k.c[4] * x0 + k.c[5] * *prev : k.c[4] * x0;
+    *x = k.c[0] * xv + k.c[1] * d;
+    if (prev) *prev = x0;
+}
+
+// Final step fused over 16-token groups, for bf16 models whose (D, p*p*C_out)
+// has an instantiated variant (final_step_supported): the stepwise feature
+// sum_j w[j] src[j] (rounded to bf16 like the unfused forecast), LayerNorm +
+// adaLN (fmod [B, 2D]: shift, scale), the final linear (W [NO, D], bias [NO])
+// and the sampler update of the latent pixels the tokens cover.  Returns
+// BC_ERR_UNSUPPORTED for other shapes (the caller then runs the separate
+// kernels).
+constexpr int kFinalMaxK = 4;   // cached features the fused final step takes
+struct FinalStepArgs {
+    const void* src[8];
+    float w[8];
+    int K;
+    int B, T, D, NO, C_out;
+    const float* fmod;
+    const void* W;
+    const void* bias;
+    SamplerCoef sc;
+    float* x;
+    float* prev;
+    LatentShape ls;
+};
+bool final_step_supported(int dt, int D, int NO, int T);
+int launch_final_step(const FinalStepArgs& a, hipStream_t s);
+
 }  // namespace bc

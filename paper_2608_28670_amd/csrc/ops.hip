@@ -468,19 +468,7 @@ __global__ void sampler_kernel(SamplerCoef k, float* x, const float* out_tok, fl
     const int tok = (f * hp + ys / ls.p) * wp + xs / ls.p;
     const int feat = ((ys % ls.p) * ls.p + xs % ls.p) * C_out + c;
     const float e = out_tok[((int64_t)b * ls.tokens() + tok) * (ls.p * ls.p * C_out) + feat];
-    const float xv = x[i];
-    if (k.mode == 0) {
-        x[i] = k.c[0] * xv + k.c[1] * e;
-        return;
-    }
-    const float x0 = (xv - k.c[2] * e) / k.c[3];
-    if (k.mode == 2) {
-        x[i] = x0;
-        return;
-    }
-    const float d = k.c[5] != 0.f ? k.c[4] * x0 + k.c[5] * prev[i] : k.c[4] * x0;
-    x[i] = k.c[0] * xv + k.c[1] * d;
-    if (prev) prev[i] = x0;
+    sampler_update(k, x + i, e, prev ? prev + i : nullptr);
 }
 
 int launch_sampler(const SamplerCoef& k, float* x, const float* out_tok, float* prev, LatentShape ls, int B, int C_out,
