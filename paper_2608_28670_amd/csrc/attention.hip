@@ -544,8 +544,16 @@ static int run_attention_dma(const AttnArgs& a, int hd, hipStream_t s) {
     dim3 grid((unsigned)nwg), block(64 * NWV);
     switch (hd) {
 #define BC_ATT_CASE(HD) case HD: launch_k(attention_dma_kernel<HD, QG, NWV, NB>, grid, block, s, a); break;
-        BC_ATT_CASE(32) BC_ATT_CASE(64) BC_ATT_CASE(72) BC_ATT_CASE(128)
+        BC_ATT_CASE(32) BC_ATT_CASE(64) BC_ATT_CASE(72)
 #undef BC_ATT_CASE
+        case 128:
+            // 64 queries per wave at d = 128 would spill: only up to 32.
+            if constexpr (QG <= 2) {
+                launch_k(attention_dma_kernel<128, QG, NWV, NB>, grid, block, s, a);
+                break;
+            } else {
+                return fail(BC_ERR_UNSUPPORTED, "head_dim 128 with %d query groups per wave", QG);
+            }
         default: return fail(BC_ERR_UNSUPPORTED, "head_dim %d (supported: 32, 64, 72, 128)", hd);
     }
     return check_launch("attention");
@@ -583,11 +591,15 @@ int launch_attention(int dtype, AttnArgs a, hipStream_t s) {
     // The direct-to-LDS kernel needs 16-byte aligned Q/K/V rows (checked above).
     // Up to 256 keys: 8 waves of 16 queries with every key tile resident in
     // LDS (one load, no barriers in the key loop); longer sequences: 8 waves
-    // of 32 queries over a double buffer.
+    // over a double buffer, 64 queries each for d <= 72 (every K/V fragment
+    // read from LDS feeds four MFMAs: LDS reads bound this loop) and 32 for
+    // d = 128 (64 would not fit the registers).
     int rc;
     if (dtype == BC_BF16) {
         const int Tk = a.Tk0 + a.Tk1;
-        rc = Tk <= 4 * kKTile ? run_attention_dma<1, 8, 4>(a, a.d, s) : run_attention_dma<2, 8, 2>(a, a.d, s);
+        if (Tk <= 4 * kKTile) rc = run_attention_dma<1, 8, 4>(a, a.d, s);
+        else if (a.d <= 72) rc = run_attention_dma<4, 8, 2>(a, a.d, s);
+        else rc = run_attention_dma<2, 8, 2>(a, a.d, s);
     } else {
         rc = run_attention<float, 1>(a, a.d, s);
     }
