@@ -8,10 +8,11 @@ model (28 blocks, D 1152, 16 x 72 heads, MLP 4608, 256 tokens), batch 16,
 50 DDIM steps, K = 3, one full step every 4 (14 of 50), bf16, random-init
 weights drawn from seed 2026.
 
-Prints one JSON line: samples/s, the dominant kernel's roofline (the fc1
-GEMM with GELU epilogue, timed with HIP events on its launch stream), the
-forecast kernel's HBM bandwidth on [8, 16384, 3072] features, the speedup over
-the all-full mask, and the oracle's CPU throughput on a bounded sample.
+Prints one JSON line: samples/s, the roofline of the dominant kernel (of the
+fc2, fc1 and self-attention kernels, the one with the most time per run, each
+timed with HIP events on its launch stream; the others follow), the forecast
+kernel's HBM bandwidth on [8, 16384, 3072] features, the speedup over the
+all-full mask, and the oracle's CPU throughput on a bounded sample.
 """
 import argparse
 import hashlib
@@ -65,7 +66,6 @@ def counters_traffic(kernel_tag, src_hash, launches_bytes_ref):
 def forecast_bench(bc, torch, dev, K=3, dtype="bf16", iters=10):
     """HBM bandwidth of the forecast kernel on K cached [8, 16384, 3072] features."""
     import synth
-    from oracle import bary  # noqa: F401  (not used for timing; weights come from the library)
     shape = synth.FORECAST_SHAPE
     n = shape[0] * shape[1] * shape[2]
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
@@ -163,7 +163,6 @@ def main():
     import synth
     import paper_2608_28670_amd as bc
     from paper_2608_28670_amd import loader
-    from oracle import bary
 
     if not os.path.exists(bc.LIB_PATH):
         from paper_2608_28670_amd import build
@@ -177,7 +176,7 @@ def main():
     params = synth.params(cfg) if host_weights else None
     dm = loader.DeviceModel(cfg, params, dev_params=None if host_weights else device_params(cfg, torch, dev))
     B = cfg.batch
-    mask = bary.make_mask(cfg.steps, cfg.interval)
+    mask = bc.make_mask(cfg.steps, cfg.interval)
     labels = synth.labels(cfg) if cfg.n_classes else None
     text = synth.text(cfg) if cfg.kind != "dit" else None
     xT = synth.latents(cfg)
@@ -213,27 +212,55 @@ def main():
     torch.cuda.synchronize()
     ms_full = (time.perf_counter() - tf) / nref * 1e3
 
-    # Dominant kernel: the fc1 GEMM (bias + GELU epilogue), HIP events on its
-    # stream.  Defined for the DiT / PixArt block (one fc1 shape per block).
+    # Kernel classes timed with per-launch HIP events on their launch stream
+    # in one extra sampling run (the events ride on the launches themselves):
+    # where a full step's time goes, and the roofline of the dominant kernel.
     nfull = int(mask.sum())
-    roofline = None
+    classes = {"gemm_gelu": bc.PROF_GEMM_GELU, "gemm_down": bc.PROF_GEMM_DOWN, "gemm_gated": bc.PROF_GEMM_GATE,
+               "gemm_bias": bc.PROF_GEMM_BIAS, "attention": bc.PROF_ATTENTION, "layernorm": bc.PROF_LAYERNORM}
+    cap = 16 * nfull * cfg.depth + 1024
+    for c in classes.values():
+        bc.profile_enable(c, cap)
+    run(mask)
+    breakdown, times = {}, {}
+    for name, c in classes.items():
+        t = bc.profile_times(c, cap).astype(np.float64)
+        times[name] = t
+        if len(t):
+            breakdown[name] = {"ms_per_run": round(float(t.sum()), 3), "launches": len(t),
+                               "avg_us": round(float(t.mean()) * 1e3, 2)}
+    roofline, others = None, []
     if cfg.kind in ("dit", "pixart"):
-        launches = nfull * cfg.depth
-        bc.profile_enable(bc.PROF_GEMM_GELU, launches)
-        run(mask)
-        gemm_ms, gemm_n = bc.profile_collect(bc.PROF_GEMM_GELU)
         M_rows = B * cfg.tokens
-        flops = 2.0 * M_rows * cfg.mlp * cfg.hidden
-        avg_s = gemm_ms / gemm_n / 1e3
-        achieved = flops / avg_s / 1e12
+        nb = nfull * cfg.depth
         gemm_hash = source_hash("gemm.hip", "gemm.h", "hip_common.h")
-        roofline = {"bound": "mfma", "kernel": "gemm fc1 (bias+GELU)",
-                    "shape": [M_rows, cfg.mlp, cfg.hidden], "flops_per_launch": flops,
-                    "avg_us": round(avg_s * 1e6, 2), "launches": gemm_n,
-                    "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                    "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                    "traffic": counters_traffic(f"gemm_fc1_{cfg.name}", gemm_hash, None) if cfg.name == "dit_xl2" else None,
-                    "source_hash": gemm_hash}
+        att_hash = source_hash("attention.hip", "attention.h", "hip_common.h")
+        # One launch per block and full step for each candidate.  PixArt's
+        # caption MLP (once per run, before the loop) is the first GELU GEMM;
+        # its cross-attention follows each self-attention.
+        att = times["attention"] if cfg.kind == "dit" else times["attention"][0::2]
+        cands = [
+            ("gemm fc2 (gated residual, MLP down projection)", times["gemm_down"], "mfma",
+             2.0 * M_rows * cfg.hidden * cfg.mlp, [M_rows, cfg.hidden, cfg.mlp], f"gemm_fc2_{cfg.name}", gemm_hash),
+            ("gemm fc1 (bias+GELU)", times["gemm_gelu"][-nb:], "mfma",
+             2.0 * M_rows * cfg.mlp * cfg.hidden, [M_rows, cfg.mlp, cfg.hidden], f"gemm_fc1_{cfg.name}", gemm_hash),
+            ("self-attention", att, "mfma",
+             4.0 * B * cfg.heads * cfg.tokens * cfg.tokens * cfg.head_dim,
+             [B, cfg.heads, cfg.tokens, cfg.head_dim], f"attention_{cfg.name}", att_hash),
+        ]
+        recs = []
+        for name, t, bound, flops, shape, tag, h in cands:
+            assert len(t) == nb, (name, len(t), nb)
+            avg_s = float(t.mean()) / 1e3
+            achieved = flops / avg_s / 1e12
+            recs.append((float(t.sum()), {
+                "bound": bound, "kernel": name, "shape": shape, "flops_per_launch": flops,
+                "avg_us": round(avg_s * 1e6, 2), "launches": len(t), "ms_per_run": round(float(t.sum()), 3),
+                "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": counters_traffic(tag, h, None), "source_hash": h}))
+        recs.sort(key=lambda r: -r[0])
+        roofline, others = recs[0][1], [r[1] for r in recs[1:]]
 
     forecast = None
     if not args.no_forecast:
@@ -273,6 +300,8 @@ def main():
         "speedup_vs_all_full": round(ms_full / ms_per_step, 3),
         "ms_all_full": round(ms_full, 3),
         "roofline": roofline,
+        "roofline_others": others,
+        "kernel_classes": breakdown,
         "forecast": forecast,
         "cpu_baseline": cpu,
     }

@@ -338,10 +338,16 @@ int bc_attention_workspace_size(int B, int H, int Tq, int Tk, int d, int dtype, 
  * While enabled for a kernel class, every launch of that class is bracketed by
  * two events (at most max_launches).  bc_profile_collect waits for them and
  * returns the summed duration and the number of launches, then disables.
- * Classes: 0 forecast, 1 GEMM with GELU epilogue, 2 GEMM gated residual,
- * 3 GEMM bias (QKV), 4 attention, 5 layernorm-modulate. */
+ * Classes: 0 forecast, 1 GEMM with GELU epilogue, 2 GEMM gated residual with
+ * K <= N (attention output projection), 3 GEMM bias (QKV), 4 attention,
+ * 5 layernorm-modulate, 6 GEMM gated residual with K > N (MLP down
+ * projection). */
 int bc_profile_enable(int kernel_class, int max_launches);
 int bc_profile_collect(int kernel_class, double* total_ms, int* launches);
+/* As bc_profile_collect, but writes each launch's duration in ms, in launch
+ * order, to ms_out (host, max_out entries; later launches are dropped) and
+ * their number to *launches. */
+int bc_profile_times(int kernel_class, float* ms_out, int max_out, int* launches);
 
 #ifdef __cplusplus
 }

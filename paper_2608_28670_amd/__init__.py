@@ -24,7 +24,7 @@ BLOCK_DIT, BLOCK_PIXART, BLOCK_DUAL, BLOCK_SINGLE = range(4)
 MODEL_DIT, MODEL_PIXART, MODEL_MMDIT = range(3)
 SAMPLER_DDIM, SAMPLER_DPMPP2M, SAMPLER_EULER = range(3)
 EPI_BIAS, EPI_BIAS_GELU, EPI_GATE_RES = range(3)
-PROF_FORECAST, PROF_GEMM_GELU, PROF_GEMM_GATE, PROF_GEMM_BIAS, PROF_ATTENTION, PROF_LAYERNORM = range(6)
+PROF_FORECAST, PROF_GEMM_GELU, PROF_GEMM_GATE, PROF_GEMM_BIAS, PROF_ATTENTION, PROF_LAYERNORM, PROF_GEMM_DOWN = range(7)
 SAMPLERS = {"ddim": SAMPLER_DDIM, "dpmpp2m": SAMPLER_DPMPP2M, "euler": SAMPLER_EULER}
 
 
@@ -123,6 +123,7 @@ _SIGS = {
                                               C.POINTER(C.c_size_t)]),
     "bc_profile_enable": (C.c_int, [C.c_int, C.c_int]),
     "bc_profile_collect": (C.c_int, [C.c_int, C.POINTER(C.c_double), C.POINTER(C.c_int)]),
+    "bc_profile_times": (C.c_int, [C.c_int, C.POINTER(C.c_float), C.c_int, C.POINTER(C.c_int)]),
 }
 
 
@@ -392,3 +393,11 @@ def profile_collect(kernel_class: int):
     ms, n = C.c_double(), C.c_int()
     _check(lib().bc_profile_collect(kernel_class, C.byref(ms), C.byref(n)))
     return ms.value, n.value
+
+
+def profile_times(kernel_class: int, max_launches: int) -> np.ndarray:
+    """Per-launch durations (ms) of an enabled class, in launch order; disables it."""
+    ms = np.zeros(max_launches, np.float32)
+    n = C.c_int()
+    _check(lib().bc_profile_times(kernel_class, ms.ctypes.data_as(C.POINTER(C.c_float)), max_launches, C.byref(n)))
+    return ms[:n.value]

@@ -869,7 +869,8 @@ int launch_gemm(int dtype, int epi, const GemmArgs& g, hipStream_t s) {
                     (long long)g.lda, (long long)g.ldw, epc);
     if ((reinterpret_cast<uintptr_t>(g.A) | reinterpret_cast<uintptr_t>(g.W)) % 16)
         return fail(BC_ERR_UNSUPPORTED, "GEMM operands must be 16-byte aligned");
-    const int cls = epi == BC_EPI_GATE_RES ? PROF_GEMM_GATE : g.e.gelu_from < g.N ? PROF_GEMM_GELU : PROF_GEMM_BIAS;
+    const int cls = epi == BC_EPI_GATE_RES ? (g.K > g.N ? PROF_GEMM_DOWN : PROF_GEMM_GATE)
+                    : g.e.gelu_from < g.N ? PROF_GEMM_GELU : PROF_GEMM_BIAS;
     prof_begin(cls, s);
     int rc;
     if (dtype == BC_BF16) {

@@ -69,6 +69,21 @@ int bc_profile_enable(int kernel_class, int max_launches) {
     return BC_OK;
 }
 
+int bc_profile_times(int kernel_class, float* ms_out, int max_out, int* launches) {
+    clear_error();
+    if (kernel_class < 0 || kernel_class >= PROF_NCLASS) return fail(BC_ERR_INVALID_ARG, "class %d", kernel_class);
+    if (!ms_out || max_out < 0) return fail(BC_ERR_INVALID_ARG, "ms_out");
+    ClassTimer& t = g_timer[kernel_class];
+    const int n = t.used < max_out ? t.used : max_out;
+    for (int i = 0; i < n; ++i) {
+        if (hipEventSynchronize(t.stop[i]) != hipSuccess) { release(t); return fail(BC_ERR_HIP, "event sync"); }
+        if (hipEventElapsedTime(&ms_out[i], t.start[i], t.stop[i]) != hipSuccess) { release(t); return fail(BC_ERR_HIP, "elapsed"); }
+    }
+    if (launches) *launches = n;
+    release(t);
+    return BC_OK;
+}
+
 int bc_profile_collect(int kernel_class, double* total_ms, int* launches) {
     clear_error();
     if (kernel_class < 0 || kernel_class >= PROF_NCLASS) return fail(BC_ERR_INVALID_ARG, "class %d", kernel_class);

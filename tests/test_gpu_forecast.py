@@ -134,3 +134,24 @@ def test_forecast_full_size_sampled(bclib, K, dt):
     nodes = [flat[K - 1 - j, idx].astype(np.float64) for j in range(K)]
     exact, scale = _exact(nodes, w)
     check(out[torch.from_numpy(idx).to(DEV)].float().cpu().numpy(), exact, scale, dt)
+
+
+def test_profile_times_per_launch(bclib):
+    """Per-launch HIP-event durations of a kernel class, in launch order; the
+    pool caps the count and collecting disables the class."""
+    K, n = 2, 1 << 16
+    storage = torch.randn((K, n), device=DEV)
+    ring = bclib.CacheRing(K, storage)
+    for j in range(K):
+        ring.push(None, float(K - j))
+    out = torch.empty(n, device=DEV)
+    bclib.profile_enable(bclib.PROF_FORECAST, 3)
+    for _ in range(5):
+        bclib.bary_extrapolate(ring, [2.0, -1.0], out)
+    t = bclib.profile_times(bclib.PROF_FORECAST, 8)
+    assert len(t) == 3 and np.all(t > 0) and np.all(np.isfinite(t))
+    bclib.bary_extrapolate(ring, [2.0, -1.0], out)
+    assert len(bclib.profile_times(bclib.PROF_FORECAST, 8)) == 0
+    sl = ring.state()[3]                                    # slots, newest first
+    ref = 2.0 * storage[int(sl[0])] - storage[int(sl[1])]
+    torch.testing.assert_close(out, ref, rtol=1e-6, atol=1e-6)
