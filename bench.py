@@ -36,6 +36,7 @@ def parse():
     ap.add_argument("--workload", default="dit_xl2")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-forecast", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="skip timing the HIP-graph replay of the run")
     ap.add_argument("--cpu-steps", type=int, default=9, help="oracle sample: first N steps of one sample")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run one 1 GiB device copy through the library (counter calibration)")
@@ -201,6 +202,23 @@ def main():
     ms_per_step = elapsed / args.steps * 1e3
     value = B * args.steps / elapsed
 
+    # The same run replayed from a HIP graph captured once (bc_sample_graph_*).
+    graph = None
+    if not args.no_graph:
+        g = dm.sample_graph(x, mask, labels=tl, text=tt)
+        for _ in range(max(1, args.warmup)):
+            x.copy_(x0)
+            g.launch()
+        torch.cuda.synchronize()
+        tg = time.perf_counter()
+        for _ in range(args.steps):
+            x.copy_(x0)
+            g.launch()
+        torch.cuda.synchronize()
+        eg = time.perf_counter() - tg
+        graph = {"value": round(B * args.steps / eg, 3), "ms_per_step": round(eg / args.steps * 1e3, 3)}
+        del g
+
     # Speedup reference: the same sampler with every step full.
     full = np.ones(cfg.steps, np.uint8)
     run(full)
@@ -297,6 +315,7 @@ def main():
                                f"MLP {cfg.mlp}, {cfg.tokens} tokens, batch {B}, {cfg.steps} {cfg.sampler} steps, "
                                f"K={cfg.K}, full every {cfg.interval} ({nfull}/{cfg.steps}), random-init weights",
                    "global_batch": B, "parallelism": "none (1 GPU)"},
+        "graph_replay": graph,
         "speedup_vs_all_full": round(ms_full / ms_per_step, 3),
         "ms_all_full": round(ms_full, 3),
         "roofline": roofline,

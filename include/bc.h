@@ -310,6 +310,28 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
               const int64_t* labels, const void* text, void* ws, size_t ws_bytes,
               void* stream);
 
+/* The same sampling run captured once as a HIP graph and replayed, for
+ * callers whose loop is launch-bound (small models, short schedules).
+ * bc_sample_graph_create runs nothing: it records into a graph exactly the
+ * work bc_sample would enqueue with these arguments, on `stream`, which must
+ * not be the null stream and must not be capturing; kernel timing
+ * (bc_profile_enable) must be off.  The ring's host state is left as it was.
+ * bc_sample_graph_launch replays the run on `stream` (any stream) and leaves
+ * the ring's host state as bc_sample would.  Every replay reads x_T from and
+ * writes the sample to the same `latents` buffer (refill it in between), and
+ * reads the same labels, text, weights and workspace, which must stay
+ * allocated and in place while the graph exists; the graph holds no device
+ * memory of its own.  Replays on one ring and workspace must not overlap.
+ * Errors: as bc_sample; STATE (timing on, or the stream already capturing);
+ * HIP (capture, instantiation or launch). */
+typedef struct bc_sample_graph bc_sample_graph;
+int bc_sample_graph_create(const bc_model* m, int B, int sampler, int S, const uint8_t* mask, int K,
+                           const bc_bary_params* p, bc_cache_ring* ring, float* latents,
+                           const int64_t* labels, const void* text, void* ws, size_t ws_bytes,
+                           void* stream, bc_sample_graph** out);
+int bc_sample_graph_launch(bc_sample_graph* g, void* stream);
+int bc_sample_graph_destroy(bc_sample_graph* g);
+
 /* ------------------------------------------------------------------------ */
 /* Building blocks exposed for measurement and tests                         */
 /* ------------------------------------------------------------------------ */

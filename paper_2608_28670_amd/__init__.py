@@ -115,6 +115,11 @@ _SIGS = {
     "bc_sample": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int,
                             C.POINTER(BaryParams), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
                             C.c_void_p, C.c_size_t, C.c_void_p]),
+    "bc_sample_graph_create": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int,
+                                         C.POINTER(BaryParams), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                         C.c_void_p, C.c_size_t, C.c_void_p, C.POINTER(C.c_void_p)]),
+    "bc_sample_graph_launch": (C.c_int, [C.c_void_p, C.c_void_p]),
+    "bc_sample_graph_destroy": (C.c_int, [C.c_void_p]),
     "bc_linear": (C.c_int, [C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
                             C.c_int, C.c_void_p, C.c_void_p, C.c_int, C.c_int, C.c_void_p]),
     "bc_attention": (C.c_int, [C.c_int, C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_void_p,
@@ -383,6 +388,35 @@ def sample(model: Model, B: int, sampler: str, mask, K: int, ring: CacheRing, la
     _check(lib().bc_sample(model.h, B, SAMPLERS[sampler], len(m), _ptr(m), K, C.byref(p) if p else None,
                            ring.h, dev_ptr(latents), dev_ptr(labels), dev_ptr(text), dev_ptr(ws),
                            ws.numel() * ws.element_size(), stream_handle(stream)))
+
+
+class SampleGraph:
+    """A sampling run captured once as a HIP graph (bc_sample_graph_create);
+    launch() replays it.  Every buffer the capture saw (latents, labels, text,
+    workspace, ring storage, weights) must stay alive and in place."""
+
+    def __init__(self, model: Model, B: int, sampler: str, mask, K: int, ring: CacheRing, latents, ws,
+                 labels=None, text=None, p: Optional[BaryParams] = None, stream=None):
+        import torch
+        self.stream = stream if stream is not None else torch.cuda.Stream()
+        self._keep = (model, ring, latents, ws, labels, text)
+        m = np.ascontiguousarray(mask, dtype=np.uint8)
+        h = C.c_void_p()
+        # The capture stream must see the caller's pending work before the run is recorded.
+        self.stream.wait_stream(torch.cuda.current_stream())
+        _check(lib().bc_sample_graph_create(model.h, B, SAMPLERS[sampler], len(m), _ptr(m), K,
+                                            C.byref(p) if p else None, ring.h, dev_ptr(latents),
+                                            dev_ptr(labels), dev_ptr(text), dev_ptr(ws),
+                                            ws.numel() * ws.element_size(), self.stream.cuda_stream, C.byref(h)))
+        self.h = h
+
+    def launch(self, stream=None):
+        _check(lib().bc_sample_graph_launch(self.h, stream_handle(stream)))
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            _lib.bc_sample_graph_destroy(self.h)
+            self.h = None
 
 
 def profile_enable(kernel_class: int, max_launches: int):

@@ -73,6 +73,7 @@ void prof_end(int cls, hipStream_t s);
 // Next start/stop event pair of the class bracketed by prof_begin/prof_end on
 // this thread, if that class is being timed.
 bool prof_take(hipEvent_t* start, hipEvent_t* stop);
+bool prof_any_enabled();                 // some kernel class is being timed
 
 // Kernel launch that, inside a timed bracket, has the runtime stamp the
 // kernel's own start and end into the class's events (the same interval a

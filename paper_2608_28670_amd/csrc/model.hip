@@ -759,3 +759,74 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
 }
 
 }  // extern "C"
+
+// A captured sampling run: the instantiated graph and the ring's host state
+// at the end of the run (restored on every replay).
+struct bc_sample_graph {
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+    bc_cache_ring* ring = nullptr;
+    bc_cache_ring final_state;
+};
+
+extern "C" {
+
+int bc_sample_graph_create(const bc_model* m, int B, int sampler, int S, const uint8_t* mask, int K,
+                           const bc_bary_params* p, bc_cache_ring* ring, float* latents, const int64_t* labels,
+                           const void* text, void* ws, size_t ws_bytes, void* stream, bc_sample_graph** out) {
+    clear_error();
+    if (!out || !ring) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
+    *out = nullptr;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (!s) return fail(BC_ERR_INVALID_ARG, "graph capture needs a stream other than the null stream");
+    if (prof_any_enabled()) return fail(BC_ERR_STATE, "kernel timing is enabled; collect it before capturing");
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(s, &cs) != hipSuccess) return fail(BC_ERR_HIP, "hipStreamIsCapturing failed");
+    if (cs != hipStreamCaptureStatusNone) return fail(BC_ERR_STATE, "the stream is already capturing");
+    const bc_cache_ring before = *ring;
+    if (hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal) != hipSuccess)
+        return fail(BC_ERR_HIP, "hipStreamBeginCapture failed");
+    const int rc = bc_sample(m, B, sampler, S, mask, K, p, ring, latents, labels, text, ws, ws_bytes, stream);
+    hipGraph_t graph = nullptr;
+    const hipError_t ec = hipStreamEndCapture(s, &graph);
+    const bc_cache_ring after = *ring;
+    *ring = before;   // nothing ran: the ring's host state is as it was
+    if (rc != BC_OK || ec != hipSuccess || !graph) {
+        if (graph) (void)hipGraphDestroy(graph);
+        (void)hipGetLastError();
+        return rc != BC_OK ? rc : fail(BC_ERR_HIP, "stream capture failed: %s", hipGetErrorString(ec));
+    }
+    hipGraphExec_t exec = nullptr;
+    const hipError_t ei = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    if (ei != hipSuccess) {
+        (void)hipGraphDestroy(graph);
+        return fail(BC_ERR_HIP, "hipGraphInstantiate failed: %s", hipGetErrorString(ei));
+    }
+    bc_sample_graph* g = new bc_sample_graph;
+    g->graph = graph;
+    g->exec = exec;
+    g->ring = ring;
+    g->final_state = after;
+    *out = g;
+    return BC_OK;
+}
+
+int bc_sample_graph_launch(bc_sample_graph* g, void* stream) {
+    clear_error();
+    if (!g) return fail(BC_ERR_INVALID_ARG, "NULL graph");
+    const hipError_t e = hipGraphLaunch(g->exec, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(BC_ERR_HIP, "hipGraphLaunch failed: %s", hipGetErrorString(e));
+    *g->ring = g->final_state;
+    return BC_OK;
+}
+
+int bc_sample_graph_destroy(bc_sample_graph* g) {
+    clear_error();
+    if (!g) return BC_OK;
+    if (g->exec) (void)hipGraphExecDestroy(g->exec);
+    if (g->graph) (void)hipGraphDestroy(g->graph);
+    delete g;
+    return BC_OK;
+}
+
+}  // extern "C"

@@ -46,58 +46,82 @@ template <> struct Vec4<bf16> {
     }
 };
 
-template <typename Tin, typename Tout, int NC>
+// Each wave takes RPW consecutive rows: the next row's chunks are loaded
+// while the current one is reduced, and the modulation vectors (one pair per
+// sample) are loaded once per sample instead of once per row.
+template <typename Tin, typename Tout, int NC, int RPW>
 __global__ __launch_bounds__(256) void ln_mod_kernel(const Tin* __restrict__ x, int64_t rows, int D,
                                                      const float* __restrict__ shift,
                                                      const float* __restrict__ scale, int64_t ld_mod, int rps,
                                                      Tout* __restrict__ h) {
     const int lane = threadIdx.x & 63;
-    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (row >= rows) return;
+    const int64_t row0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * RPW;
+    if (row0 >= rows) return;
     const int nch = D >> 2;
-    const Tin* xr = x + row * D;
-    const int64_t b = row / rps;
-    const float* sh = shift + b * ld_mod;
-    const float* sc = scale + b * ld_mod;
-    // The row and its modulation vectors are all loaded up front, so the two
-    // reductions overlap the modulation loads.
-    float v[NC][4], s4[NC][4], c4[NC][4];
-    float sum = 0.f;
+    float v[2][NC][4], s4[NC][4], c4[NC][4];
+    auto load_row = [&](int64_t row, float (&dst)[NC][4]) {
+        const Tin* xr = x + row * D;
 #pragma unroll
-    for (int j = 0; j < NC; ++j) {
-        const int c = lane + 64 * j;
-        if (c < nch) {
-            Vec4<Tin>::load(xr + 4 * c, v[j]);
-            Vec4<float>::load(sh + 4 * c, s4[j]);
-            Vec4<float>::load(sc + 4 * c, c4[j]);
-        } else {
+        for (int j = 0; j < NC; ++j) {
+            const int c = lane + 64 * j;
+            if (c < nch) Vec4<Tin>::load(xr + 4 * c, dst[j]);
+            else {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) v[j][e] = s4[j][e] = c4[j][e] = 0.f;
-        }
-        sum += (v[j][0] + v[j][1]) + (v[j][2] + v[j][3]);
-    }
-    const float mean = wave_sum(sum) / (float)D;
-    float sq = 0.f;
-#pragma unroll
-    for (int j = 0; j < NC; ++j) {
-        if (lane + 64 * j < nch) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float d = v[j][e] - mean;
-                sq += d * d;
+                for (int e = 0; e < 4; ++e) dst[j][e] = 0.f;
             }
         }
-    }
-    const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + kLnEps);
-    Tout* hr = h + row * D;
+    };
+    load_row(row0, v[0]);
+    int64_t cur_b = -1;
 #pragma unroll
-    for (int j = 0; j < NC; ++j) {
-        const int c = lane + 64 * j;
-        if (c < nch) {
-            float o[4];
+    for (int i = 0; i < RPW; ++i) {
+        const int64_t row = row0 + i;
+        if (row >= rows) break;
+        if (i + 1 < RPW && row + 1 < rows) load_row(row + 1, v[(i + 1) & 1]);
+        const int64_t b = row / rps;
+        if (b != cur_b) {
+            cur_b = b;
+            const float* sh = shift + b * ld_mod;
+            const float* sc = scale + b * ld_mod;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) o[e] = (v[j][e] - mean) * rstd * (1.0f + c4[j][e]) + s4[j][e];
-            Vec4<Tout>::store(hr + 4 * c, o);
+            for (int j = 0; j < NC; ++j) {
+                const int c = lane + 64 * j;
+                if (c < nch) {
+                    Vec4<float>::load(sh + 4 * c, s4[j]);
+                    Vec4<float>::load(sc + 4 * c, c4[j]);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) s4[j][e] = c4[j][e] = 0.f;
+                }
+            }
+        }
+        const float (&r)[NC][4] = v[i & 1];
+        float sum = 0.f;
+#pragma unroll
+        for (int j = 0; j < NC; ++j) sum += (r[j][0] + r[j][1]) + (r[j][2] + r[j][3]);
+        const float mean = wave_sum(sum) / (float)D;
+        float sq = 0.f;
+#pragma unroll
+        for (int j = 0; j < NC; ++j) {
+            if (lane + 64 * j < nch) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float d = r[j][e] - mean;
+                    sq += d * d;
+                }
+            }
+        }
+        const float rstd = 1.0f / sqrtf(wave_sum(sq) / (float)D + kLnEps);
+        Tout* hr = h + row * D;
+#pragma unroll
+        for (int j = 0; j < NC; ++j) {
+            const int c = lane + 64 * j;
+            if (c < nch) {
+                float o[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o[e] = (r[j][e] - mean) * rstd * (1.0f + c4[j][e]) + s4[j][e];
+                Vec4<Tout>::store(hr + 4 * c, o);
+            }
         }
     }
 }
@@ -105,16 +129,17 @@ __global__ __launch_bounds__(256) void ln_mod_kernel(const Tin* __restrict__ x, 
 template <typename Tin, typename Tout>
 static int run_ln(const void* x, int64_t rows, int D, const float* shift, const float* scale, int64_t ld_mod, int rps,
                   void* h, hipStream_t s) {
+    constexpr int RPW = 2;
     const int nc = (D / 4 + 63) / 64;
-    dim3 g((unsigned)((rows + 3) / 4)), b(256);
+    dim3 g((unsigned)((rows + 4 * RPW - 1) / (4 * RPW))), b(256);
     const Tin* xi = static_cast<const Tin*>(x);
     Tout* ho = static_cast<Tout*>(h);
-    if (nc <= 1) launch_k(ln_mod_kernel<Tin, Tout, 1>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nc <= 2) launch_k(ln_mod_kernel<Tin, Tout, 2>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nc <= 5) launch_k(ln_mod_kernel<Tin, Tout, 5>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nc <= 8) launch_k(ln_mod_kernel<Tin, Tout, 8>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nc <= 12) launch_k(ln_mod_kernel<Tin, Tout, 12>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nc <= 16) launch_k(ln_mod_kernel<Tin, Tout, 16>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
+    if (nc <= 1) launch_k(ln_mod_kernel<Tin, Tout, 1, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 2) launch_k(ln_mod_kernel<Tin, Tout, 2, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 5) launch_k(ln_mod_kernel<Tin, Tout, 5, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 8) launch_k(ln_mod_kernel<Tin, Tout, 8, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 12) launch_k(ln_mod_kernel<Tin, Tout, 12, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 16) launch_k(ln_mod_kernel<Tin, Tout, 16, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
     else return fail(BC_ERR_UNSUPPORTED, "LayerNorm width %d > 4096", D);
     return check_launch("ln_mod");
 }

@@ -33,6 +33,12 @@ void prof_begin(int cls, hipStream_t) { g_pending = g_timer[cls].on ? cls : -1; 
 
 void prof_end(int, hipStream_t) { g_pending = -1; }
 
+bool prof_any_enabled() {
+    for (const ClassTimer& t : g_timer)
+        if (t.on) return true;
+    return false;
+}
+
 bool prof_take(hipEvent_t* start, hipEvent_t* stop) {
     if (g_pending < 0) return false;
     ClassTimer& t = g_timer[g_pending];

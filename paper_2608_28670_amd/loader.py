@@ -13,7 +13,7 @@ from typing import Dict, List, Optional
 import numpy as np
 
 from . import (BF16, BLOCK_DIT, BLOCK_DUAL, BLOCK_PIXART, BLOCK_SINGLE, F32, MODEL_DIT, MODEL_MMDIT,
-               MODEL_PIXART, BlockWeights, CacheRing, Model, ModelDesc, block_weights, sample)
+               MODEL_PIXART, BlockWeights, CacheRing, Model, ModelDesc, SampleGraph, block_weights, sample)
 
 _KIND = {"dit": MODEL_DIT, "pixart": MODEL_PIXART, "mmdit": MODEL_MMDIT}
 
@@ -108,6 +108,13 @@ class DeviceModel:
             storage = torch.empty((K, numel), dtype=torch_dtype(self.cfg), device=self.device)
             self._ring[key] = CacheRing(K, storage)
         return self._ws[(B, S)], self._ring[key]
+
+    def sample_graph(self, x, mask, K: Optional[int] = None, labels=None, text=None, p=None):
+        """The same run captured as a HIP graph on x's buffer; .launch() replays it in place."""
+        K = K or self.cfg.K
+        B = x.shape[0]
+        ws, ring = self.buffers(B, K, len(mask))
+        return SampleGraph(self.model, B, self.cfg.sampler, mask, K, ring, x, ws, labels=labels, text=text, p=p)
 
     def sample(self, x, mask, K: Optional[int] = None, labels=None, text=None, p=None, stream=None):
         """BaryCache sampling in place on x (fp32 device latents [B, ...])."""
