@@ -493,7 +493,21 @@ template <int BK> __device__ __forceinline__ int wslot(int c, int r) {
 // 0 applies the epilogue.  (For small outputs: 128 x 144 tiles of 2 x 2 waves
 // of 64 x 80 / 64 x 64 in two groups keep eight waves per CU with large wave
 // tiles where a one-round grid has only 256 tiles.)
-template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int BK, int KG>
+// Wait until at most `later` groups of Q direct-to-LDS loads (issued after the
+// group waited for) are outstanding; `later` >= LMAX waits for all.
+template <int Q, int L = 0, int LMAX = 3> __device__ __forceinline__ void wait_groups(int later) {
+    if constexpr (L >= LMAX) {
+        wait_vmcnt<0>();
+    } else {
+        if (later <= L) {
+            wait_vmcnt<L * Q>();
+            return;
+        }
+        wait_groups<Q, L + 1, LMAX>(later);
+    }
+}
+
+template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int BK, int KG, int PIPE = 0>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KG) void gemm_wide_kernel(GemmArgs g) {
     typedef bf16 T;
     typedef Mma<bf16> MM;
@@ -582,6 +596,78 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KG) void gemm_wide_kernel(
     // Loads this wave issues per k-step (waves below NOCT % NW get one more).
     const bool more = NOCT % NW == 0 || wave < NOCT % NW;
     const int frow = lane & 15, grp = lane >> 4;
+    if constexpr (PIPE) {
+        // Software-pipelined k loop: the barrier sits between the two 32-wide
+        // halves of a k-step, so the fragments of the next step's first half
+        // are read from LDS while this step's second-half MFMAs run, and the
+        // second half's fragments while the first half's run.  Stage kt's
+        // buffer is last read before the middle barrier of step kt, so the
+        // loads of step kt + STAGES - 1 may overwrite it at the top of kt + 1.
+        static_assert(KG == 1 && BK == 64 && STAGES >= 3 && STAGES <= 5, "pipelined k loop");
+        // Fragments live across the loop as 32-bit words (a bf16 vector
+        // carried around the loop is split into halves and re-packed with
+        // byte permutes, which makes the MFMAs wait on the next reads).
+        u32x4 fa[2][TM], fb[2][TN];
+        auto read = [&](int kt, int kk, u32x4 (&a)[TM], u32x4 (&b)[TN]) {
+            const T* st = sm + (kt % STAGES) * STAGE;
+            const int c = kk * 4 + grp;
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int r = wm * WM + i * 16 + frow;
+                a[i] = *reinterpret_cast<const u32x4*>(st + r * BK + wslot<BK>(c, r) * 8);
+            }
+            // Waves with the smaller column share read their last block twice
+            // rather than leaving a fragment conditionally unset.
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int r = BM + (j0 + (NREM != 0 && j >= jn ? jn - 1 : j)) * 16 + frow;
+                b[j] = *reinterpret_cast<const u32x4*>(st + r * BK + wslot<BK>(c, r) * 8);
+            }
+        };
+        // Unconditional: the accumulators past a wave's share (j >= jn) take
+        // the duplicated block and are never stored; branch-free issue.
+        auto mma = [&](const u32x4 (&a)[TM], const u32x4 (&b)[TN]) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = MM::mma(__builtin_bit_cast(MM::frag, b[j]), __builtin_bit_cast(MM::frag, a[i]), acc[i][j]);
+        };
+        // Stage j's loads are done once at most (loads issued after them) are
+        // outstanding: min(STAGES - 2, nk - 1 - j) groups of QMAX (or QMAX - 1).
+        auto wait_stage = [&](int j) {
+            const int later = min(STAGES - 2, nk - 1 - j);
+            if (more) wait_groups<QMAX, 0, STAGES - 1>(later);
+            else wait_groups<QMAX - 1, 0, STAGES - 1>(later);
+        };
+        wait_stage(0);
+        __syncthreads();
+        read(0, 0, fa[0], fb[0]);
+        // All but the last step; the last one (no next stage) is peeled so
+        // that no control-flow merge sits between a step's second-half reads
+        // and its MFMAs (the merged wait counts would make them wait).
+        // In each half the fragment reads are issued first, ahead of the
+        // MFMAs on the other buffer, so their latency hides behind them.
+        for (int kt = 0; kt + 1 < nk; ++kt) {
+            if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+            __builtin_amdgcn_sched_barrier(0);
+            read(kt, 1, fa[1], fb[1]);
+            mma(fa[0], fb[0]);
+            __builtin_amdgcn_sched_group_barrier(0x100, TM + TN, 0);   // DS reads
+            __builtin_amdgcn_sched_group_barrier(0x008, TM * TN, 0);   // MFMAs
+            wait_stage(kt + 1);
+            __syncthreads();
+            __builtin_amdgcn_sched_barrier(0);
+            read(kt + 1, 0, fa[0], fb[0]);
+            mma(fa[1], fb[1]);
+            __builtin_amdgcn_sched_group_barrier(0x100, TM + TN, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, TM * TN, 0);
+        }
+        if (EPI == BC_EPI_GATE_RES && !STAGE_GATED) pf.load(g, bm + wm * WM, bn + j0 * 16, lane, jn);
+        read(nk - 1, 1, fa[1], fb[1]);
+        mma(fa[0], fb[0]);
+        mma(fa[1], fb[1]);
+    } else
     for (int kt = 0; kt < nk; ++kt) {
         if (STAGES > 2 && kt + STAGES - 2 < nk) {
             if (more) wait_vmcnt<(STAGES - 2) * QMAX>();
@@ -738,10 +824,10 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KG) void gemm_wide_kernel(
     epilogue_t<EPI, TM, TN>(g, acc, bm + wm * WM, bn + j0 * 16, lane, jn, pf);
 }
 
-template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES = 2, int BK = 64, int KG = 1>
+template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES = 2, int BK = 64, int KG = 1, int PIPE = 0>
 static void launch_wide(const GemmArgs& g, hipStream_t s) {
     const unsigned tiles = (unsigned)(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN));
-    launch_k(gemm_wide_kernel<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, BK, KG>, dim3(tiles),
+    launch_k(gemm_wide_kernel<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, BK, KG, PIPE>, dim3(tiles),
              dim3(64 * WAVES_M * WAVES_N * KG), s, g);
 }
 
@@ -816,7 +902,7 @@ static int run_gemm(const GemmArgs& g, hipStream_t s) {
                 launch_wide<EPI, 128, 432, 2, 4>(g, s);
             } else if (tiles144 <= 256) {
                 if (EPI == BC_EPI_BIAS && g.K % 128 == 0) launch_wide<EPI, 128, 144, 2, 2, 2, 64, 2>(g, s);
-                else launch_wide<EPI, 128, 144, 2, 4, 4>(g, s);
+                else launch_wide<EPI, 128, 144, 2, 4, 3, 64, 1, 1>(g, s);
             } else {
                 launch_wide<EPI, 128, 128, 4, 2>(g, s);
             }
