@@ -322,11 +322,15 @@ template <int HD> struct KvLayout {
 // query's scores: with both operands equal, v_permlane16_swap returns the
 // value of lane l in one result and of lane l ^ 16 in the other (likewise
 // v_permlane32_swap for l ^ 32), so no LDS round trip is needed.
+// Maximum without the NaN-quieting canonicalisation that fmaxf's IEEE
+// semantics add per operand (gfx950 has a native three-input form); scores
+// are finite or -inf.
+__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
 __device__ __forceinline__ float group_max(float v) {
     const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    v = vmax(__uint_as_float(a[0]), __uint_as_float(a[1]));
     const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+    return vmax(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 __device__ __forceinline__ float group_sum(float v) {
     const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
@@ -373,14 +377,25 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
     // fills LDS chunk 64 j + L = (row, slot) and fetches the global chunk that
     // belongs there.  Keys past the end are clamped to the last key (finite
     // data; their scores are masked).
+    // This wave's instructions and its lane's (row, chunk) in each are fixed:
+    // worked out once, so a tile's issue only offsets the key.
+    constexpr int NJ = (LY::CPR + NWV - 1) / NWV;
+    int irow[NJ], icol[NJ];
+#pragma unroll
+    for (int q = 0; q < NJ; ++q) {
+        const int c = 64 * (wave + NWV * q) + lane;
+        const int row = c / LY::CPR, slot = c % LY::CPR;
+        irow[q] = row;
+        icol[q] = col0 + 8 * (LY::SWZ ? slot ^ ((row / LY::RPB) % LY::CPR) : slot);
+    }
     auto issue = [&](int k0, int buf) {
-        for (int j = wave; j < LY::CPR; j += NWV) {
-            const int c = 64 * j + lane;
-            const int row = c / LY::CPR, slot = c % LY::CPR;
-            const int chunk = LY::SWZ ? slot ^ ((row / LY::RPB) % LY::CPR) : slot;
-            const int key = min(k0 + row, Tk - 1);
-            const bf16* kr = seg_row<bf16>(a.k0, a.k1, a.Tk0, a.Tk1, a.ldk, b, key) + col0 + chunk * 8;
-            const bf16* vr = seg_row<bf16>(a.v0, a.v1, a.Tk0, a.Tk1, a.ldv, b, key) + col0 + chunk * 8;
+#pragma unroll
+        for (int q = 0; q < NJ; ++q) {
+            const int j = wave + NWV * q;
+            if (j >= LY::CPR) break;
+            const int key = min(k0 + irow[q], Tk - 1);
+            const bf16* kr = seg_row<bf16>(a.k0, a.k1, a.Tk0, a.Tk1, a.ldk, b, key) + icol[q];
+            const bf16* vr = seg_row<bf16>(a.v0, a.v1, a.Tk0, a.Tk1, a.ldv, b, key) + icol[q];
             dma16a(kr, &sK[buf][64 * j * 8]);
             dma16a(vr, &sV[buf][64 * j * 8]);
         }
@@ -420,13 +435,22 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
 
 
     // Scores, online softmax and the P V update of one 64-key tile at k0.
+    // Keys past Tk (in the last tile only) start their score accumulators at
+    // -inf, so the MFMAs themselves mask them: one select per score slot per
+    // tile, shared by the query groups, instead of a compare and select per
+    // score.
     auto tile = [&](int k0, const bf16* K, const bf16* V) {
+        f32x4 init[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) init[j][r] = k0 + 16 * j + 4 * grp + r < Tk ? 0.f : -INFINITY;
 
         f32x4 s[QG][4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
 #pragma unroll
-            for (int g = 0; g < QG; ++g) s[g][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int g = 0; g < QG; ++g) s[g][j] = init[j];
             const int krow = 16 * j + ql;
 #pragma unroll
             for (int c = 0; c < S::n32x; ++c) {
@@ -441,24 +465,15 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
         // The reference max m_run moves only when some lane's row max exceeds
         // it by more than 8 (log2 units), so the rescale of O and l is rare
         // after the first tiles; until then p = 2^(s c - m c) stays below 2^8.
-        // Keys past Tk exist only in the last tile.
-        const bool tail = k0 + kKTile > Tk;
         const float c = a.scale_log2;
 #pragma unroll
         for (int g = 0; g < QG; ++g) {
-            if (tail) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        if (k0 + 16 * j + 4 * grp + r >= Tk) s[g][j][r] = -INFINITY;
-            }
             float mloc = -INFINITY;
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                mloc = fmaxf(fmaxf(mloc, fmaxf(s[g][j][0], s[g][j][1])), fmaxf(s[g][j][2], s[g][j][3]));
+                mloc = vmax(vmax(mloc, vmax(s[g][j][0], s[g][j][1])), vmax(s[g][j][2], s[g][j][3]));
             mloc = group_max(mloc);
-            const float m_cand = fmaxf(m_run[g], mloc);
+            const float m_cand = vmax(m_run[g], mloc);
             if (__any((m_cand - m_run[g]) * c > 8.0f)) {     // true on the first tile (m_run = -inf)
                 const float alpha = __builtin_amdgcn_exp2f((m_run[g] - m_cand) * c);
                 l_run[g] *= alpha;
@@ -592,14 +607,20 @@ int launch_attention(int dtype, AttnArgs a, hipStream_t s) {
     // Up to 256 keys: 8 waves of 16 queries with every key tile resident in
     // LDS (one load, no barriers in the key loop); longer sequences: 8 waves
     // over a double buffer, 64 queries each for d <= 72 (every K/V fragment
-    // read from LDS feeds four MFMAs: LDS reads bound this loop) and 32 for
-    // d = 128 (64 would not fit the registers).
+    // read from LDS feeds four MFMAs) and 32 for d = 128 (64 would not fit
+    // the registers), fewer when that would leave the grid short of
+    // workgroups.
     int rc;
     if (dtype == BC_BF16) {
-        const int Tk = a.Tk0 + a.Tk1;
+        const int Tk = a.Tk0 + a.Tk1, Tq = a.Tq0 + a.Tq1;
+        // Workgroups of 128 / 256 / 512 queries; the larger shapes only when
+        // they still give the grid a full round of workgroups.
+        const int64_t bh = (int64_t)a.B * a.H;
+        const int64_t n512 = (Tq + 511) / 512 * bh, n256 = (Tq + 255) / 256 * bh;
         if (Tk <= 4 * kKTile) rc = run_attention_dma<1, 8, 4>(a, a.d, s);
-        else if (a.d <= 72) rc = run_attention_dma<4, 8, 2>(a, a.d, s);
-        else rc = run_attention_dma<2, 8, 2>(a, a.d, s);
+        else if (a.d <= 72 && n512 >= 256) rc = run_attention_dma<4, 8, 2>(a, a.d, s);
+        else if (n256 >= 128) rc = run_attention_dma<2, 8, 2>(a, a.d, s);
+        else rc = run_attention_dma<1, 8, 2>(a, a.d, s);
     } else {
         rc = run_attention<float, 1>(a, a.d, s);
     }

@@ -69,6 +69,8 @@ def test_linear_rejects_bad_k(bclib):
     ("bf16", 2, 3, 200, 200, 72), ("bf16", 1, 2, 100, 37, 128), ("bf16", 2, 2, 64, 64, 32),
     ("bf16", 1, 1, 130, 257, 64), ("bf16", 1, 1, 1, 1, 72), ("bf16", 16, 16, 256, 256, 72),
     ("bf16", 1, 2, 1100, 700, 72), ("bf16", 2, 1, 600, 1030, 32), ("bf16", 1, 2, 520, 333, 128),
+    # enough (sample, head) pairs for the 256- and 512-query workgroups
+    ("bf16", 8, 32, 300, 300, 72), ("bf16", 8, 32, 300, 270, 64), ("bf16", 4, 32, 300, 333, 128),
     ("f32", 2, 4, 64, 64, 32), ("f32", 1, 2, 77, 131, 64)])
 def test_attention(bclib, dt, B, H, Tq, Tk, d):
     q = _inputs(f"q{Tq}{d}", (B, Tq, H, d), dt)
