@@ -346,6 +346,10 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
     constexpr int QT = 16 * QG * NWV;
     static_assert(NB >= 2, "buffers");
     constexpr int TILE = kKTile * HD + 32;     // elements per K or V tile (+ slack for d >= HD operand reads)
+    // When HD is not a multiple of 16 the last output block has padding rows:
+    // the P V MFMAs then also produce the softmax row sums (no per-score adds,
+    // and the deferred rescale of O covers them).
+    constexpr bool ROWSUM = HD % 16 != 0;
     __shared__ __attribute__((aligned(1024))) bf16 sK[NB][TILE];
     __shared__ __attribute__((aligned(1024))) bf16 sV[NB][TILE];
 
@@ -476,7 +480,7 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
             const float m_cand = vmax(m_run[g], mloc);
             if (__any((m_cand - m_run[g]) * c > 8.0f)) {     // true on the first tile (m_run = -inf)
                 const float alpha = __builtin_amdgcn_exp2f((m_run[g] - m_cand) * c);
-                l_run[g] *= alpha;
+                if constexpr (!ROWSUM) l_run[g] *= alpha;
 #pragma unroll
                 for (int i = 0; i < S::DV / 16; ++i) o[g][i] *= alpha;
                 m_run[g] = m_cand;
@@ -489,9 +493,9 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
                 for (int r = 0; r < 4; ++r) {
                     const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[g][j][r], c, -mc));
                     s[g][j][r] = p;
-                    lsum += p;
+                    if constexpr (!ROWSUM) lsum += p;
                 }
-            l_run[g] += lsum;   // this lane's keys only; summed over the group at the end
+            if constexpr (!ROWSUM) l_run[g] += lsum;   // this lane's keys only; summed over the group at the end
         }
 
 #pragma unroll
@@ -513,8 +517,12 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
                     (__attribute__((address_space(3))) s16x4*)(V + LY::at(kb0, d0)));
                 const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
                     (__attribute__((address_space(3))) s16x4*)(V + LY::at(kb0 + 16, d0)));
-                const bf16x8 vf = __builtin_bit_cast(bf16x8, u32x4{__builtin_bit_cast(u32x2, lo).x, __builtin_bit_cast(u32x2, lo).y,
-                                                                  __builtin_bit_cast(u32x2, hi).x, __builtin_bit_cast(u32x2, hi).y});
+                bf16x8 vf = __builtin_bit_cast(bf16x8, u32x4{__builtin_bit_cast(u32x2, lo).x, __builtin_bit_cast(u32x2, lo).y,
+                                                            __builtin_bit_cast(u32x2, hi).x, __builtin_bit_cast(u32x2, hi).y});
+                // Padding rows d >= HD of the last block take ones: their
+                // output rows become the row sums of P (as rounded for the MFMA).
+                if (ROWSUM && i == S::DV / 16 - 1 && (lane & 15) >= HD - 16 * i)
+                    vf = __builtin_bit_cast(bf16x8, u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
 #pragma unroll
                 for (int g = 0; g < QG; ++g) o[g][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[g], o[g][i], 0, 0, 0);
             }
@@ -537,7 +545,17 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
 
 #pragma unroll
     for (int g = 0; g < QG; ++g) {
-        const float inv = 1.f / group_sum(l_run[g]);   // all lanes take part in the exchange
+        float lsum;
+        if constexpr (ROWSUM) {
+            // Output rows 4 (l / 16) + r of the last block: lanes 32-63 hold the
+            // padding rows (the row sums), lanes 0-31 take them from l ^ 32.
+            const float mine = o[g][S::DV / 16 - 1][0];
+            const float other = __shfl_xor(mine, 32);
+            lsum = lane < 32 ? other : mine;
+        } else {
+            lsum = group_sum(l_run[g]);   // all lanes take part in the exchange
+        }
+        const float inv = 1.f / lsum;
         if (myq[g] < Tq) {
             bf16* orow = const_cast<bf16*>(seg_row<bf16>(a.o0, a.o1, a.Tq0, a.Tq1, a.ldo, b, myq[g])) + col0;
 #pragma unroll
