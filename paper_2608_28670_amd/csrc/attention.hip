@@ -346,10 +346,11 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
     constexpr int QT = 16 * QG * NWV;
     static_assert(NB >= 2, "buffers");
     constexpr int TILE = kKTile * HD + 32;     // elements per K or V tile (+ slack for d >= HD operand reads)
-    // When HD is not a multiple of 16 the last output block has padding rows:
-    // the P V MFMAs then also produce the softmax row sums (no per-score adds,
-    // and the deferred rescale of O covers them).
-    constexpr bool ROWSUM = HD % 16 != 0;
+    // The softmax row sums come from the MFMAs, as P times a V column of
+    // ones (no per-score adds): when HD is not a multiple of 16 the padding
+    // rows of the last output block carry them (the deferred rescale of O
+    // covers them); otherwise one more 16-row block of ones, osum.
+    constexpr bool PADSUM = HD % 16 != 0;
     __shared__ __attribute__((aligned(1024))) bf16 sK[NB][TILE];
     __shared__ __attribute__((aligned(1024))) bf16 sV[NB][TILE];
 
@@ -427,12 +428,12 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
         }
     }
 
-    f32x4 o[QG][S::DV / 16];
-    float m_run[QG], l_run[QG];
+    f32x4 o[QG][S::DV / 16], osum[QG];
+    float m_run[QG];
 #pragma unroll
     for (int g = 0; g < QG; ++g) {
         m_run[g] = -INFINITY;
-        l_run[g] = 0.f;
+        osum[g] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int i = 0; i < S::DV / 16; ++i) o[g][i] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
@@ -480,22 +481,19 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
             const float m_cand = vmax(m_run[g], mloc);
             if (__any((m_cand - m_run[g]) * c > 8.0f)) {     // true on the first tile (m_run = -inf)
                 const float alpha = __builtin_amdgcn_exp2f((m_run[g] - m_cand) * c);
-                if constexpr (!ROWSUM) l_run[g] *= alpha;
+                if constexpr (!PADSUM) osum[g] *= alpha;
 #pragma unroll
                 for (int i = 0; i < S::DV / 16; ++i) o[g][i] *= alpha;
                 m_run[g] = m_cand;
             }
             const float mc = m_run[g] * c;
-            float lsum = 0.f;
 #pragma unroll
             for (int j = 0; j < 4; ++j)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[g][j][r], c, -mc));
                     s[g][j][r] = p;
-                    if constexpr (!ROWSUM) lsum += p;
                 }
-            if constexpr (!ROWSUM) l_run[g] += lsum;   // this lane's keys only; summed over the group at the end
         }
 
 #pragma unroll
@@ -521,10 +519,15 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
                                                             __builtin_bit_cast(u32x2, hi).x, __builtin_bit_cast(u32x2, hi).y});
                 // Padding rows d >= HD of the last block take ones: their
                 // output rows become the row sums of P (as rounded for the MFMA).
-                if (ROWSUM && i == S::DV / 16 - 1 && (lane & 15) >= HD - 16 * i)
+                if (PADSUM && i == S::DV / 16 - 1 && (lane & 15) >= HD - 16 * i)
                     vf = __builtin_bit_cast(bf16x8, u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
 #pragma unroll
                 for (int g = 0; g < QG; ++g) o[g][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[g], o[g][i], 0, 0, 0);
+            }
+            if constexpr (!PADSUM) {
+                const bf16x8 ones = __builtin_bit_cast(bf16x8, u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
+#pragma unroll
+                for (int g = 0; g < QG; ++g) osum[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[g], osum[g], 0, 0, 0);
             }
         }
     };
@@ -546,14 +549,14 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
 #pragma unroll
     for (int g = 0; g < QG; ++g) {
         float lsum;
-        if constexpr (ROWSUM) {
+        if constexpr (PADSUM) {
             // Output rows 4 (l / 16) + r of the last block: lanes 32-63 hold the
             // padding rows (the row sums), lanes 0-31 take them from l ^ 32.
             const float mine = o[g][S::DV / 16 - 1][0];
             const float other = __shfl_xor(mine, 32);
             lsum = lane < 32 ? other : mine;
         } else {
-            lsum = group_sum(l_run[g]);   // all lanes take part in the exchange
+            lsum = osum[g][0];     // every row of the ones block is the sum
         }
         const float inv = 1.f / lsum;
         if (myq[g] < Tq) {
