@@ -37,6 +37,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-forecast", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="skip timing the HIP-graph replay of the run")
+    ap.add_argument("--kernels-only", action="store_true",
+                    help="only launch the roofline kernels (fc2, fc1, self-attention of the workload's block, the "
+                         "K = 3 forecast) a few times each through the C ABI, for hardware-counter passes")
     ap.add_argument("--cpu-steps", type=int, default=9, help="oracle sample: first N steps of one sample")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run one 1 GiB device copy through the library (counter calibration)")
@@ -152,8 +155,57 @@ def cpu_baseline(cfg, params, labels, xT, mask, nsteps):
                        f"forecast steps; numpy fp64 on {cores} host threads")}
 
 
+def kernels_only(args):
+    """The roofline kernels at the workload's shapes, each launched `args.steps`
+    times on synthetic operands (no sampling loop): the program the byte
+    counters are collected on."""
+    import torch
+
+    import synth
+    import paper_2608_28670_amd as bc
+    if not os.path.exists(bc.LIB_PATH):
+        from paper_2608_28670_amd import build
+        build.build()
+    dev = "cuda:0"
+    cfg = synth.CONFIGS[args.workload]
+    M, D, F = cfg.batch * cfg.tokens, cfg.hidden, cfg.mlp
+    g = torch.Generator(device=dev)
+    g.manual_seed(synth.SEED)
+
+    def rnd(*shape, dt=torch.bfloat16, scale=0.02):
+        t = torch.empty(shape, dtype=torch.float32, device=dev)
+        t.normal_(0.0, scale, generator=g)
+        return t.to(dt)
+
+    h, w1, b1, hm = rnd(M, D), rnd(F, D), rnd(F), torch.empty((M, F), dtype=torch.bfloat16, device=dev)
+    w2, b2 = rnd(D, F), rnd(D)
+    x, gate = rnd(M, D, dt=torch.float32, scale=1.0), rnd(cfg.batch, D, dt=torch.float32, scale=1.0)
+    H, dh, T = cfg.heads, cfg.head_dim, cfg.tokens
+    q, k, v = (rnd(cfg.batch, T, H, dh, scale=1.0) for _ in range(3))
+    o = torch.empty_like(q)
+    for _ in range(args.steps):
+        bc.linear(h, w1, b1, hm, bc.EPI_BIAS_GELU)
+        bc.linear(hm, w2, b2, x, bc.EPI_GATE_RES, res=x, gate=gate, rows_per_gate=T)
+        bc.attention(q, k, v, o)
+    torch.cuda.synchronize()
+    del h, w1, b1, hm, w2, b2, x, gate, q, k, v, o
+    torch.cuda.empty_cache()
+    forecast_bench(bc, torch, dev, K=3, dtype="bf16", iters=args.steps)
+    if args.calib_copy:
+        n = 1 << 29
+        src = torch.ones(n, dtype=torch.bfloat16, device=dev)
+        store = torch.empty((1, n), dtype=torch.bfloat16, device=dev)
+        ring = bc.CacheRing(1, store)
+        ring.push(src, 0.0)
+        torch.cuda.synchronize()
+    print(json.dumps({"kernels_only": args.workload, "launches_each": args.steps}))
+
+
 def main():
     args = parse()
+    if args.kernels_only:
+        kernels_only(args)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
