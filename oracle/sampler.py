@@ -92,11 +92,17 @@ class Sampler:
 
 def sample(model: Model, x_T: np.ndarray, mask: Sequence[int], K: int,
            labels=None, text=None, p: Optional[bary.Params] = None,
-           trace: Optional[Dict[str, list]] = None) -> np.ndarray:
+           trace: Optional[Dict[str, list]] = None, cfg_scale: Optional[float] = None) -> np.ndarray:
     """The BaryCache sampling loop (Sec. 3.3) from x_T; returns the final latent.
 
+    `cfg_scale` (class-conditional DiT only): classifier-free guidance as the
+    paper's class-to-image runs use it (Sec. 4.1): the model runs on the batch
+    twice, with the labels and with the null class (index n_classes), and the
+    update takes out_u + s (out_c - out_u).  The stepwise feature, and so the
+    cache, covers both halves.
+
     `trace`, if given, collects per step: 'feat' (the stepwise feature used),
-    'out' (model output) and 'x' (latent after the update)."""
+    'out' (model output, guided) and 'x' (latent after the update)."""
     cfg = model.cfg
     S = len(mask)
     B = x_T.shape[0]
@@ -105,17 +111,25 @@ def sample(model: Model, x_T: np.ndarray, mask: Sequence[int], K: int,
     tin = model_time(cfg.sampler, S)
     smp = Sampler(cfg.sampler, S, cfg.in_ch)
     ctx = model.context(text) if cfg.kind != "dit" else None
+    guided = cfg_scale is not None
+    if guided:
+        if cfg.kind != "dit" or not cfg.n_classes:
+            raise ValueError("classifier-free guidance needs a class-conditional DiT")
+        labels = np.concatenate([np.asarray(labels), np.full(B, cfg.n_classes, dtype=np.int64)])
+    Bm = 2 * B if guided else B
     x = np.asarray(x_T, dtype=np.float64)
     for k in range(S):
-        cond = model.condition(tin[k], B, labels, text)
+        cond = model.condition(tin[k], Bm, labels, text)
         if mask[k]:
-            feat = model.stack(model.embed(x), cond, ctx)
+            feat = model.stack(model.embed(np.concatenate([x, x]) if guided else x), cond, ctx)
             ring.push(feat, k)
         else:
             st = steps[k]
             feat = bary.forecast([ring.slots[i] for i in st.slots], st.w)
-        out = model.final(feat, cond)
-        x = smp.step(k, x, np.asarray(out, dtype=np.float64))
+        out = np.asarray(model.final(feat, cond), dtype=np.float64)
+        if guided:
+            out = out[B:] + cfg_scale * (out[:B] - out[B:])
+        x = smp.step(k, x, out)
         if trace is not None:
             trace.setdefault("feat", []).append(feat)
             trace.setdefault("out", []).append(out)

@@ -276,3 +276,47 @@ def test_bf16_rounding_matches_torch():
     a = synth.normal("probe", (1000,), 3.0)
     ref = torch.from_numpy(a).to(torch.bfloat16).to(torch.float32).numpy()
     assert np.array_equal(synth.bf16_round(a), ref)
+
+
+# ---------------------------------------------------------------------------
+# classifier-free guidance (Sec. 4.1: the class-to-image runs use scale 1.5)
+# ---------------------------------------------------------------------------
+
+def _cond_tiny(**kw):
+    return synth.scaled(synth.CONFIGS["tiny"], n_classes=10, **kw)
+
+
+def _cfg_run(cfg, s, labels, mask):
+    M = om.Model(cfg, synth.params(cfg))
+    xT = synth.latents(cfg).astype(np.float64)
+    return osm.sample(M, xT, mask, cfg.K, labels=labels, cfg_scale=s)
+
+
+def test_cfg_scale_one_is_the_conditional_run_and_zero_the_null_class():
+    cfg = _cond_tiny(steps=6)
+    mask = bary.make_mask(6, 3)
+    labels = np.array([3, 7])
+    cond = _cfg_run(cfg, None, labels, mask)
+    null = _cfg_run(cfg, None, np.full(2, cfg.n_classes), mask)
+    np.testing.assert_allclose(_cfg_run(cfg, 1.0, labels, mask), cond, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(_cfg_run(cfg, 0.0, labels, mask), null, rtol=1e-12, atol=1e-14)
+    assert not np.allclose(cond, null)
+
+
+def test_cfg_one_step_is_affine_in_the_scale():
+    # one DDIM step is affine in the model output, and the guided output is
+    # affine in s: x(s) = x(0) + s (x(1) - x(0))
+    cfg = _cond_tiny(steps=1)
+    mask = np.ones(1, np.uint8)
+    labels = np.array([1, 9])
+    x0, x1, x15 = (_cfg_run(cfg, s, labels, mask) for s in (0.0, 1.0, 1.5))
+    np.testing.assert_allclose(x15, x0 + 1.5 * (x1 - x0), rtol=1e-11, atol=1e-13)
+
+
+def test_cfg_caches_both_halves():
+    cfg = _cond_tiny(steps=6)
+    M = om.Model(cfg, synth.params(cfg))
+    tr = {}
+    osm.sample(M, synth.latents(cfg).astype(np.float64), bary.make_mask(6, 3), cfg.K,
+               labels=np.array([0, 5]), cfg_scale=1.5, trace=tr)
+    assert tr["feat"][1].shape[0] == 4 and tr["out"][1].shape[0] == 2
