@@ -310,6 +310,20 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
               const int64_t* labels, const void* text, void* ws, size_t ws_bytes,
               void* stream);
 
+/* bc_sample with classifier-free guidance, as the paper's class-to-image runs
+ * use it (Sec. 4.1, scale 1.5): a class-conditional DiT runs on a model batch
+ * of 2B samples, the B `labels` and then B copies of the null class (row
+ * n_classes of the class table), both reading the same latents; the stepwise
+ * feature, and so every ring slot, covers all 2B samples (ring slots of
+ * 2B*T*D elements); the update takes out_u + cfg_scale (out_c - out_u).
+ * Workspace: bc_sample_workspace_size(m, 2B, S) bytes; B <= 32.
+ * Errors: as bc_sample; UNSUPPORTED for models without classes; INVALID_ARG
+ * for a non-finite scale. */
+int bc_sample_cfg(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
+                  int K, const bc_bary_params* p, bc_cache_ring* ring, float* latents,
+                  const int64_t* labels, float cfg_scale, void* ws, size_t ws_bytes,
+                  void* stream);
+
 /* The same sampling run captured once as a HIP graph and replayed, for
  * callers whose loop is launch-bound (small models, short schedules).
  * bc_sample_graph_create runs nothing: it records into a graph exactly the

@@ -115,6 +115,9 @@ _SIGS = {
     "bc_sample": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int,
                             C.POINTER(BaryParams), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
                             C.c_void_p, C.c_size_t, C.c_void_p]),
+    "bc_sample_cfg": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int,
+                                C.POINTER(BaryParams), C.c_void_p, C.c_void_p, C.c_void_p, C.c_float,
+                                C.c_void_p, C.c_size_t, C.c_void_p]),
     "bc_sample_graph_create": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int,
                                          C.POINTER(BaryParams), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
                                          C.c_void_p, C.c_size_t, C.c_void_p, C.POINTER(C.c_void_p)]),
@@ -388,6 +391,15 @@ def sample(model: Model, B: int, sampler: str, mask, K: int, ring: CacheRing, la
     _check(lib().bc_sample(model.h, B, SAMPLERS[sampler], len(m), _ptr(m), K, C.byref(p) if p else None,
                            ring.h, dev_ptr(latents), dev_ptr(labels), dev_ptr(text), dev_ptr(ws),
                            ws.numel() * ws.element_size(), stream_handle(stream)))
+
+
+def sample_cfg(model: Model, B: int, sampler: str, mask, K: int, ring: CacheRing, latents, ws, labels,
+               cfg_scale: float, p: Optional[BaryParams] = None, stream=None):
+    """Guided sampling (bc_sample_cfg): ring slots and workspace for a model batch of 2B."""
+    m = np.ascontiguousarray(mask, dtype=np.uint8)
+    _check(lib().bc_sample_cfg(model.h, B, SAMPLERS[sampler], len(m), _ptr(m), K, C.byref(p) if p else None,
+                               ring.h, dev_ptr(latents), dev_ptr(labels), float(cfg_scale), dev_ptr(ws),
+                               ws.numel() * ws.element_size(), stream_handle(stream)))
 
 
 class SampleGraph:

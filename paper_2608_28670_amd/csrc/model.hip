@@ -279,6 +279,7 @@ struct SampleWs {
     float *out, *prev;                        // model output (token layout), DPM-Solver++ history
     int full_chunk;                           // full steps whose modulation is held at once
     size_t bytes;
+    int64_t* labels2;     // labels of a guided batch (the conditional half, then the null class)
 };
 
 static int64_t latent_spatial(const bc_model_desc& d) { return (int64_t)d.frames * d.height * d.width; }
@@ -334,6 +335,7 @@ static SampleWs carve_sample(const bc_model_desc& d, int B, int S, void* base) {
     w.feat = c.take<char>((size_t)B * T * D * esz);
     w.out = c.take<float>((size_t)B * d.out_ch * latent_spatial(d) * f4);
     w.prev = c.take<float>((size_t)B * d.in_ch * latent_spatial(d) * f4);
+    w.labels2 = c.take<int64_t>((size_t)B * sizeof(int64_t));
     w.bytes = c.off + 256;
     return w;
 }
@@ -517,18 +519,22 @@ int bc_sample_workspace_size(const bc_model* m, int B, int S, size_t* bytes) {
     return BC_OK;
 }
 
-int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask, int K, const bc_bary_params* p,
-              bc_cache_ring* ring, float* latents, const int64_t* labels, const void* text, void* ws,
-              size_t ws_bytes, void* stream) {
-    clear_error();
+}  // extern "C"
+
+// The loop of bc_sample; guided: classifier-free guidance with scale cfg over
+// a model batch of 2B (labels, then the null class) for B latents.
+static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_t* mask, int K, const bc_bary_params* p,
+                      bc_cache_ring* ring, float* latents, const int64_t* labels, const void* text, bool guided,
+                      float cfg, void* ws, size_t ws_bytes, void* stream) {
     if (!m || !mask || !ring || !latents || !ws) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
     const bc_model_desc& d = m->d;
-    if (B < 1 || B > 64) return fail(BC_ERR_INVALID_ARG, "B=%d outside [1, 64]", B);
+    const int Bm = guided ? 2 * B : B;     // model batch
+    if (B < 1 || Bm > 64) return fail(BC_ERR_INVALID_ARG, "B=%d outside [1, %d]", B, guided ? 32 : 64);
     if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(BC_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
     const int T = model_tokens(d), D = d.D;
     if (K != ring->K) return fail(BC_ERR_INVALID_ARG, "K=%d but the ring has %d slots", K, ring->K);
-    if (ring->dtype != d.dtype || ring->numel != (int64_t)B * T * D)
-        return fail(BC_ERR_INVALID_ARG, "ring must hold %lld elements of the model dtype per slot", (long long)B * T * D);
+    if (ring->dtype != d.dtype || ring->numel != (int64_t)Bm * T * D)
+        return fail(BC_ERR_INVALID_ARG, "ring must hold %lld elements of the model dtype per slot", (long long)Bm * T * D);
     if (d.kind == BC_MODEL_DIT && d.n_classes && !labels) return fail(BC_ERR_INVALID_ARG, "class labels required");
     if (d.kind != BC_MODEL_DIT && !text) return fail(BC_ERR_INVALID_ARG, "text input required");
     std::vector<int32_t> tau(S > 0 ? S : 1);
@@ -536,7 +542,7 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
     BC_TRY(bc_make_schedule(sampler, S, tau.data(), tin.data()));
     std::vector<bc_plan_step> plan(S);
     BC_TRY(bc_plan(S, mask, nullptr, K, p, plan.data()));
-    const SampleWs w = carve_sample(d, B, S, ws);
+    const SampleWs w = carve_sample(d, Bm, S, ws);
     if (ws_bytes < w.bytes) return fail(BC_ERR_INVALID_ARG, "workspace %zu < %zu bytes", ws_bytes, w.bytes);
 
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -549,9 +555,11 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
     bc_cache_reset(ring);
     const bc_block_weights* blk = m->w.blocks;
     const bc_model_weights& mw = m->w;
-    const bc_block_desc bd_main = block_desc_of(d, B, d.kind == BC_MODEL_DIT ? BC_BLOCK_DIT
-                                                      : d.kind == BC_MODEL_PIXART ? BC_BLOCK_PIXART : BC_BLOCK_DUAL);
-    const bc_block_desc bd_single = block_desc_of(d, B, BC_BLOCK_SINGLE);
+    const bc_block_desc bd_main = block_desc_of(d, Bm, d.kind == BC_MODEL_DIT ? BC_BLOCK_DIT
+                                                       : d.kind == BC_MODEL_PIXART ? BC_BLOCK_PIXART : BC_BLOCK_DUAL);
+    const bc_block_desc bd_single = block_desc_of(d, Bm, BC_BLOCK_SINGLE);
+    if (guided) BC_TRY(launch_cfg_labels(labels, B, d.n_classes, w.labels2, s));
+    const int64_t* mlabels = guided ? w.labels2 : labels;
 
     // Per-run text context.
     if (d.kind == BC_MODEL_PIXART) {
@@ -576,20 +584,20 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
         BC_TRY(launch_skinny(dt, skinny1(mw.t_w2, mw.t_b2, D, D, n, w.t1 + (int64_t)k0 * D, w.temb + (int64_t)k0 * D, 0, 0), s));
     }
     const bool lab = d.kind == BC_MODEL_DIT && d.n_classes;
-    BC_TRY(launch_build_cond(dt, w.temb, S, B, D, lab ? mw.y_table : nullptr, lab ? labels : nullptr, d.n_classes + 1,
+    BC_TRY(launch_build_cond(dt, w.temb, S, Bm, D, lab ? mw.y_table : nullptr, lab ? mlabels : nullptr, d.n_classes + 1,
                              d.kind == BC_MODEL_MMDIT ? w.txtp : nullptr, w.c, s));
     if (d.kind == BC_MODEL_PIXART) {
         const void* ft[2] = {mw.final_w_mod, static_cast<const char*>(mw.final_w_mod) + D * esz};
-        BC_TRY(launch_add_tables(dt, w.c, D, ft, 2, D, S * B, w.fmod, 2 * D, s));
+        BC_TRY(launch_add_tables(dt, w.c, D, ft, 2, D, S * Bm, w.fmod, 2 * D, s));
     } else {
         for (int k0 = 0; k0 < S; k0 += kMaxSeg) {
             const int n = std::min(kMaxSeg, S - k0);
             RowList rl;
             for (int i = 0; i < n; ++i) rl.row[i] = k0 + i;
-            BC_TRY(launch_gather_silu(dt, w.c, B, D, rl, n,
-                                      static_cast<char*>(w.sc) + (int64_t)k0 * B * D * esz, s));
+            BC_TRY(launch_gather_silu(dt, w.c, Bm, D, rl, n,
+                                      static_cast<char*>(w.sc) + (int64_t)k0 * Bm * D * esz, s));
         }
-        GemmArgs fg = gemm_args(w.sc, D, mw.final_w_mod, D, S * B, 2 * D, D);
+        GemmArgs fg = gemm_args(w.sc, D, mw.final_w_mod, D, S * Bm, 2 * D, D);
         fg.e.bias = mw.final_b_mod;
         fg.e.out = w.fmod;
         fg.e.ldo = 2 * D;
@@ -609,8 +617,8 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
         for (int i = 0; i < n; ++i) rl.row[i] = full_steps[f0 + i];
         // (PixArt has no class or text term in c, so c is the timestep
         // embedding and SiLU(c) is t6's input.)
-        BC_TRY(launch_gather_silu(dt, w.c, B, D, rl, n, w.sc, s));
-        const int rows = n * B;
+        BC_TRY(launch_gather_silu(dt, w.c, Bm, D, rl, n, w.sc, s));
+        const int rows = n * Bm;
         if (d.kind == BC_MODEL_PIXART) {
             GemmArgs tg = gemm_args(w.sc, D, mw.t6_w, D, rows, 6 * D, D);
             tg.e.bias = mw.t6_b;
@@ -654,14 +662,14 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
 
     // The fused final step needs 16-byte aligned ring slots and weights (checked
     // here once) and an instantiated (D, p*p*C_out).
-    const bool fused_final = final_step_supported(dt, D, d.patch * d.patch * d.out_ch, T) &&
+    const bool fused_final = !guided && final_step_supported(dt, D, d.patch * d.patch * d.out_ch, T) &&
                              reinterpret_cast<uintptr_t>(ring->storage) % 16 == 0 && (ring->numel * esz) % 16 == 0 &&
                              reinterpret_cast<uintptr_t>(mw.final_w) % 16 == 0;
 
     int full_index = 0;
     for (int k = 0; k < S; ++k) {
         const bc_plan_step& st = plan[k];
-        const float* fmod = w.fmod + (int64_t)k * B * 2 * D;
+        const float* fmod = w.fmod + (int64_t)k * Bm * 2 * D;
         const void* feat;
         if (st.is_full) {
             void* slot = nullptr;
@@ -673,9 +681,9 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
             const int fi = full_index % w.full_chunk;
             if (fi == 0) BC_TRY(chunk_mods(full_index));
             ++full_index;
-            const float* mods = w.mods + (int64_t)fi * B * ldm;
-            const float* mods_s = w.mods_s + (int64_t)fi * B * lds;
-            BC_TRY(launch_patch_embed(dt, latents, ls, B, mw.patch_w, mw.patch_b, mw.pos, D, w.x_img, s));
+            const float* mods = w.mods + (int64_t)fi * Bm * ldm;
+            const float* mods_s = w.mods_s + (int64_t)fi * Bm * lds;
+            BC_TRY(launch_patch_embed(dt, latents, ls, Bm, B, mw.patch_w, mw.patch_b, mw.pos, D, w.x_img, s));
             if (d.kind == BC_MODEL_MMDIT) {
                 BC_TRY(launch_convert(dt, text, BC_F32, w.x_txt, (int64_t)B * Tt * D, s));
                 for (int l = 0; l < d.depth; ++l)
@@ -746,16 +754,38 @@ int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask,
         }
         // Final layer: LayerNorm + adaLN, then the linear to p*p*C_out per token
         // (token layout; the sampler reads it back through unpatchify).
-        BC_TRY(launch_ln_mod(dt, feat, (int64_t)B * T, D, fmod, fmod + D, 2 * D, T, dt, w.bb.h, s));
-        GemmArgs fg = gemm_args(w.bb.h, D, mw.final_w, D, B * T, NO, D);
+        BC_TRY(launch_ln_mod(dt, feat, (int64_t)Bm * T, D, fmod, fmod + D, 2 * D, T, dt, w.bb.h, s));
+        GemmArgs fg = gemm_args(w.bb.h, D, mw.final_w, D, Bm * T, NO, D);
         fg.e.bias = mw.final_b;
         fg.e.out = w.out;
         fg.e.ldo = NO;
         fg.e.out_f32 = 1;
         BC_TRY(launch_gemm(dt, BC_EPI_BIAS, fg, s));
-        BC_TRY(launch_sampler(sc, latents, w.out, w.prev, ls, B, d.out_ch, s));
+        BC_TRY(launch_sampler(sc, latents, w.out, w.prev, ls, B, d.out_ch, s, cfg, guided ? (int64_t)B * T * NO : 0));
     }
     return BC_OK;
+}
+
+extern "C" {
+
+int bc_sample(const bc_model* m, int B, int sampler, int S, const uint8_t* mask, int K, const bc_bary_params* p,
+              bc_cache_ring* ring, float* latents, const int64_t* labels, const void* text, void* ws,
+              size_t ws_bytes, void* stream) {
+    clear_error();
+    return sample_run(m, B, sampler, S, mask, K, p, ring, latents, labels, text, false, 1.f, ws, ws_bytes, stream);
+}
+
+int bc_sample_cfg(const bc_model* m, int B, int sampler, int S, const uint8_t* mask, int K, const bc_bary_params* p,
+                  bc_cache_ring* ring, float* latents, const int64_t* labels, float cfg_scale, void* ws,
+                  size_t ws_bytes, void* stream) {
+    clear_error();
+    if (!m) return fail(BC_ERR_INVALID_ARG, "NULL model");
+    if (m->d.kind != BC_MODEL_DIT || m->d.n_classes <= 0)
+        return fail(BC_ERR_UNSUPPORTED, "classifier-free guidance needs a class-conditional DiT");
+    if (!labels) return fail(BC_ERR_INVALID_ARG, "class labels required");
+    if (!std::isfinite(cfg_scale)) return fail(BC_ERR_INVALID_ARG, "guidance scale must be finite");
+    return sample_run(m, B, sampler, S, mask, K, p, ring, latents, labels, nullptr, true, cfg_scale, ws, ws_bytes,
+                      stream);
 }
 
 }  // extern "C"

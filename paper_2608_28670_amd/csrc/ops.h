@@ -65,8 +65,13 @@ struct LatentShape {
 };
 
 // x[b, tok, :] = patchify(lat)[b, tok, :] W^T + bias + pos[tok, :], fp32 out.
-int launch_patch_embed(int dt, const float* lat, LatentShape ls, int B, const void* W, const void* bias,
+// Model batch B reads latent sample b % lat_B (lat_B < B: the same latents
+// for both halves of a guided batch).
+int launch_patch_embed(int dt, const float* lat, LatentShape ls, int B, int lat_B, const void* W, const void* bias,
                        const void* pos, int D, float* x, hipStream_t s);
+
+// Labels of a guided batch: out[b] = labels[b], out[B + b] = null_id, b < B.
+int launch_cfg_labels(const int64_t* labels, int B, int64_t null_id, int64_t* out, hipStream_t s);
 
 // Sampler update on fp32 latents x [B, C, F, H, W] from the model output in
 // token layout out_tok [B*T, p*p*C_out] (first C channels used):
@@ -75,8 +80,11 @@ int launch_patch_embed(int dt, const float* lat, LatentShape ls, int B, const vo
 //     D = c4 x0 + c5 prev; x = c0 x + c1 D; prev = x0 (prev may be NULL if c5 == 0)
 //   mode 2: x = x0 computed as in mode 1 (final step)
 struct SamplerCoef { float c[6]; int mode; };
+// Guided (uncond_off > 0): the output used is u + cfg (c - u), with c at the
+// element's own position and u uncond_off elements further (the null-class
+// half of the batch).
 int launch_sampler(const SamplerCoef& k, float* x, const float* out_tok, float* prev, LatentShape ls, int B, int C_out,
-                   hipStream_t s);
+                   hipStream_t s, float cfg = 1.f, int64_t uncond_off = 0);
 
 // The update of one latent element from its model output e (the modes above).
 __device__ __forceinline__ void sampler_update(const SamplerCoef& k, float* x, float e, float* prev) {

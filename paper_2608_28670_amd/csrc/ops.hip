@@ -439,11 +439,13 @@ int launch_convert(int in_dt, const void* in, int out_dt, void* out, int64_t n, 
 template <typename T>
 __global__ __launch_bounds__(256) void patch_embed_kernel(const float* __restrict__ lat, LatentShape ls,
                                                           const T* __restrict__ W, const T* __restrict__ bias,
-                                                          const T* __restrict__ pos, int D, float* __restrict__ x) {
+                                                          const T* __restrict__ pos, int D, int lat_B,
+                                                          float* __restrict__ x) {
     __shared__ float patch[kMaxPatch];
     const int Tn = ls.tokens();
     const int row = blockIdx.x;
-    const int b = row / Tn, tok = row - b * Tn;
+    const int bm = row / Tn, tok = row - bm * Tn;
+    const int b = bm % lat_B;
     const int hp = ls.H / ls.p, wp = ls.W / ls.p;
     const int f = tok / (hp * wp), ti = (tok / wp) % hp, tj = tok % wp;
     const int PD = ls.p * ls.p * ls.C;
@@ -460,17 +462,29 @@ __global__ __launch_bounds__(256) void patch_embed_kernel(const float* __restric
     }
 }
 
-int launch_patch_embed(int dt, const float* lat, LatentShape ls, int B, const void* W, const void* bias,
+int launch_patch_embed(int dt, const float* lat, LatentShape ls, int B, int lat_B, const void* W, const void* bias,
                        const void* pos, int D, float* x, hipStream_t s) {
     if (ls.p * ls.p * ls.C > kMaxPatch) return fail(BC_ERR_UNSUPPORTED, "patch of %d values", ls.p * ls.p * ls.C);
+    if (lat_B < 1 || lat_B > B) return fail(BC_ERR_INVALID_ARG, "latent batch %d for a model batch of %d", lat_B, B);
     const unsigned rows = (unsigned)(B * ls.tokens());
     if (dt == BC_BF16)
         patch_embed_kernel<bf16><<<rows, 256, 0, s>>>(lat, ls, static_cast<const bf16*>(W), static_cast<const bf16*>(bias),
-                                                      static_cast<const bf16*>(pos), D, x);
+                                                      static_cast<const bf16*>(pos), D, lat_B, x);
     else
         patch_embed_kernel<float><<<rows, 256, 0, s>>>(lat, ls, static_cast<const float*>(W), static_cast<const float*>(bias),
-                                                       static_cast<const float*>(pos), D, x);
+                                                       static_cast<const float*>(pos), D, lat_B, x);
     return check_launch("patch_embed");
+}
+
+__global__ void cfg_labels_kernel(const int64_t* labels, int B, int64_t null_id, int64_t* out) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < B) out[i] = labels[i];
+    else if (i < 2 * B) out[i] = null_id;
+}
+
+int launch_cfg_labels(const int64_t* labels, int B, int64_t null_id, int64_t* out, hipStream_t s) {
+    cfg_labels_kernel<<<1, 128, 0, s>>>(labels, B, null_id, out);
+    return check_launch("cfg_labels");
 }
 
 // ---------------------------------------------------------------------------
@@ -480,7 +494,7 @@ int launch_patch_embed(int dt, const float* lat, LatentShape ls, int B, const vo
 // output); element (b, c, f, y, x) of the latent is read from token
 // (f, y/p, x/p), feature ((y%p)*p + x%p)*C_out + c, which is unpatchify.
 __global__ void sampler_kernel(SamplerCoef k, float* x, const float* out_tok, float* prev, LatentShape ls, int B,
-                               int C_out) {
+                               int C_out, float cfg, int64_t uncond_off) {
     const int64_t S = (int64_t)ls.F * ls.H * ls.W;
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= (int64_t)B * ls.C * S) return;
@@ -492,14 +506,19 @@ __global__ void sampler_kernel(SamplerCoef k, float* x, const float* out_tok, fl
     const int hp = ls.H / ls.p, wp = ls.W / ls.p;
     const int tok = (f * hp + ys / ls.p) * wp + xs / ls.p;
     const int feat = ((ys % ls.p) * ls.p + xs % ls.p) * C_out + c;
-    const float e = out_tok[((int64_t)b * ls.tokens() + tok) * (ls.p * ls.p * C_out) + feat];
+    const int64_t o = ((int64_t)b * ls.tokens() + tok) * (ls.p * ls.p * C_out) + feat;
+    float e = out_tok[o];
+    if (uncond_off > 0) {
+        const float u = out_tok[o + uncond_off];
+        e = __builtin_fmaf(cfg, e - u, u);
+    }
     sampler_update(k, x + i, e, prev ? prev + i : nullptr);
 }
 
 int launch_sampler(const SamplerCoef& k, float* x, const float* out_tok, float* prev, LatentShape ls, int B, int C_out,
-                   hipStream_t s) {
+                   hipStream_t s, float cfg, int64_t uncond_off) {
     const int64_t n = (int64_t)B * ls.C * ls.F * ls.H * ls.W;
-    sampler_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(k, x, out_tok, prev, ls, B, C_out);
+    sampler_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(k, x, out_tok, prev, ls, B, C_out, cfg, uncond_off);
     return check_launch("sampler");
 }
 

@@ -13,7 +13,8 @@ from typing import Dict, List, Optional
 import numpy as np
 
 from . import (BF16, BLOCK_DIT, BLOCK_DUAL, BLOCK_PIXART, BLOCK_SINGLE, F32, MODEL_DIT, MODEL_MMDIT,
-               MODEL_PIXART, BlockWeights, CacheRing, Model, ModelDesc, SampleGraph, block_weights, sample)
+               MODEL_PIXART, BlockWeights, CacheRing, Model, ModelDesc, SampleGraph, block_weights, sample,
+               sample_cfg)
 
 _KIND = {"dit": MODEL_DIT, "pixart": MODEL_PIXART, "mmdit": MODEL_MMDIT}
 
@@ -115,6 +116,14 @@ class DeviceModel:
         B = x.shape[0]
         ws, ring = self.buffers(B, K, len(mask))
         return SampleGraph(self.model, B, self.cfg.sampler, mask, K, ring, x, ws, labels=labels, text=text, p=p)
+
+    def sample_cfg(self, x, mask, labels, cfg_scale: float, K: Optional[int] = None, p=None, stream=None):
+        """Classifier-free guided sampling in place on x (B latents; model batch 2B)."""
+        K = K or self.cfg.K
+        B = x.shape[0]
+        ws, ring = self.buffers(2 * B, K, len(mask))
+        sample_cfg(self.model, B, self.cfg.sampler, mask, K, ring, x, ws, labels, cfg_scale, p=p, stream=stream)
+        return ring
 
     def sample(self, x, mask, K: Optional[int] = None, labels=None, text=None, p=None, stream=None):
         """BaryCache sampling in place on x (fp32 device latents [B, ...])."""

@@ -333,3 +333,63 @@ def test_sample_rejects_bad_inputs(bclib):
     assert e.value.code == bclib.ERR_INVALID_ARG
     with pytest.raises(bclib.BCError):
         dm.sample(x, np.ones(3, np.uint8), K=9)
+
+
+# ---------------------------------------------------------------------------
+# classifier-free guidance (bc_sample_cfg)
+# ---------------------------------------------------------------------------
+
+def _run_cfg(cfg, P, B, mask, labels, s):
+    from paper_2608_28670_amd import loader
+    dm = loader.DeviceModel(cfg, P)
+    xT = synth.latents(cfg, batch=B)
+    x = _f32(xT)
+    ring = dm.sample_cfg(x, mask, torch.from_numpy(labels).to(DEV), s)
+    torch.cuda.synchronize()
+    return xT, x.cpu().numpy(), ring
+
+
+def test_sample_cfg_tiny_conditional_fp32(bclib):
+    cfg = synth.scaled(synth.CONFIGS["tiny"], n_classes=10)
+    P = synth.params(cfg)
+    mask = bary.make_mask(cfg.steps, cfg.interval)
+    labels = np.array([4, 9], np.int64)
+    xT, got, ring = _run_cfg(cfg, P, 2, mask, labels, 1.5)
+    exp = osm.sample(om.Model(cfg, P), xT.astype(np.float64), mask, cfg.K, labels=labels, cfg_scale=1.5)
+    err = rel_l2(got, exp)
+    print(f"tiny conditional fp32, cfg 1.5: rel-L2 {err:.2e}")
+    assert err <= 1e-4
+    _check_ring(ring, mask, cfg.K)
+    assert ring.numel == 2 * 2 * cfg.tokens * cfg.hidden
+
+
+def test_sample_cfg_dit_xl2_reduced_depth(bclib):
+    cfg = synth.scaled(synth.CONFIGS["dit_xl2"], depth=2, batch=2)
+    P = synth.params(cfg)
+    mask = bary.make_mask(cfg.steps, cfg.interval)
+    labels = synth.labels(cfg, batch=2)
+    xT, got, _ = _run_cfg(cfg, P, 2, mask, labels, 1.5)
+    exp = osm.sample(om.Model(cfg, P), xT.astype(np.float64), mask, cfg.K, labels=labels, cfg_scale=1.5)
+    err = rel_l2(got, exp)
+    print(f"dit_xl2 depth 2, cfg 1.5: rel-L2 {err:.2e}")
+    assert err <= 2e-2
+
+
+def test_sample_cfg_scale_one_is_the_conditional_run(bclib):
+    cfg = synth.scaled(synth.CONFIGS["tiny"], n_classes=10)
+    P = synth.params(cfg)
+    mask = bary.make_mask(cfg.steps, cfg.interval)
+    labels = np.array([1, 6], np.int64)
+    _, guided, _ = _run_cfg(cfg, P, 2, mask, labels, 1.0)
+    _, plain, _ = _run_sample(bclib, cfg, P, 2, mask, labels=labels)
+    assert rel_l2(guided, plain.astype(np.float64)) <= 1e-5
+
+
+def test_sample_cfg_rejects_unconditional_model(bclib):
+    from paper_2608_28670_amd import loader
+    cfg = synth.CONFIGS["tiny"]
+    dm = loader.DeviceModel(cfg, synth.params(cfg))
+    x = _f32(synth.latents(cfg))
+    with pytest.raises(bclib.BCError) as e:
+        dm.sample_cfg(x, bary.make_mask(cfg.steps, cfg.interval), torch.zeros(2, dtype=torch.int64, device=DEV), 1.5)
+    assert e.value.code == bclib.ERR_UNSUPPORTED
