@@ -259,6 +259,20 @@ class Model:
         z = np.concatenate([a, gelu_tanh(y[..., 3 * D:])], axis=-1)
         return x + g[:, None, :] * linear(z, P[pre + "w_2"], P[pre + "b_2"])
 
+    def probe(self, x, cond):
+        """The feature an adaptive schedule watches: the first block's modulated
+        attention input LN(x)(1 + scale1) + shift1 on the embedded latent x
+        (image stream of the first dual block for MMDiT).  It costs the
+        embedding, one modulation and one LayerNorm, not the stack."""
+        cfg, P = self.cfg, self.P
+        D = cfg.hidden
+        if cfg.kind in ("dit", "pixart"):
+            shift, scale = self.block_mod(0, cond)[:2]
+        else:
+            m = linear(silu(cond["c"]), P["dual.0.img.w_mod"], P["dual.0.img.b_mod"])
+            shift, scale = m[:, :D], m[:, D:2 * D]
+        return modulate(layer_norm(x), shift, scale)
+
     def stack(self, x, cond, ctx):
         """Eq. 5: the stepwise feature, i.e. the image-token output of the whole
         layer stack."""

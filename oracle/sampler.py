@@ -15,6 +15,15 @@ text-to-video, 50 steps (Sec. 4.1).  The precise samplers below are readings:
 The loop itself is Sec. 3.3: on a full step run the stack and store its output
 in the cache; otherwise forecast it from the cache with Eq. 13; then the final
 layer and the sampler update.
+
+The adaptive schedule (Sec. 4.5, Table 5) is described only as a TeaCache-style
+rule: relative changes of a feature probe accumulate, and a full step runs when
+the accumulated drift reaches the threshold l.  Readings taken here: the probe
+is the first block's modulated attention input (Model.probe) at the current
+latent and step; the change at step k is the relative L1 distance
+sum|p_k - p_{k-1}| / sum|p_{k-1}| over the whole batch (no rescaling
+polynomial: its coefficients are fitted to trained weights); steps 0 and S-1
+always run the stack; a full step resets the accumulator to zero.
 """
 from __future__ import annotations
 
@@ -135,3 +144,88 @@ def sample(model: Model, x_T: np.ndarray, mask: Sequence[int], K: int,
             trace.setdefault("out", []).append(out)
             trace.setdefault("x", []).append(x)
     return x
+
+
+def relative_l1(cur: np.ndarray, prev: np.ndarray) -> float:
+    """sum|cur - prev| / sum|prev| over every element (0/0 = 0, x/0 = inf)."""
+    num = float(np.abs(np.asarray(cur, np.float64) - np.asarray(prev, np.float64)).sum())
+    den = float(np.abs(np.asarray(prev, np.float64)).sum())
+    if den == 0.0:
+        return 0.0 if num == 0.0 else math.inf
+    return num / den
+
+
+class AdaptiveRule:
+    """The accumulate-and-trigger decision of the adaptive schedule: step k runs
+    the stack if it is the first or the last step, or if the changes summed
+    since the last full step reach `ell`; a full step empties the sum."""
+
+    def __init__(self, ell: float, S: int):
+        if not ell >= 0.0:
+            raise ValueError("the threshold must be >= 0")
+        self.ell, self.S, self.acc = float(ell), S, 0.0
+        self.compared = 0.0   # the sum the last decision compared with ell
+
+    def full(self, k: int, change: float) -> bool:
+        if k == 0 or k == self.S - 1:
+            self.acc = self.compared = 0.0
+            return True
+        self.acc += change
+        self.compared = self.acc
+        if self.acc >= self.ell:
+            self.acc = 0.0
+            return True
+        return False
+
+
+def adaptive_mask(changes: Sequence[float], ell: float) -> List[int]:
+    """The mask the rule gives for a fixed sequence of changes (changes[0] is
+    unused: step 0 has no previous probe)."""
+    rule = AdaptiveRule(ell, len(changes))
+    return [1 if rule.full(k, float(c)) else 0 for k, c in enumerate(changes)]
+
+
+def sample_adaptive(model: Model, x_T: np.ndarray, S: int, ell: float, K: int, labels=None, text=None,
+                    p: Optional[bary.Params] = None, trace: Optional[Dict[str, list]] = None):
+    """The sampling loop under the adaptive schedule: at every step the probe
+    decides (AdaptiveRule) whether the stack runs; a skipped step forecasts
+    with the weights of the full steps taken so far (Eq. 8-13: the plan of a
+    step depends only on the steps before it).
+
+    Returns (final latent, realised mask, changes); changes[k] is the probe's
+    relative L1 change at step k >= 1 (changes[0] = 0)."""
+    cfg = model.cfg
+    B = x_T.shape[0]
+    ring = bary.Ring(K)
+    tin = model_time(cfg.sampler, S)
+    smp = Sampler(cfg.sampler, S, cfg.in_ch)
+    ctx = model.context(text) if cfg.kind != "dit" else None
+    rule = AdaptiveRule(ell, S)
+    x = np.asarray(x_T, dtype=np.float64)
+    mask: List[int] = []
+    changes: List[float] = []
+    prev = None
+    for k in range(S):
+        cond = model.condition(tin[k], B, labels, text)
+        emb = model.embed(x)
+        pr = model.probe(emb, cond)
+        change = relative_l1(pr, prev) if k > 0 else 0.0
+        prev = pr
+        full = rule.full(k, change)
+        if trace is not None:
+            trace.setdefault("acc", []).append(rule.compared)
+        mask.append(1 if full else 0)
+        changes.append(change)
+        if full:
+            feat = model.stack(emb, cond, ctx)
+            ring.push(feat, k)
+        else:
+            st = bary.plan(mask, K, None, p)[k]
+            feat = bary.forecast([ring.slots[i] for i in st.slots], st.w)
+        out = np.asarray(model.final(feat, cond), dtype=np.float64)
+        x = smp.step(k, x, out)
+        if trace is not None:
+            trace.setdefault("feat", []).append(feat)
+            trace.setdefault("probe", []).append(pr)
+            trace.setdefault("x", []).append(x)
+    return x, mask, changes
