@@ -37,6 +37,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-forecast", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="skip timing the HIP-graph replay of the run")
+    ap.add_argument("--adaptive-ell", type=float, default=0.13,
+                    help="threshold of the timed adaptive-schedule run (negative: skip it)")
     ap.add_argument("--kernels-only", action="store_true",
                     help="only launch the roofline kernels (fc2, fc1, self-attention of the workload's block, the "
                          "K = 3 forecast) a few times each through the C ABI, for hardware-counter passes")
@@ -271,6 +273,35 @@ def main():
         graph = {"value": round(B * args.steps / eg, 3), "ms_per_step": round(eg / args.steps * 1e3, 3)}
         del g
 
+    # The adaptive schedule (decided during the run from the first block's
+    # modulated input; one host read-back per step), timed like `value`.
+    adaptive = None
+    if args.adaptive_ell >= 0:
+        def run_adaptive():
+            x.copy_(x0)
+            return dm.sample_adaptive(x, cfg.steps, args.adaptive_ell, labels=tl, text=tt)
+        for _ in range(max(1, args.warmup)):
+            run_adaptive()
+        torch.cuda.synchronize()
+        ta = time.perf_counter()
+        for _ in range(args.steps):
+            _, amask, _ = run_adaptive()
+        torch.cuda.synchronize()
+        ea = time.perf_counter() - ta
+        # The fixed-mask loop under the realised mask: the probe's and the
+        # read-backs' cost is the difference.
+        run(amask)
+        torch.cuda.synchronize()
+        tfm = time.perf_counter()
+        for _ in range(args.steps):
+            run(amask)
+        torch.cuda.synchronize()
+        efm = time.perf_counter() - tfm
+        adaptive = {"ell": args.adaptive_ell, "full_steps": int(amask.sum()),
+                    "value": round(B * args.steps / ea, 3), "ms_per_step": round(ea / args.steps * 1e3, 3),
+                    "ms_fixed_loop_same_mask": round(efm / args.steps * 1e3, 3),
+                    "mask": "".join(str(int(v)) for v in amask)}
+
     # Speedup reference: the same sampler with every step full.
     full = np.ones(cfg.steps, np.uint8)
     run(full)
@@ -368,6 +399,7 @@ def main():
                                f"K={cfg.K}, full every {cfg.interval} ({nfull}/{cfg.steps}), random-init weights",
                    "global_batch": B, "parallelism": "none (1 GPU)"},
         "graph_replay": graph,
+        "adaptive": adaptive,
         "speedup_vs_all_full": round(ms_full / ms_per_step, 3),
         "ms_all_full": round(ms_full, 3),
         "roofline": roofline,

@@ -324,6 +324,40 @@ int bc_sample_cfg(const bc_model* m, int B, int sampler, int S, const uint8_t* m
                   const int64_t* labels, float cfg_scale, void* ws, size_t ws_bytes,
                   void* stream);
 
+/* Bytes of workspace bc_sample_adaptive needs: bc_sample's plus the previous
+ * step's probe (B*T*D elements of the model dtype), the first block's
+ * (shift, scale) for every step and sample (S*B*2*D floats) and 8 KiB of
+ * reduction partials. */
+int bc_sample_adaptive_workspace_size(const bc_model* m, int B, int S, size_t* bytes);
+
+/* The sampling loop under the adaptive schedule of Sec. 4.5 (Table 5): the
+ * full/forecast decision is taken during the run from a feature probe instead
+ * of a fixed mask.  At every step the latent is embedded and the first block's
+ * modulated LayerNorm LN(x)(1 + scale1) + shift1 (image stream of the first
+ * dual block for MMDIT) is the probe; for k >= 1 its change is
+ *   change[k] = sum |probe_k - probe_{k-1}| / sum |probe_{k-1}|
+ * over all B*T*D elements (sums in fp32 per workgroup, combined in double;
+ * 0/0 = 0, x/0 = +inf).  Changes accumulate (in double, on the host) since the
+ * last full step; step k runs the layer stack when k == 0, k == S-1, or the sum
+ * reaches ell, and a full step empties the sum.  Forecast steps use the plan of
+ * the full steps taken so far (Eq. 8-13), so the run equals bc_sample under the
+ * mask it realises.  ell = 0: every step full; ell = +inf: only the first and
+ * last.
+ *   ell:        threshold, >= 0 (+inf allowed).
+ *   mask_out:   host uint8 [S]: the realised mask (1 = full step).
+ *   change_out: host double [S] or NULL: change[k] (change[0] = 0).
+ *   ws:         bc_sample_adaptive_workspace_size(m, B, S) bytes, 256-byte aligned.
+ * Other arguments as bc_sample.  The decision needs the change on the host:
+ * the call copies two doubles back and synchronises `stream` once per step
+ * after the first, so it returns when the run has finished, and it cannot be
+ * captured into a graph.  Errors: as bc_sample; INVALID_ARG for a NaN or
+ * negative threshold or NULL mask_out; HIP if the read-back fails (mask_out
+ * and change_out then hold the steps decided so far). */
+int bc_sample_adaptive(const bc_model* m, int B, int sampler, int S, double ell, int K,
+                       const bc_bary_params* p, bc_cache_ring* ring, float* latents,
+                       const int64_t* labels, const void* text, void* ws, size_t ws_bytes,
+                       void* stream, uint8_t* mask_out, double* change_out);
+
 /* The same sampling run captured once as a HIP graph and replayed, for
  * callers whose loop is launch-bound (small models, short schedules).
  * bc_sample_graph_create runs nothing: it records into a graph exactly the

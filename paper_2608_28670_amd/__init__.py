@@ -118,6 +118,10 @@ _SIGS = {
     "bc_sample_cfg": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int,
                                 C.POINTER(BaryParams), C.c_void_p, C.c_void_p, C.c_void_p, C.c_float,
                                 C.c_void_p, C.c_size_t, C.c_void_p]),
+    "bc_sample_adaptive_workspace_size": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.POINTER(C.c_size_t)]),
+    "bc_sample_adaptive": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_double, C.c_int,
+                                     C.POINTER(BaryParams), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                     C.c_void_p, C.c_size_t, C.c_void_p, C.c_void_p, C.c_void_p]),
     "bc_sample_graph_create": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int,
                                          C.POINTER(BaryParams), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
                                          C.c_void_p, C.c_size_t, C.c_void_p, C.POINTER(C.c_void_p)]),
@@ -384,6 +388,11 @@ class Model:
         _check(lib().bc_sample_workspace_size(self.h, B, S, C.byref(n)))
         return n.value
 
+    def adaptive_workspace_size(self, B: int, S: int) -> int:
+        n = C.c_size_t()
+        _check(lib().bc_sample_adaptive_workspace_size(self.h, B, S, C.byref(n)))
+        return n.value
+
 
 def sample(model: Model, B: int, sampler: str, mask, K: int, ring: CacheRing, latents, ws,
            labels=None, text=None, p: Optional[BaryParams] = None, stream=None):
@@ -400,6 +409,19 @@ def sample_cfg(model: Model, B: int, sampler: str, mask, K: int, ring: CacheRing
     _check(lib().bc_sample_cfg(model.h, B, SAMPLERS[sampler], len(m), _ptr(m), K, C.byref(p) if p else None,
                                ring.h, dev_ptr(latents), dev_ptr(labels), float(cfg_scale), dev_ptr(ws),
                                ws.numel() * ws.element_size(), stream_handle(stream)))
+
+
+def sample_adaptive(model: Model, B: int, sampler: str, S: int, ell: float, K: int, ring: CacheRing, latents,
+                    ws, labels=None, text=None, p: Optional[BaryParams] = None, stream=None):
+    """Adaptive-schedule sampling (bc_sample_adaptive); returns (mask, changes)
+    as numpy arrays.  Synchronises the stream at every step."""
+    mask = np.zeros(S, dtype=np.uint8)
+    change = np.zeros(S, dtype=np.float64)
+    _check(lib().bc_sample_adaptive(model.h, B, SAMPLERS[sampler], S, float(ell), K, C.byref(p) if p else None,
+                                    ring.h, dev_ptr(latents), dev_ptr(labels), dev_ptr(text), dev_ptr(ws),
+                                    ws.numel() * ws.element_size(), stream_handle(stream), _ptr(mask),
+                                    _ptr(change)))
+    return mask, change
 
 
 class SampleGraph:

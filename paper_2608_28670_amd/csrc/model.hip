@@ -280,6 +280,12 @@ struct SampleWs {
     int full_chunk;                           // full steps whose modulation is held at once
     size_t bytes;
     int64_t* labels2;     // labels of a guided batch (the conditional half, then the null class)
+    // Adaptive schedule only: the previous step's probe [B*T, D] (model dtype),
+    // the first block's (shift, scale) of every (step, sample) [S*B, 2D], and
+    // the change measure's partial and final sums.
+    void* probe;
+    float *pmod, *part;
+    double* sums;
 };
 
 static int64_t latent_spatial(const bc_model_desc& d) { return (int64_t)d.frames * d.height * d.width; }
@@ -294,7 +300,7 @@ static int64_t mod_width(const bc_model_desc& d) {
     return d.kind == BC_MODEL_MMDIT ? (int64_t)2 * d.depth * 6 * d.D : (int64_t)d.depth * 6 * d.D;
 }
 
-static SampleWs carve_sample(const bc_model_desc& d, int B, int S, void* base) {
+static SampleWs carve_sample(const bc_model_desc& d, int B, int S, void* base, bool adaptive = false) {
     Carver c(base);
     SampleWs w;
     const int T = model_tokens(d), D = d.D, F = d.mlp;
@@ -336,6 +342,10 @@ static SampleWs carve_sample(const bc_model_desc& d, int B, int S, void* base) {
     w.out = c.take<float>((size_t)B * d.out_ch * latent_spatial(d) * f4);
     w.prev = c.take<float>((size_t)B * d.in_ch * latent_spatial(d) * f4);
     w.labels2 = c.take<int64_t>((size_t)B * sizeof(int64_t));
+    w.probe = c.take<char>(adaptive ? (size_t)B * T * D * esz : 0);
+    w.pmod = c.take<float>(adaptive ? (size_t)SB * 2 * D * f4 : 0);
+    w.part = c.take<float>(adaptive ? (size_t)kRelL1Blocks * 2 * f4 : 0);
+    w.sums = c.take<double>(adaptive ? 2 * sizeof(double) : 0);
     w.bytes = c.off + 256;
     return w;
 }
@@ -519,14 +529,48 @@ int bc_sample_workspace_size(const bc_model* m, int B, int S, size_t* bytes) {
     return BC_OK;
 }
 
+int bc_sample_adaptive_workspace_size(const bc_model* m, int B, int S, size_t* bytes) {
+    clear_error();
+    if (!m || !bytes) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
+    if (B < 1 || B > 64) return fail(BC_ERR_INVALID_ARG, "B=%d outside [1, 64]", B);
+    if (S < 1 || S > 1000) return fail(BC_ERR_INVALID_ARG, "S=%d outside [1, 1000]", S);
+    *bytes = carve_sample(m->d, B, S, nullptr, true).bytes;
+    return BC_OK;
+}
+
 }  // extern "C"
 
+// Pinned host memory for the adaptive schedule's per-step read-back of two
+// doubles (a copy into pageable memory costs tens of microseconds more per
+// step).  One buffer per host thread, allocated on first use and kept until
+// the process ends.
+static double* readback_buffer() {
+    thread_local double* buf = nullptr;
+    if (!buf) {
+        void* p = nullptr;
+        if (hipHostMalloc(&p, 256, hipHostMallocDefault) != hipSuccess) return nullptr;
+        buf = static_cast<double*>(p);
+    }
+    return buf;
+}
+
+// The adaptive schedule's threshold and outputs (host arrays of S entries).
+struct AdaptiveIO {
+    double ell;
+    uint8_t* mask_out;
+    double* change_out;   // may be NULL
+};
+
 // The loop of bc_sample; guided: classifier-free guidance with scale cfg over
-// a model batch of 2B (labels, then the null class) for B latents.
+// a model batch of 2B (labels, then the null class) for B latents.  With `ad`
+// the mask is not given but decided step by step (adaptive schedule), which
+// reads two sums back to the host at every step after the first.
 static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_t* mask, int K, const bc_bary_params* p,
                       bc_cache_ring* ring, float* latents, const int64_t* labels, const void* text, bool guided,
-                      float cfg, void* ws, size_t ws_bytes, void* stream) {
-    if (!m || !mask || !ring || !latents || !ws) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
+                      float cfg, void* ws, size_t ws_bytes, void* stream, const AdaptiveIO* ad = nullptr) {
+    if (!m || !(mask || ad) || !ring || !latents || !ws) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
+    if (ad && (guided || !ad->mask_out || !(ad->ell >= 0.0)))
+        return fail(BC_ERR_INVALID_ARG, "adaptive schedule: mask_out required, threshold >= 0, no guidance");
     const bc_model_desc& d = m->d;
     const int Bm = guided ? 2 * B : B;     // model batch
     if (B < 1 || Bm > 64) return fail(BC_ERR_INVALID_ARG, "B=%d outside [1, %d]", B, guided ? 32 : 64);
@@ -540,9 +584,12 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
     std::vector<int32_t> tau(S > 0 ? S : 1);
     std::vector<double> tin(S > 0 ? S : 1);
     BC_TRY(bc_make_schedule(sampler, S, tau.data(), tin.data()));
+    if (S < 1 || S > 1000) return fail(BC_ERR_INVALID_ARG, "S=%d outside [1, 1000]", S);
     std::vector<bc_plan_step> plan(S);
-    BC_TRY(bc_plan(S, mask, nullptr, K, p, plan.data()));
-    const SampleWs w = carve_sample(d, Bm, S, ws);
+    std::vector<uint8_t> amask(S, 1);      // adaptive: the mask decided so far
+    if (!ad) BC_TRY(bc_plan(S, mask, nullptr, K, p, plan.data()));
+    else BC_TRY(bc_plan(S, amask.data(), nullptr, K, p, plan.data()));   // validates K and p
+    const SampleWs w = carve_sample(d, Bm, S, ws, ad != nullptr);
     if (ws_bytes < w.bytes) return fail(BC_ERR_INVALID_ARG, "workspace %zu < %zu bytes", ws_bytes, w.bytes);
 
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -604,15 +651,44 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
         fg.e.out_f32 = 1;
         BC_TRY(launch_gemm(dt, BC_EPI_BIAS, fg, s));
     }
+    if (ad) {
+        // The probe's modulation, the first block's (shift, scale), for every
+        // step: SiLU(c) times the first 2D rows of the first block's (image
+        // stream) modulation weights; PixArt: t6's first 2D entries plus the
+        // block's table.
+        if (d.kind == BC_MODEL_PIXART) {
+            for (int k0 = 0; k0 < S; k0 += kMaxSeg) {
+                const int n = std::min(kMaxSeg, S - k0);
+                RowList rl;
+                for (int i = 0; i < n; ++i) rl.row[i] = k0 + i;
+                BC_TRY(launch_gather_silu(dt, w.c, Bm, D, rl, n,
+                                          static_cast<char*>(w.sc) + (int64_t)k0 * Bm * D * esz, s));
+            }
+        }
+        const bool px = d.kind == BC_MODEL_PIXART;
+        GemmArgs pg = gemm_args(w.sc, D, px ? mw.t6_w : blk[0].img.w_mod, D, S * Bm, 2 * D, D);
+        pg.e.bias = px ? mw.t6_b : blk[0].img.b_mod;
+        pg.e.out = w.pmod;
+        pg.e.ldo = 2 * D;
+        pg.e.out_f32 = 1;
+        BC_TRY(launch_gemm(dt, BC_EPI_BIAS, pg, s));
+        if (px) {
+            const void* tab[1] = {blk[0].img.w_mod};
+            BC_TRY(launch_add_tables(dt, w.pmod, 2 * D, tab, 1, 2 * D, S * Bm, w.pmod, 2 * D, s));
+        }
+    }
     std::vector<int> full_steps;
-    for (int k = 0; k < S; ++k)
+    for (int k = 0; k < S && !ad; ++k)
         if (plan[k].is_full) full_steps.push_back(k);
+    // Full steps whose modulation is computed together (one at a time when
+    // they are decided during the loop).
+    const int chunk = ad ? 1 : w.full_chunk;
     const int64_t ldm = mod_width(d);
     const int64_t lds = (int64_t)d.depth_single * 3 * D;
     // Block modulation of a chunk of full steps: rows (i, b) for the i-th full
     // step of the chunk; w.sc is reused for the gathered SiLU(c) rows.
     auto chunk_mods = [&](int f0) -> int {
-        const int n = std::min<int>(w.full_chunk, (int)full_steps.size() - f0);
+        const int n = std::min<int>(chunk, (int)full_steps.size() - f0);
         RowList rl;
         for (int i = 0; i < n; ++i) rl.row[i] = full_steps[f0 + i];
         // (PixArt has no class or text term in c, so c is the timestep
@@ -667,7 +743,40 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
                              reinterpret_cast<uintptr_t>(mw.final_w) % 16 == 0;
 
     int full_index = 0;
+    double acc = 0.0;   // adaptive: changes summed since the last full step
     for (int k = 0; k < S; ++k) {
+        if (ad) {
+            // Probe at this step's latent: the embedding (which a full step
+            // then uses) and the first block's modulated LayerNorm.
+            BC_TRY(launch_patch_embed(dt, latents, ls, Bm, B, mw.patch_w, mw.patch_b, mw.pos, D, w.x_img, s));
+            BC_TRY(launch_ln_mod(BC_F32, w.x_img, (int64_t)Bm * T, D, w.pmod + (int64_t)k * Bm * 2 * D,
+                                 w.pmod + (int64_t)k * Bm * 2 * D + D, 2 * D, T, dt, w.bb.h, s));
+            const int64_t n = (int64_t)Bm * T * D;
+            double change = 0.0;
+            if (k == 0) {
+                BC_TRY(launch_copy(w.bb.h, w.probe, n * (int64_t)esz, s));
+            } else {
+                BC_TRY(launch_rel_l1(dt, w.bb.h, w.probe, n, w.part, w.sums, s));
+                double* sums = readback_buffer();
+                if (!sums) return fail(BC_ERR_HIP, "adaptive change readback: no pinned host buffer");
+                hipError_t e = hipMemcpyAsync(sums, w.sums, 2 * sizeof(double), hipMemcpyDeviceToHost, s);
+                if (e == hipSuccess) e = hipStreamSynchronize(s);
+                if (e != hipSuccess) return fail(BC_ERR_HIP, "adaptive change readback: %s", hipGetErrorString(e));
+                change = sums[1] > 0.0 ? sums[0] / sums[1] : sums[0] == 0.0 ? 0.0 : INFINITY;
+            }
+            bool full = true;
+            if (k > 0 && k < S - 1) {
+                acc += change;
+                full = acc >= ad->ell;
+            }
+            if (full) acc = 0.0;
+            amask[k] = full ? 1 : 0;
+            ad->mask_out[k] = amask[k];
+            if (ad->change_out) ad->change_out[k] = change;
+            // The plan of step k depends only on the steps up to k.
+            BC_TRY(bc_plan(k + 1, amask.data(), nullptr, K, p, plan.data()));
+            if (full) full_steps.push_back(k);
+        }
         const bc_plan_step& st = plan[k];
         const float* fmod = w.fmod + (int64_t)k * Bm * 2 * D;
         const void* feat;
@@ -678,12 +787,13 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
             out.ptr = slot;
             out.dt = dt;
             // Block modulation of this full step (computed a chunk of full steps at a time).
-            const int fi = full_index % w.full_chunk;
+            const int fi = full_index % chunk;
             if (fi == 0) BC_TRY(chunk_mods(full_index));
             ++full_index;
             const float* mods = w.mods + (int64_t)fi * Bm * ldm;
             const float* mods_s = w.mods_s + (int64_t)fi * Bm * lds;
-            BC_TRY(launch_patch_embed(dt, latents, ls, Bm, B, mw.patch_w, mw.patch_b, mw.pos, D, w.x_img, s));
+            if (!ad)   // (the adaptive loop embedded the latent for its probe)
+                BC_TRY(launch_patch_embed(dt, latents, ls, Bm, B, mw.patch_w, mw.patch_b, mw.pos, D, w.x_img, s));
             if (d.kind == BC_MODEL_MMDIT) {
                 BC_TRY(launch_convert(dt, text, BC_F32, w.x_txt, (int64_t)B * Tt * D, s));
                 for (int l = 0; l < d.depth; ++l)
@@ -786,6 +896,17 @@ int bc_sample_cfg(const bc_model* m, int B, int sampler, int S, const uint8_t* m
     if (!std::isfinite(cfg_scale)) return fail(BC_ERR_INVALID_ARG, "guidance scale must be finite");
     return sample_run(m, B, sampler, S, mask, K, p, ring, latents, labels, nullptr, true, cfg_scale, ws, ws_bytes,
                       stream);
+}
+
+int bc_sample_adaptive(const bc_model* m, int B, int sampler, int S, double ell, int K, const bc_bary_params* p,
+                       bc_cache_ring* ring, float* latents, const int64_t* labels, const void* text, void* ws,
+                       size_t ws_bytes, void* stream, uint8_t* mask_out, double* change_out) {
+    clear_error();
+    if (!mask_out) return fail(BC_ERR_INVALID_ARG, "mask_out required");
+    if (!(ell >= 0.0)) return fail(BC_ERR_INVALID_ARG, "threshold must be >= 0 (got %g)", ell);
+    const AdaptiveIO io{ell, mask_out, change_out};
+    return sample_run(m, B, sampler, S, nullptr, K, p, ring, latents, labels, text, false, 1.f, ws, ws_bytes, stream,
+                      &io);
 }
 
 }  // extern "C"

@@ -103,6 +103,14 @@ __device__ __forceinline__ void sampler_update(const SamplerCoef& k, float* x, f
     if (prev) *prev = x0;
 }
 
+// Change measure of the adaptive schedule: over n elements of `dt`,
+// sums[0] = sum |cur - prev| and sums[1] = sum |prev| (fp32 per thread and
+// workgroup, the kRelL1Blocks partials `part` [2 * kRelL1Blocks] then added in
+// double in a fixed order: the same inputs give the same sums), and prev = cur
+// afterwards.  cur and prev 16-byte aligned.
+constexpr int kRelL1Blocks = 1024;
+int launch_rel_l1(int dt, const void* cur, void* prev, int64_t n, float* part, double* sums, hipStream_t s);
+
 // Final step fused over 16-token groups, for bf16 models whose (D, p*p*C_out)
 // has an instantiated variant (final_step_supported): the stepwise feature
 // sum_j w[j] src[j] (rounded to bf16 like the unfused forecast), LayerNorm +

@@ -2,6 +2,7 @@
 // modulation, the skinny linear layers of the conditioning path, patch
 // embedding, the final layer, sampler updates and element-wise helpers.
 // All statistics and accumulations are fp32.
+#include <algorithm>
 #include <cmath>
 
 #include "ops.h"
@@ -520,6 +521,106 @@ int launch_sampler(const SamplerCoef& k, float* x, const float* out_tok, float* 
     const int64_t n = (int64_t)B * ls.C * ls.F * ls.H * ls.W;
     sampler_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(k, x, out_tok, prev, ls, B, C_out, cfg, uncond_off);
     return check_launch("sampler");
+}
+
+// ---------------------------------------------------------------------------
+// Relative L1 change of the adaptive schedule's probe: 16-byte chunks of cur
+// and prev, |cur - prev| and |prev| summed per thread, per wave (butterfly)
+// and per workgroup in a fixed order; prev takes cur's bytes in the same pass.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void abs_sums(const u32x4& c, const u32x4& p, float& sd, float& sp, bf16*) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float cl = __uint_as_float(c[i] << 16), ch = __uint_as_float(c[i] & 0xffff0000u);
+        const float pl = __uint_as_float(p[i] << 16), ph = __uint_as_float(p[i] & 0xffff0000u);
+        sd += fabsf(cl - pl) + fabsf(ch - ph);
+        sp += fabsf(pl) + fabsf(ph);
+    }
+}
+__device__ __forceinline__ void abs_sums(const u32x4& c, const u32x4& p, float& sd, float& sp, float*) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float cf = __uint_as_float(c[i]), pf = __uint_as_float(p[i]);
+        sd += fabsf(cf - pf);
+        sp += fabsf(pf);
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void rel_l1_kernel(const T* __restrict__ cur, T* __restrict__ prev, int64_t n,
+                                                     float* __restrict__ part) {
+    constexpr int E = 16 / (int)sizeof(T);
+    const int64_t nc = n / E;
+    const u32x4* c4 = reinterpret_cast<const u32x4*>(cur);
+    u32x4* p4 = reinterpret_cast<u32x4*>(prev);
+    float sd = 0.f, sp = 0.f;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < nc; i += (int64_t)gridDim.x * 256) {
+        const u32x4 c = c4[i], p = p4[i];
+        abs_sums(c, p, sd, sp, (T*)nullptr);
+        p4[i] = c;
+    }
+    if (blockIdx.x == 0) {
+        for (int64_t i = nc * E + threadIdx.x; i < n; i += 256) {
+            const float c = ld(cur + i), p = ld(prev + i);
+            sd += fabsf(c - p);
+            sp += fabsf(p);
+            prev[i] = cur[i];
+        }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        sd += __shfl_xor(sd, o);
+        sp += __shfl_xor(sp, o);
+    }
+    __shared__ float red[2][4];
+    const int wv = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        red[0][wv] = sd;
+        red[1][wv] = sp;
+    }
+    __syncthreads();
+    if (threadIdx.x < 2) {
+        const float* r = red[threadIdx.x];
+        part[2 * blockIdx.x + threadIdx.x] = ((r[0] + r[1]) + r[2]) + r[3];
+    }
+}
+
+__global__ __launch_bounds__(256) void rel_l1_sum_kernel(const float* __restrict__ part, int nblk,
+                                                         double* __restrict__ sums) {
+    __shared__ double ra[256], rb[256];
+    const int t = threadIdx.x;
+    double a = 0.0, b = 0.0;
+    for (int i = t; i < nblk; i += 256) {
+        a += (double)part[2 * i];
+        b += (double)part[2 * i + 1];
+    }
+    ra[t] = a;
+    rb[t] = b;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if (t < h) {
+            ra[t] += ra[t + h];
+            rb[t] += rb[t + h];
+        }
+        __syncthreads();
+    }
+    if (t < 2) sums[t] = t == 0 ? ra[0] : rb[0];
+}
+
+int launch_rel_l1(int dt, const void* cur, void* prev, int64_t n, float* part, double* sums, hipStream_t s) {
+    if (n < 1) return fail(BC_ERR_INVALID_ARG, "rel_l1: n=%lld", (long long)n);
+    if (reinterpret_cast<uintptr_t>(cur) % 16 || reinterpret_cast<uintptr_t>(prev) % 16)
+        return fail(BC_ERR_INVALID_ARG, "rel_l1: buffers must be 16-byte aligned");
+    const int64_t nc = n / (16 / (int64_t)dtype_size(dt));
+    const int nblk = (int)std::min<int64_t>(kRelL1Blocks, std::max<int64_t>(1, (nc + 1023) / 1024));
+    if (dt == BC_BF16)
+        rel_l1_kernel<bf16><<<nblk, 256, 0, s>>>(static_cast<const bf16*>(cur), static_cast<bf16*>(prev), n, part);
+    else
+        rel_l1_kernel<float><<<nblk, 256, 0, s>>>(static_cast<const float*>(cur), static_cast<float*>(prev), n, part);
+    const int rc = check_launch("rel_l1");
+    if (rc != BC_OK) return rc;
+    rel_l1_sum_kernel<<<1, 256, 0, s>>>(part, nblk, sums);
+    return check_launch("rel_l1_sum");
 }
 
 }  // namespace bc

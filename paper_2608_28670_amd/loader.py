@@ -14,7 +14,7 @@ import numpy as np
 
 from . import (BF16, BLOCK_DIT, BLOCK_DUAL, BLOCK_PIXART, BLOCK_SINGLE, F32, MODEL_DIT, MODEL_MMDIT,
                MODEL_PIXART, BlockWeights, CacheRing, Model, ModelDesc, SampleGraph, block_weights, sample,
-               sample_cfg)
+               sample_adaptive, sample_cfg)
 
 _KIND = {"dit": MODEL_DIT, "pixart": MODEL_PIXART, "mmdit": MODEL_MMDIT}
 
@@ -103,12 +103,17 @@ class DeviceModel:
         if (B, S) not in self._ws:
             n = self.model.workspace_size(B, S)
             self._ws[(B, S)] = torch.empty(n, dtype=torch.uint8, device=self.device)
+        return self._ws[(B, S)], self.ring(B, K)
+
+    def ring(self, B: int, K: int) -> CacheRing:
+        """Ring of K slots of B*T*D elements (allocated once, reused)."""
+        import torch
         key = (B, K)
         if key not in self._ring:
             numel = B * self.cfg.tokens * self.cfg.hidden
             storage = torch.empty((K, numel), dtype=torch_dtype(self.cfg), device=self.device)
             self._ring[key] = CacheRing(K, storage)
-        return self._ws[(B, S)], self._ring[key]
+        return self._ring[key]
 
     def sample_graph(self, x, mask, K: Optional[int] = None, labels=None, text=None, p=None):
         """The same run captured as a HIP graph on x's buffer; .launch() replays it in place."""
@@ -116,6 +121,21 @@ class DeviceModel:
         B = x.shape[0]
         ws, ring = self.buffers(B, K, len(mask))
         return SampleGraph(self.model, B, self.cfg.sampler, mask, K, ring, x, ws, labels=labels, text=text, p=p)
+
+    def sample_adaptive(self, x, S: int, ell: float, K: Optional[int] = None, labels=None, text=None, p=None,
+                        stream=None):
+        """Adaptive-schedule sampling in place on x; returns (ring, mask, changes)."""
+        import torch
+        K = K or self.cfg.K
+        B = x.shape[0]
+        key = ("adaptive", B, S)
+        if key not in self._ws:
+            self._ws[key] = torch.empty(self.model.adaptive_workspace_size(B, S), dtype=torch.uint8,
+                                        device=self.device)
+        ring = self.ring(B, K)
+        mask, change = sample_adaptive(self.model, B, self.cfg.sampler, S, ell, K, ring, x, self._ws[key],
+                                       labels=labels, text=text, p=p, stream=stream)
+        return ring, mask, change
 
     def sample_cfg(self, x, mask, labels, cfg_scale: float, K: Optional[int] = None, p=None, stream=None):
         """Classifier-free guided sampling in place on x (B latents; model batch 2B)."""
