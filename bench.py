@@ -117,6 +117,8 @@ def device_params(cfg, torch, dev):
     for name, shape in synth.param_shapes(cfg):
         t = torch.empty(shape, dtype=torch.float32, device=dev)
         t.normal_(0.0, cfg.param_scale, generator=g)
+        if name.endswith("_norm"):   # RMSNorm scales sit around 1
+            t.add_(1.0)
         out[name] = t.to(dt)
         del t
     return out

@@ -51,6 +51,49 @@ def layer_norm(x, eps=LN_EPS):
     return (x - mu) / np.sqrt(var + eps)
 
 
+def rms_norm(x, w, eps=LN_EPS):
+    """RMSNorm over the last axis with a learned scale: x / sqrt(mean(x^2) + eps) * w."""
+    return x / np.sqrt((x * x).mean(-1, keepdims=True) + eps) * w
+
+
+def rope_axes(head_dim):
+    """Head dimensions given to the (frame, row, column) axes of the 3D rotary
+    embedding: head_dim/8 to the frame index and the rest split evenly between
+    row and column (128 -> 16, 56, 56, the split of the video model's 3D RoPE)."""
+    dt = head_dim // 8
+    dh = (head_dim - dt) // 2
+    axes = (dt, dh, head_dim - dt - dh)
+    if any(d % 2 for d in axes):
+        raise ValueError("the 3D rotary embedding needs head_dim % 32 == 0")
+    return axes
+
+
+def rope_angles(grid, head_dim, theta):
+    """Rotation angle of every (token, pair) [T, head_dim/2] for a (F, H, W)
+    token grid in (frame, row, column) order.  Pair i holds dimensions 2i and
+    2i + 1; in an axis of d dimensions its j-th pair turns by
+    pos * theta^(-2j / d), pos being the token's index along that axis."""
+    F, H, W = grid
+    f, h, w = np.meshgrid(np.arange(F), np.arange(H), np.arange(W), indexing="ij")
+    pos = [f.reshape(-1), h.reshape(-1), w.reshape(-1)]
+    cols = []
+    for p_a, d in zip(pos, rope_axes(head_dim)):
+        freq = theta ** (-np.arange(0, d, 2, dtype=np.float64) / d)
+        cols.append(p_a[:, None].astype(np.float64) * freq[None, :])
+    return np.concatenate(cols, axis=1)
+
+
+def apply_rope(x, ang):
+    """Rotate each pair (x[..., 2i], x[..., 2i+1]) of x [..., T, head_dim] by
+    ang [T, head_dim/2]."""
+    c, s = np.cos(ang), np.sin(ang)
+    x0, x1 = x[..., 0::2], x[..., 1::2]
+    out = np.empty_like(x)
+    out[..., 0::2] = x0 * c - x1 * s
+    out[..., 1::2] = x0 * s + x1 * c
+    return out
+
+
 def modulate(h, shift, scale):
     """h * (1 + scale) + shift, with per-sample [B, D] vectors broadcast over tokens."""
     return h * (1.0 + scale[:, None, :]) + shift[:, None, :]
@@ -192,6 +235,27 @@ class Model:
         y = linear(h, P["final_w"], P["final_b"])
         return unpatchify(y, cfg.p, cfg.latent, cfg.out_ch)
 
+    # -- query/key processing of the video model's blocks -------------------------
+    def token_grid(self):
+        cfg = self.cfg
+        if len(cfg.latent) == 3:
+            return 1, cfg.latent[1] // cfg.p, cfg.latent[2] // cfg.p
+        return cfg.latent[1], cfg.latent[2] // cfg.p, cfg.latent[3] // cfg.p
+
+    def qk(self, q, k, pre, n_img):
+        """RMSNorm (per head, learned scales pre+q_norm / pre+k_norm) and the 3D
+        rotary embedding of the first n_img tokens, on q, k [B, H, T, hd]."""
+        cfg, P = self.cfg, self.P
+        if cfg.qk_norm:
+            q = rms_norm(q, P[pre + "q_norm"])
+            k = rms_norm(k, P[pre + "k_norm"])
+        if cfg.rope_theta and n_img:
+            ang = rope_angles(self.token_grid(), cfg.head_dim, cfg.rope_theta)
+            q, k = q.copy(), k.copy()
+            q[:, :, :n_img] = apply_rope(q[:, :, :n_img], ang)
+            k[:, :, :n_img] = apply_rope(k[:, :, :n_img], ang)
+        return q, k
+
     # -- blocks ----------------------------------------------------------------
     def block_mod(self, l, cond):
         """The six [B, D] modulation vectors of DiT/PixArt block l."""
@@ -226,15 +290,19 @@ class Model:
         cfg, P = self.cfg, self.P
         D, H = cfg.hidden, cfg.heads
         Ti = xi.shape[1]
-        mods, hs, qkvs = {}, {}, {}
+        mods, qs, ks, vs = {}, [], [], []
         for s, x in (("img", xi), ("txt", xt)):
             pre = f"dual.{l}.{s}."
             m = linear(silu(cond["c"]), P[pre + "w_mod"], P[pre + "b_mod"])
             mods[s] = [m[:, i * D:(i + 1) * D] for i in range(6)]
             h = modulate(layer_norm(x), mods[s][0], mods[s][1])
-            qkvs[s] = linear(h, P[pre + "w_qkv"], P[pre + "b_qkv"])
-        qkv = np.concatenate([qkvs["img"], qkvs["txt"]], axis=1)
-        q, k, v = (split_heads(qkv[..., i * D:(i + 1) * D], H) for i in range(3))
+            qkv = linear(h, P[pre + "w_qkv"], P[pre + "b_qkv"])
+            q, k, v = (split_heads(qkv[..., i * D:(i + 1) * D], H) for i in range(3))
+            q, k = self.qk(q, k, pre, Ti if s == "img" else 0)
+            qs.append(q)
+            ks.append(k)
+            vs.append(v)
+        q, k, v = (np.concatenate(z, axis=2) for z in (qs, ks, vs))
         a = merge_heads(attention(q, k, v))
         outs = []
         for s, x, a_s in (("img", xi, a[:, :Ti]), ("txt", xt, a[:, Ti:])):
@@ -246,7 +314,7 @@ class Model:
             outs.append(x + g2[:, None, :] * linear(mm, P[pre + "w_fc2"], P[pre + "b_fc2"]))
         return outs[0], outs[1]
 
-    def single_block(self, l, x, cond):
+    def single_block(self, l, x, cond, n_img=0):
         cfg, P = self.cfg, self.P
         D, H = cfg.hidden, cfg.heads
         pre = f"single.{l}."
@@ -255,6 +323,7 @@ class Model:
         h = modulate(layer_norm(x), s, sc)
         y = linear(h, P[pre + "w_1"], P[pre + "b_1"])
         q, k, v = (split_heads(y[..., i * D:(i + 1) * D], H) for i in range(3))
+        q, k = self.qk(q, k, pre, n_img)
         a = merge_heads(attention(q, k, v))
         z = np.concatenate([a, gelu_tanh(y[..., 3 * D:])], axis=-1)
         return x + g[:, None, :] * linear(z, P[pre + "w_2"], P[pre + "b_2"])
@@ -287,5 +356,5 @@ class Model:
         Ti = x.shape[1]
         z = np.concatenate([x, xt], axis=1)
         for l in range(cfg.depth_single):
-            z = self.single_block(l, z, cond)
+            z = self.single_block(l, z, cond, Ti)
         return z[:, :Ti]

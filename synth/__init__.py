@@ -94,6 +94,8 @@ class ModelConfig:
     ctx_tokens: int = 0    # pixart cross-attention context length
     ctx_dim: int = 0       # pixart raw text width
     txt_tokens: int = 0    # mmdit text stream tokens
+    qk_norm: bool = False  # mmdit: RMSNorm (learned scale) on each head's queries and keys
+    rope_theta: float = 0.0  # mmdit: 3D rotary embedding of the image tokens' queries and keys (0: none)
     param_scale: float = 0.02
     latent_scale: float = 1.0
     freq_dim: int = 256
@@ -140,7 +142,7 @@ CONFIGS: Dict[str, ModelConfig] = {
     "hunyuan": ModelConfig(
         name="hunyuan", kind="mmdit", depth=20, depth_single=40, hidden=3072, heads=24, head_dim=128,
         mlp=12288, in_ch=16, out_ch=16, patch=(2,), latent=(16, 9, 60, 106), batch=1, steps=50,
-        sampler="euler", K=3, interval=5, dtype="bf16", txt_tokens=256),
+        sampler="euler", K=3, interval=5, dtype="bf16", txt_tokens=256, qk_norm=True, rope_theta=256.0),
 }
 
 
@@ -194,19 +196,26 @@ def param_shapes(cfg: ModelConfig) -> List[Tuple[str, Tuple[int, ...]]]:
                         (q + "w_o", (D, D)), (q + "b_o", (D,)),
                         (q + "w_fc1", (F, D)), (q + "b_fc1", (F,)),
                         (q + "w_fc2", (D, F)), (q + "b_fc2", (D,))]
+                if cfg.qk_norm:
+                    out += [(q + "q_norm", (cfg.head_dim,)), (q + "k_norm", (cfg.head_dim,))]
         for l in range(cfg.depth_single):
             p = f"single.{l}."
             out += [(p + "w_mod", (3 * D, D)), (p + "b_mod", (3 * D,)),
                     (p + "w_1", (3 * D + F, D)), (p + "b_1", (3 * D + F,)),
                     (p + "w_2", (D, D + F)), (p + "b_2", (D,))]
+            if cfg.qk_norm:
+                out += [(p + "q_norm", (cfg.head_dim,)), (p + "k_norm", (cfg.head_dim,))]
         out += [("final_w_mod", (2 * D, D)), ("final_b_mod", (2 * D,))]
     out += [("final_w", (cfg.out_patch_dim, D)), ("final_b", (cfg.out_patch_dim,))]
     return out
 
 
 def param(cfg: ModelConfig, name: str, shape, seed: int = SEED) -> np.ndarray:
-    """One parameter tensor: N(0,1)*scale, rounded to bf16 values for bf16 models."""
+    """One parameter tensor: N(0,1)*scale (norm scales: 1 + N(0,1)*scale),
+    rounded to bf16 values for bf16 models."""
     a = normal(f"{cfg.name}/{name}", shape, cfg.param_scale, seed)
+    if name.endswith("_norm"):
+        a = (a + 1.0).astype(np.float32)
     return bf16_round(a) if cfg.dtype == "bf16" else a
 
 
