@@ -186,6 +186,16 @@ typedef struct {
     int T_txt;      /* DUAL / SINGLE: text tokens per sample, else 0 */
     int T_ctx;      /* PIXART: context tokens per sample, else 0 */
     int dtype;      /* weights and activations: BC_F32 or BC_BF16 */
+    /* DUAL / SINGLE: 3D rotary embedding of the image tokens' queries and keys
+     * (the video model's attention).  The T image tokens form an
+     * rope_f x rope_h x rope_w grid in (frame, row, column) order; pair i of a
+     * head (dims 2i, 2i+1) lies in the frame, row or column axis (head_dim/8,
+     * 7 head_dim/16, 7 head_dim/16 dims) and turns by pos * theta^(-2j/d_axis),
+     * j its pair index within the axis.  rope_theta <= 0: none (then the grid
+     * is ignored); else the grid product must be T and head_dim % 32 == 0.
+     * Text tokens are never rotated. */
+    int rope_f, rope_h, rope_w;
+    double rope_theta;
 } bc_block_desc;
 
 /* One stream's parameters, device pointers in the block's dtype.
@@ -194,13 +204,18 @@ typedef struct {
  *   PIXART: w_mod is the per-block table [6, D] (b_mod unused), the rest as DIT.
  *   SINGLE: w_mod [3D, D], b_mod [3D]; w_qkv is the fused input projection
  *     [3D + mlp, D] with bias b_qkv; w_o is the fused output projection
- *     [D, D + mlp] with bias b_o; the fc pointers are unused. */
+ *     [D, D + mlp] with bias b_o; the fc pointers are unused.
+ *   q_norm, k_norm (DUAL / SINGLE, optional, both or neither): [head_dim]
+ *     scales of the RMSNorm applied to every head of the stream's queries and
+ *     keys before attention (x / sqrt(mean(x^2) + 1e-6) * scale), ahead of the
+ *     rotary embedding. */
 typedef struct {
     const void *w_mod, *b_mod;
     const void *w_qkv, *b_qkv;
     const void *w_o, *b_o;
     const void *w_fc1, *b_fc1;
     const void *w_fc2, *b_fc2;
+    const void *q_norm, *k_norm;
 } bc_stream_weights;
 
 typedef struct {
@@ -252,6 +267,9 @@ typedef struct {
     int txt_tokens;    /* MMDIT text: [B, txt_tokens, D] */
     int freq_dim;      /* timestep sinusoid width, even */
     int dtype;         /* BC_F32 or BC_BF16: weights, activations and the ring */
+    double rope_theta; /* MMDIT: 3D rotary embedding of the image tokens over the
+                          (frames, height/patch, width/patch) grid, as in
+                          bc_block_desc; <= 0: none.  Other kinds: 0. */
 } bc_model_desc;
 
 /* Device pointers in the model dtype.  Token features are patches in

@@ -50,10 +50,12 @@ class PlanStep(C.Structure):
 
 class BlockDesc(C.Structure):
     _fields_ = [(n, C.c_int) for n in ("kind", "B", "T", "D", "heads", "head_dim", "mlp",
-                                       "T_txt", "T_ctx", "dtype")]
+                                       "T_txt", "T_ctx", "dtype", "rope_f", "rope_h", "rope_w")] + \
+               [("rope_theta", C.c_double)]
 
 
-_STREAM_FIELDS = ("w_mod", "b_mod", "w_qkv", "b_qkv", "w_o", "b_o", "w_fc1", "b_fc1", "w_fc2", "b_fc2")
+_STREAM_FIELDS = ("w_mod", "b_mod", "w_qkv", "b_qkv", "w_o", "b_o", "w_fc1", "b_fc1", "w_fc2", "b_fc2",
+                  "q_norm", "k_norm")
 
 
 class StreamWeights(C.Structure):
@@ -69,7 +71,7 @@ class ModelDesc(C.Structure):
     _fields_ = [(n, C.c_int) for n in ("kind", "depth", "depth_single", "D", "heads", "head_dim", "mlp",
                                        "in_ch", "out_ch", "patch", "frames", "height", "width",
                                        "n_classes", "ctx_tokens", "ctx_dim", "txt_tokens", "freq_dim",
-                                       "dtype")]
+                                       "dtype")] + [("rope_theta", C.c_double)]
 
 
 _MODEL_PTRS = ("t_w1", "t_b1", "t_w2", "t_b2", "patch_w", "patch_b", "pos", "y_table", "t6_w", "t6_b",
@@ -321,10 +323,13 @@ def attention(q, k, v, out, ws=None, stream=None):
                               stream_handle(stream)))
 
 
-def block_desc(kind, B, T, D, heads, head_dim, mlp, dtype, T_txt=0, T_ctx=0) -> BlockDesc:
+def block_desc(kind, B, T, D, heads, head_dim, mlp, dtype, T_txt=0, T_ctx=0, rope=None) -> BlockDesc:
+    """rope: (frames, rows, columns, theta) of the image-token grid, or None."""
     d = BlockDesc()
     d.kind, d.B, d.T, d.D, d.heads, d.head_dim, d.mlp = kind, B, T, D, heads, head_dim, mlp
     d.T_txt, d.T_ctx, d.dtype = T_txt, T_ctx, dtype
+    if rope is not None:
+        d.rope_f, d.rope_h, d.rope_w, d.rope_theta = rope
     return d
 
 

@@ -143,8 +143,12 @@ static int dual_block(const bc_block_desc& d, const bc_block_weights& w, float* 
     char* at_t = at_i + (int64_t)Mi * D * esz;
     BC_TRY(launch_ln_mod(BC_F32, x, Mi, D, mi, mi + D, ld_mod, T, dt, bb.h, s));
     BC_TRY(plain(dt, bb.h, D, w.img.w_qkv, w.img.b_qkv, Mi, 3 * D, D, qkv_i, false, s));
+    BC_TRY(launch_qk_norm_rope(dt, qkv_i, Mi, 3 * D, D, d.heads, d.head_dim, w.img.q_norm, w.img.k_norm, T, T,
+                               d.rope_f, d.rope_h, d.rope_w, d.rope_theta, s));
     BC_TRY(launch_ln_mod(BC_F32, xt, Mt, D, mt, mt + D, ld_mod, Tt, dt, bb.h, s));
     BC_TRY(plain(dt, bb.h, D, w.txt.w_qkv, w.txt.b_qkv, Mt, 3 * D, D, qkv_t, false, s));
+    BC_TRY(launch_qk_norm_rope(dt, qkv_t, Mt, 3 * D, D, d.heads, d.head_dim, w.txt.q_norm, w.txt.k_norm, Tt, 0, 0, 0,
+                               0, 0.0, s));
     AttnArgs a = {};
     a.q0 = qkv_i; a.q1 = qkv_t; a.Tq0 = T; a.Tq1 = Tt; a.ldq = 3 * D;
     a.k0 = qkv_i + D * esz; a.k1 = qkv_t + D * esz; a.Tk0 = T; a.Tk1 = Tt; a.ldk = 3 * D;
@@ -181,6 +185,8 @@ static int single_block(const bc_block_desc& d, const bc_block_weights& w, float
     g.e.off2 = D;
     g.e.gelu_from = 3 * D;
     BC_TRY(launch_gemm(dt, BC_EPI_BIAS, g, s));
+    BC_TRY(launch_qk_norm_rope(dt, bb.qkv, M, 3 * D, D, d.heads, d.head_dim, w.img.q_norm, w.img.k_norm, L, d.T,
+                               d.rope_f, d.rope_h, d.rope_w, d.rope_theta, s));
     AttnArgs a = {};
     a.q0 = a.q1 = bb.qkv; a.Tq0 = L; a.ldq = 3 * D;
     a.k0 = a.k1 = static_cast<char*>(bb.qkv) + D * esz; a.Tk0 = L; a.ldk = 3 * D;
@@ -202,6 +208,14 @@ static int check_block_desc(const bc_block_desc& d) {
     if ((d.kind == BC_BLOCK_PIXART) != (d.T_ctx > 0)) return fail(BC_ERR_INVALID_ARG, "T_ctx only for PIXART");
     if (!attention_supported(d.head_dim)) return fail(BC_ERR_UNSUPPORTED, "head_dim %d", d.head_dim);
     if (d.dtype == BC_F32 && d.head_dim > 64) return fail(BC_ERR_UNSUPPORTED, "fp32 blocks need head_dim <= 64");
+    if (d.rope_theta > 0.0) {
+        if (d.kind != BC_BLOCK_DUAL && d.kind != BC_BLOCK_SINGLE)
+            return fail(BC_ERR_INVALID_ARG, "rotary embedding only for DUAL / SINGLE blocks");
+        if (d.rope_f < 1 || d.rope_h < 1 || d.rope_w < 1 || (int64_t)d.rope_f * d.rope_h * d.rope_w != d.T ||
+            d.head_dim % 32 || !std::isfinite(d.rope_theta))
+            return fail(BC_ERR_INVALID_ARG, "rotary grid %d x %d x %d for T=%d, head_dim %d", d.rope_f, d.rope_h,
+                        d.rope_w, d.T, d.head_dim);
+    }
     const int epc = d.dtype == BC_BF16 ? 8 : 4;
     if (d.D % 16 || d.mlp % epc || d.D > 4096) return fail(BC_ERR_UNSUPPORTED, "D=%d mlp=%d", d.D, d.mlp);
     return BC_OK;
@@ -210,6 +224,9 @@ static int check_block_desc(const bc_block_desc& d) {
 static bool have(const void* p) { return p != nullptr; }
 
 static int check_stream_weights(const bc_stream_weights& w, int kind) {
+    if (have(w.q_norm) != have(w.k_norm)) return fail(BC_ERR_INVALID_ARG, "q_norm and k_norm go together");
+    if (have(w.q_norm) && kind != BC_BLOCK_DUAL && kind != BC_BLOCK_SINGLE)
+        return fail(BC_ERR_INVALID_ARG, "QK norm only for DUAL / SINGLE blocks");
     bool ok = have(w.w_mod) && have(w.w_qkv) && have(w.b_qkv) && have(w.w_o) && have(w.b_o);
     if (kind != BC_BLOCK_PIXART) ok = ok && have(w.b_mod);
     if (kind != BC_BLOCK_SINGLE) ok = ok && have(w.w_fc1) && have(w.b_fc1) && have(w.w_fc2) && have(w.b_fc2);
@@ -362,6 +379,11 @@ static bc_block_desc block_desc_of(const bc_model_desc& d, int B, int kind) {
     b.T_txt = (kind == BC_BLOCK_DUAL || kind == BC_BLOCK_SINGLE) ? d.txt_tokens : 0;
     b.T_ctx = kind == BC_BLOCK_PIXART ? d.ctx_tokens : 0;
     b.dtype = d.dtype;
+    const bool rope = d.kind == BC_MODEL_MMDIT && d.rope_theta > 0.0;
+    b.rope_f = rope ? d.frames : 0;
+    b.rope_h = rope ? d.height / d.patch : 0;
+    b.rope_w = rope ? d.width / d.patch : 0;
+    b.rope_theta = rope ? d.rope_theta : 0.0;
     return b;
 }
 
@@ -487,6 +509,8 @@ int bc_model_create(const bc_model_desc* dp, const bc_model_weights* wp, bc_mode
     if (d.kind == BC_MODEL_PIXART && (d.ctx_tokens < 1 || d.ctx_dim < 1 || d.ctx_dim % 8))
         return fail(BC_ERR_INVALID_ARG, "PixArt context %d x %d", d.ctx_tokens, d.ctx_dim);
     if (d.kind == BC_MODEL_MMDIT && d.txt_tokens < 1) return fail(BC_ERR_INVALID_ARG, "MMDiT needs txt_tokens");
+    if (d.rope_theta != 0.0 && (d.kind != BC_MODEL_MMDIT || !(d.rope_theta > 0.0) || !std::isfinite(d.rope_theta)))
+        return fail(BC_ERR_INVALID_ARG, "rope_theta only for MMDIT, > 0 and finite");
     const int kinds[2] = {d.kind == BC_MODEL_DIT ? BC_BLOCK_DIT : d.kind == BC_MODEL_PIXART ? BC_BLOCK_PIXART : BC_BLOCK_DUAL,
                           BC_BLOCK_SINGLE};
     for (int k = 0; k < (d.kind == BC_MODEL_MMDIT ? 2 : 1); ++k) {

@@ -103,6 +103,16 @@ __device__ __forceinline__ void sampler_update(const SamplerCoef& k, float* x, f
     if (prev) *prev = x0;
 }
 
+// Queries and keys of the video model's attention, in place on the QKV
+// buffer (rows of ld elements: q at columns [0, D), k at [D, 2D)): per head,
+// RMSNorm with the scales wq / wk ([head_dim], or NULL for none; eps 1e-6,
+// fp32), then for the first n_img rows of every rows_per_sample the 3D rotary
+// embedding over a gf x gh x gw token grid (theta <= 0: none).  head_dim
+// <= 128, even; with the rotation a multiple of 32.
+int launch_qk_norm_rope(int dt, void* qkv, int64_t rows, int64_t ld, int D, int heads, int head_dim, const void* wq,
+                        const void* wk, int rows_per_sample, int n_img, int gf, int gh, int gw, double theta,
+                        hipStream_t s);
+
 // Change measure of the adaptive schedule: over n elements of `dt`,
 // sums[0] = sum |cur - prev| and sums[1] = sum |prev| (fp32 per thread and
 // workgroup, the kRelL1Blocks partials `part` [2 * kRelL1Blocks] then added in

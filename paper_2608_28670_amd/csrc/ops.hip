@@ -524,6 +524,182 @@ int launch_sampler(const SamplerCoef& k, float* x, const float* out_tok, float* 
 }
 
 // ---------------------------------------------------------------------------
+// QK RMSNorm + 3D rotary embedding: one wave per (row, head, q|k); lane i
+// holds the pair (2i, 2i + 1) of the head, so the rotation is lane-local and
+// the RMS is one wave reduction.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void qk_norm_rope_kernel(T* __restrict__ qkv, int64_t rows, int64_t ldr, int D,
+                                                           int heads, int hd, const T* __restrict__ wq,
+                                                           const T* __restrict__ wk, int L, int n_img, int gf,
+                                                           int gh, int gw, float log2_theta) {
+    const int64_t wid = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 6;
+    const int lane = threadIdx.x & 63;
+    if (wid >= rows * heads * 2) return;   // whole waves
+    const int qk = (int)(wid & 1);
+    const int64_t rh = wid >> 1;
+    const int h = (int)(rh % heads);
+    const int64_t r = rh / heads;
+    T* p = qkv + r * ldr + (int64_t)qk * D + (int64_t)h * hd;
+    const bool act = 2 * lane < hd;
+    float x0 = 0.f, x1 = 0.f;
+    if (act) {
+        x0 = ld(p + 2 * lane);
+        x1 = ld(p + 2 * lane + 1);
+    }
+    const T* w = qk ? wk : wq;
+    if (w) {
+        float ss = x0 * x0 + x1 * x1;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+        const float inv = 1.0f / sqrtf(ss / (float)hd + 1e-6f);
+        if (act) {
+            x0 = x0 * inv * ld(w + 2 * lane);
+            x1 = x1 * inv * ld(w + 2 * lane + 1);
+        }
+    }
+    const int t = (int)(r % L);
+    if (log2_theta > 0.f && t < n_img && act) {
+        const int d_f = hd / 8, d_h = (hd - d_f) / 2, d_w = hd - d_f - d_h;
+        const int e = 2 * lane;
+        const int col = t % gw, row = (t / gw) % gh, fr = t / (gw * gh);
+        int pos, j, da;
+        if (e < d_f) { pos = fr; j = e / 2; da = d_f; }
+        else if (e < d_f + d_h) { pos = row; j = (e - d_f) / 2; da = d_h; }
+        else { pos = col; j = (e - d_f - d_h) / 2; da = d_w; }
+        const float freq = exp2f(-(float)(2 * j) / (float)da * log2_theta);
+        float sn, cs;
+        sincosf((float)pos * freq, &sn, &cs);
+        const float y0 = x0 * cs - x1 * sn, y1 = x0 * sn + x1 * cs;
+        x0 = y0;
+        x1 = y1;
+    }
+    if (act) {
+        p[2 * lane] = (T)x0;
+        p[2 * lane + 1] = (T)x1;
+    }
+}
+
+// bf16 variant for head_dim = 8 * CPH with CPH a power of two (64, 128): one
+// wave per (row, q|k) walks the row in 16-byte chunks, lane l taking chunks
+// l, l + 64, ...  Since 64 is a multiple of CPH, lane l always holds the same
+// four pairs (chunk l % CPH) of whichever head a chunk belongs to: it loads its
+// eight norm scales and works out its four rotations once per row.  A head's
+// RMS is a reduction over the CPH lanes that hold it.
+template <int CPH>
+__global__ __launch_bounds__(256) void qk_norm_rope_row_kernel(bf16* __restrict__ qkv, int64_t rows, int64_t ldr,
+                                                               int D, const bf16* __restrict__ wq,
+                                                               const bf16* __restrict__ wk, int L, int n_img, int gf,
+                                                               int gh, int gw, float log2_theta) {
+    constexpr int HD = 8 * CPH;
+    const int64_t wid = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 6;
+    const int lane = threadIdx.x & 63;
+    if (wid >= rows * 2) return;   // whole waves
+    const int qk = (int)(wid & 1);
+    const int64_t r = wid >> 1;
+    bf16* p = qkv + r * ldr + (int64_t)qk * D;
+    const int nch = D / 8;
+    const int e0 = (lane % CPH) * 8;   // first element of this lane's chunk within its head
+    const bf16* w = qk ? wk : wq;
+    float wv[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) wv[k] = w ? ld(w + e0 + k) : 1.f;
+    const int t = (int)(r % L);
+    const bool rot = log2_theta > 0.f && t < n_img;
+    float cs[4], sn[4];
+    if (rot) {
+        constexpr int d_f = HD / 8, d_h = (HD - d_f) / 2, d_w = HD - d_f - d_h;
+        const int col = t % gw, row = (t / gw) % gh, fr = t / (gw * gh);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = e0 + 2 * q;
+            int pos, j, da;
+            if (e < d_f) { pos = fr; j = e / 2; da = d_f; }
+            else if (e < d_f + d_h) { pos = row; j = (e - d_f) / 2; da = d_h; }
+            else { pos = col; j = (e - d_f - d_h) / 2; da = d_w; }
+            const float freq = exp2f(-(float)(2 * j) / (float)da * log2_theta);
+            sincosf((float)pos * freq, &sn[q], &cs[q]);
+        }
+    }
+    for (int c0 = 0; c0 < nch; c0 += 64) {
+        const int c = c0 + lane;
+        const bool act = c < nch;
+        u32x4 u = u32x4{0u, 0u, 0u, 0u};
+        if (act) u = *reinterpret_cast<const u32x4*>(p + (int64_t)c * 8);
+        float v[8];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            v[2 * k] = __uint_as_float(u[k] << 16);
+            v[2 * k + 1] = __uint_as_float(u[k] & 0xffff0000u);
+        }
+        if (w) {
+            float ss = 0.f;
+#pragma unroll
+            for (int k = 0; k < 8; ++k) ss += v[k] * v[k];
+#pragma unroll
+            for (int o = 1; o < CPH; o <<= 1) ss += __shfl_xor(ss, o);
+            const float inv = 1.0f / sqrtf(ss / (float)HD + 1e-6f);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) v[k] = v[k] * inv * wv[k];
+        }
+        if (rot) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float y0 = v[2 * q] * cs[q] - v[2 * q + 1] * sn[q];
+                const float y1 = v[2 * q] * sn[q] + v[2 * q + 1] * cs[q];
+                v[2 * q] = y0;
+                v[2 * q + 1] = y1;
+            }
+        }
+        if (act) {
+            u32x4 o;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const bf16 lo = (bf16)v[2 * k], hi = (bf16)v[2 * k + 1];
+                o[k] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+            }
+            *reinterpret_cast<u32x4*>(p + (int64_t)c * 8) = o;
+        }
+    }
+}
+
+int launch_qk_norm_rope(int dt, void* qkv, int64_t rows, int64_t ld, int D, int heads, int head_dim, const void* wq,
+                        const void* wk, int rows_per_sample, int n_img, int gf, int gh, int gw, double theta,
+                        hipStream_t s) {
+    const bool rope = theta > 0.0 && n_img > 0;
+    if (!wq && !wk && !rope) return BC_OK;
+    if (head_dim < 2 || head_dim > 128 || head_dim % 2 || heads * head_dim != D || rows_per_sample < 1 ||
+        (rope && (head_dim % 32 || (int64_t)gf * gh * gw != n_img)))
+        return fail(BC_ERR_INVALID_ARG, "qk_norm_rope: head_dim %d, grid %d x %d x %d for %d tokens", head_dim, gf, gh,
+                    gw, n_img);
+    const int64_t waves = rows * heads * 2;
+    if (waves < 1) return BC_OK;
+    const float l2t = rope ? (float)std::log2(theta) : 0.f;
+    const bool aligned = reinterpret_cast<uintptr_t>(qkv) % 16 == 0 && ld % 8 == 0 && D % 8 == 0;
+    if (dt == BC_BF16 && aligned && (head_dim == 128 || head_dim == 64)) {
+        const unsigned gr = (unsigned)((rows * 2 + 3) / 4);
+        bf16* q = static_cast<bf16*>(qkv);
+        const bf16 *a = static_cast<const bf16*>(wq), *b = static_cast<const bf16*>(wk);
+        const int ni = rope ? n_img : 0;
+        if (head_dim == 128)
+            qk_norm_rope_row_kernel<16><<<gr, 256, 0, s>>>(q, rows, ld, D, a, b, rows_per_sample, ni, gf, gh, gw, l2t);
+        else
+            qk_norm_rope_row_kernel<8><<<gr, 256, 0, s>>>(q, rows, ld, D, a, b, rows_per_sample, ni, gf, gh, gw, l2t);
+        return check_launch("qk_norm_rope_row");
+    }
+    const unsigned g = (unsigned)((waves + 3) / 4);
+    if (dt == BC_BF16)
+        qk_norm_rope_kernel<bf16><<<g, 256, 0, s>>>(static_cast<bf16*>(qkv), rows, ld, D, heads, head_dim,
+                                                    static_cast<const bf16*>(wq), static_cast<const bf16*>(wk),
+                                                    rows_per_sample, rope ? n_img : 0, gf, gh, gw, l2t);
+    else
+        qk_norm_rope_kernel<float><<<g, 256, 0, s>>>(static_cast<float*>(qkv), rows, ld, D, heads, head_dim,
+                                                     static_cast<const float*>(wq), static_cast<const float*>(wk),
+                                                     rows_per_sample, rope ? n_img : 0, gf, gh, gw, l2t);
+    return check_launch("qk_norm_rope");
+}
+
+// ---------------------------------------------------------------------------
 // Relative L1 change of the adaptive schedule's probe: 16-byte chunks of cur
 // and prev, |cur - prev| and |prev| summed per thread, per wave (butterfly)
 // and per workgroup in a fixed order; prev takes cur's bytes in the same pass.

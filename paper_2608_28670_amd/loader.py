@@ -44,7 +44,17 @@ def model_desc(cfg) -> ModelDesc:
     d.ctx_tokens, d.ctx_dim, d.txt_tokens = cfg.ctx_tokens, cfg.ctx_dim, cfg.txt_tokens
     d.freq_dim = cfg.freq_dim
     d.dtype = BF16 if cfg.dtype == "bf16" else F32
+    d.rope_theta = getattr(cfg, "rope_theta", 0.0) if cfg.kind == "mmdit" else 0.0
     return d
+
+
+def rope_grid(cfg):
+    """(frames, rows, columns, theta) of the image-token grid for block
+    descriptors, or None when the model has no rotary embedding."""
+    if cfg.kind != "mmdit" or not getattr(cfg, "rope_theta", 0.0):
+        return None
+    f = 1 if len(cfg.latent) == 3 else cfg.latent[1]
+    return f, cfg.latent[-2] // cfg.p, cfg.latent[-1] // cfg.p, cfg.rope_theta
 
 
 def _stream(P, pre):
@@ -52,7 +62,8 @@ def _stream(P, pre):
             "w_qkv": P.get(pre + "w_qkv"), "b_qkv": P.get(pre + "b_qkv"),
             "w_o": P.get(pre + "w_o"), "b_o": P.get(pre + "b_o"),
             "w_fc1": P.get(pre + "w_fc1"), "b_fc1": P.get(pre + "b_fc1"),
-            "w_fc2": P.get(pre + "w_fc2"), "b_fc2": P.get(pre + "b_fc2")}
+            "w_fc2": P.get(pre + "w_fc2"), "b_fc2": P.get(pre + "b_fc2"),
+            "q_norm": P.get(pre + "q_norm"), "k_norm": P.get(pre + "k_norm")}
 
 
 def block_list(cfg, P) -> List[BlockWeights]:
@@ -71,7 +82,8 @@ def block_list(cfg, P) -> List[BlockWeights]:
             pre = f"single.{l}."
             out.append(block_weights({"w_mod": P[pre + "w_mod"], "b_mod": P[pre + "b_mod"],
                                       "w_qkv": P[pre + "w_1"], "b_qkv": P[pre + "b_1"],
-                                      "w_o": P[pre + "w_2"], "b_o": P[pre + "b_2"]}))
+                                      "w_o": P[pre + "w_2"], "b_o": P[pre + "b_2"],
+                                      "q_norm": P.get(pre + "q_norm"), "k_norm": P.get(pre + "k_norm")}))
     return out
 
 

@@ -31,9 +31,11 @@ def _block_call(bc, cfg, P, kind, x, c, x_txt=None, ctx=None, l=0):
     blocks = loader.block_list(cfg, dP)
     dtc = bc.BF16 if cfg.dtype == "bf16" else bc.F32
     B = x.shape[0]
+    mm = kind in (bc.BLOCK_DUAL, bc.BLOCK_SINGLE)
     desc = bc.block_desc(kind, B, cfg.tokens, cfg.hidden, cfg.heads, cfg.head_dim, cfg.mlp, dtc,
-                         T_txt=cfg.txt_tokens if kind in (bc.BLOCK_DUAL, bc.BLOCK_SINGLE) else 0,
-                         T_ctx=cfg.ctx_tokens if kind == bc.BLOCK_PIXART else 0)
+                         T_txt=cfg.txt_tokens if mm else 0,
+                         T_ctx=cfg.ctx_tokens if kind == bc.BLOCK_PIXART else 0,
+                         rope=loader.rope_grid(cfg) if mm else None)
     ws = torch.empty(bc.block_workspace_size(desc), dtype=torch.uint8, device=DEV)
     tx = _f32(x)
     tt = _f32(x_txt) if x_txt is not None else None
@@ -90,8 +92,12 @@ def _mm_cfg(**kw):
     return synth.scaled(synth.CONFIGS["hunyuan"], **base)
 
 
-def test_dual_block(bclib):
-    cfg = _mm_cfg()
+# qk: QK RMSNorm and rotary embedding (head_dim 128: the row-wise kernel;
+# head_dim 32: the per-head kernel), or neither.
+@pytest.mark.parametrize("qk,hd", [(True, 128), (True, 32), (False, 128)], ids=["qknorm_rope", "qknorm_rope_hd32", "plain"])
+def test_dual_block(bclib, qk, hd):
+    geo = dict(hidden=4 * hd, heads=4, head_dim=hd, mlp=16 * hd) if hd != 128 else {}
+    cfg = _mm_cfg(**geo) if qk else _mm_cfg(qk_norm=False, rope_theta=0.0)
     P = synth.params(cfg)
     M = om.Model(cfg, P)
     B = 2
@@ -100,20 +106,36 @@ def test_dual_block(bclib):
     c = synth.normal("dblk/c", (B, cfg.hidden), 0.5)
     ei, et = M.dual_block(0, x.astype(np.float64), xt.astype(np.float64), {"c": c.astype(np.float64)})
     gi, gt = _block_call(bclib, cfg, P, bclib.BLOCK_DUAL, x, c, x_txt=xt)
-    _check_block(gi, x, ei, 2e-2)
+    ui = _check_block(gi, x, ei, 2e-2)
     _check_block(gt, xt, et, 2e-2)
+    if qk:
+        # The rotation moves this block's update by 5e-2 (theta 1e4 instead of
+        # 256: 3e-2) while bf16 rounding leaves about 3e-3: gate the update at
+        # 1e-2 and check that the result is far from the unrotated block.
+        assert ui <= 1e-2
+        ni, _ = om.Model(synth.scaled(cfg, rope_theta=0.0), P).dual_block(
+            0, x.astype(np.float64), xt.astype(np.float64), {"c": c.astype(np.float64)})
+        assert rel_l2(gi - x, ni - x) > 3e-2
 
 
-def test_single_block(bclib):
-    cfg = _mm_cfg()
+# qk: QK RMSNorm and rotary embedding (head_dim 128: the row-wise kernel;
+# head_dim 32: the per-head kernel), or neither.
+@pytest.mark.parametrize("qk,hd", [(True, 128), (True, 32), (False, 128)], ids=["qknorm_rope", "qknorm_rope_hd32", "plain"])
+def test_single_block(bclib, qk, hd):
+    geo = dict(hidden=4 * hd, heads=4, head_dim=hd, mlp=16 * hd) if hd != 128 else {}
+    cfg = _mm_cfg(**geo) if qk else _mm_cfg(qk_norm=False, rope_theta=0.0)
     P = synth.params(cfg)
     M = om.Model(cfg, P)
     B = 2
     x = synth.normal("sblk/x", (B, cfg.tokens + cfg.txt_tokens, cfg.hidden))
     c = synth.normal("sblk/c", (B, cfg.hidden), 0.5)
-    exp = M.single_block(0, x.astype(np.float64), {"c": c.astype(np.float64)})
+    exp = M.single_block(0, x.astype(np.float64), {"c": c.astype(np.float64)}, cfg.tokens)
     got, _ = _block_call(bclib, cfg, P, bclib.BLOCK_SINGLE, x, c, l=1)
-    _check_block(got, x, exp, 2e-2)
+    upd = _check_block(got, x, exp, 2e-2)
+    if qk:   # as for the dual-stream block
+        assert upd <= 1e-2
+        none = M.single_block(0, x.astype(np.float64), {"c": c.astype(np.float64)}, 0)
+        assert rel_l2(got - x, none - x) > 3e-2
 
 
 # Full token shapes of the PixArt (4096 tokens) and HunyuanVideo (14 310 + 256
@@ -162,7 +184,7 @@ def test_single_block_full_tokens(bclib):
     M = om.Model(cfg, P, dtype=np.float32)
     x = synth.normal("sfull/x", (1, cfg.tokens + cfg.txt_tokens, cfg.hidden))
     c = synth.normal("sfull/c", (1, cfg.hidden), 0.5)
-    exp = M.single_block(0, x.astype(np.float32), {"c": c.astype(np.float32)}).astype(np.float64)
+    exp = M.single_block(0, x.astype(np.float32), {"c": c.astype(np.float32)}, cfg.tokens).astype(np.float64)
     got, _ = _block_call(bclib, cfg, P, bclib.BLOCK_SINGLE, x, c, l=1)
     _check_block(got, x, exp, 2e-2)
 
@@ -176,6 +198,17 @@ def test_block_rejects_bad_shapes(bclib):
     with pytest.raises(bclib.BCError) as e:
         bclib.block_workspace_size(desc)
     assert e.value.code == bclib.ERR_INVALID_ARG
+    # rotary grid: its product must be T; head_dim a multiple of 32 (72 is a
+    # head dim the attention kernel takes); DUAL / SINGLE blocks only
+    for kind, heads, hd, grid in [(bclib.BLOCK_DUAL, 2, 128, (2, 4, 3)), (bclib.BLOCK_DUAL, 2, 72, (2, 4, 4)),
+                                  (bclib.BLOCK_DIT, 2, 128, (2, 4, 4))]:
+        desc = bclib.block_desc(kind, 1, 32, heads * hd, heads, hd, 512, bclib.BF16,
+                                T_txt=8 if kind == bclib.BLOCK_DUAL else 0, rope=grid + (256.0,))
+        with pytest.raises(bclib.BCError) as e:
+            bclib.block_workspace_size(desc)
+        assert e.value.code == bclib.ERR_INVALID_ARG
+    ok = bclib.block_desc(bclib.BLOCK_DUAL, 1, 32, 256, 2, 128, 512, bclib.BF16, T_txt=8, rope=(2, 4, 4, 256.0))
+    assert bclib.block_workspace_size(ok) > 0
 
 
 # ---------------------------------------------------------------------------
