@@ -133,8 +133,8 @@ def cpu_baseline(cfg, params, labels, xT, mask, nsteps):
     x = xT[:1].astype(np.float64)
     lab = labels[:1]
     steps = bary.plan(mask, cfg.K)
-    tin = osm.model_time(cfg.sampler, cfg.steps)
-    smp = osm.Sampler(cfg.sampler, cfg.steps, cfg.in_ch)
+    tin = osm.model_time(cfg.sampler, cfg.steps, cfg.flow_shift)
+    smp = osm.Sampler(cfg.sampler, cfg.steps, cfg.in_ch, cfg.flow_shift)
     ring = bary.Ring(cfg.K)
     t_full, t_fc = [], []
     for k in range(min(nsteps, cfg.steps)):

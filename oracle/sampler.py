@@ -11,7 +11,9 @@ text-to-video, 50 steps (Sec. 4.1).  The precise samplers below are readings:
   * "trailing" integer timesteps tau_k = 999 - floor(1000 k / S);
   * DDIM with eta = 0 (deterministic); the last step maps to alpha_bar = 1;
   * DPM-Solver++(2M) in the data-prediction form with the same timesteps;
-  * Euler on the flow-matching ODE with sigma_k = 1 - k/S, model time 1000 sigma.
+  * Euler on the flow-matching ODE with sigma_k = 1 - k/S, model time 1000 sigma;
+    optionally time-shifted, sigma -> s sigma / (1 + (s - 1) sigma), the
+    schedule the published video model samples with (shift 7).
 The loop itself is Sec. 3.3: on a full step run the stack and store its output
 in the cache; otherwise forecast it from the cache with Eq. 13; then the final
 layer and the sampler update.
@@ -48,18 +50,29 @@ def timesteps(S: int) -> np.ndarray:
     return np.array([T_TRAIN - 1 - (T_TRAIN * k) // S for k in range(S)], dtype=np.int32)
 
 
-def model_time(sampler: str, S: int) -> np.ndarray:
+def shifted_sigma(sigma, shift: float = 1.0):
+    """The time shift of a flow-matching schedule: s sigma / (1 + (s - 1) sigma)
+    (s = 1: unchanged).  It keeps 0 and 1 fixed and, for s > 1, spends more of
+    the steps at high noise."""
+    return shift * sigma / (1.0 + (shift - 1.0) * sigma)
+
+
+def flow_sigma(k: int, S: int, shift: float = 1.0) -> float:
+    return shifted_sigma(1.0 - k / S, shift)
+
+
+def model_time(sampler: str, S: int, shift: float = 1.0) -> np.ndarray:
     """The time value fed to the timestep embedding at each step."""
     if sampler == "euler":
-        return np.array([T_TRAIN * (1.0 - k / S) for k in range(S)], dtype=np.float64)
+        return np.array([T_TRAIN * flow_sigma(k, S, shift) for k in range(S)], dtype=np.float64)
     return timesteps(S).astype(np.float64)
 
 
 class Sampler:
     """One update rule; `step(k, x, out)` returns the next latent."""
 
-    def __init__(self, kind: str, S: int, C: int):
-        self.kind, self.S, self.C = kind, S, C
+    def __init__(self, kind: str, S: int, C: int, shift: float = 1.0):
+        self.kind, self.S, self.C, self.shift = kind, S, C, shift
         self.ab = alpha_bar_table()
         self.tau = timesteps(S)
         self.prev_x0 = None
@@ -94,7 +107,7 @@ class Sampler:
             return (sg2 / sg) * x - al2 * (math.exp(-h) - 1.0) * d
         if self.kind == "euler":
             v = out[:, :self.C]
-            s, s2 = 1.0 - k / self.S, 1.0 - (k + 1) / self.S
+            s, s2 = flow_sigma(k, self.S, self.shift), flow_sigma(k + 1, self.S, self.shift)
             return x + (s2 - s) * v
         raise ValueError(self.kind)
 
@@ -117,8 +130,9 @@ def sample(model: Model, x_T: np.ndarray, mask: Sequence[int], K: int,
     B = x_T.shape[0]
     steps = bary.plan(mask, K, None, p)
     ring = bary.Ring(K)
-    tin = model_time(cfg.sampler, S)
-    smp = Sampler(cfg.sampler, S, cfg.in_ch)
+    shift = getattr(cfg, "flow_shift", 1.0)
+    tin = model_time(cfg.sampler, S, shift)
+    smp = Sampler(cfg.sampler, S, cfg.in_ch, shift)
     ctx = model.context(text) if cfg.kind != "dit" else None
     guided = cfg_scale is not None
     if guided:
@@ -197,8 +211,9 @@ def sample_adaptive(model: Model, x_T: np.ndarray, S: int, ell: float, K: int, l
     cfg = model.cfg
     B = x_T.shape[0]
     ring = bary.Ring(K)
-    tin = model_time(cfg.sampler, S)
-    smp = Sampler(cfg.sampler, S, cfg.in_ch)
+    shift = getattr(cfg, "flow_shift", 1.0)
+    tin = model_time(cfg.sampler, S, shift)
+    smp = Sampler(cfg.sampler, S, cfg.in_ch, shift)
     ctx = model.context(text) if cfg.kind != "dit" else None
     rule = AdaptiveRule(ell, S)
     x = np.asarray(x_T, dtype=np.float64)

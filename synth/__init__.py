@@ -96,6 +96,7 @@ class ModelConfig:
     txt_tokens: int = 0    # mmdit text stream tokens
     qk_norm: bool = False  # mmdit: RMSNorm (learned scale) on each head's queries and keys
     rope_theta: float = 0.0  # mmdit: 3D rotary embedding of the image tokens' queries and keys (0: none)
+    flow_shift: float = 1.0  # euler: time shift of the flow-matching schedule (1: none)
     param_scale: float = 0.02
     latent_scale: float = 1.0
     freq_dim: int = 256
@@ -142,7 +143,8 @@ CONFIGS: Dict[str, ModelConfig] = {
     "hunyuan": ModelConfig(
         name="hunyuan", kind="mmdit", depth=20, depth_single=40, hidden=3072, heads=24, head_dim=128,
         mlp=12288, in_ch=16, out_ch=16, patch=(2,), latent=(16, 9, 60, 106), batch=1, steps=50,
-        sampler="euler", K=3, interval=5, dtype="bf16", txt_tokens=256, qk_norm=True, rope_theta=256.0),
+        sampler="euler", K=3, interval=5, dtype="bf16", txt_tokens=256, qk_norm=True, rope_theta=256.0,
+        flow_shift=7.0),
 }
 
 

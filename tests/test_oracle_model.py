@@ -187,14 +187,32 @@ def test_dpmpp_first_step_equals_ddim():
     np.testing.assert_allclose(a, b, rtol=1e-12, atol=1e-12)
 
 
-def test_euler_constant_velocity():
-    smp = osm.Sampler("euler", 50, 4)
+@pytest.mark.parametrize("shift", [1.0, 7.0])
+def test_euler_constant_velocity(shift):
+    # The steps telescope: sum_k (sigma_{k+1} - sigma_k) = sigma_S - sigma_0 = -1
+    # for any shift, so a constant velocity v moves x by exactly -v.
+    smp = osm.Sampler("euler", 50, 4, shift)
     x1 = np.full((1, 4, 2, 2), 3.0)
     v = np.full_like(x1, 0.75)
     x = x1
     for k in range(50):
         x = smp.step(k, x, v)
     np.testing.assert_allclose(x, x1 - v, rtol=1e-13)
+
+
+def test_time_shift_closed_forms():
+    assert osm.shifted_sigma(0.5, 7.0) == pytest.approx(3.5 / 4.0, rel=1e-15)   # 7 (1/2) / (1 + 6 (1/2))
+    assert osm.shifted_sigma(0.0, 7.0) == 0.0 and osm.shifted_sigma(1.0, 7.0) == 1.0
+    sig = np.linspace(0, 1, 101)
+    np.testing.assert_array_equal(osm.shifted_sigma(sig, 1.0), sig)
+    sh = osm.shifted_sigma(sig, 7.0)
+    assert np.all(np.diff(sh) > 0) and np.all(sh[1:-1] > sig[1:-1])          # increasing, above the diagonal
+    # the inverse map is the shift by 1/s
+    np.testing.assert_allclose(osm.shifted_sigma(sh, 1.0 / 7.0), sig, rtol=1e-13, atol=1e-15)
+    # model times: 1000 sigma'(k) with sigma = 1 - k/S
+    tm = osm.model_time("euler", 4, 7.0)
+    np.testing.assert_allclose(tm, [1000.0, 1000.0 * 7 * 0.75 / (1 + 6 * 0.75), 1000.0 * 3.5 / 4.0,
+                                    1000.0 * 7 * 0.25 / (1 + 6 * 0.25)], rtol=1e-15)
 
 
 # ---------------------------------------------------------------------------
