@@ -270,6 +270,9 @@ typedef struct {
     double rope_theta; /* MMDIT: 3D rotary embedding of the image tokens over the
                           (frames, height/patch, width/patch) grid, as in
                           bc_block_desc; <= 0: none.  Other kinds: 0. */
+    double flow_shift; /* EULER sampler: time shift of the flow-matching schedule,
+                          sigma_k = s u / (1 + (s - 1) u) with u = 1 - k/S; model
+                          time 1000 sigma_k.  0 or 1: none; else > 0. */
 } bc_model_desc;
 
 /* Device pointers in the model dtype.  Token features are patches in
@@ -299,6 +302,10 @@ typedef enum { BC_SAMPLER_DDIM = 0, BC_SAMPLER_DPMPP2M = 1, BC_SAMPLER_EULER = 2
  * and time_out[k] the value fed to the timestep embedding (tau for the
  * noise-prediction samplers, 1000 (1 - k/S) for Euler).  Either may be NULL. */
 int bc_make_schedule(int sampler, int S, int32_t* tau_out, double* time_out);
+/* As bc_make_schedule, with the flow-matching time shift s of bc_model_desc
+ * applied to the EULER model times (1000 s u / (1 + (s - 1) u), u = 1 - k/S;
+ * s = 0 or 1: none).  Errors: INVALID_ARG for s < 0 or not finite. */
+int bc_make_schedule_shifted(int sampler, int S, double flow_shift, int32_t* tau_out, double* time_out);
 
 /* Bytes of workspace bc_sample needs for B samples and an S-step schedule
  * (the per-step conditioning of the whole schedule is held at once). */

@@ -71,7 +71,7 @@ class ModelDesc(C.Structure):
     _fields_ = [(n, C.c_int) for n in ("kind", "depth", "depth_single", "D", "heads", "head_dim", "mlp",
                                        "in_ch", "out_ch", "patch", "frames", "height", "width",
                                        "n_classes", "ctx_tokens", "ctx_dim", "txt_tokens", "freq_dim",
-                                       "dtype")] + [("rope_theta", C.c_double)]
+                                       "dtype")] + [("rope_theta", C.c_double), ("flow_shift", C.c_double)]
 
 
 _MODEL_PTRS = ("t_w1", "t_b1", "t_w2", "t_b2", "patch_w", "patch_b", "pos", "y_table", "t6_w", "t6_b",
@@ -113,6 +113,7 @@ _SIGS = {
     "bc_model_create": (C.c_int, [C.POINTER(ModelDesc), C.POINTER(ModelWeights), C.POINTER(C.c_void_p)]),
     "bc_model_destroy": (C.c_int, [C.c_void_p]),
     "bc_make_schedule": (C.c_int, [C.c_int, C.c_int, C.c_void_p, C.c_void_p]),
+    "bc_make_schedule_shifted": (C.c_int, [C.c_int, C.c_int, C.c_double, C.c_void_p, C.c_void_p]),
     "bc_sample_workspace_size": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.POINTER(C.c_size_t)]),
     "bc_sample": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int,
                             C.POINTER(BaryParams), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
@@ -245,10 +246,10 @@ def plan(mask, K: int, coords=None, p: Optional[BaryParams] = None) -> List[Plan
     return list(out)
 
 
-def make_schedule(sampler: str, S: int):
+def make_schedule(sampler: str, S: int, flow_shift: float = 1.0):
     tau = np.zeros(S, dtype=np.int32)
     tm = np.zeros(S, dtype=np.float64)
-    _check(lib().bc_make_schedule(SAMPLERS[sampler], S, _ptr(tau), _ptr(tm)))
+    _check(lib().bc_make_schedule_shifted(SAMPLERS[sampler], S, float(flow_shift), _ptr(tau), _ptr(tm)))
     return tau, tm
 
 

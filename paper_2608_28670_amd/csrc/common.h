@@ -19,6 +19,13 @@ constexpr int kMaxK = 8;
 int bary_weights(const double* s, int K, double t, const bc_bary_params& p, double* w);
 bool params_valid(const bc_bary_params& p);
 
+// sigma of step k of an S-step flow-matching (Euler) schedule with the time
+// shift s: s u / (1 + (s - 1) u), u = 1 - k / S (s = 0 or 1: u itself).
+inline double flow_sigma(int k, int S, double s) {
+    const double u = 1.0 - (double)k / S;
+    return (s == 0.0 || s == 1.0) ? u : s * u / (1.0 + (s - 1.0) * u);
+}
+
 }  // namespace bc
 
 // Cache context handle (Sec. 3.2, Eq. 6): host metadata over caller storage.

@@ -397,13 +397,14 @@ static void alpha_bar(double* ab) {
 }
 
 // Sampler coefficients of step k (see launch_sampler for their meaning).
-static SamplerCoef sampler_coef(int sampler, int k, int S, const int32_t* tau, const double* ab, double* h_prev) {
+static SamplerCoef sampler_coef(int sampler, int k, int S, const int32_t* tau, const double* ab, double* h_prev,
+                                double shift) {
     SamplerCoef c;
     std::memset(&c, 0, sizeof c);
     if (sampler == BC_SAMPLER_EULER) {
         c.mode = 0;
         c.c[0] = 1.f;
-        c.c[1] = (float)((1.0 - (double)(k + 1) / S) - (1.0 - (double)k / S));
+        c.c[1] = (float)(flow_sigma(k + 1, S, shift) - flow_sigma(k, S, shift));
         return c;
     }
     const double a = ab[tau[k]];
@@ -511,6 +512,8 @@ int bc_model_create(const bc_model_desc* dp, const bc_model_weights* wp, bc_mode
     if (d.kind == BC_MODEL_MMDIT && d.txt_tokens < 1) return fail(BC_ERR_INVALID_ARG, "MMDiT needs txt_tokens");
     if (d.rope_theta != 0.0 && (d.kind != BC_MODEL_MMDIT || !(d.rope_theta > 0.0) || !std::isfinite(d.rope_theta)))
         return fail(BC_ERR_INVALID_ARG, "rope_theta only for MMDIT, > 0 and finite");
+    if (!(d.flow_shift >= 0.0) || !std::isfinite(d.flow_shift))
+        return fail(BC_ERR_INVALID_ARG, "flow_shift %g", d.flow_shift);
     const int kinds[2] = {d.kind == BC_MODEL_DIT ? BC_BLOCK_DIT : d.kind == BC_MODEL_PIXART ? BC_BLOCK_PIXART : BC_BLOCK_DUAL,
                           BC_BLOCK_SINGLE};
     for (int k = 0; k < (d.kind == BC_MODEL_MMDIT ? 2 : 1); ++k) {
@@ -607,7 +610,7 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
     if (d.kind != BC_MODEL_DIT && !text) return fail(BC_ERR_INVALID_ARG, "text input required");
     std::vector<int32_t> tau(S > 0 ? S : 1);
     std::vector<double> tin(S > 0 ? S : 1);
-    BC_TRY(bc_make_schedule(sampler, S, tau.data(), tin.data()));
+    BC_TRY(bc_make_schedule_shifted(sampler, S, d.flow_shift, tau.data(), tin.data()));
     if (S < 1 || S > 1000) return fail(BC_ERR_INVALID_ARG, "S=%d outside [1, 1000]", S);
     std::vector<bc_plan_step> plan(S);
     std::vector<uint8_t> amask(S, 1);      // adaptive: the mask decided so far
@@ -647,7 +650,7 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
 
     // Conditioning of every step, computed before the loop: it depends only on
     // the schedule, the labels and the text, never on the latents.
-    BC_TRY(launch_step_sinusoid(sampler, S, d.freq_dim, w.e, s));
+    BC_TRY(launch_step_sinusoid(sampler, S, d.freq_dim, d.flow_shift, w.e, s));
     for (int k0 = 0; k0 < S; k0 += 64) {
         const int n = std::min(64, S - k0);
         BC_TRY(launch_skinny(dt, skinny1(mw.t_w1, mw.t_b1, D, d.freq_dim, n, w.e + (int64_t)k0 * d.freq_dim,
@@ -849,7 +852,7 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
             feat = slot;
         }
         const int NO = d.patch * d.patch * d.out_ch;
-        const SamplerCoef sc = sampler_coef(sampler, k, S, tau.data(), ab, &h_prev);
+        const SamplerCoef sc = sampler_coef(sampler, k, S, tau.data(), ab, &h_prev, d.flow_shift);
         if (fused_final && (st.is_full || st.count <= kFinalMaxK)) {
             // Stepwise feature (the new slot, or the forecast from the ring), final
             // layer and sampler update in one pass over the tokens.

@@ -32,8 +32,8 @@ int launch_skinny(int dt, const SkinnyArgs& a, hipStream_t s);
 
 // Timestep sinusoid of every step k < S: e[k, :] = [cos(t_k f_i), sin(t_k f_i)],
 // f_i = 10000^(-i/half), where t_k is the step's model time (999 - floor(1000k/S),
-// or 1000 (1 - k/S) for the flow-matching Euler sampler); fp32 out.
-int launch_step_sinusoid(int sampler, int S, int dim, float* e, hipStream_t s);
+// or 1000 flow_sigma(k, S, shift) for the flow-matching Euler sampler); fp32 out.
+int launch_step_sinusoid(int sampler, int S, int dim, double shift, float* e, hipStream_t s);
 
 // Per-(step, sample) conditioning c[k*B + b, :] = temb[k, :] + extra, where
 // extra is table[labels[b], :] (table in `dt`, if labels), or add[b, :] (fp32,

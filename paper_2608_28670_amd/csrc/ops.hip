@@ -287,20 +287,23 @@ int launch_skinny(int dt, const SkinnyArgs& a, hipStream_t s) {
 // ---------------------------------------------------------------------------
 // Conditioning helpers
 // ---------------------------------------------------------------------------
-__global__ void step_sinusoid_kernel(int sampler, int S, int half, float* e) {
+__global__ void step_sinusoid_kernel(int sampler, int S, int half, double shift, float* e) {
     const int k = blockIdx.y;
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= half || k >= S) return;
-    const double t = sampler == BC_SAMPLER_EULER ? 1000.0 * (1.0 - (double)k / S) : (double)(999 - (1000 * k) / S);
+    // Euler: 1000 sigma_k with the time shift (the device copy of flow_sigma).
+    const double u = 1.0 - (double)k / S;
+    const double sig = (shift == 0.0 || shift == 1.0) ? u : shift * u / (1.0 + (shift - 1.0) * u);
+    const double t = sampler == BC_SAMPLER_EULER ? 1000.0 * sig : (double)(999 - (1000 * k) / S);
     const double f = exp(-log(10000.0) * (double)i / (double)half);
     const double ang = t * f;
     e[(int64_t)k * 2 * half + i] = (float)cos(ang);
     e[(int64_t)k * 2 * half + half + i] = (float)sin(ang);
 }
 
-int launch_step_sinusoid(int sampler, int S, int dim, float* e, hipStream_t s) {
+int launch_step_sinusoid(int sampler, int S, int dim, double shift, float* e, hipStream_t s) {
     const int half = dim / 2;
-    step_sinusoid_kernel<<<dim3((half + 127) / 128, S), 128, 0, s>>>(sampler, S, half, e);
+    step_sinusoid_kernel<<<dim3((half + 127) / 128, S), 128, 0, s>>>(sampler, S, half, shift, e);
     return check_launch("sinusoid");
 }
 

@@ -218,18 +218,24 @@ int bc_plan(int S, const uint8_t* mask, const double* coords, int K, const bc_ba
     return BC_OK;
 }
 
-int bc_make_schedule(int sampler, int S, int32_t* tau_out, double* time_out) {
+int bc_make_schedule_shifted(int sampler, int S, double flow_shift, int32_t* tau_out, double* time_out) {
     bc::clear_error();
     if (S < 1 || S > 1000) return bc::fail(BC_ERR_INVALID_ARG, "S=%d outside [1, 1000]", S);
     if (sampler != BC_SAMPLER_DDIM && sampler != BC_SAMPLER_DPMPP2M && sampler != BC_SAMPLER_EULER)
         return bc::fail(BC_ERR_INVALID_ARG, "unknown sampler %d", sampler);
+    if (!(flow_shift >= 0.0) || !std::isfinite(flow_shift))
+        return bc::fail(BC_ERR_INVALID_ARG, "flow shift %g", flow_shift);
     for (int k = 0; k < S; ++k) {
         const int tau = 999 - (1000 * k) / S;
         if (tau_out) tau_out[k] = tau;
         if (time_out)
-            time_out[k] = sampler == BC_SAMPLER_EULER ? 1000.0 * (1.0 - (double)k / S) : (double)tau;
+            time_out[k] = sampler == BC_SAMPLER_EULER ? 1000.0 * bc::flow_sigma(k, S, flow_shift) : (double)tau;
     }
     return BC_OK;
+}
+
+int bc_make_schedule(int sampler, int S, int32_t* tau_out, double* time_out) {
+    return bc_make_schedule_shifted(sampler, S, 1.0, tau_out, time_out);
 }
 
 }  // extern "C"

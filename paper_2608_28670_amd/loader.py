@@ -45,6 +45,7 @@ def model_desc(cfg) -> ModelDesc:
     d.freq_dim = cfg.freq_dim
     d.dtype = BF16 if cfg.dtype == "bf16" else F32
     d.rope_theta = getattr(cfg, "rope_theta", 0.0) if cfg.kind == "mmdit" else 0.0
+    d.flow_shift = getattr(cfg, "flow_shift", 1.0)
     return d
 
 

@@ -55,7 +55,7 @@ CASES = {
     "dit_xl2_depth2": (lambda: synth.scaled(synth.CONFIGS["dit_xl2"], depth=2, batch=2), 0.12, 2e-2, 2e-2),
     "pixart_reduced": (lambda: synth.scaled(synth.CONFIGS["pixart"], depth=2, latent=(4, 32, 32), batch=1), 0.09,
                        2e-2, 2e-2),
-    "mmdit_reduced": (_mm_cfg, 0.1, 2e-2, 2e-2),
+    "mmdit_reduced": (_mm_cfg, 0.05, 2e-2, 2e-2),
 }
 
 

@@ -114,8 +114,16 @@ def test_plan_rejects_bad_masks(bclib):
             bclib.plan(np.array(m, np.uint8), 2)
 
 
-@pytest.mark.parametrize("sampler,S", [("ddim", 10), ("ddim", 50), ("dpmpp2m", 20), ("euler", 50)])
-def test_schedule_bit_exact(bclib, sampler, S):
-    tau, tm = bclib.make_schedule(sampler, S)
+@pytest.mark.parametrize("sampler,S,shift", [("ddim", 10, 1.0), ("ddim", 50, 1.0), ("dpmpp2m", 20, 1.0),
+                                             ("euler", 50, 1.0), ("euler", 50, 7.0), ("euler", 12, 3.0)])
+def test_schedule_bit_exact(bclib, sampler, S, shift):
+    tau, tm = bclib.make_schedule(sampler, S, shift)
     assert np.array_equal(tau, osm.timesteps(S))
-    assert np.array_equal(tm, osm.model_time(sampler, S))
+    assert np.array_equal(tm, osm.model_time(sampler, S, shift))
+
+
+def test_schedule_rejects_bad_shift(bclib):
+    for shift in (-1.0, float("nan"), float("inf")):
+        with pytest.raises(bclib.BCError) as e:
+            bclib.make_schedule("euler", 10, shift)
+        assert e.value.code == bclib.ERR_INVALID_ARG
