@@ -267,8 +267,11 @@ class Model:
             m = linear(silu(cond["c"]), P[f"blocks.{l}.w_mod"], P[f"blocks.{l}.b_mod"])
         return [m[:, i * D:(i + 1) * D] for i in range(6)]
 
-    def dit_block(self, l, x, mod, ctx=None):
-        """One DiT (or PixArt) block on the residual stream x [B, T, D]."""
+    def dit_block(self, l, x, mod, ctx=None, modules=None):
+        """One DiT (or PixArt) block on the residual stream x [B, T, D].
+        `modules`, if a list, receives the block's module outputs before their
+        gates (attention, PixArt's cross-attention, MLP): the sites that
+        blockwise caching keeps (Sec. 3.1, Eq. 4: the increments M_q)."""
         cfg, P = self.cfg, self.P
         pre = f"blocks.{l}."
         s1, sc1, g1, s2, sc2, g2 = mod
@@ -277,14 +280,30 @@ class Model:
         qkv = linear(h, P[pre + "w_qkv"], P[pre + "b_qkv"])
         q, k, v = (split_heads(qkv[..., i * D:(i + 1) * D], H) for i in range(3))
         a = merge_heads(attention(q, k, v))
-        x = x + g1[:, None, :] * linear(a, P[pre + "w_o"], P[pre + "b_o"])
+        o = linear(a, P[pre + "w_o"], P[pre + "b_o"])
+        x = x + g1[:, None, :] * o
+        outs = [o]
         if cfg.kind == "pixart":
             kx, vx = ctx["kv"][l]
             qx = split_heads(linear(x, P[pre + "wx_q"], P[pre + "bx_q"]), H)
-            x = x + linear(merge_heads(attention(qx, kx, vx)), P[pre + "wx_o"], P[pre + "bx_o"])
+            o = linear(merge_heads(attention(qx, kx, vx)), P[pre + "wx_o"], P[pre + "bx_o"])
+            x = x + o
+            outs.append(o)
         h = modulate(layer_norm(x), s2, sc2)
         m = gelu_tanh(linear(h, P[pre + "w_fc1"], P[pre + "b_fc1"]))
-        return x + g2[:, None, :] * linear(m, P[pre + "w_fc2"], P[pre + "b_fc2"])
+        o = linear(m, P[pre + "w_fc2"], P[pre + "b_fc2"])
+        outs.append(o)
+        if modules is not None:
+            modules.extend(outs)
+        return x + g2[:, None, :] * o
+
+    def module_gates(self, l, mod):
+        """The gates of block l's module sites, in the order dit_block records
+        them (the cross-attention of PixArt has none: a gate of one)."""
+        g1, g2 = mod[2], mod[5]
+        if self.cfg.kind == "pixart":
+            return [g1, np.ones_like(g1), g2]
+        return [g1, g2]
 
     def dual_block(self, l, xi, xt, cond):
         cfg, P = self.cfg, self.P

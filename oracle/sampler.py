@@ -26,6 +26,14 @@ latent and step; the change at step k is the relative L1 distance
 sum|p_k - p_{k-1}| / sum|p_{k-1}| over the whole batch (no rescaling
 polynomial: its coefficients are fitted to trained weights); steps 0 and S-1
 always run the stack; a full step resets the accumulator to zero.
+
+Blockwise mode (Sec. 4.5, Tables 5 and 6) caches every module's output instead
+of the stack's.  The paper fixes only its two ends (Br = 1 is stepwise
+caching; the blockwise rows of Table 5 take Br = 0); what is built is Br = 0:
+a full step keeps each module's output before its gate (attention, PixArt's
+cross-attention, MLP) in a ring of its own, and a skipped step embeds the
+current latent and adds, block by block, each module's forecast (Eq. 13 with
+the same weights for every site) times the current step's gate.
 """
 from __future__ import annotations
 
@@ -244,3 +252,47 @@ def sample_adaptive(model: Model, x_T: np.ndarray, S: int, ell: float, K: int, l
             trace.setdefault("probe", []).append(pr)
             trace.setdefault("x", []).append(x)
     return x, mask, changes
+
+
+def sample_blockwise(model: Model, x_T: np.ndarray, mask: Sequence[int], K: int, labels=None, text=None,
+                     p: Optional[bary.Params] = None, trace: Optional[Dict[str, list]] = None) -> np.ndarray:
+    """The sampling loop in blockwise mode (Br = 0) for DiT and PixArt models:
+    the cache holds every module site of every block (one ring slot is the list
+    of the sites' outputs of one full step)."""
+    cfg = model.cfg
+    if cfg.kind not in ("dit", "pixart"):
+        raise ValueError("blockwise mode is built for DiT and PixArt blocks")
+    S = len(mask)
+    B = x_T.shape[0]
+    steps = bary.plan(mask, K, None, p)
+    ring = bary.Ring(K)
+    shift = getattr(cfg, "flow_shift", 1.0)
+    tin = model_time(cfg.sampler, S, shift)
+    smp = Sampler(cfg.sampler, S, cfg.in_ch, shift)
+    ctx = model.context(text) if cfg.kind != "dit" else None
+    x = np.asarray(x_T, dtype=np.float64)
+    for k in range(S):
+        cond = model.condition(tin[k], B, labels, text)
+        emb = model.embed(x)
+        h = emb
+        if mask[k]:
+            sites: list = []
+            for l in range(cfg.depth):
+                h = model.dit_block(l, h, model.block_mod(l, cond), ctx, modules=sites)
+            ring.push(sites, k)
+        else:
+            st = steps[k]
+            nodes = [ring.slots[i] for i in st.slots]
+            i = 0
+            for l in range(cfg.depth):
+                for g in model.module_gates(l, model.block_mod(l, cond)):
+                    h = h + g[:, None, :] * bary.forecast([n[i] for n in nodes], st.w)
+                    i += 1
+        feat = h
+        out = np.asarray(model.final(feat, cond), dtype=np.float64)
+        if trace is not None:
+            trace.setdefault("x_in", []).append(x)
+            trace.setdefault("emb", []).append(emb)
+            trace.setdefault("feat", []).append(feat)
+        x = smp.step(k, x, out)
+    return x
