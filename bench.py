@@ -37,6 +37,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-forecast", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="skip timing the HIP-graph replay of the run")
+    ap.add_argument("--no-blockwise", action="store_true", help="skip timing the blockwise-mode run")
     ap.add_argument("--adaptive-ell", type=float, default=0.13,
                     help="threshold of the timed adaptive-schedule run (negative: skip it)")
     ap.add_argument("--kernels-only", action="store_true",
@@ -304,6 +305,29 @@ def main():
                     "ms_fixed_loop_same_mask": round(efm / args.steps * 1e3, 3),
                     "mask": "".join(str(int(v)) for v in amask)}
 
+    # Blockwise mode (Br = 0) under the same mask: every module's output is
+    # cached, so the cache is 2 (DiT) or 3 (PixArt) tensors per block instead
+    # of one per run; timed like `value`.
+    blockwise = None
+    if not args.no_blockwise and cfg.kind in ("dit", "pixart"):
+        def run_blockwise():
+            x.copy_(x0)
+            return dm.sample_blockwise(x, mask, labels=tl, text=tt)
+        for _ in range(max(1, args.warmup)):
+            sites = run_blockwise()
+        torch.cuda.synchronize()
+        tb = time.perf_counter()
+        for _ in range(args.steps):
+            sites = run_blockwise()
+        torch.cuda.synchronize()
+        eb = time.perf_counter() - tb
+        blockwise = {"value": round(B * args.steps / eb, 3), "ms_per_step": round(eb / args.steps * 1e3, 3),
+                     "sites": int(sites.shape[0]), "cache_bytes": int(sites.numel() * sites.element_size()),
+                     "stepwise_cache_bytes": int(cfg.K * B * cfg.tokens * cfg.hidden * sites.element_size())}
+        del sites
+        dm._ring = {k: v for k, v in dm._ring.items() if not (isinstance(k, tuple) and k[0] == "sites")}
+        torch.cuda.empty_cache()
+
     # Speedup reference: the same sampler with every step full.
     full = np.ones(cfg.steps, np.uint8)
     run(full)
@@ -402,6 +426,7 @@ def main():
                    "global_batch": B, "parallelism": "none (1 GPU)"},
         "graph_replay": graph,
         "adaptive": adaptive,
+        "blockwise": blockwise,
         "speedup_vs_all_full": round(ms_full / ms_per_step, 3),
         "ms_all_full": round(ms_full, 3),
         "roofline": roofline,

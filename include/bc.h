@@ -349,6 +349,32 @@ int bc_sample_cfg(const bc_model* m, int B, int sampler, int S, const uint8_t* m
                   const int64_t* labels, float cfg_scale, void* ws, size_t ws_bytes,
                   void* stream);
 
+/* Blockwise mode (Sec. 4.5, Tables 5 and 6; the blockwise ratio Br = 0): the
+ * cache holds, instead of the stack's output, every module's output before its
+ * gate: per DIT block the attention output projection and the MLP output
+ * (2 sites), per PIXART block also the cross-attention output (3 sites).
+ * The number of sites of a model (depth * sites per block). */
+int bc_blockwise_sites(const bc_model* m, int* nsites);
+
+/* The sampling loop in blockwise mode.  A full step (mask[k] = 1) runs the
+ * blocks and writes each module output ([B*T, D], model dtype) into its site's
+ * ring slot (head + 1) mod K before adding it, gated, to the residual stream.
+ * A forecast step embeds the current latent and adds, block by block, every
+ * site's forecast (Eq. 13, the plan's weights for all sites) times the current
+ * step's gate (the cross-attention has none), in one pass; the stream is then
+ * the stepwise feature for the final layer.  Br = 1 is bc_sample itself; ratios
+ * in between are not defined by the paper and not provided.
+ *   site_storage: device [nsites][K][B*T*D] elements of the model dtype,
+ *                 caller-owned, 16-byte aligned (bc_blockwise_sites).
+ *   K:            1..8 slots per site.
+ *   ws:           bc_sample_workspace_size(m, B, S) bytes.
+ * Other arguments as bc_sample (no ring: the sites are the cache).
+ * Errors: as bc_sample; UNSUPPORTED for MMDIT models. */
+int bc_sample_blockwise(const bc_model* m, int B, int sampler, int S, const uint8_t* mask, int K,
+                        const bc_bary_params* p, void* site_storage, float* latents,
+                        const int64_t* labels, const void* text, void* ws, size_t ws_bytes,
+                        void* stream);
+
 /* Bytes of workspace bc_sample_adaptive needs: bc_sample's plus the previous
  * step's probe (B*T*D elements of the model dtype), the first block's
  * (shift, scale) for every step and sample (S*B*2*D floats) and 8 KiB of

@@ -121,6 +121,10 @@ _SIGS = {
     "bc_sample_cfg": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int,
                                 C.POINTER(BaryParams), C.c_void_p, C.c_void_p, C.c_void_p, C.c_float,
                                 C.c_void_p, C.c_size_t, C.c_void_p]),
+    "bc_blockwise_sites": (C.c_int, [C.c_void_p, C.POINTER(C.c_int)]),
+    "bc_sample_blockwise": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int,
+                                      C.POINTER(BaryParams), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                      C.c_void_p, C.c_size_t, C.c_void_p]),
     "bc_sample_adaptive_workspace_size": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.POINTER(C.c_size_t)]),
     "bc_sample_adaptive": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_double, C.c_int,
                                      C.POINTER(BaryParams), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
@@ -394,6 +398,11 @@ class Model:
         _check(lib().bc_sample_workspace_size(self.h, B, S, C.byref(n)))
         return n.value
 
+    def blockwise_sites(self) -> int:
+        n = C.c_int()
+        _check(lib().bc_blockwise_sites(self.h, C.byref(n)))
+        return n.value
+
     def adaptive_workspace_size(self, B: int, S: int) -> int:
         n = C.c_size_t()
         _check(lib().bc_sample_adaptive_workspace_size(self.h, B, S, C.byref(n)))
@@ -415,6 +424,15 @@ def sample_cfg(model: Model, B: int, sampler: str, mask, K: int, ring: CacheRing
     _check(lib().bc_sample_cfg(model.h, B, SAMPLERS[sampler], len(m), _ptr(m), K, C.byref(p) if p else None,
                                ring.h, dev_ptr(latents), dev_ptr(labels), float(cfg_scale), dev_ptr(ws),
                                ws.numel() * ws.element_size(), stream_handle(stream)))
+
+
+def sample_blockwise(model: Model, B: int, sampler: str, mask, K: int, site_storage, latents, ws, labels=None,
+                     text=None, p: Optional[BaryParams] = None, stream=None):
+    """Blockwise-mode sampling (bc_sample_blockwise) in place on latents."""
+    m = np.ascontiguousarray(mask, dtype=np.uint8)
+    _check(lib().bc_sample_blockwise(model.h, B, SAMPLERS[sampler], len(m), _ptr(m), K, C.byref(p) if p else None,
+                                     dev_ptr(site_storage), dev_ptr(latents), dev_ptr(labels), dev_ptr(text),
+                                     dev_ptr(ws), ws.numel() * ws.element_size(), stream_handle(stream)))
 
 
 def sample_adaptive(model: Model, B: int, sampler: str, S: int, ell: float, K: int, ring: CacheRing, latents,

@@ -96,8 +96,12 @@ static int plain(int dt, const void* A, int64_t lda, const void* W, const void* 
 
 // One DiT or PixArt block on x [B*T, D] (fp32).  mod: [B, >= 6D] fp32 rows
 // ld_mod apart, ordered (shift1, scale1, gate1, shift2, scale2, gate2).
+// sites (blockwise mode): the block's module outputs before their gates
+// (attention, PixArt's cross-attention, MLP) are written there ([B*T, D] in
+// the block dtype) and then added to x with their gates.
 static int dit_block(const bc_block_desc& d, const bc_block_weights& w, float* x, const float* mod, int64_t ld_mod,
-                     const void* ctx_kv, const BlockBufs& bb, const BlockOut* out, hipStream_t s) {
+                     const void* ctx_kv, const BlockBufs& bb, const BlockOut* out, hipStream_t s,
+                     void* const* sites = nullptr) {
     const int dt = d.dtype, D = d.D, F = d.mlp, T = d.T;
     const int M = d.B * T;
     const bc_stream_weights& sw = w.img;
@@ -111,7 +115,12 @@ static int dit_block(const bc_block_desc& d, const bc_block_weights& w, float* x
     a.o0 = a.o1 = bb.attn; a.ldo = D;
     a.B = d.B; a.H = d.heads; a.d = d.head_dim;
     BC_TRY(launch_attention(dt, a, s));
-    BC_TRY(gated(dt, bb.attn, D, sw.w_o, sw.b_o, M, D, D, x, mod + 2 * D, ld_mod, T, nullptr, s));
+    if (sites) {
+        BC_TRY(plain(dt, bb.attn, D, sw.w_o, sw.b_o, M, D, D, sites[0], false, s));
+        BC_TRY(launch_gated_add(dt, sites[0], M, D, x, mod + 2 * D, ld_mod, T, s));
+    } else {
+        BC_TRY(gated(dt, bb.attn, D, sw.w_o, sw.b_o, M, D, D, x, mod + 2 * D, ld_mod, T, nullptr, s));
+    }
     if (d.kind == BC_BLOCK_PIXART) {
         // Cross-attention to the text context: no norm, no gate.
         BC_TRY(launch_convert(BC_F32, x, dt, bb.h, (int64_t)M * D, s));
@@ -123,10 +132,20 @@ static int dit_block(const bc_block_desc& d, const bc_block_weights& w, float* x
         c.o0 = c.o1 = bb.attn; c.ldo = D;
         c.B = d.B; c.H = d.heads; c.d = d.head_dim;
         BC_TRY(launch_attention(dt, c, s));
-        BC_TRY(gated(dt, bb.attn, D, w.wx_o, w.bx_o, M, D, D, x, nullptr, 0, T, nullptr, s));
+        if (sites) {
+            BC_TRY(plain(dt, bb.attn, D, w.wx_o, w.bx_o, M, D, D, sites[1], false, s));
+            BC_TRY(launch_gated_add(dt, sites[1], M, D, x, nullptr, 0, T, s));
+        } else {
+            BC_TRY(gated(dt, bb.attn, D, w.wx_o, w.bx_o, M, D, D, x, nullptr, 0, T, nullptr, s));
+        }
     }
     BC_TRY(launch_ln_mod(BC_F32, x, M, D, mod + 3 * D, mod + 4 * D, ld_mod, T, dt, bb.h, s));
     BC_TRY(plain(dt, bb.h, D, sw.w_fc1, sw.b_fc1, M, F, D, bb.mlp, true, s));
+    if (sites) {
+        void* site = sites[d.kind == BC_BLOCK_PIXART ? 2 : 1];
+        BC_TRY(plain(dt, bb.mlp, F, sw.w_fc2, sw.b_fc2, M, D, F, site, false, s));
+        return launch_gated_add(dt, site, M, D, x, mod + 5 * D, ld_mod, T, s);
+    }
     return gated(dt, bb.mlp, F, sw.w_fc2, sw.b_fc2, M, D, F, x, mod + 5 * D, ld_mod, T, out, s);
 }
 
@@ -581,6 +600,15 @@ static double* readback_buffer() {
     return buf;
 }
 
+// Blockwise mode: the module sites' ring storage, [site][slot][B*T*D].
+struct BlockwiseIO {
+    void* storage;
+};
+
+// Module sites per block in blockwise mode (attention, PixArt's
+// cross-attention, MLP).
+static int sites_per_block(const bc_model_desc& d) { return d.kind == BC_MODEL_PIXART ? 3 : 2; }
+
 // The adaptive schedule's threshold and outputs (host arrays of S entries).
 struct AdaptiveIO {
     double ell;
@@ -594,8 +622,13 @@ struct AdaptiveIO {
 // reads two sums back to the host at every step after the first.
 static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_t* mask, int K, const bc_bary_params* p,
                       bc_cache_ring* ring, float* latents, const int64_t* labels, const void* text, bool guided,
-                      float cfg, void* ws, size_t ws_bytes, void* stream, const AdaptiveIO* ad = nullptr) {
-    if (!m || !(mask || ad) || !ring || !latents || !ws) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
+                      float cfg, void* ws, size_t ws_bytes, void* stream, const AdaptiveIO* ad = nullptr,
+                      const BlockwiseIO* bw = nullptr) {
+    if (!m || !(mask || ad) || !(ring || bw) || !latents || !ws) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
+    if (bw && (ad || guided || !bw->storage || reinterpret_cast<uintptr_t>(bw->storage) % 16))
+        return fail(BC_ERR_INVALID_ARG, "blockwise mode: 16-byte aligned site storage, fixed mask, no guidance");
+    if (bw && m->d.kind == BC_MODEL_MMDIT)
+        return fail(BC_ERR_UNSUPPORTED, "blockwise mode is built for DiT and PixArt models");
     if (ad && (guided || !ad->mask_out || !(ad->ell >= 0.0)))
         return fail(BC_ERR_INVALID_ARG, "adaptive schedule: mask_out required, threshold >= 0, no guidance");
     const bc_model_desc& d = m->d;
@@ -603,9 +636,15 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
     if (B < 1 || Bm > 64) return fail(BC_ERR_INVALID_ARG, "B=%d outside [1, %d]", B, guided ? 32 : 64);
     if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(BC_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
     const int T = model_tokens(d), D = d.D;
-    if (K != ring->K) return fail(BC_ERR_INVALID_ARG, "K=%d but the ring has %d slots", K, ring->K);
-    if (ring->dtype != d.dtype || ring->numel != (int64_t)Bm * T * D)
-        return fail(BC_ERR_INVALID_ARG, "ring must hold %lld elements of the model dtype per slot", (long long)Bm * T * D);
+    if (bw) {
+        if (K < 1 || K > kMaxK) return fail(BC_ERR_INVALID_ARG, "K=%d outside [1, %d]", K, kMaxK);
+        if (d.depth * sites_per_block(d) > kMaxSites) return fail(BC_ERR_UNSUPPORTED, "too many module sites");
+    } else {
+        if (K != ring->K) return fail(BC_ERR_INVALID_ARG, "K=%d but the ring has %d slots", K, ring->K);
+        if (ring->dtype != d.dtype || ring->numel != (int64_t)Bm * T * D)
+            return fail(BC_ERR_INVALID_ARG, "ring must hold %lld elements of the model dtype per slot",
+                        (long long)Bm * T * D);
+    }
     if (d.kind == BC_MODEL_DIT && d.n_classes && !labels) return fail(BC_ERR_INVALID_ARG, "class labels required");
     if (d.kind != BC_MODEL_DIT && !text) return fail(BC_ERR_INVALID_ARG, "text input required");
     std::vector<int32_t> tau(S > 0 ? S : 1);
@@ -626,7 +665,7 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
     double ab[1000];
     alpha_bar(ab);
     double h_prev = 0.0;
-    bc_cache_reset(ring);
+    if (ring) bc_cache_reset(ring);
     const bc_block_weights* blk = m->w.blocks;
     const bc_model_weights& mw = m->w;
     const bc_block_desc bd_main = block_desc_of(d, Bm, d.kind == BC_MODEL_DIT ? BC_BLOCK_DIT
@@ -704,9 +743,12 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
             BC_TRY(launch_add_tables(dt, w.pmod, 2 * D, tab, 1, 2 * D, S * Bm, w.pmod, 2 * D, s));
         }
     }
+    // Steps whose block modulation is needed: the full steps (known up front
+    // unless the schedule is adaptive), every step in blockwise mode (the gates
+    // of the forecast module outputs).
     std::vector<int> full_steps;
     for (int k = 0; k < S && !ad; ++k)
-        if (plan[k].is_full) full_steps.push_back(k);
+        if (plan[k].is_full || bw) full_steps.push_back(k);
     // Full steps whose modulation is computed together (one at a time when
     // they are decided during the loop).
     const int chunk = ad ? 1 : w.full_chunk;
@@ -765,7 +807,7 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
 
     // The fused final step needs 16-byte aligned ring slots and weights (checked
     // here once) and an instantiated (D, p*p*C_out).
-    const bool fused_final = !guided && final_step_supported(dt, D, d.patch * d.patch * d.out_ch, T) &&
+    const bool fused_final = !guided && !bw && final_step_supported(dt, D, d.patch * d.patch * d.out_ch, T) &&
                              reinterpret_cast<uintptr_t>(ring->storage) % 16 == 0 && (ring->numel * esz) % 16 == 0 &&
                              reinterpret_cast<uintptr_t>(mw.final_w) % 16 == 0;
 
@@ -806,6 +848,63 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
         }
         const bc_plan_step& st = plan[k];
         const float* fmod = w.fmod + (int64_t)k * Bm * 2 * D;
+        const int NO = d.patch * d.patch * d.out_ch;
+        if (bw) {
+            // Blockwise: a full step runs the blocks, writing every module's
+            // output into its site's slot; a skipped step embeds the latent and
+            // adds every site's gated forecast in one pass.  The feature is the
+            // fp32 stream.
+            const int fi = full_index % chunk;
+            if (fi == 0) BC_TRY(chunk_mods(full_index));
+            ++full_index;
+            const float* mods = w.mods + (int64_t)fi * Bm * ldm;
+            const int nq = sites_per_block(d);
+            const int64_t numel = (int64_t)Bm * T * D;
+            BC_TRY(launch_patch_embed(dt, latents, ls, Bm, B, mw.patch_w, mw.patch_b, mw.pos, D, w.x, s));
+            if (st.is_full) {
+                for (int l = 0; l < d.depth; ++l) {
+                    void* sp[3];
+                    for (int q = 0; q < nq; ++q)
+                        sp[q] = static_cast<char*>(bw->storage) +
+                                (((int64_t)(l * nq + q) * K + st.head) * numel) * (int64_t)esz;
+                    BC_TRY(dit_block(bd_main, blk[l], w.x, mods + (int64_t)l * 6 * D, ldm,
+                                     d.kind == BC_MODEL_PIXART ? static_cast<char*>(w.ctx_kv) + (int64_t)l * B * d.ctx_tokens * 2 * D * esz : nullptr,
+                                     w.bb, nullptr, s, sp));
+                }
+            } else {
+                BlockwiseArgs a;
+                std::memset(&a, 0, sizeof a);
+                a.storage = bw->storage;
+                a.numel = numel;
+                a.nsites = d.depth * nq;
+                a.K = K;
+                a.count = st.count;
+                for (int j = 0; j < st.count; ++j) {
+                    a.slot[j] = st.slots[j];
+                    a.w[j] = (float)st.w[j];
+                }
+                for (int l = 0; l < d.depth; ++l)
+                    for (int q = 0; q < nq; ++q)
+                        a.goff[l * nq + q] = q == 0 ? l * 6 * D + 2 * D : (q + 1 == nq ? l * 6 * D + 5 * D : -1);
+                a.mods = mods;
+                a.ldm = ldm;
+                a.rows_per_gate = T;
+                a.D = D;
+                a.rows = (int64_t)Bm * T;
+                a.x = w.x;
+                BC_TRY(launch_blockwise_forecast(dt, a, s));
+            }
+            const SamplerCoef sc = sampler_coef(sampler, k, S, tau.data(), ab, &h_prev, d.flow_shift);
+            BC_TRY(launch_ln_mod(BC_F32, w.x, (int64_t)Bm * T, D, fmod, fmod + D, 2 * D, T, dt, w.bb.h, s));
+            GemmArgs fg = gemm_args(w.bb.h, D, mw.final_w, D, Bm * T, NO, D);
+            fg.e.bias = mw.final_b;
+            fg.e.out = w.out;
+            fg.e.ldo = NO;
+            fg.e.out_f32 = 1;
+            BC_TRY(launch_gemm(dt, BC_EPI_BIAS, fg, s));
+            BC_TRY(launch_sampler(sc, latents, w.out, w.prev, ls, B, d.out_ch, s));
+            continue;
+        }
         const void* feat;
         if (st.is_full) {
             void* slot = nullptr;
@@ -851,7 +950,6 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
             BC_TRY(bc_cache_push(ring, nullptr, (double)k, stream));
             feat = slot;
         }
-        const int NO = d.patch * d.patch * d.out_ch;
         const SamplerCoef sc = sampler_coef(sampler, k, S, tau.data(), ab, &h_prev, d.flow_shift);
         if (fused_final && (st.is_full || st.count <= kFinalMaxK)) {
             // Stepwise feature (the new slot, or the forecast from the ring), final
@@ -923,6 +1021,24 @@ int bc_sample_cfg(const bc_model* m, int B, int sampler, int S, const uint8_t* m
     if (!std::isfinite(cfg_scale)) return fail(BC_ERR_INVALID_ARG, "guidance scale must be finite");
     return sample_run(m, B, sampler, S, mask, K, p, ring, latents, labels, nullptr, true, cfg_scale, ws, ws_bytes,
                       stream);
+}
+
+int bc_blockwise_sites(const bc_model* m, int* nsites) {
+    clear_error();
+    if (!m || !nsites) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
+    if (m->d.kind == BC_MODEL_MMDIT) return fail(BC_ERR_UNSUPPORTED, "blockwise mode is built for DiT and PixArt models");
+    *nsites = m->d.depth * sites_per_block(m->d);
+    return BC_OK;
+}
+
+int bc_sample_blockwise(const bc_model* m, int B, int sampler, int S, const uint8_t* mask, int K,
+                        const bc_bary_params* p, void* site_storage, float* latents, const int64_t* labels,
+                        const void* text, void* ws, size_t ws_bytes, void* stream) {
+    clear_error();
+    if (!site_storage) return fail(BC_ERR_INVALID_ARG, "NULL site storage");
+    const BlockwiseIO io{site_storage};
+    return sample_run(m, B, sampler, S, mask, K, p, nullptr, latents, labels, text, false, 1.f, ws, ws_bytes, stream,
+                      nullptr, &io);
 }
 
 int bc_sample_adaptive(const bc_model* m, int B, int sampler, int S, double ell, int K, const bc_bary_params* p,

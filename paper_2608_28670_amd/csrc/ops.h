@@ -113,6 +113,31 @@ int launch_qk_norm_rope(int dt, void* qkv, int64_t rows, int64_t ld, int D, int 
                         const void* wk, int rows_per_sample, int n_img, int gf, int gh, int gw, double theta,
                         hipStream_t s);
 
+// Blockwise mode.  x [rows, D] fp32 (rows of rows_per_gate tokens per sample):
+//   gated add:  x += gate[r / rows_per_gate] (.) site   (gate rows ldg floats
+//               apart; NULL: a gate of one), site [rows, D] in `dt`;
+//   forecast:   x += sum_s gate_s[r / rows_per_gate] (.) sum_j w[j] site_s(slot[j])
+//               over the nsites sites of storage [site][K slots][rows * D],
+//               gate_s at goff[s] floats into the modulation row of the sample
+//               (goff[s] < 0: a gate of one), accumulated in fp32.
+constexpr int kMaxSites = 96;
+struct BlockwiseArgs {
+    const void* storage;
+    int64_t numel;                 // rows * D
+    int nsites, K, count;
+    int slot[kMaxK];
+    float w[kMaxK];
+    int goff[kMaxSites];
+    const float* mods;
+    int64_t ldm;
+    int rows_per_gate, D;
+    int64_t rows;
+    float* x;
+};
+int launch_gated_add(int dt, const void* site, int64_t rows, int D, float* x, const float* gate, int64_t ldg,
+                     int rows_per_gate, hipStream_t s);
+int launch_blockwise_forecast(int dt, const BlockwiseArgs& a, hipStream_t s);
+
 // Change measure of the adaptive schedule: over n elements of `dt`,
 // sums[0] = sum |cur - prev| and sums[1] = sum |prev| (fp32 per thread and
 // workgroup, the kRelL1Blocks partials `part` [2 * kRelL1Blocks] then added in

@@ -703,6 +703,110 @@ int launch_qk_norm_rope(int dt, void* qkv, int64_t rows, int64_t ld, int D, int 
 }
 
 // ---------------------------------------------------------------------------
+// Blockwise mode: gated adds of module outputs into the fp32 residual stream,
+// 8 consecutive elements per thread (16-byte loads of the bf16 sites).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void load8(const bf16* p, float* v) {
+    const u32x4 u = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        v[2 * k] = __uint_as_float(u[k] << 16);
+        v[2 * k + 1] = __uint_as_float(u[k] & 0xffff0000u);
+    }
+}
+__device__ __forceinline__ void load8(const float* p, float* v) {
+    const f32x4 a = *reinterpret_cast<const f32x4*>(p), b = *reinterpret_cast<const f32x4*>(p + 4);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        v[k] = a[k];
+        v[4 + k] = b[k];
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void gated_add_kernel(const T* __restrict__ site, int64_t n8, int D,
+                                                        float* __restrict__ x, const float* __restrict__ gate,
+                                                        int64_t ldg, int rows_per_gate) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n8) return;
+    const int64_t e = i * 8, r = e / D;
+    const int d = (int)(e - r * D);
+    float v[8], xv[8], g[8];
+    load8(site + e, v);
+    load8(x + e, xv);
+    if (gate) load8(gate + (r / rows_per_gate) * ldg + d, g);
+    else {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) g[k] = 1.f;
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) xv[k] = fmaf(g[k], v[k], xv[k]);
+    *reinterpret_cast<f32x4*>(x + e) = f32x4{xv[0], xv[1], xv[2], xv[3]};
+    *reinterpret_cast<f32x4*>(x + e + 4) = f32x4{xv[4], xv[5], xv[6], xv[7]};
+}
+
+int launch_gated_add(int dt, const void* site, int64_t rows, int D, float* x, const float* gate, int64_t ldg,
+                     int rows_per_gate, hipStream_t s) {
+    if (D % 8 || reinterpret_cast<uintptr_t>(site) % 16 || reinterpret_cast<uintptr_t>(x) % 16 ||
+        (gate && (reinterpret_cast<uintptr_t>(gate) % 16 || ldg % 4)) || rows_per_gate < 1)
+        return fail(BC_ERR_INVALID_ARG, "gated_add: D %d, alignment", D);
+    const int64_t n8 = rows * D / 8;
+    if (n8 < 1) return BC_OK;
+    const unsigned g = (unsigned)((n8 + 255) / 256);
+    if (dt == BC_BF16) gated_add_kernel<bf16><<<g, 256, 0, s>>>(static_cast<const bf16*>(site), n8, D, x, gate, ldg, rows_per_gate);
+    else gated_add_kernel<float><<<g, 256, 0, s>>>(static_cast<const float*>(site), n8, D, x, gate, ldg, rows_per_gate);
+    return check_launch("gated_add");
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void blockwise_forecast_kernel(BlockwiseArgs a) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i * 8 >= a.numel) return;
+    const int64_t e = i * 8, r = e / a.D;
+    const int d = (int)(e - r * a.D);
+    const T* st = static_cast<const T*>(a.storage);
+    const float* mrow = a.mods + (r / a.rows_per_gate) * a.ldm + d;
+    float xv[8];
+    load8(a.x + e, xv);
+    for (int s = 0; s < a.nsites; ++s) {
+        float f[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < a.count; ++j) {
+            float v[8];
+            load8(st + ((int64_t)s * a.K + a.slot[j]) * a.numel + e, v);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) f[k] = fmaf(a.w[j], v[k], f[k]);
+        }
+        float g[8];
+        if (a.goff[s] >= 0) load8(mrow + a.goff[s], g);
+        else {
+#pragma unroll
+            for (int k = 0; k < 8; ++k) g[k] = 1.f;
+        }
+#pragma unroll
+        for (int k = 0; k < 8; ++k) xv[k] = fmaf(g[k], f[k], xv[k]);
+    }
+    *reinterpret_cast<f32x4*>(a.x + e) = f32x4{xv[0], xv[1], xv[2], xv[3]};
+    *reinterpret_cast<f32x4*>(a.x + e + 4) = f32x4{xv[4], xv[5], xv[6], xv[7]};
+}
+
+int launch_blockwise_forecast(int dt, const BlockwiseArgs& a, hipStream_t s) {
+    if (a.D % 8 || a.numel % 8 || a.nsites < 1 || a.nsites > kMaxSites || a.count < 1 || a.count > a.K ||
+        a.K > kMaxK || a.ldm % 4 || reinterpret_cast<uintptr_t>(a.storage) % 16 ||
+        reinterpret_cast<uintptr_t>(a.x) % 16 || reinterpret_cast<uintptr_t>(a.mods) % 16)
+        return fail(BC_ERR_INVALID_ARG, "blockwise forecast: %d sites, count %d of %d", a.nsites, a.count, a.K);
+    for (int j = 0; j < a.count; ++j)
+        if (a.slot[j] < 0 || a.slot[j] >= a.K) return fail(BC_ERR_INVALID_ARG, "blockwise forecast: slot %d", a.slot[j]);
+    for (int q = 0; q < a.nsites; ++q)
+        if (a.goff[q] >= 0 && a.goff[q] % 4)   // (negative: no gate)
+            return fail(BC_ERR_INVALID_ARG, "blockwise forecast: gate offset %d", a.goff[q]);
+    const int64_t n8 = a.numel / 8;
+    const unsigned g = (unsigned)((n8 + 255) / 256);
+    if (dt == BC_BF16) blockwise_forecast_kernel<bf16><<<g, 256, 0, s>>>(a);
+    else blockwise_forecast_kernel<float><<<g, 256, 0, s>>>(a);
+    return check_launch("blockwise_forecast");
+}
+
+// ---------------------------------------------------------------------------
 // Relative L1 change of the adaptive schedule's probe: 16-byte chunks of cur
 // and prev, |cur - prev| and |prev| summed per thread, per wave (butterfly)
 // and per workgroup in a fixed order; prev takes cur's bytes in the same pass.

@@ -14,7 +14,7 @@ import numpy as np
 
 from . import (BF16, BLOCK_DIT, BLOCK_DUAL, BLOCK_PIXART, BLOCK_SINGLE, F32, MODEL_DIT, MODEL_MMDIT,
                MODEL_PIXART, BlockWeights, CacheRing, Model, ModelDesc, SampleGraph, block_weights, sample,
-               sample_adaptive, sample_cfg)
+               sample_adaptive, sample_blockwise, sample_cfg)
 
 _KIND = {"dit": MODEL_DIT, "pixart": MODEL_PIXART, "mmdit": MODEL_MMDIT}
 
@@ -134,6 +134,22 @@ class DeviceModel:
         B = x.shape[0]
         ws, ring = self.buffers(B, K, len(mask))
         return SampleGraph(self.model, B, self.cfg.sampler, mask, K, ring, x, ws, labels=labels, text=text, p=p)
+
+    def sample_blockwise(self, x, mask, K: Optional[int] = None, labels=None, text=None, p=None, stream=None):
+        """Blockwise-mode sampling in place on x; returns the site storage
+        [sites, K, B*T*D] (allocated once per (B, K) and reused)."""
+        import torch
+        K = K or self.cfg.K
+        B = x.shape[0]
+        ws, _ = self.buffers(B, K, len(mask))
+        key = ("sites", B, K)
+        if key not in self._ring:
+            n = self.model.blockwise_sites()
+            self._ring[key] = torch.empty((n, K, B * self.cfg.tokens * self.cfg.hidden), dtype=torch_dtype(self.cfg),
+                                          device=self.device)
+        sample_blockwise(self.model, B, self.cfg.sampler, mask, K, self._ring[key], x, ws, labels=labels, text=text,
+                         p=p, stream=stream)
+        return self._ring[key]
 
     def sample_adaptive(self, x, S: int, ell: float, K: Optional[int] = None, labels=None, text=None, p=None,
                         stream=None):
