@@ -896,15 +896,15 @@ static int run_gemm(const GemmArgs& g, hipStream_t s) {
         const bool dma = g.K % 64 == 0 && g.lda % 8 == 0 && g.ldw % 8 == 0;
         if (dma && wide_ok(g, EPI)) {
             if (tiles288 >= 256) {
-                if (g.N % 288 != 0 && g.N % 256 == 0) launch_wide<EPI, 256, 256, 4, 2>(g, s);
-                else launch_wide<EPI, 256, 288, 4, 2>(g, s);
+                if (g.N % 288 != 0 && g.N % 256 == 0) launch_wide<EPI, 256, 256, 4, 4>(g, s);
+                else launch_wide<EPI, 256, 288, 4, 3>(g, s);
             } else if (g.N % 432 == 0 && (int64_t)((g.M + 127) / 128) * (g.N / 432) >= 256) {
-                launch_wide<EPI, 128, 432, 2, 4>(g, s);
+                launch_wide<EPI, 128, 432, 4, 3>(g, s);
             } else if (tiles144 <= 256) {
                 if (EPI == BC_EPI_BIAS && g.K % 128 == 0) launch_wide<EPI, 128, 144, 2, 2, 2, 64, 2>(g, s);
-                else launch_wide<EPI, 128, 144, 2, 4, 3, 64, 1, 1>(g, s);
+                else launch_wide<EPI, 128, 144, 4, 4, 4, 64, 1, 1>(g, s);
             } else {
-                launch_wide<EPI, 128, 128, 4, 2>(g, s);
+                launch_wide<EPI, 128, 128, 4, 4>(g, s);
             }
         } else if (dma) {
             launch_dma<EPI, 128, 128, 4, 2, 2>(g, s);
