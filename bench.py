@@ -259,6 +259,58 @@ def main():
     ms_per_step = elapsed / args.steps * 1e3
     value = B * args.steps / elapsed
 
+    # Kernel classes timed with per-launch HIP events on their launch stream
+    # in one extra sampling run (the events ride on the launches themselves),
+    # right after the timed runs and in the same state: where a full step's
+    # time goes, and the roofline of the dominant kernel.
+    nfull = int(mask.sum())
+    classes = {"gemm_gelu": bc.PROF_GEMM_GELU, "gemm_down": bc.PROF_GEMM_DOWN, "gemm_gated": bc.PROF_GEMM_GATE,
+               "gemm_bias": bc.PROF_GEMM_BIAS, "attention": bc.PROF_ATTENTION, "layernorm": bc.PROF_LAYERNORM}
+    cap = 16 * nfull * cfg.depth + 1024
+    for c in classes.values():
+        bc.profile_enable(c, cap)
+    run(mask)
+    breakdown, times = {}, {}
+    for name, c in classes.items():
+        t = bc.profile_times(c, cap).astype(np.float64)
+        times[name] = t
+        if len(t):
+            breakdown[name] = {"ms_per_run": round(float(t.sum()), 3), "launches": len(t),
+                               "avg_us": round(float(t.mean()) * 1e3, 2)}
+    roofline, others = None, []
+    if cfg.kind in ("dit", "pixart"):
+        M_rows = B * cfg.tokens
+        nb = nfull * cfg.depth
+        gemm_hash = source_hash("gemm.hip", "gemm.h", "hip_common.h")
+        att_hash = source_hash("attention.hip", "attention.h", "hip_common.h")
+        # One launch per block and full step for each candidate.  PixArt's
+        # caption MLP (once per run, before the loop) is the first GELU GEMM;
+        # its cross-attention follows each self-attention.
+        att = times["attention"] if cfg.kind == "dit" else times["attention"][0::2]
+        cands = [
+            ("gemm fc2 (gated residual, MLP down projection)", times["gemm_down"], "mfma",
+             2.0 * M_rows * cfg.hidden * cfg.mlp, [M_rows, cfg.hidden, cfg.mlp], f"gemm_fc2_{cfg.name}", gemm_hash),
+            ("gemm fc1 (bias+GELU)", times["gemm_gelu"][-nb:], "mfma",
+             2.0 * M_rows * cfg.mlp * cfg.hidden, [M_rows, cfg.mlp, cfg.hidden], f"gemm_fc1_{cfg.name}", gemm_hash),
+            ("self-attention", att, "mfma",
+             4.0 * B * cfg.heads * cfg.tokens * cfg.tokens * cfg.head_dim,
+             [B, cfg.heads, cfg.tokens, cfg.head_dim], f"attention_{cfg.name}", att_hash),
+        ]
+        recs = []
+        for name, t, bound, flops, shape, tag, h in cands:
+            assert len(t) == nb, (name, len(t), nb)
+            avg_s = float(t.mean()) / 1e3
+            achieved = flops / avg_s / 1e12
+            recs.append((float(t.sum()), {
+                "bound": bound, "kernel": name, "shape": shape, "flops_per_launch": flops,
+                "avg_us": round(avg_s * 1e6, 2), "launches": len(t), "ms_per_run": round(float(t.sum()), 3),
+                "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": counters_traffic(tag, h, None), "source_hash": h}))
+        recs.sort(key=lambda r: -r[0])
+        roofline, others = recs[0][1], [r[1] for r in recs[1:]]
+
+
     # The same run replayed from a HIP graph captured once (bc_sample_graph_*).
     graph = None
     if not args.no_graph:
@@ -338,56 +390,6 @@ def main():
         run(full)
     torch.cuda.synchronize()
     ms_full = (time.perf_counter() - tf) / nref * 1e3
-
-    # Kernel classes timed with per-launch HIP events on their launch stream
-    # in one extra sampling run (the events ride on the launches themselves):
-    # where a full step's time goes, and the roofline of the dominant kernel.
-    nfull = int(mask.sum())
-    classes = {"gemm_gelu": bc.PROF_GEMM_GELU, "gemm_down": bc.PROF_GEMM_DOWN, "gemm_gated": bc.PROF_GEMM_GATE,
-               "gemm_bias": bc.PROF_GEMM_BIAS, "attention": bc.PROF_ATTENTION, "layernorm": bc.PROF_LAYERNORM}
-    cap = 16 * nfull * cfg.depth + 1024
-    for c in classes.values():
-        bc.profile_enable(c, cap)
-    run(mask)
-    breakdown, times = {}, {}
-    for name, c in classes.items():
-        t = bc.profile_times(c, cap).astype(np.float64)
-        times[name] = t
-        if len(t):
-            breakdown[name] = {"ms_per_run": round(float(t.sum()), 3), "launches": len(t),
-                               "avg_us": round(float(t.mean()) * 1e3, 2)}
-    roofline, others = None, []
-    if cfg.kind in ("dit", "pixart"):
-        M_rows = B * cfg.tokens
-        nb = nfull * cfg.depth
-        gemm_hash = source_hash("gemm.hip", "gemm.h", "hip_common.h")
-        att_hash = source_hash("attention.hip", "attention.h", "hip_common.h")
-        # One launch per block and full step for each candidate.  PixArt's
-        # caption MLP (once per run, before the loop) is the first GELU GEMM;
-        # its cross-attention follows each self-attention.
-        att = times["attention"] if cfg.kind == "dit" else times["attention"][0::2]
-        cands = [
-            ("gemm fc2 (gated residual, MLP down projection)", times["gemm_down"], "mfma",
-             2.0 * M_rows * cfg.hidden * cfg.mlp, [M_rows, cfg.hidden, cfg.mlp], f"gemm_fc2_{cfg.name}", gemm_hash),
-            ("gemm fc1 (bias+GELU)", times["gemm_gelu"][-nb:], "mfma",
-             2.0 * M_rows * cfg.mlp * cfg.hidden, [M_rows, cfg.mlp, cfg.hidden], f"gemm_fc1_{cfg.name}", gemm_hash),
-            ("self-attention", att, "mfma",
-             4.0 * B * cfg.heads * cfg.tokens * cfg.tokens * cfg.head_dim,
-             [B, cfg.heads, cfg.tokens, cfg.head_dim], f"attention_{cfg.name}", att_hash),
-        ]
-        recs = []
-        for name, t, bound, flops, shape, tag, h in cands:
-            assert len(t) == nb, (name, len(t), nb)
-            avg_s = float(t.mean()) / 1e3
-            achieved = flops / avg_s / 1e12
-            recs.append((float(t.sum()), {
-                "bound": bound, "kernel": name, "shape": shape, "flops_per_launch": flops,
-                "avg_us": round(avg_s * 1e6, 2), "launches": len(t), "ms_per_run": round(float(t.sum()), 3),
-                "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": counters_traffic(tag, h, None), "source_hash": h}))
-        recs.sort(key=lambda r: -r[0])
-        roofline, others = recs[0][1], [r[1] for r in recs[1:]]
 
     forecast = None
     if not args.no_forecast:
