@@ -365,13 +365,14 @@ int bc_blockwise_sites(const bc_model* m, int* nsites);
  * the stepwise feature for the final layer.  Br = 1 is bc_sample itself; ratios
  * in between are not defined by the paper and not provided.
  *   site_storage: device [nsites][K][B*T*D] elements of the model dtype,
- *                 caller-owned, 16-byte aligned (bc_blockwise_sites).
+ *                 caller-owned, 16-byte aligned (bc_blockwise_sites);
+ *   site_bytes:   its size in bytes (INVALID_ARG if smaller than that).
  *   K:            1..8 slots per site.
  *   ws:           bc_sample_workspace_size(m, B, S) bytes.
  * Other arguments as bc_sample (no ring: the sites are the cache).
  * Errors: as bc_sample; UNSUPPORTED for MMDIT models. */
 int bc_sample_blockwise(const bc_model* m, int B, int sampler, int S, const uint8_t* mask, int K,
-                        const bc_bary_params* p, void* site_storage, float* latents,
+                        const bc_bary_params* p, void* site_storage, size_t site_bytes, float* latents,
                         const int64_t* labels, const void* text, void* ws, size_t ws_bytes,
                         void* stream);
 

@@ -123,8 +123,8 @@ _SIGS = {
                                 C.c_void_p, C.c_size_t, C.c_void_p]),
     "bc_blockwise_sites": (C.c_int, [C.c_void_p, C.POINTER(C.c_int)]),
     "bc_sample_blockwise": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int,
-                                      C.POINTER(BaryParams), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
-                                      C.c_void_p, C.c_size_t, C.c_void_p]),
+                                      C.POINTER(BaryParams), C.c_void_p, C.c_size_t, C.c_void_p, C.c_void_p,
+                                      C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
     "bc_sample_adaptive_workspace_size": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.POINTER(C.c_size_t)]),
     "bc_sample_adaptive": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_double, C.c_int,
                                      C.POINTER(BaryParams), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
@@ -431,7 +431,8 @@ def sample_blockwise(model: Model, B: int, sampler: str, mask, K: int, site_stor
     """Blockwise-mode sampling (bc_sample_blockwise) in place on latents."""
     m = np.ascontiguousarray(mask, dtype=np.uint8)
     _check(lib().bc_sample_blockwise(model.h, B, SAMPLERS[sampler], len(m), _ptr(m), K, C.byref(p) if p else None,
-                                     dev_ptr(site_storage), dev_ptr(latents), dev_ptr(labels), dev_ptr(text),
+                                     dev_ptr(site_storage), site_storage.numel() * site_storage.element_size(),
+                                     dev_ptr(latents), dev_ptr(labels), dev_ptr(text),
                                      dev_ptr(ws), ws.numel() * ws.element_size(), stream_handle(stream)))
 
 

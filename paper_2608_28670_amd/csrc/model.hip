@@ -603,6 +603,7 @@ static double* readback_buffer() {
 // Blockwise mode: the module sites' ring storage, [site][slot][B*T*D].
 struct BlockwiseIO {
     void* storage;
+    size_t bytes;
 };
 
 // Module sites per block in blockwise mode (attention, PixArt's
@@ -639,6 +640,8 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
     if (bw) {
         if (K < 1 || K > kMaxK) return fail(BC_ERR_INVALID_ARG, "K=%d outside [1, %d]", K, kMaxK);
         if (d.depth * sites_per_block(d) > kMaxSites) return fail(BC_ERR_UNSUPPORTED, "too many module sites");
+        const size_t need = (size_t)d.depth * sites_per_block(d) * K * Bm * T * D * dtype_size(d.dtype);
+        if (bw->bytes < need) return fail(BC_ERR_INVALID_ARG, "site storage %zu < %zu bytes", bw->bytes, need);
     } else {
         if (K != ring->K) return fail(BC_ERR_INVALID_ARG, "K=%d but the ring has %d slots", K, ring->K);
         if (ring->dtype != d.dtype || ring->numel != (int64_t)Bm * T * D)
@@ -1032,11 +1035,11 @@ int bc_blockwise_sites(const bc_model* m, int* nsites) {
 }
 
 int bc_sample_blockwise(const bc_model* m, int B, int sampler, int S, const uint8_t* mask, int K,
-                        const bc_bary_params* p, void* site_storage, float* latents, const int64_t* labels,
-                        const void* text, void* ws, size_t ws_bytes, void* stream) {
+                        const bc_bary_params* p, void* site_storage, size_t site_bytes, float* latents,
+                        const int64_t* labels, const void* text, void* ws, size_t ws_bytes, void* stream) {
     clear_error();
     if (!site_storage) return fail(BC_ERR_INVALID_ARG, "NULL site storage");
-    const BlockwiseIO io{site_storage};
+    const BlockwiseIO io{site_storage, site_bytes};
     return sample_run(m, B, sampler, S, mask, K, p, nullptr, latents, labels, text, false, 1.f, ws, ws_bytes, stream,
                       nullptr, &io);
 }

@@ -99,3 +99,7 @@ def test_blockwise_errors(bclib):
     with pytest.raises(bclib.BCError) as e:     # K outside 1..8
         bclib.sample_blockwise(dt.model, tiny.batch, tiny.sampler, mask, 9, store, x, ws)
     assert e.value.code == bclib.ERR_INVALID_ARG
+    with pytest.raises(bclib.BCError) as e:     # storage one slot short
+        short = store[:2 * tiny.depth * (tiny.K - 1) * tiny.batch * tiny.tokens * tiny.hidden]
+        bclib.sample_blockwise(dt.model, tiny.batch, tiny.sampler, mask, tiny.K, short, x, ws)
+    assert e.value.code == bclib.ERR_INVALID_ARG
