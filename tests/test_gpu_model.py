@@ -263,6 +263,36 @@ def test_sample_tiny_all_full_and_k1(bclib):
     assert rel_l2(got, _oracle_sample(cfg, P, xT, ones)) <= 1e-4
 
 
+def test_sample_bf16_k8_mixes_fused_and_separate_final(bclib):
+    """K = 8 on the bf16 DiT: forecast steps with up to 4 cached features take
+    the fused final step, those with 5 to 8 the separate forecast, LayerNorm,
+    final GEMM and sampler kernels, within one run."""
+    cfg = synth.scaled(synth.CONFIGS["dit_xl2"], depth=2, batch=2, K=8, steps=24, interval=2)
+    P = synth.params(cfg)
+    mask = bary.make_mask(cfg.steps, cfg.interval)
+    counts = [st.count for st, m in zip(bary.plan(mask, cfg.K), mask) if not m]
+    assert min(counts) <= 4 and max(counts) == 8
+    labels = synth.labels(cfg, batch=2)
+    xT, got, ring = _run_sample(bclib, cfg, P, 2, mask, labels=labels)
+    err = rel_l2(got, _oracle_sample(cfg, P, xT, mask, labels=labels))
+    print(f"dit_xl2 depth 2, K 8: final latents rel-L2 {err:.2e}")
+    assert err <= 2e-2
+    _check_ring(ring, mask, cfg.K)
+
+
+@pytest.mark.parametrize("mask", [[1], [1, 1], [1, 0], [1, 0, 0]], ids=["S1", "S2_full", "S2_fc", "S3_fc"])
+def test_sample_shortest_schedules(bclib, mask):
+    mask = np.array(mask, np.uint8)
+    for name, B, tol in (("tiny", 2, 1e-4), ("dit_xl2", 2, 2e-2)):
+        cfg = synth.scaled(synth.CONFIGS[name], steps=len(mask), **({"depth": 2, "batch": 2} if name != "tiny" else {}))
+        P = synth.params(cfg)
+        labels = synth.labels(cfg, batch=B) if cfg.n_classes else None
+        xT, got, ring = _run_sample(bclib, cfg, P, B, mask, labels=labels)
+        err = rel_l2(got, _oracle_sample(cfg, P, xT, mask, labels=labels))
+        assert err <= tol, (name, err)
+        _check_ring(ring, mask, cfg.K)
+
+
 def test_sample_dit_xl2_reduced_depth(bclib):
     cfg = synth.scaled(synth.CONFIGS["dit_xl2"], depth=2, batch=2)
     P = synth.params(cfg)
