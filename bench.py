@@ -377,7 +377,7 @@ def main():
                      "sites": int(sites.shape[0]), "cache_bytes": int(sites.numel() * sites.element_size()),
                      "stepwise_cache_bytes": int(cfg.K * B * cfg.tokens * cfg.hidden * sites.element_size())}
         del sites
-        dm._ring = {k: v for k, v in dm._ring.items() if not (isinstance(k, tuple) and k[0] == "sites")}
+        dm.release_blockwise()
         torch.cuda.empty_cache()
 
     # Speedup reference: the same sampler with every step full.

@@ -109,14 +109,19 @@ class DeviceModel:
         self.model = Model(model_desc(cfg), model_weights(cfg, self.P), block_list(cfg, self.P))
         self._ws = {}
         self._ring = {}
+        self._sites = {}
 
-    def buffers(self, B: int, K: int, S: int):
-        """Workspace and ring storage for batch B and S steps (allocated once, reused)."""
+    def workspace(self, B: int, S: int):
+        """bc_sample's workspace for batch B and S steps (allocated once, reused)."""
         import torch
         if (B, S) not in self._ws:
             n = self.model.workspace_size(B, S)
             self._ws[(B, S)] = torch.empty(n, dtype=torch.uint8, device=self.device)
-        return self._ws[(B, S)], self.ring(B, K)
+        return self._ws[(B, S)]
+
+    def buffers(self, B: int, K: int, S: int):
+        """Workspace and ring storage for batch B and S steps (allocated once, reused)."""
+        return self.workspace(B, S), self.ring(B, K)
 
     def ring(self, B: int, K: int) -> CacheRing:
         """Ring of K slots of B*T*D elements (allocated once, reused)."""
@@ -141,15 +146,19 @@ class DeviceModel:
         import torch
         K = K or self.cfg.K
         B = x.shape[0]
-        ws, _ = self.buffers(B, K, len(mask))
-        key = ("sites", B, K)
-        if key not in self._ring:
+        ws = self.workspace(B, len(mask))
+        key = (B, K)
+        if key not in self._sites:
             n = self.model.blockwise_sites()
-            self._ring[key] = torch.empty((n, K, B * self.cfg.tokens * self.cfg.hidden), dtype=torch_dtype(self.cfg),
-                                          device=self.device)
-        sample_blockwise(self.model, B, self.cfg.sampler, mask, K, self._ring[key], x, ws, labels=labels, text=text,
-                         p=p, stream=stream)
-        return self._ring[key]
+            self._sites[key] = torch.empty((n, K, B * self.cfg.tokens * self.cfg.hidden), dtype=torch_dtype(self.cfg),
+                                           device=self.device)
+        sample_blockwise(self.model, B, self.cfg.sampler, mask, K, self._sites[key], x, ws, labels=labels,
+                         text=text, p=p, stream=stream)
+        return self._sites[key]
+
+    def release_blockwise(self):
+        """Drop the blockwise site storage (it is sites * K times the stepwise ring)."""
+        self._sites.clear()
 
     def sample_adaptive(self, x, S: int, ell: float, K: Optional[int] = None, labels=None, text=None, p=None,
                         stream=None):
