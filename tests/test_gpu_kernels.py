@@ -27,8 +27,13 @@ def _dev(a, dt):
 
 
 @pytest.mark.parametrize("dt", ["bf16", "f32"])
+# Beyond the small and model shapes, four bf16 shapes reach each multi-round tile
+# of the wide kernel with a ragged row tail: 256 x 288 with a ragged column tile
+# (4100 x 4616), 256 x 256 (4100 x 4352), 128 x 432 (4000 x 3456) and 128 x 128
+# (4000 x 2304).
 @pytest.mark.parametrize("M,N,K", [(300, 200, 136), (128, 128, 64), (1, 16, 8), (517, 384, 1152),
-                                   (4096, 1152, 1152), (4100, 4612, 1152), (130, 260, 192), (1000, 1160, 256)])
+                                   (4096, 1152, 1152), (4100, 4612, 1152), (130, 260, 192), (1000, 1160, 256),
+                                   (4100, 4616, 64), (4100, 4352, 128), (4000, 3456, 64), (4000, 2304, 64)])
 @pytest.mark.parametrize("epi", ["bias", "gelu", "gate"])
 def test_linear(bclib, dt, M, N, K, epi):
     if dt == "f32" and M * N * K > 1e8:
