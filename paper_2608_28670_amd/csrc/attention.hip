@@ -15,6 +15,7 @@
 // streams of joint attention): position p of sample b is row b*T0 + p of
 // segment 0 if p < T0, else row b*T1 + (p - T0) of segment 1.  Head h of a row
 // is the d consecutive elements starting at column h*d.
+#include <type_traits>
 #include "attention.h"
 
 namespace bc {
@@ -339,7 +340,7 @@ __device__ __forceinline__ float group_sum(float v) {
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
-template <int HD, int QG, int NWV, int NB>
+template <int HD, int QG, int NWV, int NB, bool STREAM>
 __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
     typedef AttnShape<bf16, HD> S;
     typedef KvLayout<HD> LY;
@@ -393,7 +394,22 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
         irow[q] = row;
         icol[q] = col0 + 8 * (LY::SWZ ? slot ^ ((row / LY::RPB) % LY::CPR) : slot);
     }
-    auto issue = [&](int k0, int buf) {
+    // STREAM (the instantiations for long key sequences, whose tiles stream
+    // through the buffers): a tile that lies wholly inside one key segment
+    // is addressed from one row pointer, common to the workgroup, plus each
+    // lane's fixed offset (when offsets within a tile fit 32 bits).  The tile
+    // that crosses the segment boundary or runs past the last key, and every
+    // tile of the other instantiations, take the per-row path.
+    const bool off32 = STREAM && (int64_t)kKTile * (a.ldk > a.ldv ? a.ldk : a.ldv) < ((int64_t)1 << 31);
+    int koff[NJ], voff[NJ];
+    if constexpr (STREAM) {
+#pragma unroll
+        for (int q = 0; q < NJ; ++q) {
+            koff[q] = (int)(irow[q] * a.ldk + icol[q]);     // used only when off32
+            voff[q] = (int)(irow[q] * a.ldv + icol[q]);
+        }
+    }
+    auto issue_rows = [&](int k0, int buf) {
 #pragma unroll
         for (int q = 0; q < NJ; ++q) {
             const int j = wave + NWV * q;
@@ -405,11 +421,36 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
             dma16a(vr, &sV[buf][64 * j * 8]);
         }
     };
+    auto issue = [&](int k0, int buf) {
+        if constexpr (!STREAM) {
+            issue_rows(k0, buf);
+            return;
+        }
+        const bf16 *kb = nullptr, *vb = nullptr;
+        if (off32 && k0 + kKTile <= a.Tk0) {
+            kb = static_cast<const bf16*>(a.k0) + ((int64_t)b * a.Tk0 + k0) * a.ldk;
+            vb = static_cast<const bf16*>(a.v0) + ((int64_t)b * a.Tk0 + k0) * a.ldv;
+        } else if (off32 && k0 >= a.Tk0 && k0 + kKTile <= Tk) {
+            kb = static_cast<const bf16*>(a.k1) + ((int64_t)b * a.Tk1 + (k0 - a.Tk0)) * a.ldk;
+            vb = static_cast<const bf16*>(a.v1) + ((int64_t)b * a.Tk1 + (k0 - a.Tk0)) * a.ldv;
+        }
+        if (kb) {
+#pragma unroll
+            for (int q = 0; q < NJ; ++q) {
+                const int j = wave + NWV * q;
+                if (j >= LY::CPR) break;
+                dma16a(kb + koff[q], &sK[buf][64 * j * 8]);
+                dma16a(vb + voff[q], &sV[buf][64 * j * 8]);
+            }
+        } else {
+            issue_rows(k0, buf);
+        }
+    };
     const int ntiles = (Tk + kKTile - 1) / kKTile;
     const bool resident = ntiles <= NB;
     // K/V loads go out first so that their latency overlaps the Q loads.
     if (resident) {
-        for (int t = 0; t < ntiles; ++t) issue(t * kKTile, t);
+        for (int t = 0; t < ntiles; ++t) issue_rows(t * kKTile, t);
     } else {
         issue(0, 0);
     }
@@ -440,16 +481,20 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
 
 
     // Scores, online softmax and the P V update of one 64-key tile at k0.
-    // Keys past Tk (in the last tile only) start their score accumulators at
-    // -inf, so the MFMAs themselves mask them: one select per score slot per
-    // tile, shared by the query groups, instead of a compare and select per
-    // score.
-    auto tile = [&](int k0, const bf16* K, const bf16* V) {
+    // Keys past Tk occur in the last tile only.  Two ways to mask them:
+    //   * branch (the streaming loop of the STREAM instantiations): after the MFMAs, their scores are set
+    //     to -inf under a branch taken once per workgroup, so the other tiles
+    //     spend no instructions on the mask;
+    //   * select (otherwise): their score accumulators
+    //     start at -inf, one select per score slot shared by the query groups,
+    //     which keeps the tile one basic block for the scheduler.
+    auto tile = [&](int k0, const bf16* K, const bf16* V, auto branch_mask) __attribute__((always_inline)) {
+        constexpr bool BRANCH = decltype(branch_mask)::value;
         f32x4 init[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) init[j][r] = k0 + 16 * j + 4 * grp + r < Tk ? 0.f : -INFINITY;
+            for (int r = 0; r < 4; ++r) init[j][r] = BRANCH || k0 + 16 * j + 4 * grp + r < Tk ? 0.f : -INFINITY;
 
         f32x4 s[QG][4];
 #pragma unroll
@@ -463,6 +508,16 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
 #pragma unroll
                 for (int g = 0; g < QG; ++g) s[g][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[g][c], s[g][j], 0, 0, 0);
             }
+        }
+        if (BRANCH && k0 + kKTile > Tk) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    if (k0 + 16 * j + 4 * grp + r >= Tk) {
+#pragma unroll
+                        for (int g = 0; g < QG; ++g) s[g][j][r] = -INFINITY;
+                    }
         }
 
         // Softmax in the log2 domain on raw scores (the scale is positive, so
@@ -535,14 +590,14 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
     if (resident) {
         __builtin_amdgcn_s_waitcnt((0 & 15) | (7 << 4) | (15 << 8));   // vmcnt(0): this wave's loads
         __syncthreads();
-        for (int t = 0; t < ntiles; ++t) tile(t * kKTile, sK[t], sV[t]);
+        for (int t = 0; t < ntiles; ++t) tile(t * kKTile, sK[t], sV[t], std::false_type{});
     } else {
         for (int t = 0; t < ntiles; ++t) {
             const int buf = t & 1;
             __builtin_amdgcn_s_waitcnt((0 & 15) | (7 << 4) | (15 << 8));   // vmcnt(0): this wave's loads of tile t
             __syncthreads();
             if (t + 1 < ntiles) issue((t + 1) * kKTile, buf ^ 1);
-            tile(t * kKTile, sK[buf], sV[buf]);
+            tile(t * kKTile, sK[buf], sV[buf], std::integral_constant<bool, STREAM>{});
         }
     }
 
@@ -572,20 +627,20 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
     }
 }
 
-template <int QG, int NWV, int NB>
+template <int QG, int NWV, int NB, bool STREAM = true>
 static int run_attention_dma(const AttnArgs& a, int hd, hipStream_t s) {
     const int Tq = a.Tq0 + a.Tq1;
     const int64_t nwg = (int64_t)((Tq + 16 * QG * NWV - 1) / (16 * QG * NWV)) * a.H * a.B;
     if (nwg > 0x7fffffff) return fail(BC_ERR_UNSUPPORTED, "attention grid too large");
     dim3 grid((unsigned)nwg), block(64 * NWV);
     switch (hd) {
-#define BC_ATT_CASE(HD) case HD: launch_k(attention_dma_kernel<HD, QG, NWV, NB>, grid, block, s, a); break;
+#define BC_ATT_CASE(HD) case HD: launch_k(attention_dma_kernel<HD, QG, NWV, NB, STREAM>, grid, block, s, a); break;
         BC_ATT_CASE(32) BC_ATT_CASE(64) BC_ATT_CASE(72)
 #undef BC_ATT_CASE
         case 128:
             // 64 queries per wave at d = 128 would spill: only up to 32.
             if constexpr (QG <= 2) {
-                launch_k(attention_dma_kernel<128, QG, NWV, NB>, grid, block, s, a);
+                launch_k(attention_dma_kernel<128, QG, NWV, NB, STREAM>, grid, block, s, a);
                 break;
             } else {
                 return fail(BC_ERR_UNSUPPORTED, "head_dim 128 with %d query groups per wave", QG);
@@ -638,7 +693,7 @@ int launch_attention(int dtype, AttnArgs a, hipStream_t s) {
         // they still give the grid a full round of workgroups.
         const int64_t bh = (int64_t)a.B * a.H;
         const int64_t n512 = (Tq + 511) / 512 * bh, n256 = (Tq + 255) / 256 * bh;
-        if (Tk <= 4 * kKTile) rc = run_attention_dma<1, 8, 4>(a, a.d, s);
+        if (Tk <= 4 * kKTile) rc = run_attention_dma<1, 8, 4, false>(a, a.d, s);
         else if (a.d <= 72 && n512 >= 256) rc = run_attention_dma<4, 8, 2>(a, a.d, s);
         else if (n256 >= 128) rc = run_attention_dma<2, 8, 2>(a, a.d, s);
         else rc = run_attention_dma<1, 8, 2>(a, a.d, s);
