@@ -11,6 +11,7 @@ namespace bc {
 
 constexpr float kLnEps = 1e-6f;
 constexpr int kMaxPatch = 256;
+constexpr int kPatchRows = 16;     // tokens per patch-embedding workgroup
 
 // ---------------------------------------------------------------------------
 // LayerNorm + modulate: one wave per row, the row cached in registers as
@@ -443,26 +444,48 @@ int launch_convert(int in_dt, const void* in, int out_dt, void* out, int64_t n, 
 template <typename T>
 __global__ __launch_bounds__(256) void patch_embed_kernel(const float* __restrict__ lat, LatentShape ls,
                                                           const T* __restrict__ W, const T* __restrict__ bias,
-                                                          const T* __restrict__ pos, int D, int lat_B,
+                                                          const T* __restrict__ pos, int D, int lat_B, int rows,
                                                           float* __restrict__ x) {
-    __shared__ float patch[kMaxPatch];
+    // kPatchRows tokens per workgroup: each thread reads its columns' weight
+    // rows once for all of them (the weights are [D, p*p*C], one row per
+    // output column), and each output still sums its patch in order q = 0, 1, ...
+    __shared__ float patch[kPatchRows][kMaxPatch];
     const int Tn = ls.tokens();
-    const int row = blockIdx.x;
-    const int bm = row / Tn, tok = row - bm * Tn;
-    const int b = bm % lat_B;
+    const int row0 = blockIdx.x * kPatchRows;
     const int hp = ls.H / ls.p, wp = ls.W / ls.p;
-    const int f = tok / (hp * wp), ti = (tok / wp) % hp, tj = tok % wp;
     const int PD = ls.p * ls.p * ls.C;
-    for (int q = threadIdx.x; q < PD; q += blockDim.x) {
-        const int ph = q / (ls.p * ls.C), pw = (q / ls.C) % ls.p, ch = q % ls.C;
-        patch[q] = lat[((((int64_t)b * ls.C + ch) * ls.F + f) * ls.H + ti * ls.p + ph) * ls.W + tj * ls.p + pw];
+    for (int i = threadIdx.x; i < kPatchRows * PD; i += blockDim.x) {
+        const int r = i / PD, q = i - r * PD, row = row0 + r;
+        float v = 0.f;
+        if (row < rows) {
+            const int bm = row / Tn, tok = row - bm * Tn;
+            const int b = bm % lat_B;
+            const int f = tok / (hp * wp), ti = (tok / wp) % hp, tj = tok % wp;
+            const int ph = q / (ls.p * ls.C), pw = (q / ls.C) % ls.p, ch = q % ls.C;
+            v = lat[((((int64_t)b * ls.C + ch) * ls.F + f) * ls.H + ti * ls.p + ph) * ls.W + tj * ls.p + pw];
+        }
+        patch[r][q] = v;
     }
     __syncthreads();
     for (int c = threadIdx.x; c < D; c += blockDim.x) {
         const T* wr = W + (int64_t)c * PD;
-        float acc = 0.f;
-        for (int q = 0; q < PD; ++q) acc = __builtin_fmaf(patch[q], ld(wr + q), acc);
-        x[(int64_t)row * D + c] = acc + ld(bias + c) + ld(pos + (int64_t)tok * D + c);
+        float acc[kPatchRows];
+#pragma unroll
+        for (int r = 0; r < kPatchRows; ++r) acc[r] = 0.f;
+        for (int q = 0; q < PD; ++q) {
+            const float w = ld(wr + q);
+#pragma unroll
+            for (int r = 0; r < kPatchRows; ++r) acc[r] = __builtin_fmaf(patch[r][q], w, acc[r]);
+        }
+        const float bc = ld(bias + c);
+#pragma unroll
+        for (int r = 0; r < kPatchRows; ++r) {
+            const int row = row0 + r;
+            if (row < rows) {
+                const int tok = row % Tn;
+                x[(int64_t)row * D + c] = acc[r] + bc + ld(pos + (int64_t)tok * D + c);
+            }
+        }
     }
 }
 
@@ -470,13 +493,15 @@ int launch_patch_embed(int dt, const float* lat, LatentShape ls, int B, int lat_
                        const void* pos, int D, float* x, hipStream_t s) {
     if (ls.p * ls.p * ls.C > kMaxPatch) return fail(BC_ERR_UNSUPPORTED, "patch of %d values", ls.p * ls.p * ls.C);
     if (lat_B < 1 || lat_B > B) return fail(BC_ERR_INVALID_ARG, "latent batch %d for a model batch of %d", lat_B, B);
-    const unsigned rows = (unsigned)(B * ls.tokens());
+    const int rows = B * ls.tokens();
+    if (rows <= 0) return BC_OK;
+    const unsigned grid = (unsigned)((rows + kPatchRows - 1) / kPatchRows);
     if (dt == BC_BF16)
-        patch_embed_kernel<bf16><<<rows, 256, 0, s>>>(lat, ls, static_cast<const bf16*>(W), static_cast<const bf16*>(bias),
-                                                      static_cast<const bf16*>(pos), D, lat_B, x);
+        patch_embed_kernel<bf16><<<grid, 256, 0, s>>>(lat, ls, static_cast<const bf16*>(W), static_cast<const bf16*>(bias),
+                                                      static_cast<const bf16*>(pos), D, lat_B, rows, x);
     else
-        patch_embed_kernel<float><<<rows, 256, 0, s>>>(lat, ls, static_cast<const float*>(W), static_cast<const float*>(bias),
-                                                       static_cast<const float*>(pos), D, lat_B, x);
+        patch_embed_kernel<float><<<grid, 256, 0, s>>>(lat, ls, static_cast<const float*>(W), static_cast<const float*>(bias),
+                                                       static_cast<const float*>(pos), D, lat_B, rows, x);
     return check_launch("patch_embed");
 }
 
