@@ -2,6 +2,7 @@
 // modulation, the skinny linear layers of the conditioning path, patch
 // embedding, the final layer, sampler updates and element-wise helpers.
 // All statistics and accumulations are fp32.
+#include <type_traits>
 #include <algorithm>
 #include <cmath>
 
@@ -11,7 +12,6 @@ namespace bc {
 
 constexpr float kLnEps = 1e-6f;
 constexpr int kMaxPatch = 256;
-constexpr int kPatchRows = 16;     // tokens per patch-embedding workgroup
 
 // ---------------------------------------------------------------------------
 // LayerNorm + modulate: one wave per row, the row cached in registers as
@@ -441,7 +441,7 @@ int launch_convert(int in_dt, const void* in, int out_dt, void* out, int64_t n, 
 // ---------------------------------------------------------------------------
 // One workgroup per token: gather its p*p*C patch values once (LDS), then
 // each thread produces output features of the row.
-template <typename T>
+template <typename T, int kPatchRows>
 __global__ __launch_bounds__(256) void patch_embed_kernel(const float* __restrict__ lat, LatentShape ls,
                                                           const T* __restrict__ W, const T* __restrict__ bias,
                                                           const T* __restrict__ pos, int D, int lat_B, int rows,
@@ -449,6 +449,8 @@ __global__ __launch_bounds__(256) void patch_embed_kernel(const float* __restric
     // kPatchRows tokens per workgroup: each thread reads its columns' weight
     // rows once for all of them (the weights are [D, p*p*C], one row per
     // output column), and each output still sums its patch in order q = 0, 1, ...
+    // Large patches (the video model's 64 values) take 16 tokens per
+    // workgroup; small ones one, which keeps enough workgroups in flight.
     __shared__ float patch[kPatchRows][kMaxPatch];
     const int Tn = ls.tokens();
     const int row0 = blockIdx.x * kPatchRows;
@@ -495,13 +497,20 @@ int launch_patch_embed(int dt, const float* lat, LatentShape ls, int B, int lat_
     if (lat_B < 1 || lat_B > B) return fail(BC_ERR_INVALID_ARG, "latent batch %d for a model batch of %d", lat_B, B);
     const int rows = B * ls.tokens();
     if (rows <= 0) return BC_OK;
-    const unsigned grid = (unsigned)((rows + kPatchRows - 1) / kPatchRows);
-    if (dt == BC_BF16)
-        patch_embed_kernel<bf16><<<grid, 256, 0, s>>>(lat, ls, static_cast<const bf16*>(W), static_cast<const bf16*>(bias),
-                                                      static_cast<const bf16*>(pos), D, lat_B, rows, x);
-    else
-        patch_embed_kernel<float><<<grid, 256, 0, s>>>(lat, ls, static_cast<const float*>(W), static_cast<const float*>(bias),
-                                                       static_cast<const float*>(pos), D, lat_B, rows, x);
+    auto go = [&](auto tpb) {
+        constexpr int TPB = decltype(tpb)::value;
+        const unsigned grid = (unsigned)((rows + TPB - 1) / TPB);
+        if (dt == BC_BF16)
+            patch_embed_kernel<bf16, TPB><<<grid, 256, 0, s>>>(lat, ls, static_cast<const bf16*>(W),
+                                                               static_cast<const bf16*>(bias),
+                                                               static_cast<const bf16*>(pos), D, lat_B, rows, x);
+        else
+            patch_embed_kernel<float, TPB><<<grid, 256, 0, s>>>(lat, ls, static_cast<const float*>(W),
+                                                                static_cast<const float*>(bias),
+                                                                static_cast<const float*>(pos), D, lat_B, rows, x);
+    };
+    if (ls.p * ls.p * ls.C >= 32) go(std::integral_constant<int, 16>{});
+    else go(std::integral_constant<int, 1>{});
     return check_launch("patch_embed");
 }
 
