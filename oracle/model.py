@@ -21,8 +21,9 @@ architectures written out as math, with these readings:
   * dual-stream block: image and text streams each with their own modulation,
     projections and MLP, attention joint over the concatenated tokens; single-
     stream block: one fused projection to [qkv | mlp], one fused output
-    projection of [attention | GELU(mlp)], one gate.  RoPE, QK-norm, the token
-    refiner and guidance embedding are left out;
+    projection of [attention | GELU(mlp)], one gate; queries and keys take a
+    per-head RMSNorm and a 3D rotary embedding of the image tokens (Model.qk).
+    The token refiner and guidance embedding are left out;
   * the cached feature is the image-token part of the last block's output; the
     final layer runs on every step, full or forecast.
 """
