@@ -55,6 +55,10 @@ const char* bc_status_str(int status);
 const char* bc_last_error(void);
 /* ABI version, (major << 16) | minor. */
 int bc_version(void);
+/* Hash of the sources, headers and compiler flags the library was built from
+ * (a NUL-terminated hex string owned by the library), so a caller can refuse a
+ * library that is older than its sources. */
+const char* bc_build_id(void);
 
 /* ------------------------------------------------------------------------ */
 /* Barycentric weights (host, fp64)                                          */
@@ -463,13 +467,19 @@ int bc_attention_workspace_size(int B, int H, int Tq, int Tk, int d, int dtype, 
  * Classes: 0 forecast, 1 GEMM with GELU epilogue, 2 GEMM gated residual with
  * K <= N (attention output projection), 3 GEMM bias (QKV), 4 attention,
  * 5 layernorm-modulate, 6 GEMM gated residual with K > N (MLP down
- * projection). */
+ * projection), 7 device copy (the ring push's copy path). */
 int bc_profile_enable(int kernel_class, int max_launches);
 int bc_profile_collect(int kernel_class, double* total_ms, int* launches);
 /* As bc_profile_collect, but writes each launch's duration in ms, in launch
  * order, to ms_out (host, max_out entries; later launches are dropped) and
  * their number to *launches. */
 int bc_profile_times(int kernel_class, float* ms_out, int max_out, int* launches);
+/* As bc_profile_times, and work_out[i] (host, may be NULL) receives launch i's
+ * algorithmic work: 2 M N K FLOPs for a GEMM, 4 B H Tq Tk d FLOPs for
+ * attention (Q K^T and P V), bytes read plus written for the forecast
+ * (n (K s_in + s_out)), the LayerNorm (rows D (s_in + s_out)) and a copy
+ * (2 bytes).  A launch that is not the first of its library call records 0. */
+int bc_profile_records(int kernel_class, float* ms_out, double* work_out, int max_out, int* launches);
 
 #ifdef __cplusplus
 }

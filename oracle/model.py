@@ -268,11 +268,14 @@ class Model:
             m = linear(silu(cond["c"]), P[f"blocks.{l}.w_mod"], P[f"blocks.{l}.b_mod"])
         return [m[:, i * D:(i + 1) * D] for i in range(6)]
 
-    def dit_block(self, l, x, mod, ctx=None, modules=None):
+    def dit_block(self, l, x, mod, ctx=None, modules=None, rows=None):
         """One DiT (or PixArt) block on the residual stream x [B, T, D].
         `modules`, if a list, receives the block's module outputs before their
         gates (attention, PixArt's cross-attention, MLP): the sites that
-        blockwise caching keeps (Sec. 3.1, Eq. 4: the increments M_q)."""
+        blockwise caching keeps (Sec. 3.1, Eq. 4: the increments M_q).
+        `rows`, if given, is a list of token indices: keys and values still
+        come from every token, but only those tokens' outputs are computed and
+        returned ([B, len(rows), D]); every other step is per token."""
         cfg, P = self.cfg, self.P
         pre = f"blocks.{l}."
         s1, sc1, g1, s2, sc2, g2 = mod
@@ -280,6 +283,8 @@ class Model:
         h = modulate(layer_norm(x), s1, sc1)
         qkv = linear(h, P[pre + "w_qkv"], P[pre + "b_qkv"])
         q, k, v = (split_heads(qkv[..., i * D:(i + 1) * D], H) for i in range(3))
+        if rows is not None:
+            x, q = x[:, rows], q[:, :, rows]
         a = merge_heads(attention(q, k, v))
         o = linear(a, P[pre + "w_o"], P[pre + "b_o"])
         x = x + g1[:, None, :] * o
@@ -306,7 +311,10 @@ class Model:
             return [g1, np.ones_like(g1), g2]
         return [g1, g2]
 
-    def dual_block(self, l, xi, xt, cond):
+    def dual_block(self, l, xi, xt, cond, rows=None):
+        """Dual-stream block on image tokens xi [B, Ti, D] and text tokens
+        xt [B, Tt, D]; returns both streams.  `rows` = (image rows, text rows):
+        only those tokens' outputs are computed (keys and values from all)."""
         cfg, P = self.cfg, self.P
         D, H = cfg.hidden, cfg.heads
         Ti = xi.shape[1]
@@ -323,6 +331,10 @@ class Model:
             ks.append(k)
             vs.append(v)
         q, k, v = (np.concatenate(z, axis=2) for z in (qs, ks, vs))
+        if rows is not None:
+            ri, rt = list(rows[0]), list(rows[1])
+            q = q[:, :, ri + [Ti + r for r in rt]]
+            xi, xt, Ti = xi[:, ri], xt[:, rt], len(ri)
         a = merge_heads(attention(q, k, v))
         outs = []
         for s, x, a_s in (("img", xi, a[:, :Ti]), ("txt", xt, a[:, Ti:])):
@@ -334,7 +346,10 @@ class Model:
             outs.append(x + g2[:, None, :] * linear(mm, P[pre + "w_fc2"], P[pre + "b_fc2"]))
         return outs[0], outs[1]
 
-    def single_block(self, l, x, cond, n_img=0):
+    def single_block(self, l, x, cond, n_img=0, rows=None):
+        """Single-stream block on x [B, T_img + T_txt, D] (the first n_img
+        tokens are image tokens).  `rows`: token indices whose outputs alone
+        are computed (keys and values from all tokens)."""
         cfg, P = self.cfg, self.P
         D, H = cfg.hidden, cfg.heads
         pre = f"single.{l}."
@@ -344,6 +359,8 @@ class Model:
         y = linear(h, P[pre + "w_1"], P[pre + "b_1"])
         q, k, v = (split_heads(y[..., i * D:(i + 1) * D], H) for i in range(3))
         q, k = self.qk(q, k, pre, n_img)
+        if rows is not None:
+            x, y, q = x[:, rows], y[:, rows], q[:, :, rows]
         a = merge_heads(attention(q, k, v))
         z = np.concatenate([a, gelu_tanh(y[..., 3 * D:])], axis=-1)
         return x + g[:, None, :] * linear(z, P[pre + "w_2"], P[pre + "b_2"])

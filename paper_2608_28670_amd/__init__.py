@@ -24,7 +24,8 @@ BLOCK_DIT, BLOCK_PIXART, BLOCK_DUAL, BLOCK_SINGLE = range(4)
 MODEL_DIT, MODEL_PIXART, MODEL_MMDIT = range(3)
 SAMPLER_DDIM, SAMPLER_DPMPP2M, SAMPLER_EULER = range(3)
 EPI_BIAS, EPI_BIAS_GELU, EPI_GATE_RES = range(3)
-PROF_FORECAST, PROF_GEMM_GELU, PROF_GEMM_GATE, PROF_GEMM_BIAS, PROF_ATTENTION, PROF_LAYERNORM, PROF_GEMM_DOWN = range(7)
+PROF_FORECAST, PROF_GEMM_GELU, PROF_GEMM_GATE, PROF_GEMM_BIAS, PROF_ATTENTION, PROF_LAYERNORM, PROF_GEMM_DOWN, \
+    PROF_COPY = range(8)
 SAMPLERS = {"ddim": SAMPLER_DDIM, "dpmpp2m": SAMPLER_DPMPP2M, "euler": SAMPLER_EULER}
 
 
@@ -93,6 +94,7 @@ _SIGS = {
     "bc_status_str": (C.c_char_p, [C.c_int]),
     "bc_last_error": (C.c_char_p, []),
     "bc_version": (C.c_int, []),
+    "bc_build_id": (C.c_char_p, []),
     "bc_bary_params_default": (None, [C.POINTER(BaryParams)]),
     "bc_bary_weights": (C.c_int, [C.c_void_p, C.c_int, C.c_double, C.c_void_p]),
     "bc_bary_weights_ex": (C.c_int, [C.c_void_p, C.c_int, C.c_double, C.POINTER(BaryParams), C.c_void_p]),
@@ -143,17 +145,43 @@ _SIGS = {
     "bc_profile_enable": (C.c_int, [C.c_int, C.c_int]),
     "bc_profile_collect": (C.c_int, [C.c_int, C.POINTER(C.c_double), C.POINTER(C.c_int)]),
     "bc_profile_times": (C.c_int, [C.c_int, C.POINTER(C.c_float), C.c_int, C.POINTER(C.c_int)]),
+    "bc_profile_records": (C.c_int, [C.c_int, C.POINTER(C.c_float), C.POINTER(C.c_double), C.c_int,
+                                     C.POINTER(C.c_int)]),
 }
 
 
+def built_id() -> Optional[str]:
+    """The source hash the built library reports, without loading it into
+    this process for use (None if it is missing)."""
+    if not os.path.exists(LIB_PATH):
+        return None
+    L = C.CDLL(LIB_PATH)
+    fn = L.bc_build_id
+    fn.restype = C.c_char_p
+    return fn().decode()
+
+
+def is_current() -> bool:
+    """True if the built library was built from the sources in this tree."""
+    from . import build
+    return built_id() == build.source_hash()
+
+
 def lib() -> C.CDLL:
-    """The loaded library.  Raises if it has not been built."""
+    """The loaded library.  Raises if it has not been built, or if it was
+    built from other sources than those in this tree."""
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"{LIB_PATH} is missing: build it with `python -c 'import __graft_entry__ as g; "
                               f"g.build()'` or `python paper_2608_28670_amd/build.py`")
+        from . import build
         L = C.CDLL(LIB_PATH)
+        L.bc_build_id.restype = C.c_char_p
+        have, want = L.bc_build_id().decode(), build.source_hash()
+        if have != want:
+            raise ImportError(f"{LIB_PATH} was built from other sources (build id {have}, sources {want}): "
+                              f"rebuild it with `python paper_2608_28670_amd/build.py`")
         for name, (res, args) in _SIGS.items():
             fn = getattr(L, name)
             fn.restype = res
@@ -494,3 +522,16 @@ def profile_times(kernel_class: int, max_launches: int) -> np.ndarray:
     n = C.c_int()
     _check(lib().bc_profile_times(kernel_class, ms.ctypes.data_as(C.POINTER(C.c_float)), max_launches, C.byref(n)))
     return ms[:n.value]
+
+
+def profile_records(kernel_class: int, max_launches: int):
+    """(durations in ms, algorithmic work) of an enabled class's launches, in
+    launch order; disables it.  Work: FLOPs (GEMM, attention) or bytes
+    (forecast, LayerNorm, copy); 0 for a launch that is not the first of its
+    library call."""
+    ms = np.zeros(max_launches, np.float32)
+    work = np.zeros(max_launches, np.float64)
+    n = C.c_int()
+    _check(lib().bc_profile_records(kernel_class, ms.ctypes.data_as(C.POINTER(C.c_float)),
+                                    work.ctypes.data_as(C.POINTER(C.c_double)), max_launches, C.byref(n)))
+    return ms[:n.value], work[:n.value]

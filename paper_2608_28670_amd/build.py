@@ -6,6 +6,7 @@ library next to this file.  Object files go to _build/.
 """
 from __future__ import annotations
 
+import hashlib
 import os
 import shutil
 import subprocess
@@ -49,6 +50,25 @@ def sources():
     return hip, cpp
 
 
+INCLUDE = os.path.join(os.path.dirname(HERE), "include")
+
+
+def source_hash() -> str:
+    """Hash of everything the library is built from: every source and header
+    under csrc/ and include/, and the compiler flags.  The built library
+    returns the value it was built with from bc_build_id()."""
+    h = hashlib.sha256()
+    files = [os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith((".hip", ".h", ".cpp"))]
+    files += [os.path.join(INCLUDE, f) for f in os.listdir(INCLUDE) if f.endswith(".h")]
+    for path in sorted(files, key=os.path.basename):
+        h.update(os.path.basename(path).encode() + b"\0")
+        with open(path, "rb") as f:
+            h.update(f.read())
+        h.update(b"\0")
+    h.update(" ".join(HIP_FLAGS + CXX_FLAGS).encode())
+    return h.hexdigest()[:20]
+
+
 def build(jobs: int | None = None, verbose: bool = False) -> str:
     """Compile every source and link libbarycache.so; returns its path."""
     os.makedirs(BUILD, exist_ok=True)
@@ -68,7 +88,12 @@ def build(jobs: int | None = None, verbose: bool = False) -> str:
         for o in outs:
             if o.strip():
                 print(o)
-    objs = [os.path.join(BUILD, f + ".o") for f in hip + cpp]
+    # the build id: the source hash, exported as bc_build_id()
+    bid_src = os.path.join(BUILD, "build_id.cpp")
+    with open(bid_src, "w") as f:
+        f.write('extern "C" const char* bc_build_id(void) { return "%s"; }\n' % source_hash())
+    _run(["g++", *CXX_FLAGS, "-c", bid_src, "-o", bid_src + ".o"])
+    objs = [os.path.join(BUILD, f + ".o") for f in hip + cpp] + [bid_src + ".o"]
     tmp = LIB + ".tmp"
     _run([_hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs,
           f"-L{ROCM}/lib", "-lamdhip64", f"-Wl,-rpath,{ROCM}/lib"])

@@ -678,7 +678,7 @@ int launch_attention(int dtype, AttnArgs a, hipStream_t s) {
         return fail(BC_ERR_UNSUPPORTED, "attention rows must be 16-byte aligned");
     if (dtype == BC_F32 && a.d > 64) return fail(BC_ERR_UNSUPPORTED, "fp32 attention supports head_dim <= 64");
     a.scale_log2 = 1.4426950408889634f / sqrtf((float)a.d);
-    prof_begin(PROF_ATTENTION, s);
+    prof_begin(PROF_ATTENTION, s, 4.0 * a.B * a.H * (double)(a.Tq0 + a.Tq1) * (double)(a.Tk0 + a.Tk1) * a.d);
     // The direct-to-LDS kernel needs 16-byte aligned Q/K/V rows (checked above).
     // Up to 256 keys: 8 waves of 16 queries with every key tile resident in
     // LDS (one load, no barriers in the key loop); longer sequences: 8 waves

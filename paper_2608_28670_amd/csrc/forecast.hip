@@ -162,7 +162,7 @@ int launch_forecast(const void* const* src, const float* w, int K, int64_t n, in
     a.out = out;
     a.n = n;
     int rc;
-    prof_begin(PROF_FORECAST, s);
+    prof_begin(PROF_FORECAST, s, (double)n * (K * dtype_size(in_dt) + dtype_size(out_dt)));
     if (in_dt == BC_BF16 && out_dt == BC_BF16) rc = run_forecast<bf16, bf16>(a, K, s);
     else if (in_dt == BC_BF16) rc = run_forecast<bf16, float>(a, K, s);
     else if (out_dt == BC_BF16) rc = run_forecast<float, bf16>(a, K, s);
@@ -199,10 +199,14 @@ static unsigned grid_for(int64_t items) {
 
 int launch_copy(const void* src, void* dst, int64_t bytes, hipStream_t s) {
     if (bytes <= 0) return BC_OK;
+    prof_begin(PROF_COPY, s, 2.0 * (double)bytes);
     if ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst) | (uintptr_t)bytes) % 16 == 0)
-        copy16_kernel<<<grid_for(bytes / 16), kThreads, 0, s>>>(static_cast<const uint4*>(src), static_cast<uint4*>(dst), bytes / 16);
+        launch_k(copy16_kernel, dim3(grid_for(bytes / 16)), dim3(kThreads), s, static_cast<const uint4*>(src),
+                 static_cast<uint4*>(dst), bytes / 16);
     else
-        copy1_kernel<<<grid_for(bytes), kThreads, 0, s>>>(static_cast<const uint8_t*>(src), static_cast<uint8_t*>(dst), bytes);
+        launch_k(copy1_kernel, dim3(grid_for(bytes)), dim3(kThreads), s, static_cast<const uint8_t*>(src),
+                 static_cast<uint8_t*>(dst), bytes);
+    prof_end(PROF_COPY, s);
     return check_launch("copy");
 }
 

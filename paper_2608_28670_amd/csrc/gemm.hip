@@ -928,7 +928,7 @@ int launch_gemm_grouped(int dtype, const GemmArgs& g0, const GemmSeg& sg, int ns
     if (dma) {
         for (int i = 0; i < nseg; ++i)
             if (reinterpret_cast<uintptr_t>(sg.W[i]) % 16) return fail(BC_ERR_UNSUPPORTED, "misaligned segment weight");
-        prof_begin(PROF_GEMM_BIAS, s);
+        prof_begin(PROF_GEMM_BIAS, s, 2.0 * g.M * (double)g.N * g.K);
         const unsigned tiles = (unsigned)(((g.M + 127) / 128) * (g.N / 128));
         launch_k(gemm_dma_seg_kernel<BC_EPI_BIAS, 128, 128, 4, 2, 2>, dim3(tiles), dim3(512), s, g, sg);
         prof_end(PROF_GEMM_BIAS, s);
@@ -957,7 +957,7 @@ int launch_gemm(int dtype, int epi, const GemmArgs& g, hipStream_t s) {
         return fail(BC_ERR_UNSUPPORTED, "GEMM operands must be 16-byte aligned");
     const int cls = epi == BC_EPI_GATE_RES ? (g.K > g.N ? PROF_GEMM_DOWN : PROF_GEMM_GATE)
                     : g.e.gelu_from < g.N ? PROF_GEMM_GELU : PROF_GEMM_BIAS;
-    prof_begin(cls, s);
+    prof_begin(cls, s, 2.0 * g.M * (double)g.N * g.K);
     int rc;
     if (dtype == BC_BF16) {
         rc = epi == BC_EPI_GATE_RES ? run_gemm<bf16, BC_EPI_GATE_RES>(g, s) : run_gemm<bf16, BC_EPI_BIAS>(g, s);

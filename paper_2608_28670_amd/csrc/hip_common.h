@@ -67,8 +67,11 @@ int check_launch(const char* what);
 
 // Kernel classes timed by bc_profile_*; see bc.h.
 enum ProfClass { PROF_FORECAST = 0, PROF_GEMM_GELU = 1, PROF_GEMM_GATE = 2, PROF_GEMM_BIAS = 3,
-                 PROF_ATTENTION = 4, PROF_LAYERNORM = 5, PROF_GEMM_DOWN = 6, PROF_NCLASS = 7 };
-void prof_begin(int cls, hipStream_t s);
+                 PROF_ATTENTION = 4, PROF_LAYERNORM = 5, PROF_GEMM_DOWN = 6, PROF_COPY = 7, PROF_NCLASS = 8 };
+// Open a timed bracket of class `cls`; `work` is the bracket's algorithmic
+// work (FLOPs for GEMMs and attention, bytes moved for the memory-bound
+// classes), recorded with the first launch inside it.
+void prof_begin(int cls, hipStream_t s, double work = 0.0);
 void prof_end(int cls, hipStream_t s);
 // Next start/stop event pair of the class bracketed by prof_begin/prof_end on
 // this thread, if that class is being timed.

@@ -588,17 +588,22 @@ int bc_sample_adaptive_workspace_size(const bc_model* m, int B, int S, size_t* b
 
 // Pinned host memory for the adaptive schedule's per-step read-back of two
 // doubles (a copy into pageable memory costs tens of microseconds more per
-// step).  One buffer per host thread, allocated on first use and kept until
-// the process ends.
-static double* readback_buffer() {
-    thread_local double* buf = nullptr;
-    if (!buf) {
-        void* p = nullptr;
-        if (hipHostMalloc(&p, 256, hipHostMallocDefault) != hipSuccess) return nullptr;
-        buf = static_cast<double*>(p);
+// step).  Allocated on the run's first read-back and freed when the run
+// returns, so the library holds no host memory between calls.
+struct PinnedReadback {
+    double* buf = nullptr;
+    double* get() {
+        if (!buf) {
+            void* p = nullptr;
+            if (hipHostMalloc(&p, 256, hipHostMallocDefault) != hipSuccess) return nullptr;
+            buf = static_cast<double*>(p);
+        }
+        return buf;
     }
-    return buf;
-}
+    ~PinnedReadback() {
+        if (buf) (void)hipHostFree(buf);
+    }
+};
 
 // Blockwise mode: the module sites' ring storage, [site][slot][B*T*D].
 struct BlockwiseIO {
@@ -816,6 +821,7 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
 
     int full_index = 0;
     double acc = 0.0;   // adaptive: changes summed since the last full step
+    PinnedReadback readback;
     for (int k = 0; k < S; ++k) {
         if (ad) {
             // Probe at this step's latent: the embedding (which a full step
@@ -829,7 +835,7 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
                 BC_TRY(launch_copy(w.bb.h, w.probe, n * (int64_t)esz, s));
             } else {
                 BC_TRY(launch_rel_l1(dt, w.bb.h, w.probe, n, w.part, w.sums, s));
-                double* sums = readback_buffer();
+                double* sums = readback.get();
                 if (!sums) return fail(BC_ERR_HIP, "adaptive change readback: no pinned host buffer");
                 hipError_t e = hipMemcpyAsync(sums, w.sums, 2 * sizeof(double), hipMemcpyDeviceToHost, s);
                 if (e == hipSuccess) e = hipStreamSynchronize(s);

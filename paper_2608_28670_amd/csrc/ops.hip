@@ -151,7 +151,7 @@ int launch_ln_mod(int in_dt, const void* x, int64_t rows, int D, const float* sh
     if (rows <= 0) return BC_OK;
     if (D % 4 || ld_mod % 4 || (reinterpret_cast<uintptr_t>(shift) | reinterpret_cast<uintptr_t>(scale)) % 16)
         return fail(BC_ERR_UNSUPPORTED, "LayerNorm needs D and the modulation rows in 16-byte units");
-    prof_begin(PROF_LAYERNORM, s);
+    prof_begin(PROF_LAYERNORM, s, (double)rows * D * (dtype_size(in_dt) + dtype_size(out_dt)));
     int rc;
     if (in_dt == BC_F32 && out_dt == BC_BF16) rc = run_ln<float, bf16>(x, rows, D, shift, scale, ld_mod, rows_per_sample, h, s);
     else if (in_dt == BC_F32) rc = run_ln<float, float>(x, rows, D, shift, scale, ld_mod, rows_per_sample, h, s);

@@ -14,6 +14,7 @@ struct ClassTimer {
     bool on = false;
     int used = 0;
     std::vector<hipEvent_t> start, stop;
+    std::vector<double> work;
 };
 ClassTimer g_timer[PROF_NCLASS];
 
@@ -22,14 +23,19 @@ void release(ClassTimer& t) {
     for (hipEvent_t e : t.stop) (void)hipEventDestroy(e);
     t.start.clear();
     t.stop.clear();
+    t.work.clear();
     t.on = false;
     t.used = 0;
 }
 }  // namespace
 
 thread_local int g_pending = -1;   // class of the open bracket on this thread, -1 if none
+thread_local double g_pending_work = 0.0;   // its work, until the first launch takes it
 
-void prof_begin(int cls, hipStream_t) { g_pending = g_timer[cls].on ? cls : -1; }
+void prof_begin(int cls, hipStream_t, double work) {
+    g_pending = g_timer[cls].on ? cls : -1;
+    g_pending_work = work;
+}
 
 void prof_end(int, hipStream_t) { g_pending = -1; }
 
@@ -45,6 +51,8 @@ bool prof_take(hipEvent_t* start, hipEvent_t* stop) {
     if (!t.on || t.used >= (int)t.start.size()) return false;
     *start = t.start[t.used];
     *stop = t.stop[t.used];
+    t.work[t.used] = g_pending_work;
+    g_pending_work = 0.0;
     ++t.used;
     return true;
 }
@@ -63,6 +71,7 @@ int bc_profile_enable(int kernel_class, int max_launches) {
     release(t);
     t.start.resize(max_launches);
     t.stop.resize(max_launches);
+    t.work.assign(max_launches, 0.0);
     for (int i = 0; i < max_launches; ++i) {
         if (hipEventCreate(&t.start[i]) != hipSuccess || hipEventCreate(&t.stop[i]) != hipSuccess) {
             t.start.resize(i);
@@ -75,7 +84,7 @@ int bc_profile_enable(int kernel_class, int max_launches) {
     return BC_OK;
 }
 
-int bc_profile_times(int kernel_class, float* ms_out, int max_out, int* launches) {
+int bc_profile_records(int kernel_class, float* ms_out, double* work_out, int max_out, int* launches) {
     clear_error();
     if (kernel_class < 0 || kernel_class >= PROF_NCLASS) return fail(BC_ERR_INVALID_ARG, "class %d", kernel_class);
     if (!ms_out || max_out < 0) return fail(BC_ERR_INVALID_ARG, "ms_out");
@@ -84,10 +93,15 @@ int bc_profile_times(int kernel_class, float* ms_out, int max_out, int* launches
     for (int i = 0; i < n; ++i) {
         if (hipEventSynchronize(t.stop[i]) != hipSuccess) { release(t); return fail(BC_ERR_HIP, "event sync"); }
         if (hipEventElapsedTime(&ms_out[i], t.start[i], t.stop[i]) != hipSuccess) { release(t); return fail(BC_ERR_HIP, "elapsed"); }
+        if (work_out) work_out[i] = t.work[i];
     }
     if (launches) *launches = n;
     release(t);
     return BC_OK;
+}
+
+int bc_profile_times(int kernel_class, float* ms_out, int max_out, int* launches) {
+    return bc_profile_records(kernel_class, ms_out, nullptr, max_out, launches);
 }
 
 int bc_profile_collect(int kernel_class, double* total_ms, int* launches) {

@@ -11,6 +11,7 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line("markers", "slow: long-running CPU oracle case")
+    config.addinivalue_line("markers", "fullsize: GPU parity at a workload's full size (minutes of host work)")
 
 
 def pytest_collection_modifyitems(config, items):
@@ -20,10 +21,12 @@ def pytest_collection_modifyitems(config, items):
 
 
 def ensure_built():
-    """Build the library if nothing is built yet (the driver builds first)."""
-    from paper_2608_28670_amd import LIB_PATH
-    if not os.path.exists(LIB_PATH):
+    """Build the library if nothing is built, or if what is built does not
+    match the sources in this tree (bc_build_id against the source hash)."""
+    import paper_2608_28670_amd as bc
+    if not bc.is_current():
         from paper_2608_28670_amd import build
+        print(f"libbarycache.so is missing or stale (build id {bc.built_id()}); rebuilding", file=sys.stderr)
         build.build()
 
 

@@ -107,35 +107,6 @@ def test_empty_forecast_and_invalid_args(bclib):
         bclib.bary_extrapolate(ring, [float("nan")], torch.empty(16, device=DEV))
 
 
-@pytest.mark.parametrize("K,dt", [(3, "bf16"), (5, "f32")])
-def test_forecast_full_size_sampled(bclib, K, dt):
-    """The microbenchmark shape [8, 16384, 3072] in the bench's launch
-    configuration, checked on 20000 sampled elements."""
-    shape = synth.FORECAST_SHAPE
-    feats = synth.forecast_features(K, shape, dtype=dt)
-    s, t = synth.forecast_times(K)
-    w = bary.bary_weights(s, t)
-    n = int(np.prod(shape))
-    storage = torch.empty((K, n), dtype=TDT[dt], device=DEV)
-    for j in range(K):
-        storage[j].copy_(torch.from_numpy(feats[j].reshape(n)).to(TDT[dt]))
-    ring = bclib.CacheRing(K, storage)
-    for j in reversed(range(K)):
-        idx = ring.next_slot()
-        assert idx == storage[(K - 1 - j) % K].data_ptr()
-        ring.push(None, s[j])
-    # node j lives in slot K-1-j: storage row K-1-j was filled with feats[K-1-j]
-    out = torch.empty(n, dtype=TDT[dt], device=DEV)
-    bclib.bary_extrapolate(ring, w, out)
-    torch.cuda.synchronize()
-    idx = np.random.default_rng(0).integers(0, n, 20000)
-    idx = np.concatenate([idx, [0, n - 1]])
-    flat = feats.reshape(K, n)
-    nodes = [flat[K - 1 - j, idx].astype(np.float64) for j in range(K)]
-    exact, scale = _exact(nodes, w)
-    check(out[torch.from_numpy(idx).to(DEV)].float().cpu().numpy(), exact, scale, dt)
-
-
 def test_profile_times_per_launch(bclib):
     """Per-launch HIP-event durations of a kernel class, in launch order; the
     pool caps the count and collecting disables the class."""

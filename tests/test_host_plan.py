@@ -127,3 +127,23 @@ def test_schedule_rejects_bad_shift(bclib):
         with pytest.raises(bclib.BCError) as e:
             bclib.make_schedule("euler", 10, shift)
         assert e.value.code == bclib.ERR_INVALID_ARG
+
+
+def test_host_logic_under_address_and_ub_sanitizers(tmp_path):
+    """The host plan library (plan.cpp: weights, mask, plan, schedules) built
+    with -fsanitize=address,undefined and driven by random and adversarial
+    arguments (tests/native/plan_fuzz.cpp); any memory or undefined-behaviour
+    error aborts the run."""
+    exe = tmp_path / "plan_fuzz"
+    csrc = os.path.join(ROOT, "paper_2608_28670_amd", "csrc")
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+           "-fno-sanitize-recover=undefined", "-I", csrc, "-I", os.path.join(ROOT, "include"),
+           os.path.join(ROOT, "tests", "native", "plan_fuzz.cpp"), os.path.join(csrc, "plan.cpp"), "-o", str(exe)]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1:abort_on_error=0", UBSAN_OPTIONS="print_stacktrace=1")
+    env.pop("LD_PRELOAD", None)
+    r = subprocess.run([str(exe)], capture_output=True, text=True, env=env, timeout=300)
+    print(r.stdout)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "failures 0" in r.stdout

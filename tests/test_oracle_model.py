@@ -338,3 +338,39 @@ def test_cfg_caches_both_halves():
     osm.sample(M, synth.latents(cfg).astype(np.float64), bary.make_mask(6, 3), cfg.K,
                labels=np.array([0, 5]), cfg_scale=1.5, trace=tr)
     assert tr["feat"][1].shape[0] == 4 and tr["out"][1].shape[0] == 2
+
+
+# ---------------------------------------------------------------------------
+# outputs at sampled query rows (used for full-size parity)
+# ---------------------------------------------------------------------------
+
+def test_block_rows_equal_rows_of_the_full_output():
+    """`rows=` computes the same outputs as the whole block at those rows."""
+    cfg = tiny()
+    M = om.Model(cfg, synth.params(cfg))
+    x = np.random.default_rng(12).normal(size=(2, cfg.tokens, cfg.hidden))
+    mod = M.block_mod(0, M.condition(321.0, 2))
+    rows = [0, 5, 17, cfg.tokens - 1]
+    np.testing.assert_allclose(M.dit_block(0, x, mod, rows=rows), M.dit_block(0, x, mod)[:, rows],
+                               rtol=1e-12, atol=1e-14)
+    pc = synth.scaled(synth.CONFIGS["pixart"], depth=1, hidden=64, heads=2, head_dim=32, mlp=128,
+                      latent=(4, 8, 8), batch=2, ctx_tokens=5, ctx_dim=16)
+    Mp = om.Model(pc, synth.params(pc))
+    ctx = Mp.context(synth.text(pc))
+    xp = np.random.default_rng(13).normal(size=(2, pc.tokens, pc.hidden))
+    cond = Mp.condition(40.0, 2)
+    np.testing.assert_allclose(Mp.dit_block(0, xp, Mp.block_mod(0, cond), ctx, rows=[3, 9]),
+                               Mp.dit_block(0, xp, Mp.block_mod(0, cond), ctx)[:, [3, 9]], rtol=1e-12, atol=1e-14)
+    hc = synth.scaled(synth.CONFIGS["hunyuan"], depth=1, depth_single=1, hidden=64, heads=2, head_dim=32,
+                      mlp=128, latent=(16, 2, 4, 6), txt_tokens=3)
+    Mh = om.Model(hc, synth.params(hc))
+    g = np.random.default_rng(14)
+    xi, xt = g.normal(size=(2, hc.tokens, 64)), g.normal(size=(2, 3, 64))
+    c = {"c": g.normal(size=(2, 64))}
+    fi, ft = Mh.dual_block(0, xi, xt, c)
+    ri, rt = Mh.dual_block(0, xi, xt, c, rows=([1, 11], [0, 2]))
+    np.testing.assert_allclose(ri, fi[:, [1, 11]], rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(rt, ft[:, [0, 2]], rtol=1e-12, atol=1e-14)
+    z = np.concatenate([xi, xt], axis=1)
+    np.testing.assert_allclose(Mh.single_block(0, z, c, hc.tokens, rows=[0, 7, hc.tokens + 1]),
+                               Mh.single_block(0, z, c, hc.tokens)[:, [0, 7, hc.tokens + 1]], rtol=1e-12, atol=1e-14)
