@@ -253,6 +253,21 @@ int bc_dit_block_forward(const bc_block_desc* d, const bc_block_weights* w,
                          float* x, float* x_txt, const float* c, const void* ctx,
                          void* ws, size_t ws_bytes, void* stream);
 
+/* bc_dit_block_forward for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the workspace is a device array of bc_noalloc_scratch_bytes()
+ * bytes (96 MiB) inside the library, one per GPU, held from the library's load
+ * until the process ends; the call allocates nothing.  The caller still owns
+ * x, x_txt, c, ctx and the weights; arguments as bc_dit_block_forward.  Calls
+ * on one GPU share that array and leave their intermediates in it: calls that
+ * overlap on one GPU (other streams or host threads) race, so serialise them.
+ * Errors: as bc_dit_block_forward; INVALID_ARG when the shape needs more
+ * workspace than the array holds (bc_block_workspace_size > the limit), before
+ * anything is enqueued; HIP if the array's device address cannot be found. */
+int bc_dit_block_forward_noalloc(const bc_block_desc* d, const bc_block_weights* w,
+                                 float* x, float* x_txt, const float* c, const void* ctx, void* stream);
+size_t bc_noalloc_scratch_bytes(void);
+
 /* ------------------------------------------------------------------------ */
 /* Whole model and the sampling loop (Sec. 3.3)                              */
 /* ------------------------------------------------------------------------ */

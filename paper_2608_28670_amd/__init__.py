@@ -112,6 +112,9 @@ _SIGS = {
     "bc_dit_block_forward": (C.c_int, [C.POINTER(BlockDesc), C.POINTER(BlockWeights), C.c_void_p,
                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
                                        C.c_void_p]),
+    "bc_dit_block_forward_noalloc": (C.c_int, [C.POINTER(BlockDesc), C.POINTER(BlockWeights), C.c_void_p,
+                                               C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]),
+    "bc_noalloc_scratch_bytes": (C.c_size_t, []),
     "bc_model_create": (C.c_int, [C.POINTER(ModelDesc), C.POINTER(ModelWeights), C.POINTER(C.c_void_p)]),
     "bc_model_destroy": (C.c_int, [C.c_void_p]),
     "bc_make_schedule": (C.c_int, [C.c_int, C.c_int, C.c_void_p, C.c_void_p]),
@@ -393,6 +396,17 @@ def dit_block_forward(desc: BlockDesc, w: BlockWeights, x, c, ws, x_txt=None, ct
     _check(lib().bc_dit_block_forward(C.byref(desc), C.byref(w), dev_ptr(x), dev_ptr(x_txt), dev_ptr(c),
                                       dev_ptr(ctx), dev_ptr(ws), ws.numel() * ws.element_size(),
                                       stream_handle(stream)))
+
+
+def dit_block_forward_noalloc(desc: BlockDesc, w: BlockWeights, x, c, x_txt=None, ctx=None, stream=None):
+    """bc_dit_block_forward with the library's own static workspace (no
+    allocation; calls on one GPU share it and must not overlap)."""
+    _check(lib().bc_dit_block_forward_noalloc(C.byref(desc), C.byref(w), dev_ptr(x), dev_ptr(x_txt), dev_ptr(c),
+                                              dev_ptr(ctx), stream_handle(stream)))
+
+
+def noalloc_scratch_bytes() -> int:
+    return int(lib().bc_noalloc_scratch_bytes())
 
 
 # ---------------------------------------------------------------------------

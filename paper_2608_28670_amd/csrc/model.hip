@@ -9,6 +9,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -507,6 +508,66 @@ int bc_dit_block_forward(const bc_block_desc* dp, const bc_block_weights* wp, fl
     if (d.kind == BC_BLOCK_SINGLE) return single_block(d, w, x, mod, 3 * D, bb, nullptr, s);
     BC_TRY(launch_skinny(d.dtype, skinny1(w.txt.w_mod, w.txt.b_mod, 6 * D, D, d.B, c, mod_t, 1, 0), s));
     return dual_block(d, w, x, x_txt, mod, mod_t, 6 * D, bb, s);
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Allocation-free block forward: the workspace of bc_dit_block_forward is a
+// file-scope device array, so the call needs no allocation by the library or
+// the caller.  Each GPU the library runs on holds its own copy of the array
+// (kNoAllocScratchBytes) from module load until the process ends.  Host code
+// never passes the array's name to a kernel (on the host it only stands in for
+// the symbol): its device address is looked up once per device with
+// hipGetSymbolAddress and kept.
+// ---------------------------------------------------------------------------
+namespace bc {
+
+constexpr size_t kNoAllocScratchBytes = size_t(96) << 20;
+constexpr int kNoAllocMaxDevices = 64;
+
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kNoAllocMaxDevices];
+
+// Device address of `scratch` on the current device (looked up on the first
+// call on that device).
+static int scratch_address(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(BC_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kNoAllocMaxDevices) return fail(BC_ERR_UNSUPPORTED, "device %d", dev);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(BC_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return BC_OK;
+}
+
+}  // namespace bc
+
+extern "C" {
+
+size_t bc_noalloc_scratch_bytes(void) { return kNoAllocScratchBytes; }
+
+int bc_dit_block_forward_noalloc(const bc_block_desc* dp, const bc_block_weights* wp, float* x, float* x_txt,
+                                 const float* c, const void* ctx, void* stream) {
+    clear_error();
+    if (!dp) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
+    BC_TRY(check_block_desc(*dp));
+    const size_t need = block_ws(*dp, nullptr, nullptr, nullptr, nullptr, nullptr);
+    if (need > kNoAllocScratchBytes)
+        return fail(BC_ERR_INVALID_ARG, "this block needs %zu bytes of workspace; the allocation-free entry point "
+                    "holds %zu", need, kNoAllocScratchBytes);
+    void* ws = nullptr;
+    BC_TRY(scratch_address(&ws));
+    return bc_dit_block_forward(dp, wp, x, x_txt, c, ctx, ws, kNoAllocScratchBytes, stream);
 }
 
 int bc_model_create(const bc_model_desc* dp, const bc_model_weights* wp, bc_model** out) {

@@ -24,7 +24,7 @@ def _lib_params(bc, p: bary.Params):
 
 def test_header_symbols_are_exported(bclib):
     hdr = open(os.path.join(ROOT, "include", "bc.h")).read()
-    declared = set(re.findall(r"^\s*(?:int|void|const char\*)\s+(bc_\w+)\s*\(", hdr, re.M))
+    declared = set(re.findall(r"^\s*(?:int|void|size_t|const char\*)\s+(bc_\w+)\s*\(", hdr, re.M))
     assert len(declared) >= 20
     out = subprocess.run(["nm", "-D", "--defined-only", bclib.LIB_PATH], capture_output=True, text=True).stdout
     exported = set(re.findall(r"\bT (bc_\w+)$", out, re.M))
