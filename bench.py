@@ -1,23 +1,36 @@
 """Benchmark of the BaryCache hot path on one MI355X.
 
 One step = one BaryCache sampling run of the whole batch through the full
-schedule (every full step runs the block stack, every other step the K-way
-forecast; all steps run the final layer and the sampler update), starting
-from resident noise.  Default workload: the DiT-XL/2-shaped class-conditional
-model (28 blocks, D 1152, 16 x 72 heads, MLP 4608, 256 tokens), batch 16,
-50 DDIM steps, K = 3, one full step every 4 (14 of 50), bf16, random-init
-weights drawn from seed 2026.
+schedule (every full step runs the block stack and its last block writes the
+stepwise feature into the ring; every other step forecasts it from the ring
+with Eq. 13; all steps run the final layer and the sampler update), with the
+noise, the weights and the conditioning inputs already resident in HBM.
 
-Prints one JSON line: samples/s, the roofline of the dominant kernel (of the
-fc2, fc1 and self-attention kernels, the one with the most time per run, each
-timed with HIP events on its launch stream; the others follow), the forecast
-kernel's HBM bandwidth on [8, 16384, 3072] features, the speedup over the
-all-full mask, and the oracle's CPU throughput on a bounded sample.
+Headline workload (the largest single-GPU configuration): the HunyuanVideo-
+shaped text-to-video model, 20 dual-stream + 40 single-stream blocks, hidden
+3072, 24 heads of 128, MLP 12288, QK RMSNorm and 3D RoPE, 14 310 video tokens
+(16 x 9 x 60 x 106 latent, patch 2) + 256 text tokens, batch 1, 50 Euler steps
+with time shift 7, K = 3, a full step every 5 (11 of 50), bf16, random-init
+weights from seed 2026.
+
+The JSON line also carries, measured in the same process:
+  * `roofline`: the dominant kernel of the headline run (the kernel and shape
+    with the most time per run, from per-launch HIP events on its launch
+    stream), its algorithmic FLOPs per launch over its average duration;
+  * `kernel_classes`: every kernel class's time per run and its average rate;
+  * `workloads`: the DiT-XL/2-shaped (batch 16, DDIM-50) and PixArt-shaped
+    (batch 4, DPM-Solver++(2M)-20) workloads measured the same way with
+    fewer runs, each with its own roofline;
+  * `forecast`: the forecast kernel on [8, 16384, 3072] features for every
+    K in {2, 3, 4, 5}, bf16 and fp32, and the ring push's copy path;
+  * `cpu_baseline`: the oracle on the host cores, composed from timed pieces
+    (see cpu_baseline_video).
 """
 import argparse
 import hashlib
 import json
 import os
+import platform
 import sys
 import time
 
@@ -26,6 +39,13 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
+PAPER_CONTEXT = ("The paper reports end-to-end speedups of up to 3.30x over 50-step DDIM (PixArt-Sigma 1024x1024, "
+                 "batch 4, interval N = 6, on an RTX 5090, precision not stated; Table 1, Sec. 4.1); 2.18x on "
+                 "DiT-XL/2 (N = 6, RTX 5090; Table 3) and 3.02x on HunyuanVideo (N = 7, A800; Table 2). "
+                 "Context only: other hardware, trained weights, other schedules.")
+
+CLASS_NAMES = ["forecast", "gemm_gelu", "gemm_gated", "gemm_bias", "attention", "layernorm", "gemm_down", "copy"]
+MFMA_CLASSES = {"gemm_gelu", "gemm_gated", "gemm_bias", "attention", "gemm_down"}
 
 
 def parse():
@@ -33,17 +53,17 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="dit_xl2")
+    ap.add_argument("--workload", default="hunyuan", help="headline workload (hunyuan, pixart, dit_xl2, tiny)")
+    ap.add_argument("--legs", default="dit_xl2,pixart",
+                    help="other workloads measured in the same line (comma list; empty: none)")
+    ap.add_argument("--leg-steps", type=int, default=3, help="timed runs of each other workload")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-forecast", action="store_true")
-    ap.add_argument("--no-graph", action="store_true", help="skip timing the HIP-graph replay of the run")
-    ap.add_argument("--no-blockwise", action="store_true", help="skip timing the blockwise-mode run")
-    ap.add_argument("--adaptive-ell", type=float, default=0.13,
-                    help="threshold of the timed adaptive-schedule run (negative: skip it)")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the graph-replay, adaptive and blockwise runs of the DiT-XL/2 leg")
+    ap.add_argument("--adaptive-ell", type=float, default=0.13, help="threshold of the adaptive-schedule run")
     ap.add_argument("--kernels-only", action="store_true",
-                    help="only launch the roofline kernels (fc2, fc1, self-attention of the workload's block, the "
-                         "K = 3 forecast) a few times each through the C ABI, for hardware-counter passes")
-    ap.add_argument("--cpu-steps", type=int, default=9, help="oracle sample: first N steps of one sample")
+                    help="launch only the roofline kernels at the workloads' shapes, for hardware-counter passes")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run one 1 GiB device copy through the library (counter calibration)")
     return ap.parse_args()
@@ -57,10 +77,16 @@ def source_hash(*names):
     return h.hexdigest()[:16]
 
 
-def counters_traffic(kernel_tag, src_hash, launches_bytes_ref):
-    """HBM bytes per launch from committed rocprofv3 counter summaries, or None
-    if none exist for the current kernel source."""
-    path = os.path.join(ROOT, "profiles", f"{kernel_tag}_counters.json")
+KERNEL_SOURCES = {"attention": ("attention.hip", "attention.h", "hip_common.h"),
+                  "gemm": ("gemm.hip", "gemm.h", "hip_common.h"),
+                  "forecast": ("forecast.hip", "hip_common.h")}
+
+
+def counters_traffic(tag, src_hash):
+    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated) from the
+    committed rocprofv3 counter summary of this kernel and shape, or None if
+    there is none for the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{tag}_counters.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -70,40 +96,106 @@ def counters_traffic(kernel_tag, src_hash, launches_bytes_ref):
     return c.get("hbm_bytes_per_launch")
 
 
-def forecast_bench(bc, torch, dev, K=3, dtype="bf16", iters=10):
-    """HBM bandwidth of the forecast kernel on K cached [8, 16384, 3072] features."""
-    import synth
-    shape = synth.FORECAST_SHAPE
-    n = shape[0] * shape[1] * shape[2]
-    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
-    g = torch.Generator(device=dev)
-    g.manual_seed(synth.SEED + K)
-    storage = torch.empty((K, n), dtype=tdt, device=dev)
-    for j in range(K):
-        storage[j].normal_(generator=g)
-    ring = bc.CacheRing(K, storage)
-    s, t = synth.forecast_times(K)
-    for j in reversed(range(K)):
-        ring.push(None, float(s[j]))
-    w = bc.bary_weights(s, t)
-    out = torch.empty(n, dtype=tdt, device=dev)
-    for _ in range(2):
-        bc.bary_extrapolate(ring, w, out)
-    torch.cuda.synchronize()
-    bc.profile_enable(bc.PROF_FORECAST, iters)
-    for _ in range(iters):
-        bc.bary_extrapolate(ring, w, out)
-    ms, cnt = bc.profile_collect(bc.PROF_FORECAST)
-    esz = 2 if dtype == "bf16" else 4
-    bytes_alg = (K + 1) * n * esz
-    avg_s = ms / cnt / 1e3
-    gbs = bytes_alg / avg_s / 1e9
-    del storage, out
-    torch.cuda.empty_cache()
-    return {"K": K, "dtype": dtype, "shape": list(shape), "bytes_per_launch": bytes_alg,
-            "avg_us": round(avg_s * 1e6, 2), "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
-            "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
+def ensure_library():
+    import paper_2608_28670_amd as bc
+    if not bc.is_current():
+        from paper_2608_28670_amd import build
+        print("libbarycache.so is missing or stale; rebuilding", file=sys.stderr)
+        build.build()
+    return bc
 
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------------------
+# kernel shapes of a workload (to name the launches the profiler records)
+# ---------------------------------------------------------------------------
+
+def kernel_shapes(cfg):
+    """(class, name, shape, work) of every block kernel of one full step; work
+    = algorithmic FLOPs per launch, which with the class identifies a launch."""
+    B, D, F, T = cfg.batch, cfg.hidden, cfg.mlp, cfg.tokens
+    H, hd = cfg.heads, cfg.head_dim
+    out = []
+
+    def gemm(cls, name, M, N, K):
+        out.append((cls, name, [M, N, K], 2.0 * M * N * K))
+
+    def att(name, Tq, Tk):
+        out.append(("attention", name, [B, H, Tq, Tk, hd], 4.0 * B * H * Tq * Tk * hd))
+
+    if cfg.kind in ("dit", "pixart"):
+        M = B * T
+        gemm("gemm_bias", "QKV projection", M, 3 * D, D)
+        gemm("gemm_gated", "attention output projection + gated residual", M, D, D)
+        gemm("gemm_gelu", "MLP up projection + GELU", M, F, D)
+        gemm("gemm_down", "MLP down projection + gated residual", M, D, F)
+        att("self-attention", T, T)
+        if cfg.kind == "pixart":
+            gemm("gemm_bias", "cross-attention query projection", M, D, D)
+            gemm("gemm_bias", "cross-attention output projection", M, D, D)
+            att("cross-attention", T, cfg.ctx_tokens)
+    else:
+        Tt = cfg.txt_tokens
+        for s, M in (("image", B * T), ("text", B * Tt)):
+            gemm("gemm_bias", f"dual-stream {s} QKV projection", M, 3 * D, D)
+            gemm("gemm_gated", f"dual-stream {s} output projection + gated residual", M, D, D)
+            gemm("gemm_gelu", f"dual-stream {s} MLP up projection + GELU", M, F, D)
+            gemm("gemm_down", f"dual-stream {s} MLP down projection + gated residual", M, D, F)
+        L = T + Tt
+        gemm("gemm_gelu", "single-stream [qkv | mlp] projection + GELU", B * L, 3 * D + F, D)
+        gemm("gemm_down", "single-stream output projection + gated residual", B * L, D, D + F)
+        att("joint attention (dual- and single-stream)", L, L)
+    return out
+
+
+def group_launches(records, cfg):
+    """Per (class, work) group: launches, time; named from kernel_shapes."""
+    import numpy as np
+    names = {(c, w): (n, s) for c, n, s, w in kernel_shapes(cfg)}
+    groups = []
+    for cls, (ms, work) in records.items():
+        if not len(ms):
+            continue
+        for wv in np.unique(work[work > 0]):
+            sel = work == wv
+            t = ms[sel].astype(np.float64)
+            nm = names.get((cls, float(wv)))
+            groups.append({"class": cls, "kernel": nm[0] if nm else None, "shape": nm[1] if nm else None,
+                           "work": float(wv), "launches": int(sel.sum()), "ms_per_run": float(t.sum()),
+                           "avg_us": float(t.mean()) * 1e3})
+    groups.sort(key=lambda g: -g["ms_per_run"])
+    return groups
+
+
+def roofline_of(g, tag=None, src=None):
+    avg_s = g["avg_us"] / 1e6
+    achieved = g["work"] / avg_s / 1e12
+    r = {"bound": "mfma", "kernel": g["kernel"], "class": g["class"], "shape": g["shape"],
+         "flops_per_launch": g["work"], "avg_us": round(g["avg_us"], 2), "launches": g["launches"],
+         "ms_per_run": round(g["ms_per_run"], 3), "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+         "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4)}
+    if tag is not None:
+        h = source_hash(*KERNEL_SOURCES[src])
+        r["traffic"] = counters_traffic(tag, h)
+        r["source_hash"] = h
+    else:
+        r["traffic"] = None
+    return r
+
+
+def counter_tag(cfg, g):
+    if g["class"] == "attention":
+        return f"attention_{cfg.name}", "attention"
+    short = {"gemm_down": "fc2", "gemm_gelu": "fc1", "gemm_bias": "qkv", "gemm_gated": "proj"}[g["class"]]
+    return f"gemm_{short}_{cfg.name}", "gemm"
+
+
+# ---------------------------------------------------------------------------
+# one workload
+# ---------------------------------------------------------------------------
 
 def device_params(cfg, torch, dev):
     """Random-init weights drawn on the GPU (N(0, 1) * param_scale, seeded):
@@ -125,55 +217,384 @@ def device_params(cfg, torch, dev):
     return out
 
 
-def cpu_baseline(cfg, params, labels, xT, mask, nsteps):
-    """The oracle on the host cores, on one sample and the first `nsteps` steps
-    of the schedule; per-step times composed to the whole schedule."""
+def measure(bc, torch, cfg, steps, warmup, extras=False, adaptive_ell=0.13):
+    """Time `steps` sampling runs after `warmup` runs; one more run with every
+    kernel class timed per launch; the all-full mask at the same S."""
     import numpy as np
+
+    import synth
+    from paper_2608_28670_amd import loader
+    dev = "cuda:0"
+    t0 = time.time()
+    dm = loader.DeviceModel(cfg, None, dev_params=device_params(cfg, torch, dev))
+    B = cfg.batch
+    mask = bc.make_mask(cfg.steps, cfg.interval)
+    labels = synth.labels(cfg) if cfg.n_classes else None
+    text = synth.text(cfg) if cfg.kind != "dit" else None
+    x0 = torch.from_numpy(synth.latents(cfg)).to(dev)
+    x = torch.empty_like(x0)
+    tl = torch.from_numpy(labels).to(dev) if labels is not None else None
+    tt = torch.from_numpy(text).to(dev).to(loader.torch_dtype(cfg)) if text is not None else None
+    torch.cuda.synchronize()
+    log(f"[{cfg.name}] setup {time.time() - t0:.1f} s")
+
+    def run(m):
+        x.copy_(x0)
+        dm.sample(x, m, labels=tl, text=tt)
+
+    for _ in range(warmup):
+        run(mask)
+    torch.cuda.synchronize()
+    log(f"[{cfg.name}] {warmup} warm-up runs done; timing {steps}")
+    t_start = time.perf_counter()
+    for _ in range(steps):
+        run(mask)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    res = {"value": B * steps / elapsed, "ms_per_step": elapsed / steps * 1e3, "mask": mask}
+    log(f"[{cfg.name}] {res['value']:.4g} samples/s, {res['ms_per_step']:.1f} ms per run")
+
+    # Per-launch HIP events on the launch stream, in one more run.
+    cap = 1 << 16
+    for c in range(len(CLASS_NAMES)):
+        bc.profile_enable(c, cap)
+    run(mask)
+    records = {}
+    for c, name in enumerate(CLASS_NAMES):
+        ms, work = bc.profile_records(c, cap)
+        records[name] = (ms, work)
+    classes = {}
+    for name, (ms, work) in records.items():
+        if not len(ms):
+            continue
+        t = ms.astype(np.float64)
+        e = {"ms_per_run": round(float(t.sum()), 3), "launches": int(len(t)), "avg_us": round(float(t.mean()) * 1e3, 2)}
+        if name in MFMA_CLASSES and work.sum() > 0:
+            e["tflops"] = round(float(work.sum()) / (t.sum() / 1e3) / 1e12, 1)
+            e["frac_of_mfma_peak"] = round(e["tflops"] / PEAK_BF16_TFLOPS, 4)
+        elif work.sum() > 0:
+            e["gbs"] = round(float(work.sum()) / (t.sum() / 1e3) / 1e9, 1)
+            e["frac_of_hbm_peak"] = round(e["gbs"] / PEAK_HBM_GBS, 4)
+        classes[name] = e
+    groups = [g for g in group_launches(records, cfg) if g["class"] in MFMA_CLASSES]
+    top = groups[0]
+    tag, src = counter_tag(cfg, top)
+    res["roofline"] = roofline_of(top, tag, src)
+    res["roofline_others"] = [roofline_of(g) for g in groups[1:6]]
+    res["kernel_classes"] = classes
+    res["profiled_run_ms"] = round(float(sum(float(ms.sum()) for ms, _ in records.values())), 3)
+
+    if extras:
+        res.update(extra_runs(bc, torch, cfg, dm, run, mask, x, x0, tl, tt, steps, adaptive_ell))
+
+    # Speedup reference: every step full, same sampler (kernels already warm).
+    full = np.ones(cfg.steps, np.uint8)
+    nref = 1 if res["ms_per_step"] > 1000 else 2
+    if nref > 1:
+        run(full)
+    torch.cuda.synchronize()
+    tf = time.perf_counter()
+    for _ in range(nref):
+        run(full)
+    torch.cuda.synchronize()
+    ms_full = (time.perf_counter() - tf) / nref * 1e3
+    res["ms_all_full"] = ms_full
+    res["speedup_vs_all_full"] = ms_full / res["ms_per_step"]
+    res["ideal_speedup"] = cfg.steps / int(mask.sum())
+    log(f"[{cfg.name}] all-full mask {ms_full:.1f} ms per run: speedup {res['speedup_vs_all_full']:.3f}")
+    del dm, x, x0, tl, tt
+    torch.cuda.empty_cache()
+    return res
+
+
+def extra_runs(bc, torch, cfg, dm, run, mask, x, x0, tl, tt, steps, ell):
+    """HIP-graph replay, the adaptive schedule and blockwise mode on the same
+    workload, each timed like `value`."""
+    B = cfg.batch
+    out = {}
+    g = dm.sample_graph(x, mask, labels=tl, text=tt)
+    x.copy_(x0)
+    g.launch()
+    torch.cuda.synchronize()
+    tg = time.perf_counter()
+    for _ in range(steps):
+        x.copy_(x0)
+        g.launch()
+    torch.cuda.synchronize()
+    eg = time.perf_counter() - tg
+    out["graph_replay"] = {"value": round(B * steps / eg, 3), "ms_per_step": round(eg / steps * 1e3, 3)}
+    del g
+
+    def run_adaptive():
+        x.copy_(x0)
+        return dm.sample_adaptive(x, cfg.steps, ell, labels=tl, text=tt)
+    run_adaptive()
+    torch.cuda.synchronize()
+    ta = time.perf_counter()
+    for _ in range(steps):
+        _, amask, _ = run_adaptive()
+    torch.cuda.synchronize()
+    ea = time.perf_counter() - ta
+    run(amask)
+    torch.cuda.synchronize()
+    tfm = time.perf_counter()
+    for _ in range(steps):
+        run(amask)
+    torch.cuda.synchronize()
+    efm = time.perf_counter() - tfm
+    out["adaptive"] = {"ell": ell, "full_steps": int(amask.sum()), "value": round(B * steps / ea, 3),
+                       "ms_per_step": round(ea / steps * 1e3, 3),
+                       "ms_fixed_loop_same_mask": round(efm / steps * 1e3, 3),
+                       "mask": "".join(str(int(v)) for v in amask)}
+
+    if cfg.kind in ("dit", "pixart"):
+        def run_blockwise():
+            x.copy_(x0)
+            return dm.sample_blockwise(x, mask, labels=tl, text=tt)
+        sites = run_blockwise()
+        torch.cuda.synchronize()
+        tb = time.perf_counter()
+        for _ in range(steps):
+            sites = run_blockwise()
+        torch.cuda.synchronize()
+        eb = time.perf_counter() - tb
+        out["blockwise"] = {"value": round(B * steps / eb, 3), "ms_per_step": round(eb / steps * 1e3, 3),
+                            "sites": int(sites.shape[0]), "cache_bytes": int(sites.numel() * sites.element_size()),
+                            "stepwise_cache_bytes": int(cfg.K * B * cfg.tokens * cfg.hidden * sites.element_size())}
+        del sites
+        dm.release_blockwise()
+        torch.cuda.empty_cache()
+    return out
+
+
+def workload_desc(cfg, mask):
+    nfull = int(mask.sum())
+    blocks = (f"{cfg.depth} dual-stream + {cfg.depth_single} single-stream blocks" if cfg.kind == "mmdit"
+              else f"{cfg.depth} blocks")
+    extra = ""
+    if cfg.kind == "mmdit":
+        extra = f" + {cfg.txt_tokens} text tokens, QK RMSNorm + 3D RoPE, time shift {cfg.flow_shift:g}"
+    elif cfg.kind == "pixart":
+        extra = f", cross-attention to {cfg.ctx_tokens} text tokens of width {cfg.ctx_dim}"
+    return (f"{cfg.name}: {blocks}, D {cfg.hidden}, {cfg.heads}x{cfg.head_dim} heads, MLP {cfg.mlp}, "
+            f"{cfg.tokens} tokens{extra}, batch {cfg.batch}, {cfg.steps} {cfg.sampler} steps, K={cfg.K}, "
+            f"full every {cfg.interval} ({nfull}/{cfg.steps}), random-init weights")
+
+
+# ---------------------------------------------------------------------------
+# forecast microbenchmark and the push copy
+# ---------------------------------------------------------------------------
+
+def forecast_sweep(bc, torch, iters=5):
+    """Forecast kernel HBM bandwidth on K cached [8, 16384, 3072] features for
+    K in 2..5, bf16 and fp32 (algorithmic bytes (K + 1) n s per launch), and
+    the ring push's copy path on one bf16 feature (2 n s bytes)."""
+    import synth
+    dev = "cuda:0"
+    shape = synth.FORECAST_SHAPE
+    n = shape[0] * shape[1] * shape[2]
+    out = []
+    fc_hash = source_hash(*KERNEL_SOURCES["forecast"])
+    for dt in ("bf16", "f32"):
+        tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+        esz = 2 if dt == "bf16" else 4
+        g = torch.Generator(device=dev)
+        g.manual_seed(synth.SEED)
+        storage = torch.empty((5, n), dtype=tdt, device=dev)
+        for j in range(5):
+            storage[j].normal_(generator=g)
+        res = torch.empty(n, dtype=tdt, device=dev)
+        for K in (2, 3, 4, 5):
+            ring = bc.CacheRing(K, storage[:K])
+            s, t = synth.forecast_times(K)
+            for j in reversed(range(K)):
+                ring.push(None, float(s[j]))
+            w = bc.bary_weights(s, t)
+            bc.bary_extrapolate(ring, w, res)
+            torch.cuda.synchronize()
+            bc.profile_enable(bc.PROF_FORECAST, iters)
+            for _ in range(iters):
+                bc.bary_extrapolate(ring, w, res)
+            ms, work = bc.profile_records(bc.PROF_FORECAST, iters)
+            avg_s = float(ms.mean()) / 1e3
+            bytes_alg = (K + 1) * n * esz
+            assert abs(work[0] - bytes_alg) < 1
+            gbs = bytes_alg / avg_s / 1e9
+            out.append({"K": K, "dtype": dt, "shape": list(shape), "bytes_per_launch": bytes_alg,
+                        "avg_us": round(avg_s * 1e6, 2), "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                        "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                        "traffic": counters_traffic(f"forecast_k{K}_{dt}", fc_hash)})
+            del ring
+        del storage, res
+        torch.cuda.empty_cache()
+    # the push's copy path: one bf16 feature into the next ring slot
+    src = torch.empty(n, dtype=torch.bfloat16, device=dev).normal_()
+    store = torch.empty((3, n), dtype=torch.bfloat16, device=dev)
+    ring = bc.CacheRing(3, store)
+    ring.push(src, 0.0)
+    torch.cuda.synchronize()
+    bc.profile_enable(bc.PROF_COPY, iters)
+    for i in range(iters):
+        ring.push(src, float(i + 1))
+    ms, work = bc.profile_records(bc.PROF_COPY, iters)
+    avg_s = float(ms.mean()) / 1e3
+    gbs = 2 * n * 2 / avg_s / 1e9
+    push = {"shape": list(shape), "dtype": "bf16", "bytes_per_launch": 2 * n * 2, "avg_us": round(avg_s * 1e6, 2),
+            "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+            "note": "copy path of bc_cache_push; the sampling loop itself pushes with no copy (the last block's "
+                    "epilogue writes the ring slot)"}
+    del src, store, ring
+    torch.cuda.empty_cache()
+    return out, push
+
+
+# ---------------------------------------------------------------------------
+# the oracle on the host cores
+# ---------------------------------------------------------------------------
+
+def host_info():
+    import numpy as np
+    cpu = platform.processor() or "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = "unknown"
+    try:
+        cfgs = np.show_config(mode="dicts")
+        b = cfgs.get("Build Dependencies", {}).get("blas", {})
+        blas = f"{b.get('name', '?')} {b.get('version', '')}".strip()
+    except Exception:   # older numpy: no dict mode
+        pass
+    try:
+        from threadpoolctl import threadpool_info
+        pools = [f"{p.get('internal_api')} {p.get('version')} ({p.get('num_threads')} threads)"
+                 for p in threadpool_info() if p.get("user_api") == "blas"]
+        if pools:
+            blas = "; ".join(pools)
+    except Exception:
+        pass
+    return cpu, blas
+
+
+def cpu_baseline_video(cfg):
+    """The oracle (numpy, fp32 model as the video workload's tests run it)
+    timed in pieces on one sample at the full shape and composed to a whole
+    sampling run: one dual-stream block and one single-stream block on all
+    14 566 tokens, one forecast step (Eq. 13 over K = 3 features) and one final
+    layer + Euler update; a run is 11 x (20 dual + 40 single blocks) + 39
+    forecasts + 50 final layers and updates (the embedding and conditioning
+    are left out: they take well under 1 % of a block)."""
+    import numpy as np
+
+    import synth
     from oracle import bary, model as om, sampler as osm
-    M = om.Model(cfg, params)
-    x = xT[:1].astype(np.float64)
-    lab = labels[:1]
+    one = synth.scaled(cfg, depth=1, depth_single=1, batch=1)
+    names = [n for n, _ in synth.param_shapes(one)
+             if n.startswith(("dual.0.", "single.0.", "final_", "txt_", "t_"))]
+    P = synth.params(one, names=names)
+    M = om.Model(one, P, dtype=np.float32)
+    D, T, Tt = cfg.hidden, cfg.tokens, cfg.txt_tokens
+    x = synth.normal("cpu/x", (1, T, D))
+    xt = synth.normal("cpu/xt", (1, Tt, D))
+    c = {"c": synth.normal("cpu/c", (1, D), 0.5)}
+    t0 = time.perf_counter()
+    M.dual_block(0, x, xt, c)
+    t_dual = time.perf_counter() - t0
+    log(f"[cpu] oracle dual-stream block {t_dual:.1f} s")
+    t0 = time.perf_counter()
+    M.single_block(0, np.concatenate([x, xt], axis=1), c, T)
+    t_single = time.perf_counter() - t0
+    log(f"[cpu] oracle single-stream block {t_single:.1f} s")
+    ring = [synth.normal(f"cpu/ring{j}", (1, T, D)) for j in range(3)]
+    w = bary.bary_weights([10.0, 5.0, 0.0], 12.0)
+    t0 = time.perf_counter()
+    feat = bary.forecast(ring, w)
+    t_fc = time.perf_counter() - t0
+    smp = osm.Sampler("euler", cfg.steps, cfg.in_ch, cfg.flow_shift)
+    lat = synth.latents(one).astype(np.float64)
+    t0 = time.perf_counter()
+    out = M.final(feat, c)
+    smp.step(1, lat, out)
+    t_fin = time.perf_counter() - t0
+    mask = bary.make_mask(cfg.steps, cfg.interval)
+    nfull = int(mask.sum())
+    per = nfull * (cfg.depth * t_dual + cfg.depth_single * t_single) + (cfg.steps - nfull) * t_fc + cfg.steps * t_fin
+    cores = len(os.sched_getaffinity(0))
+    cpu, blas = host_info()
+    return {"value": round(cfg.batch / per, 8), "unit": "samples/s", "cores": cores, "kind": "oracle",
+            "composed": True, "cpu_model": cpu, "blas": blas,
+            "seconds_per_sample": round(per, 1),
+            "sample": (f"oracle pieces timed once each on one sample at the full shape (numpy fp32 model, "
+                       f"{cores} host threads): dual-stream block {t_dual:.2f} s, single-stream block "
+                       f"{t_single:.2f} s (14310 + 256 tokens, D 3072), forecast K=3 {t_fc * 1e3:.0f} ms, final "
+                       f"layer + Euler update {t_fin * 1e3:.0f} ms; composed to {nfull} full steps x "
+                       f"({cfg.depth} dual + {cfg.depth_single} single blocks) + {cfg.steps - nfull} forecasts + "
+                       f"{cfg.steps} final layers")}
+
+
+def cpu_baseline_image(cfg, nsteps=9):
+    """The oracle (numpy fp64) on one sample of an image workload for the
+    first `nsteps` steps of its schedule; per-step times composed to the whole
+    schedule."""
+    import numpy as np
+
+    import synth
+    from oracle import bary, model as om, sampler as osm
+    one = synth.scaled(cfg, batch=1)
+    params = synth.params(one)
+    M = om.Model(one, params)
+    x = synth.latents(one).astype(np.float64)
+    lab = synth.labels(one) if one.n_classes else None
+    text = synth.text(one) if one.kind != "dit" else None
+    mask = bary.make_mask(cfg.steps, cfg.interval)
     steps = bary.plan(mask, cfg.K)
     tin = osm.model_time(cfg.sampler, cfg.steps, cfg.flow_shift)
     smp = osm.Sampler(cfg.sampler, cfg.steps, cfg.in_ch, cfg.flow_shift)
     ring = bary.Ring(cfg.K)
+    ctx = M.context(text) if one.kind != "dit" else None
     t_full, t_fc = [], []
     for k in range(min(nsteps, cfg.steps)):
         t0 = time.perf_counter()
-        cond = M.condition(tin[k], 1, lab)
+        cond = M.condition(tin[k], 1, lab, text)
         if mask[k]:
-            feat = M.stack(M.embed(x), cond, None)
+            feat = M.stack(M.embed(x), cond, ctx)
             ring.push(feat, k)
         else:
             st = steps[k]
             feat = bary.forecast([ring.slots[i] for i in st.slots], st.w)
-        out = M.final(feat, cond)
-        x = smp.step(k, x, out)
+        x = smp.step(k, x, M.final(feat, cond))
         (t_full if mask[k] else t_fc).append(time.perf_counter() - t0)
     nfull = int(mask.sum())
-    per_sample = nfull * np.mean(t_full) + (cfg.steps - nfull) * np.mean(t_fc)
+    per = nfull * np.mean(t_full) + (cfg.steps - nfull) * np.mean(t_fc)
     cores = len(os.sched_getaffinity(0))
-    return {"value": round(1.0 / per_sample, 6), "unit": "samples/s", "cores": cores, "kind": "oracle",
-            "sample": (f"1 sample, steps 0-{nsteps - 1} of the {cfg.steps}-step schedule "
-                       f"({len(t_full)} full at {np.mean(t_full):.2f} s, {len(t_fc)} forecast at "
-                       f"{np.mean(t_fc) * 1e3:.1f} ms), composed to {nfull} full + {cfg.steps - nfull} "
-                       f"forecast steps; numpy fp64 on {cores} host threads")}
+    return {"value": round(1.0 / per, 6), "unit": "samples/s", "cores": cores, "kind": "oracle", "composed": True,
+            "sample": (f"1 sample, steps 0-{nsteps - 1} of the {cfg.steps}-step schedule ({len(t_full)} full at "
+                       f"{np.mean(t_full):.2f} s, {len(t_fc)} forecast at {np.mean(t_fc) * 1e3:.1f} ms), composed "
+                       f"to {nfull} full + {cfg.steps - nfull} forecast steps; numpy fp64 on {cores} host threads")}
 
+
+# ---------------------------------------------------------------------------
+# counter program
+# ---------------------------------------------------------------------------
 
 def kernels_only(args):
-    """The roofline kernels at the workload's shapes, each launched `args.steps`
-    times on synthetic operands (no sampling loop): the program the byte
-    counters are collected on."""
+    """The roofline kernels at the workloads' shapes, launched through the C
+    ABI without the sampling loop: the program the rocprofv3 counter passes
+    run on.  Per workload, `steps` rounds over as many distinct weight sets as
+    the model has blocks (so weights arrive from HBM, as in the loop):
+    DiT-XL/2 QKV, out-projection, MLP up and down projections and
+    self-attention; the video model's joint attention and single-stream
+    projections; then the K = 3 bf16 forecast."""
     import torch
 
     import synth
-    import paper_2608_28670_amd as bc
-    if not os.path.exists(bc.LIB_PATH):
-        from paper_2608_28670_amd import build
-        build.build()
+    bc = ensure_library()
     dev = "cuda:0"
-    cfg = synth.CONFIGS[args.workload]
-    M, D, F = cfg.batch * cfg.tokens, cfg.hidden, cfg.mlp
     g = torch.Generator(device=dev)
     g.manual_seed(synth.SEED)
 
@@ -182,262 +603,135 @@ def kernels_only(args):
         t.normal_(0.0, scale, generator=g)
         return t.to(dt)
 
-    h, w1, b1, hm = rnd(M, D), rnd(F, D), rnd(F), torch.empty((M, F), dtype=torch.bfloat16, device=dev)
-    w2, b2 = rnd(D, F), rnd(D)
-    x, gate = rnd(M, D, dt=torch.float32, scale=1.0), rnd(cfg.batch, D, dt=torch.float32, scale=1.0)
-    H, dh, T = cfg.heads, cfg.head_dim, cfg.tokens
-    q, k, v = (rnd(cfg.batch, T, H, dh, scale=1.0) for _ in range(3))
-    o = torch.empty_like(q)
+    for name in args.workload.split(","):
+        cfg = synth.CONFIGS[name]
+        B, T, D, F, H, hd = cfg.batch, cfg.tokens, cfg.hidden, cfg.mlp, cfg.heads, cfg.head_dim
+        if cfg.kind == "mmdit":
+            L = T + cfg.txt_tokens
+            nb = 4
+            w1 = [rnd(3 * D + F, D) for _ in range(nb)]
+            w2 = [rnd(D, D + F) for _ in range(nb)]
+            b1, b2 = rnd(3 * D + F), rnd(D)
+            h = rnd(B * L, D)
+            y = torch.empty((B * L, 3 * D + F), dtype=torch.bfloat16, device=dev)
+            z = rnd(B * L, D + F)
+            xs, gate = rnd(B * L, D, dt=torch.float32, scale=1.0), rnd(B, D, dt=torch.float32, scale=1.0)
+            q, k, v = (rnd(B, L, H, hd, scale=1.0) for _ in range(3))
+            o = torch.empty_like(q)
+            for r in range(args.steps):
+                for i in range(nb):
+                    bc.linear(h, w1[i], b1, y, bc.EPI_BIAS_GELU)
+                    bc.attention(q, k, v, o)
+                    bc.linear(z, w2[i], b2, xs, bc.EPI_GATE_RES, res=xs, gate=gate, rows_per_gate=L)
+            torch.cuda.synchronize()
+            del w1, w2, h, y, z, xs, q, k, v, o
+        else:
+            M = B * T
+            nb = cfg.depth
+            wq = [rnd(3 * D, D) for _ in range(nb)]
+            wo = [rnd(D, D) for _ in range(nb)]
+            w1 = [rnd(F, D) for _ in range(nb)]
+            w2 = [rnd(D, F) for _ in range(nb)]
+            bq, bo, b1, b2 = rnd(3 * D), rnd(D), rnd(F), rnd(D)
+            h = rnd(M, D)
+            qkv = torch.empty((M, 3 * D), dtype=torch.bfloat16, device=dev)
+            a = rnd(M, D)
+            hm = torch.empty((M, F), dtype=torch.bfloat16, device=dev)
+            x, gate = rnd(M, D, dt=torch.float32, scale=1.0), rnd(B, D, dt=torch.float32, scale=1.0)
+            q, k, v = (rnd(B, T, H, hd, scale=1.0) for _ in range(3))
+            o = torch.empty_like(q)
+            for r in range(args.steps):
+                for i in range(nb):
+                    bc.linear(h, wq[i], bq, qkv, bc.EPI_BIAS)
+                    bc.attention(q, k, v, o)
+                    bc.linear(a, wo[i], bo, x, bc.EPI_GATE_RES, res=x, gate=gate, rows_per_gate=T)
+                    bc.linear(h, w1[i], b1, hm, bc.EPI_BIAS_GELU)
+                    bc.linear(hm, w2[i], b2, x, bc.EPI_GATE_RES, res=x, gate=gate, rows_per_gate=T)
+            torch.cuda.synchronize()
+            del wq, wo, w1, w2, h, qkv, a, hm, x, q, k, v, o
+        torch.cuda.empty_cache()
+    shape = synth.FORECAST_SHAPE
+    n = shape[0] * shape[1] * shape[2]
+    storage = torch.empty((3, n), dtype=torch.bfloat16, device=dev).normal_(generator=g)
+    ring = bc.CacheRing(3, storage)
+    s, t = synth.forecast_times(3)
+    for j in reversed(range(3)):
+        ring.push(None, float(s[j]))
+    out = torch.empty(n, dtype=torch.bfloat16, device=dev)
+    w = bc.bary_weights(s, t)
     for _ in range(args.steps):
-        bc.linear(h, w1, b1, hm, bc.EPI_BIAS_GELU)
-        bc.linear(hm, w2, b2, x, bc.EPI_GATE_RES, res=x, gate=gate, rows_per_gate=T)
-        bc.attention(q, k, v, o)
+        bc.bary_extrapolate(ring, w, out)
     torch.cuda.synchronize()
-    del h, w1, b1, hm, w2, b2, x, gate, q, k, v, o
-    torch.cuda.empty_cache()
-    forecast_bench(bc, torch, dev, K=3, dtype="bf16", iters=args.steps)
+    del storage, out, ring
     if args.calib_copy:
-        n = 1 << 29
-        src = torch.ones(n, dtype=torch.bfloat16, device=dev)
-        store = torch.empty((1, n), dtype=torch.bfloat16, device=dev)
+        nn = 1 << 29
+        src = torch.ones(nn, dtype=torch.bfloat16, device=dev)
+        store = torch.empty((1, nn), dtype=torch.bfloat16, device=dev)
         ring = bc.CacheRing(1, store)
         ring.push(src, 0.0)
         torch.cuda.synchronize()
-    print(json.dumps({"kernels_only": args.workload, "launches_each": args.steps}))
+    print(json.dumps({"kernels_only": args.workload, "rounds": args.steps}), flush=True)
 
+
+# ---------------------------------------------------------------------------
 
 def main():
     args = parse()
-    if args.kernels_only:
-        kernels_only(args)
-        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: the library has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
         sys.exit(2)
-    import numpy as np
+    if args.kernels_only:
+        kernels_only(args)
+        return
     import torch
 
     import synth
-    import paper_2608_28670_amd as bc
-    from paper_2608_28670_amd import loader
-
-    if not os.path.exists(bc.LIB_PATH):
-        from paper_2608_28670_amd import build
-        build.build()
-    dev = "cuda:0"
+    bc = ensure_library()
     cfg = synth.CONFIGS[args.workload]
-    t0 = time.time()
-    # Host weights (shared with the oracle's CPU baseline) for the default
-    # image workload; GPU-drawn weights for the others.
-    host_weights = args.workload == "dit_xl2"
-    params = synth.params(cfg) if host_weights else None
-    dm = loader.DeviceModel(cfg, params, dev_params=None if host_weights else device_params(cfg, torch, dev))
-    B = cfg.batch
-    mask = bc.make_mask(cfg.steps, cfg.interval)
-    labels = synth.labels(cfg) if cfg.n_classes else None
-    text = synth.text(cfg) if cfg.kind != "dit" else None
-    xT = synth.latents(cfg)
-    x0 = torch.from_numpy(xT).to(dev)
-    x = torch.empty_like(x0)
-    tl = torch.from_numpy(labels).to(dev) if labels is not None else None
-    tt = torch.from_numpy(text).to(dev).to(loader.torch_dtype(cfg)) if text is not None else None
-    print(f"setup {time.time() - t0:.1f} s", file=sys.stderr)
-
-    def run(m):
-        x.copy_(x0)
-        dm.sample(x, m, labels=tl, text=tt)
-
-    for _ in range(args.warmup):
-        run(mask)
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for _ in range(args.steps):
-        run(mask)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t_start
-    ms_per_step = elapsed / args.steps * 1e3
-    value = B * args.steps / elapsed
-
-    # Kernel classes timed with per-launch HIP events on their launch stream
-    # in one extra sampling run (the events ride on the launches themselves),
-    # right after the timed runs and in the same state: where a full step's
-    # time goes, and the roofline of the dominant kernel.
-    nfull = int(mask.sum())
-    classes = {"gemm_gelu": bc.PROF_GEMM_GELU, "gemm_down": bc.PROF_GEMM_DOWN, "gemm_gated": bc.PROF_GEMM_GATE,
-               "gemm_bias": bc.PROF_GEMM_BIAS, "attention": bc.PROF_ATTENTION, "layernorm": bc.PROF_LAYERNORM}
-    cap = 16 * nfull * cfg.depth + 1024
-    for c in classes.values():
-        bc.profile_enable(c, cap)
-    run(mask)
-    breakdown, times = {}, {}
-    for name, c in classes.items():
-        t = bc.profile_times(c, cap).astype(np.float64)
-        times[name] = t
-        if len(t):
-            breakdown[name] = {"ms_per_run": round(float(t.sum()), 3), "launches": len(t),
-                               "avg_us": round(float(t.mean()) * 1e3, 2)}
-    roofline, others = None, []
-    if cfg.kind in ("dit", "pixart"):
-        M_rows = B * cfg.tokens
-        nb = nfull * cfg.depth
-        gemm_hash = source_hash("gemm.hip", "gemm.h", "hip_common.h")
-        att_hash = source_hash("attention.hip", "attention.h", "hip_common.h")
-        # One launch per block and full step for each candidate.  PixArt's
-        # caption MLP (once per run, before the loop) is the first GELU GEMM;
-        # its cross-attention follows each self-attention.
-        att = times["attention"] if cfg.kind == "dit" else times["attention"][0::2]
-        cands = [
-            ("gemm fc2 (gated residual, MLP down projection)", times["gemm_down"], "mfma",
-             2.0 * M_rows * cfg.hidden * cfg.mlp, [M_rows, cfg.hidden, cfg.mlp], f"gemm_fc2_{cfg.name}", gemm_hash),
-            ("gemm fc1 (bias+GELU)", times["gemm_gelu"][-nb:], "mfma",
-             2.0 * M_rows * cfg.mlp * cfg.hidden, [M_rows, cfg.mlp, cfg.hidden], f"gemm_fc1_{cfg.name}", gemm_hash),
-            ("self-attention", att, "mfma",
-             4.0 * B * cfg.heads * cfg.tokens * cfg.tokens * cfg.head_dim,
-             [B, cfg.heads, cfg.tokens, cfg.head_dim], f"attention_{cfg.name}", att_hash),
-        ]
-        recs = []
-        for name, t, bound, flops, shape, tag, h in cands:
-            assert len(t) == nb, (name, len(t), nb)
-            avg_s = float(t.mean()) / 1e3
-            achieved = flops / avg_s / 1e12
-            recs.append((float(t.sum()), {
-                "bound": bound, "kernel": name, "shape": shape, "flops_per_launch": flops,
-                "avg_us": round(avg_s * 1e6, 2), "launches": len(t), "ms_per_run": round(float(t.sum()), 3),
-                "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": counters_traffic(tag, h, None), "source_hash": h}))
-        recs.sort(key=lambda r: -r[0])
-        roofline, others = recs[0][1], [r[1] for r in recs[1:]]
-
-
-    # The same run replayed from a HIP graph captured once (bc_sample_graph_*).
-    graph = None
-    if not args.no_graph:
-        g = dm.sample_graph(x, mask, labels=tl, text=tt)
-        for _ in range(max(1, args.warmup)):
-            x.copy_(x0)
-            g.launch()
-        torch.cuda.synchronize()
-        tg = time.perf_counter()
-        for _ in range(args.steps):
-            x.copy_(x0)
-            g.launch()
-        torch.cuda.synchronize()
-        eg = time.perf_counter() - tg
-        graph = {"value": round(B * args.steps / eg, 3), "ms_per_step": round(eg / args.steps * 1e3, 3)}
-        del g
-
-    # The adaptive schedule (decided during the run from the first block's
-    # modulated input; one host read-back per step), timed like `value`.
-    adaptive = None
-    if args.adaptive_ell >= 0:
-        def run_adaptive():
-            x.copy_(x0)
-            return dm.sample_adaptive(x, cfg.steps, args.adaptive_ell, labels=tl, text=tt)
-        for _ in range(max(1, args.warmup)):
-            run_adaptive()
-        torch.cuda.synchronize()
-        ta = time.perf_counter()
-        for _ in range(args.steps):
-            _, amask, _ = run_adaptive()
-        torch.cuda.synchronize()
-        ea = time.perf_counter() - ta
-        # The fixed-mask loop under the realised mask: the probe's and the
-        # read-backs' cost is the difference.
-        run(amask)
-        torch.cuda.synchronize()
-        tfm = time.perf_counter()
-        for _ in range(args.steps):
-            run(amask)
-        torch.cuda.synchronize()
-        efm = time.perf_counter() - tfm
-        adaptive = {"ell": args.adaptive_ell, "full_steps": int(amask.sum()),
-                    "value": round(B * args.steps / ea, 3), "ms_per_step": round(ea / args.steps * 1e3, 3),
-                    "ms_fixed_loop_same_mask": round(efm / args.steps * 1e3, 3),
-                    "mask": "".join(str(int(v)) for v in amask)}
-
-    # Blockwise mode (Br = 0) under the same mask: every module's output is
-    # cached, so the cache is 2 (DiT) or 3 (PixArt) tensors per block instead
-    # of one per run; timed like `value`.
-    blockwise = None
-    if not args.no_blockwise and cfg.kind in ("dit", "pixart"):
-        def run_blockwise():
-            x.copy_(x0)
-            return dm.sample_blockwise(x, mask, labels=tl, text=tt)
-        for _ in range(max(1, args.warmup)):
-            sites = run_blockwise()
-        torch.cuda.synchronize()
-        tb = time.perf_counter()
-        for _ in range(args.steps):
-            sites = run_blockwise()
-        torch.cuda.synchronize()
-        eb = time.perf_counter() - tb
-        blockwise = {"value": round(B * args.steps / eb, 3), "ms_per_step": round(eb / args.steps * 1e3, 3),
-                     "sites": int(sites.shape[0]), "cache_bytes": int(sites.numel() * sites.element_size()),
-                     "stepwise_cache_bytes": int(cfg.K * B * cfg.tokens * cfg.hidden * sites.element_size())}
-        del sites
-        dm.release_blockwise()
-        torch.cuda.empty_cache()
-
-    # Speedup reference: the same sampler with every step full.
-    full = np.ones(cfg.steps, np.uint8)
-    run(full)
-    torch.cuda.synchronize()
-    tf = time.perf_counter()
-    nref = max(1, min(3, args.steps))
-    for _ in range(nref):
-        run(full)
-    torch.cuda.synchronize()
-    ms_full = (time.perf_counter() - tf) / nref * 1e3
-
-    forecast = None
-    if not args.no_forecast:
-        del dm
-        torch.cuda.empty_cache()
-        forecast = forecast_bench(bc, torch, dev, K=3, dtype="bf16")
-        fc_hash = source_hash("forecast.hip", "hip_common.h")
-        forecast["traffic"] = counters_traffic("forecast_k3_bf16", fc_hash, None)
-        forecast["source_hash"] = fc_hash
-
-    if args.calib_copy:
-        # A plain copy of known size through the library's 16-byte copy kernel:
-        # the reference for scaling HBM byte counters.
-        n = 1 << 29
-        src = torch.ones(n, dtype=torch.bfloat16, device=dev)
-        store = torch.empty((1, n), dtype=torch.bfloat16, device=dev)
-        ring = bc.CacheRing(1, store)
-        ring.push(src, 0.0)
-        torch.cuda.synchronize()
-        del src, store, ring
-
+    head = measure(bc, torch, cfg, args.steps, args.warmup, extras=not args.no_extras and cfg.kind == "dit",
+                   adaptive_ell=args.adaptive_ell)
+    legs = {}
+    for name in [w for w in args.legs.split(",") if w and w != args.workload]:
+        lc = synth.CONFIGS[name]
+        r = measure(bc, torch, lc, args.leg_steps, 1, extras=not args.no_extras and lc.kind == "dit",
+                    adaptive_ell=args.adaptive_ell)
+        leg = {"config": workload_desc(lc, r.pop("mask")), "value": round(r.pop("value"), 3), "unit": "samples/s",
+               "ms_per_step": round(r.pop("ms_per_step"), 3), "steps": args.leg_steps, "warmup": 1,
+               "speedup_vs_all_full": round(r.pop("speedup_vs_all_full"), 3),
+               "ms_all_full": round(r.pop("ms_all_full"), 3), "ideal_speedup": round(r.pop("ideal_speedup"), 3)}
+        leg.update(r)
+        legs[name] = leg
+    forecast, push = (None, None) if args.no_forecast else forecast_sweep(bc, torch)
     cpu = None
-    if not args.no_cpu_baseline and host_weights:
-        cpu = cpu_baseline(cfg, params, labels, xT, mask, args.cpu_steps)
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline_video(cfg) if cfg.kind == "mmdit" else cpu_baseline_image(cfg)
 
-    blocks = (f"{cfg.depth} dual-stream + {cfg.depth_single} single-stream blocks" if cfg.kind == "mmdit"
-              else f"{cfg.depth} blocks")
+    mask = head.pop("mask")
     line = {
         "metric": "end-to-end samples/s at fixed skip schedule; forecast HBM GB/s; block MFMA util",
-        "value": round(value, 3), "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 3), "higher_is_better": True,
+        "value": round(head["value"], 4), "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(head["ms_per_step"], 3), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: {blocks}, D {cfg.hidden}, {cfg.heads}x{cfg.head_dim} heads, "
-                               f"MLP {cfg.mlp}, {cfg.tokens} tokens, batch {B}, {cfg.steps} {cfg.sampler} steps, "
-                               f"K={cfg.K}, full every {cfg.interval} ({nfull}/{cfg.steps}), random-init weights",
-                   "global_batch": B, "parallelism": "none (1 GPU)"},
-        "graph_replay": graph,
-        "adaptive": adaptive,
-        "blockwise": blockwise,
-        "speedup_vs_all_full": round(ms_full / ms_per_step, 3),
-        "ms_all_full": round(ms_full, 3),
-        "roofline": roofline,
-        "roofline_others": others,
-        "kernel_classes": breakdown,
+        "config": {"workload": workload_desc(cfg, mask), "global_batch": cfg.batch, "seq_len": cfg.tokens,
+                   "parallelism": "none (1 GPU)"},
+        "speedup_vs_all_full": round(head["speedup_vs_all_full"], 3),
+        "ms_all_full": round(head["ms_all_full"], 3),
+        "ideal_speedup": round(head["ideal_speedup"], 3),
+        "roofline": head["roofline"],
+        "roofline_others": head["roofline_others"],
+        "kernel_classes": head["kernel_classes"],
+        "profiled_run_ms": head["profiled_run_ms"],
+        "workloads": legs,
         "forecast": forecast,
+        "push_copy": push,
         "cpu_baseline": cpu,
+        "paper_context": PAPER_CONTEXT,
     }
-    print(json.dumps(line))
+    for k in ("graph_replay", "adaptive", "blockwise"):
+        if k in head:
+            line[k] = head[k]
+    print(json.dumps(line), flush=True)
 
 
 if __name__ == "__main__":
