@@ -21,82 +21,81 @@ struct FcArgs {
     int64_t n;       // elements
 };
 
-// Elements per thread iteration: 8 (one 16 B bf16 load, or two fp32 loads).
-constexpr int kEl = 8;
 constexpr int kThreads = 256;
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
-// 16-byte chunks per 8 elements: 1 (bf16) or 2 (fp32).
-template <typename T> struct Chunks { static constexpr int v = sizeof(T) == 2 ? 1 : 2; };
-
-template <typename Tin>
-__device__ __forceinline__ void load8(const Tin* p, u32x4* raw) {
-    const u32x4* q = reinterpret_cast<const u32x4*>(p);
-#pragma unroll
-    for (int c = 0; c < Chunks<Tin>::v; ++c) raw[c] = __builtin_nontemporal_load(q + c);
-}
+// The vector path works in units of one 16-byte input chunk per thread and
+// step: 8 bf16 or 4 fp32 elements, so every load instruction of a wave reads
+// 1 KiB of consecutive bytes of each cached feature.
+template <typename Tin> struct Unit { static constexpr int el = 16 / (int)sizeof(Tin); };
 
 template <typename Tin>
-__device__ __forceinline__ void unpack8(const u32x4* raw, float* f) {
-    if constexpr (sizeof(Tin) == 2) {
-        unpack(raw[0], f, (const bf16*)nullptr);
-    } else {
-        unpack(raw[0], f, (const float*)nullptr);
-        unpack(raw[1], f + 4, (const float*)nullptr);
-    }
+__device__ __forceinline__ void unpack_unit(const u32x4& raw, float* f) {
+    if constexpr (sizeof(Tin) == 2) unpack(raw, f, (const bf16*)nullptr);
+    else unpack(raw, f, (const float*)nullptr);
 }
 
-template <typename Tout>
-__device__ __forceinline__ void store8(Tout* p, const float* f) {
+// Store EL fp32 values as EL elements of Tout (16 bytes for bf16 -> bf16 and
+// fp32 -> fp32, 8 for fp32 -> bf16, 32 for bf16 -> fp32).
+template <typename Tout, int EL>
+__device__ __forceinline__ void store_unit(Tout* p, const float* f) {
     if constexpr (sizeof(Tout) == 2) {
-        u32x4 u;
-        uint32_t w[4];
+        uint32_t w[EL / 2];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < EL / 2; ++i) {
             bf16 lo = (bf16)f[2 * i], hi = (bf16)f[2 * i + 1];
             w[i] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
         }
-        u.x = w[0]; u.y = w[1]; u.z = w[2]; u.w = w[3];
-        __builtin_nontemporal_store(u, reinterpret_cast<u32x4*>(p));
+        if constexpr (EL == 8) {
+            u32x4 u = {w[0], w[1], w[2], w[3]};
+            __builtin_nontemporal_store(u, reinterpret_cast<u32x4*>(p));
+        } else {
+            u32x2 u = {w[0], w[1]};
+            __builtin_nontemporal_store(u, reinterpret_cast<u32x2*>(p));
+        }
     } else {
         u32x4* q = reinterpret_cast<u32x4*>(p);
-        u32x4 a, b;
-        a.x = __float_as_uint(f[0]); a.y = __float_as_uint(f[1]); a.z = __float_as_uint(f[2]); a.w = __float_as_uint(f[3]);
-        b.x = __float_as_uint(f[4]); b.y = __float_as_uint(f[5]); b.z = __float_as_uint(f[6]); b.w = __float_as_uint(f[7]);
-        __builtin_nontemporal_store(a, q);
-        __builtin_nontemporal_store(b, q + 1);
+#pragma unroll
+        for (int c = 0; c < EL / 4; ++c) {
+            u32x4 a = {__float_as_uint(f[4 * c]), __float_as_uint(f[4 * c + 1]), __float_as_uint(f[4 * c + 2]),
+                       __float_as_uint(f[4 * c + 3])};
+            __builtin_nontemporal_store(a, q + c);
+        }
     }
 }
 
-// Vector path: every pointer 16-byte aligned; covers the first n/8*8 elements.
+// Vector path: every pointer 16-byte aligned; covers the first n / EL * EL
+// elements.  A thread owns U units, threads of a workgroup consecutive units.
 template <int K, typename Tin, typename Tout, int U>
 __global__ __launch_bounds__(kThreads) void forecast_vec_kernel(FcArgs a) {
-    constexpr int NC = Chunks<Tin>::v;
-    const int64_t nv = a.n / kEl;
+    constexpr int EL = Unit<Tin>::el;
+    const int64_t nv = a.n / EL;
     const int64_t v0 = (int64_t)blockIdx.x * (kThreads * U) + threadIdx.x;
-    u32x4 raw[U][K][NC];
+    u32x4 raw[U][K];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int64_t v = v0 + (int64_t)u * kThreads;
         if (v < nv) {
 #pragma unroll
-            for (int j = 0; j < K; ++j) load8(static_cast<const Tin*>(a.src[j]) + v * kEl, raw[u][j]);
+            for (int j = 0; j < K; ++j)
+                raw[u][j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(static_cast<const Tin*>(a.src[j]) + v * EL));
         }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int64_t v = v0 + (int64_t)u * kThreads;
         if (v < nv) {
-            float acc[kEl], x[kEl];
-            unpack8<Tin>(raw[u][0], x);
+            float acc[EL], x[EL];
+            unpack_unit<Tin>(raw[u][0], x);
 #pragma unroll
-            for (int e = 0; e < kEl; ++e) acc[e] = a.w[0] * x[e];
+            for (int e = 0; e < EL; ++e) acc[e] = a.w[0] * x[e];
 #pragma unroll
             for (int j = 1; j < K; ++j) {
-                unpack8<Tin>(raw[u][j], x);
+                unpack_unit<Tin>(raw[u][j], x);
 #pragma unroll
-                for (int e = 0; e < kEl; ++e) acc[e] = __builtin_fmaf(a.w[j], x[e], acc[e]);
+                for (int e = 0; e < EL; ++e) acc[e] = __builtin_fmaf(a.w[j], x[e], acc[e]);
             }
-            store8(static_cast<Tout*>(a.out) + v * kEl, acc);
+            store_unit<Tout, EL>(static_cast<Tout*>(a.out) + v * EL, acc);
         }
     }
 }
@@ -127,20 +126,21 @@ static void launch_vec(const FcArgs& a, int K, int64_t nv, hipStream_t s) {
 
 template <typename Tin, typename Tout>
 static int run_forecast(const FcArgs& a, int K, hipStream_t s) {
-    // Large tensors: several 16-byte vectors per thread, all loads issued
-    // first; small ones (below ~32M elements): one per thread, for more
-    // workgroups in flight.
-    constexpr int U = sizeof(Tin) == 2 ? 4 : 2;
+    // Large tensors: four 16-byte units per thread, all loads issued first;
+    // small ones (below ~32M elements): one per thread, for more workgroups
+    // in flight.
+    constexpr int U = 4;
+    constexpr int EL = Unit<Tin>::el;
     bool aligned = (reinterpret_cast<uintptr_t>(a.out) % 16) == 0;
     for (int j = 0; j < K; ++j) aligned = aligned && (reinterpret_cast<uintptr_t>(a.src[j]) % 16) == 0;
     int64_t done = 0;
     if (aligned) {
-        const int64_t nv = a.n / kEl;
+        const int64_t nv = a.n / EL;
         if (nv > 0) {
             if (nv / kThreads > 0x7fffffff) return fail(BC_ERR_UNSUPPORTED, "forecast of %lld elements is too large", (long long)a.n);
             if (a.n >= ((int64_t)32 << 20)) launch_vec<Tin, Tout, U>(a, K, nv, s);
             else launch_vec<Tin, Tout, 1>(a, K, nv, s);
-            done = nv * kEl;
+            done = nv * EL;
         }
     }
     if (done < a.n) {
@@ -173,9 +173,21 @@ int launch_forecast(const void* const* src, const float* w, int K, int64_t n, in
 
 // ---- plain copies and zero fills (byte streams) ------------------------------
 
+// 16-byte chunks: each workgroup copies one contiguous run of 4 x 256
+// chunks, each thread four of them (all four loads issued before the
+// stores), non-temporal: a copied feature is not read again soon.  One pass
+// over the grid (no grid-stride loop) measured 6.3 TB/s on a 805 MB copy
+// against 5.1-5.5 TB/s for grid-stride variants.
+constexpr int kCopyU = 4;
 __global__ __launch_bounds__(kThreads) void copy16_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst, int64_t n16) {
-    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n16; i += (int64_t)gridDim.x * kThreads)
-        dst[i] = src[i];
+    const int64_t base = (int64_t)blockIdx.x * (kThreads * kCopyU) + threadIdx.x;
+    u32x4 v[kCopyU];
+#pragma unroll
+    for (int u = 0; u < kCopyU; ++u)
+        if (base + u * kThreads < n16) v[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + base + u * kThreads));
+#pragma unroll
+    for (int u = 0; u < kCopyU; ++u)
+        if (base + u * kThreads < n16) __builtin_nontemporal_store(v[u], reinterpret_cast<u32x4*>(dst + base + u * kThreads));
 }
 __global__ __launch_bounds__(kThreads) void copy1_kernel(const uint8_t* src, uint8_t* dst, int64_t n) {
     for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += (int64_t)gridDim.x * kThreads)
@@ -199,9 +211,12 @@ static unsigned grid_for(int64_t items) {
 
 int launch_copy(const void* src, void* dst, int64_t bytes, hipStream_t s) {
     if (bytes <= 0) return BC_OK;
+    const bool vec = ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst) | (uintptr_t)bytes) % 16) == 0;
+    const int64_t blocks = (bytes / 16 + kThreads * kCopyU - 1) / (kThreads * kCopyU);
+    if (vec && blocks > 0x7fffffff) return fail(BC_ERR_UNSUPPORTED, "copy of %lld bytes is too large", (long long)bytes);
     prof_begin(PROF_COPY, s, 2.0 * (double)bytes);
-    if ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst) | (uintptr_t)bytes) % 16 == 0)
-        launch_k(copy16_kernel, dim3(grid_for(bytes / 16)), dim3(kThreads), s, static_cast<const uint4*>(src),
+    if (vec)
+        launch_k(copy16_kernel, dim3((unsigned)blocks), dim3(kThreads), s, static_cast<const uint4*>(src),
                  static_cast<uint4*>(dst), bytes / 16);
     else
         launch_k(copy1_kernel, dim3(grid_for(bytes)), dim3(kThreads), s, static_cast<const uint8_t*>(src),
