@@ -66,8 +66,10 @@ __device__ __forceinline__ void store_unit(Tout* p, const float* f) {
 
 // Vector path: every pointer 16-byte aligned; covers the first n / EL * EL
 // elements.  A thread owns U units, threads of a workgroup consecutive units.
-template <int K, typename Tin, typename Tout, int U>
+template <int K, typename Tin_, typename Tout_, int U>
 __global__ __launch_bounds__(kThreads) void forecast_vec_kernel(FcArgs a) {
+    typedef elem_t<Tin_> Tin;
+    typedef elem_t<Tout_> Tout;
     constexpr int EL = Unit<Tin>::el;
     const int64_t nv = a.n / EL;
     const int64_t v0 = (int64_t)blockIdx.x * (kThreads * U) + threadIdx.x;
@@ -101,8 +103,10 @@ __global__ __launch_bounds__(kThreads) void forecast_vec_kernel(FcArgs a) {
 }
 
 // Element path: any alignment; handles [begin, n).
-template <typename Tin, typename Tout>
+template <typename Tin_, typename Tout_>
 __global__ __launch_bounds__(kThreads) void forecast_scalar_kernel(FcArgs a, int K, int64_t begin) {
+    typedef elem_t<Tin_> Tin;
+    typedef elem_t<Tout_> Tout;
     for (int64_t i = begin + (int64_t)blockIdx.x * kThreads + threadIdx.x; i < a.n;
          i += (int64_t)gridDim.x * kThreads) {
         float acc = 0.f;
@@ -116,7 +120,7 @@ static void launch_vec(const FcArgs& a, int K, int64_t nv, hipStream_t s) {
     const int64_t blocks = (nv + kThreads * U - 1) / (kThreads * U);
     dim3 g((unsigned)blocks), b(kThreads);
     switch (K) {
-#define BC_FC_CASE(KK) case KK: launch_k(forecast_vec_kernel<KK, Tin, Tout, U>, g, b, s, a); break;
+#define BC_FC_CASE(KK) case KK: launch_k(forecast_vec_kernel<KK, tag_t<Tin>, tag_t<Tout>, U>, g, b, s, a); break;
         BC_FC_CASE(1) BC_FC_CASE(2) BC_FC_CASE(3) BC_FC_CASE(4)
         BC_FC_CASE(5) BC_FC_CASE(6) BC_FC_CASE(7) BC_FC_CASE(8)
 #undef BC_FC_CASE
@@ -147,7 +151,7 @@ static int run_forecast(const FcArgs& a, int K, hipStream_t s) {
         const int64_t rest = a.n - done;
         int64_t blocks = (rest + kThreads - 1) / kThreads;
         if (blocks > 65536) blocks = 65536;
-        launch_k(forecast_scalar_kernel<Tin, Tout>, dim3((unsigned)blocks), dim3(kThreads), s, a, K, done);
+        launch_k(forecast_scalar_kernel<tag_t<Tin>, tag_t<Tout>>, dim3((unsigned)blocks), dim3(kThreads), s, a, K, done);
     }
     return check_launch("forecast");
 }

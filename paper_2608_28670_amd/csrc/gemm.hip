@@ -89,8 +89,9 @@ __device__ __forceinline__ void epilogue(const GemmArgs& g, const f32x4 (&acc)[T
 
 // Tile shape: BM x BN per workgroup, a WAVES_M x WAVES_N grid of waves, each
 // wave owning a (BM/WAVES_M) x (BN/WAVES_N) block of 16x16 MFMA tiles.
-template <typename T, int EPI, int BM, int BN, int WAVES_M, int WAVES_N>
+template <typename T_, int EPI, int BM, int BN, int WAVES_M, int WAVES_N>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(GemmArgs g) {
+    typedef elem_t<T_> T;
     constexpr int NT = 64 * WAVES_M * WAVES_N;       // threads
     constexpr int EPC = 16 / (int)sizeof(T);        // elements per 16-byte chunk
     constexpr int BK = 8 * EPC;                      // 128 bytes of K per step
@@ -850,7 +851,7 @@ static void launch_dma(const GemmArgs& g, hipStream_t s) {
 template <typename T, int EPI, int BM, int BN, int WAVES_M, int WAVES_N>
 static void launch_tile(const GemmArgs& g, hipStream_t s) {
     const unsigned tiles = (unsigned)(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN));
-    launch_k(gemm_kernel<T, EPI, BM, BN, WAVES_M, WAVES_N>, dim3(tiles), dim3(64 * WAVES_M * WAVES_N), s, g);
+    launch_k(gemm_kernel<tag_t<T>, EPI, BM, BN, WAVES_M, WAVES_N>, dim3(tiles), dim3(64 * WAVES_M * WAVES_N), s, g);
 }
 
 // The wide kernel's vector epilogue needs every column index and stride it

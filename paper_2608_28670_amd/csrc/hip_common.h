@@ -9,6 +9,17 @@
 #include "common.h"
 
 typedef __bf16 bf16;
+// Kernel template arguments name the element type through a tag, so no kernel
+// symbol carries the __bf16 type (its mangling, DF16b, is rejected or misread
+// by the demanglers that profilers use): a kernel is instantiated with float
+// or bf16_tag and declares its pointer parameters as elem_t<tag>*.
+struct bf16_tag {};
+template <typename X> struct ElemOf { typedef X type; };
+template <> struct ElemOf<bf16_tag> { typedef __bf16 type; };
+template <typename X> using elem_t = typename ElemOf<X>::type;
+template <typename X> struct TagOf { typedef X type; };
+template <> struct TagOf<__bf16> { typedef bf16_tag type; };
+template <typename X> using tag_t = typename TagOf<X>::type;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));

@@ -51,11 +51,13 @@ template <> struct Vec4<bf16> {
 // Each wave takes RPW consecutive rows: the next row's chunks are loaded
 // while the current one is reduced, and the modulation vectors (one pair per
 // sample) are loaded once per sample instead of once per row.
-template <typename Tin, typename Tout, int NC, int RPW>
-__global__ __launch_bounds__(256) void ln_mod_kernel(const Tin* __restrict__ x, int64_t rows, int D,
+template <typename Tin_, typename Tout_, int NC, int RPW>
+__global__ __launch_bounds__(256) void ln_mod_kernel(const elem_t<Tin_>* __restrict__ x, int64_t rows, int D,
                                                      const float* __restrict__ shift,
                                                      const float* __restrict__ scale, int64_t ld_mod, int rps,
-                                                     Tout* __restrict__ h) {
+                                                     elem_t<Tout_>* __restrict__ h) {
+    typedef elem_t<Tin_> Tin;
+    typedef elem_t<Tout_> Tout;
     const int lane = threadIdx.x & 63;
     const int64_t row0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * RPW;
     if (row0 >= rows) return;
@@ -136,12 +138,12 @@ static int run_ln(const void* x, int64_t rows, int D, const float* shift, const 
     dim3 g((unsigned)((rows + 4 * RPW - 1) / (4 * RPW))), b(256);
     const Tin* xi = static_cast<const Tin*>(x);
     Tout* ho = static_cast<Tout*>(h);
-    if (nc <= 1) launch_k(ln_mod_kernel<Tin, Tout, 1, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nc <= 2) launch_k(ln_mod_kernel<Tin, Tout, 2, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nc <= 5) launch_k(ln_mod_kernel<Tin, Tout, 5, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nc <= 8) launch_k(ln_mod_kernel<Tin, Tout, 8, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nc <= 12) launch_k(ln_mod_kernel<Tin, Tout, 12, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
-    else if (nc <= 16) launch_k(ln_mod_kernel<Tin, Tout, 16, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
+    if (nc <= 1) launch_k(ln_mod_kernel<tag_t<Tin>, tag_t<Tout>, 1, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 2) launch_k(ln_mod_kernel<tag_t<Tin>, tag_t<Tout>, 2, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 5) launch_k(ln_mod_kernel<tag_t<Tin>, tag_t<Tout>, 5, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 8) launch_k(ln_mod_kernel<tag_t<Tin>, tag_t<Tout>, 8, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 12) launch_k(ln_mod_kernel<tag_t<Tin>, tag_t<Tout>, 12, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
+    else if (nc <= 16) launch_k(ln_mod_kernel<tag_t<Tin>, tag_t<Tout>, 16, RPW>, g, b, s, xi, rows, D, shift, scale, ld_mod, rps, ho);
     else return fail(BC_ERR_UNSUPPORTED, "LayerNorm width %d > 4096", D);
     return check_launch("ln_mod");
 }
@@ -189,8 +191,9 @@ template <> struct SkMma<float> {
 constexpr int kSkTiles = 4;   // 16-column tiles per wave
 constexpr int kSkBatch = 8;   // k-steps of weight loads issued together
 
-template <typename T>
+template <typename T_>
 __global__ __launch_bounds__(256) void skinny_kernel(SkinnyArgs a) {
+    typedef elem_t<T_> T;
     typedef SkMma<T> MM;
     constexpr int KC = MM::KC;
     constexpr int PAD = 16 / (int)sizeof(T);
@@ -280,7 +283,7 @@ int launch_skinny(int dt, const SkinnyArgs& a, hipStream_t s) {
             return fail(BC_ERR_INVALID_ARG, "skinny linear weight %d missing or misaligned", i);
     const int Ntot = a.nseg * a.Nseg;
     const unsigned grid = (unsigned)((Ntot + 4 * kSkTiles * 16 - 1) / (4 * kSkTiles * 16));
-    if (dt == BC_BF16) skinny_kernel<bf16><<<grid, 256, 0, s>>>(a);
+    if (dt == BC_BF16) skinny_kernel<bf16_tag><<<grid, 256, 0, s>>>(a);
     else skinny_kernel<float><<<grid, 256, 0, s>>>(a);
     return check_launch("skinny linear");
 }
@@ -308,9 +311,10 @@ int launch_step_sinusoid(int sampler, int S, int dim, double shift, float* e, hi
     return check_launch("sinusoid");
 }
 
-template <typename T>
-__global__ void build_cond_kernel(const float* temb, int S, int B, int D, const T* table, const int64_t* labels,
+template <typename T_>
+__global__ void build_cond_kernel(const float* temb, int S, int B, int D, const elem_t<T_>* table, const int64_t* labels,
                                   int n_rows, const float* add, float* c) {
+    typedef elem_t<T_> T;
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= (int64_t)S * B * D) return;
     const int n = (int)(i % D);
@@ -331,13 +335,14 @@ int launch_build_cond(int dt, const float* temb, int S, int B, int D, const void
                       int n_rows, const float* add, float* c, hipStream_t s) {
     const int64_t n = (int64_t)S * B * D;
     const unsigned g = (unsigned)((n + 255) / 256);
-    if (dt == BC_BF16) build_cond_kernel<bf16><<<g, 256, 0, s>>>(temb, S, B, D, static_cast<const bf16*>(table), labels, n_rows, add, c);
+    if (dt == BC_BF16) build_cond_kernel<bf16_tag><<<g, 256, 0, s>>>(temb, S, B, D, static_cast<const bf16*>(table), labels, n_rows, add, c);
     else build_cond_kernel<float><<<g, 256, 0, s>>>(temb, S, B, D, static_cast<const float*>(table), labels, n_rows, add, c);
     return check_launch("build_cond");
 }
 
-template <typename T>
-__global__ void gather_silu_kernel(const float* c, int B, int D, RowList rows, int n, T* out) {
+template <typename T_>
+__global__ void gather_silu_kernel(const float* c, int B, int D, RowList rows, int n, elem_t<T_>* out) {
+    typedef elem_t<T_> T;
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= (int64_t)n * B * D) return;
     const int d = (int)(i % D);
@@ -351,14 +356,15 @@ int launch_gather_silu(int dt, const float* c, int B, int D, const RowList& rows
     if (n > kMaxSeg) return fail(BC_ERR_UNSUPPORTED, "gather of %d rows", n);
     const int64_t total = (int64_t)n * B * D;
     const unsigned g = (unsigned)((total + 255) / 256);
-    if (dt == BC_BF16) gather_silu_kernel<bf16><<<g, 256, 0, s>>>(c, B, D, rows, n, static_cast<bf16*>(out));
+    if (dt == BC_BF16) gather_silu_kernel<bf16_tag><<<g, 256, 0, s>>>(c, B, D, rows, n, static_cast<bf16*>(out));
     else gather_silu_kernel<float><<<g, 256, 0, s>>>(c, B, D, rows, n, static_cast<float*>(out));
     return check_launch("gather_silu");
 }
 
-template <typename T>
-__global__ void add_label_kernel(const float* t, const T* table, const int64_t* labels, int B, int D, int n_rows,
+template <typename T_>
+__global__ void add_label_kernel(const float* t, const elem_t<T_>* table, const int64_t* labels, int B, int D, int n_rows,
                                  float* c) {
+    typedef elem_t<T_> T;
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= (int64_t)B * D) return;
     const int b = (int)(i / D), n = (int)(i % D);
@@ -371,16 +377,17 @@ int launch_add_label(int dt, const float* t, const void* table, const int64_t* l
                      float* c, hipStream_t s) {
     const int64_t n = (int64_t)B * D;
     const unsigned g = (unsigned)((n + 255) / 256);
-    if (dt == BC_BF16) add_label_kernel<bf16><<<g, 256, 0, s>>>(t, static_cast<const bf16*>(table), labels, B, D, n_rows, c);
+    if (dt == BC_BF16) add_label_kernel<bf16_tag><<<g, 256, 0, s>>>(t, static_cast<const bf16*>(table), labels, B, D, n_rows, c);
     else add_label_kernel<float><<<g, 256, 0, s>>>(t, static_cast<const float*>(table), labels, B, D, n_rows, c);
     return check_launch("add_label");
 }
 
 struct TableArgs { const void* tab[kMaxSeg]; };
 
-template <typename T>
+template <typename T_>
 __global__ void add_tables_kernel(const float* vec, int64_t ld_vec, TableArgs ta, int nseg, int N, int B, float* out,
                                   int64_t ld_out) {
+    typedef elem_t<T_> T;
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= (int64_t)B * nseg * N) return;
     const int j = (int)(i % N);
@@ -396,13 +403,13 @@ int launch_add_tables(int dt, const float* vec, int64_t ld_vec, const void* cons
     for (int i = 0; i < nseg; ++i) ta.tab[i] = tables[i];
     const int64_t n = (int64_t)B * nseg * N;
     const unsigned g = (unsigned)((n + 255) / 256);
-    if (dt == BC_BF16) add_tables_kernel<bf16><<<g, 256, 0, s>>>(vec, ld_vec, ta, nseg, N, B, out, ld_out);
+    if (dt == BC_BF16) add_tables_kernel<bf16_tag><<<g, 256, 0, s>>>(vec, ld_vec, ta, nseg, N, B, out, ld_out);
     else add_tables_kernel<float><<<g, 256, 0, s>>>(vec, ld_vec, ta, nseg, N, B, out, ld_out);
     return check_launch("add_tables");
 }
 
-template <typename T>
-__global__ void token_mean_kernel(const T* x, int B, int T_, int D, float* out) {
+template <typename E_>
+__global__ void token_mean_kernel(const elem_t<E_>* x, int B, int T_, int D, float* out) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= (int64_t)B * D) return;
     const int b = (int)(i / D), n = (int)(i % D);
@@ -414,13 +421,15 @@ __global__ void token_mean_kernel(const T* x, int B, int T_, int D, float* out) 
 int launch_token_mean(int dt, const void* x, int B, int T, int D, float* out, hipStream_t s) {
     const int64_t n = (int64_t)B * D;
     const unsigned g = (unsigned)((n + 255) / 256);
-    if (dt == BC_BF16) token_mean_kernel<bf16><<<g, 256, 0, s>>>(static_cast<const bf16*>(x), B, T, D, out);
+    if (dt == BC_BF16) token_mean_kernel<bf16_tag><<<g, 256, 0, s>>>(static_cast<const bf16*>(x), B, T, D, out);
     else token_mean_kernel<float><<<g, 256, 0, s>>>(static_cast<const float*>(x), B, T, D, out);
     return check_launch("token_mean");
 }
 
-template <typename Tin, typename Tout>
-__global__ void convert_kernel(const Tin* in, Tout* out, int64_t n) {
+template <typename Tin_, typename Tout_>
+__global__ void convert_kernel(const elem_t<Tin_>* in, elem_t<Tout_>* out, int64_t n) {
+    typedef elem_t<Tin_> Tin;
+    typedef elem_t<Tout_> Tout;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
         st(out + i, ld(in + i));
 }
@@ -430,8 +439,8 @@ int launch_convert(int in_dt, const void* in, int out_dt, void* out, int64_t n, 
     int64_t blocks = (n + 255) / 256;
     if (blocks > 16384) blocks = 16384;
     const unsigned g = (unsigned)blocks;
-    if (in_dt == BC_F32 && out_dt == BC_BF16) convert_kernel<float, bf16><<<g, 256, 0, s>>>(static_cast<const float*>(in), static_cast<bf16*>(out), n);
-    else if (in_dt == BC_BF16 && out_dt == BC_F32) convert_kernel<bf16, float><<<g, 256, 0, s>>>(static_cast<const bf16*>(in), static_cast<float*>(out), n);
+    if (in_dt == BC_F32 && out_dt == BC_BF16) convert_kernel<float, bf16_tag><<<g, 256, 0, s>>>(static_cast<const float*>(in), static_cast<bf16*>(out), n);
+    else if (in_dt == BC_BF16 && out_dt == BC_F32) convert_kernel<bf16_tag, float><<<g, 256, 0, s>>>(static_cast<const bf16*>(in), static_cast<float*>(out), n);
     else return launch_copy(in, out, n * dtype_size(in_dt), s);
     return check_launch("convert");
 }
@@ -441,11 +450,12 @@ int launch_convert(int in_dt, const void* in, int out_dt, void* out, int64_t n, 
 // ---------------------------------------------------------------------------
 // One workgroup per token: gather its p*p*C patch values once (LDS), then
 // each thread produces output features of the row.
-template <typename T, int kPatchRows>
+template <typename T_, int kPatchRows>
 __global__ __launch_bounds__(256) void patch_embed_kernel(const float* __restrict__ lat, LatentShape ls,
-                                                          const T* __restrict__ W, const T* __restrict__ bias,
-                                                          const T* __restrict__ pos, int D, int lat_B, int rows,
+                                                          const elem_t<T_>* __restrict__ W, const elem_t<T_>* __restrict__ bias,
+                                                          const elem_t<T_>* __restrict__ pos, int D, int lat_B, int rows,
                                                           float* __restrict__ x) {
+    typedef elem_t<T_> T;
     // kPatchRows tokens per workgroup: each thread reads its columns' weight
     // rows once for all of them (the weights are [D, p*p*C], one row per
     // output column), and each output still sums its patch in order q = 0, 1, ...
@@ -501,7 +511,7 @@ int launch_patch_embed(int dt, const float* lat, LatentShape ls, int B, int lat_
         constexpr int TPB = decltype(tpb)::value;
         const unsigned grid = (unsigned)((rows + TPB - 1) / TPB);
         if (dt == BC_BF16)
-            patch_embed_kernel<bf16, TPB><<<grid, 256, 0, s>>>(lat, ls, static_cast<const bf16*>(W),
+            patch_embed_kernel<bf16_tag, TPB><<<grid, 256, 0, s>>>(lat, ls, static_cast<const bf16*>(W),
                                                                static_cast<const bf16*>(bias),
                                                                static_cast<const bf16*>(pos), D, lat_B, rows, x);
         else
@@ -565,11 +575,12 @@ int launch_sampler(const SamplerCoef& k, float* x, const float* out_tok, float* 
 // holds the pair (2i, 2i + 1) of the head, so the rotation is lane-local and
 // the RMS is one wave reduction.
 // ---------------------------------------------------------------------------
-template <typename T>
-__global__ __launch_bounds__(256) void qk_norm_rope_kernel(T* __restrict__ qkv, int64_t rows, int64_t ldr, int D,
-                                                           int heads, int hd, const T* __restrict__ wq,
-                                                           const T* __restrict__ wk, int L, int n_img, int gf,
+template <typename T_>
+__global__ __launch_bounds__(256) void qk_norm_rope_kernel(elem_t<T_>* __restrict__ qkv, int64_t rows, int64_t ldr, int D,
+                                                           int heads, int hd, const elem_t<T_>* __restrict__ wq,
+                                                           const elem_t<T_>* __restrict__ wk, int L, int n_img, int gf,
                                                            int gh, int gw, float log2_theta) {
+    typedef elem_t<T_> T;
     const int64_t wid = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 6;
     const int lane = threadIdx.x & 63;
     if (wid >= rows * heads * 2) return;   // whole waves
@@ -623,10 +634,10 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(T* __restrict__ qkv, 
 // four pairs (chunk l % CPH) of whichever head a chunk belongs to: it loads its
 // eight norm scales and works out its four rotations once per row.  A head's
 // RMS is a reduction over the CPH lanes that hold it.
-template <int CPH>
-__global__ __launch_bounds__(256) void qk_norm_rope_row_kernel(bf16* __restrict__ qkv, int64_t rows, int64_t ldr,
-                                                               int D, const bf16* __restrict__ wq,
-                                                               const bf16* __restrict__ wk, int L, int n_img, int gf,
+template <int CPH, typename B_>
+__global__ __launch_bounds__(256) void qk_norm_rope_row_kernel(elem_t<B_>* __restrict__ qkv, int64_t rows, int64_t ldr,
+                                                               int D, const elem_t<B_>* __restrict__ wq,
+                                                               const elem_t<B_>* __restrict__ wk, int L, int n_img, int gf,
                                                                int gh, int gw, float log2_theta) {
     constexpr int HD = 8 * CPH;
     const int64_t wid = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 6;
@@ -719,14 +730,14 @@ int launch_qk_norm_rope(int dt, void* qkv, int64_t rows, int64_t ld, int D, int 
         const bf16 *a = static_cast<const bf16*>(wq), *b = static_cast<const bf16*>(wk);
         const int ni = rope ? n_img : 0;
         if (head_dim == 128)
-            qk_norm_rope_row_kernel<16><<<gr, 256, 0, s>>>(q, rows, ld, D, a, b, rows_per_sample, ni, gf, gh, gw, l2t);
+            qk_norm_rope_row_kernel<16, bf16_tag><<<gr, 256, 0, s>>>(q, rows, ld, D, a, b, rows_per_sample, ni, gf, gh, gw, l2t);
         else
-            qk_norm_rope_row_kernel<8><<<gr, 256, 0, s>>>(q, rows, ld, D, a, b, rows_per_sample, ni, gf, gh, gw, l2t);
+            qk_norm_rope_row_kernel<8, bf16_tag><<<gr, 256, 0, s>>>(q, rows, ld, D, a, b, rows_per_sample, ni, gf, gh, gw, l2t);
         return check_launch("qk_norm_rope_row");
     }
     const unsigned g = (unsigned)((waves + 3) / 4);
     if (dt == BC_BF16)
-        qk_norm_rope_kernel<bf16><<<g, 256, 0, s>>>(static_cast<bf16*>(qkv), rows, ld, D, heads, head_dim,
+        qk_norm_rope_kernel<bf16_tag><<<g, 256, 0, s>>>(static_cast<bf16*>(qkv), rows, ld, D, heads, head_dim,
                                                     static_cast<const bf16*>(wq), static_cast<const bf16*>(wk),
                                                     rows_per_sample, rope ? n_img : 0, gf, gh, gw, l2t);
     else
@@ -757,10 +768,11 @@ __device__ __forceinline__ void load8(const float* p, float* v) {
     }
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void gated_add_kernel(const T* __restrict__ site, int64_t n8, int D,
+template <typename T_>
+__global__ __launch_bounds__(256) void gated_add_kernel(const elem_t<T_>* __restrict__ site, int64_t n8, int D,
                                                         float* __restrict__ x, const float* __restrict__ gate,
                                                         int64_t ldg, int rows_per_gate) {
+    typedef elem_t<T_> T;
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= n8) return;
     const int64_t e = i * 8, r = e / D;
@@ -787,13 +799,14 @@ int launch_gated_add(int dt, const void* site, int64_t rows, int D, float* x, co
     const int64_t n8 = rows * D / 8;
     if (n8 < 1) return BC_OK;
     const unsigned g = (unsigned)((n8 + 255) / 256);
-    if (dt == BC_BF16) gated_add_kernel<bf16><<<g, 256, 0, s>>>(static_cast<const bf16*>(site), n8, D, x, gate, ldg, rows_per_gate);
+    if (dt == BC_BF16) gated_add_kernel<bf16_tag><<<g, 256, 0, s>>>(static_cast<const bf16*>(site), n8, D, x, gate, ldg, rows_per_gate);
     else gated_add_kernel<float><<<g, 256, 0, s>>>(static_cast<const float*>(site), n8, D, x, gate, ldg, rows_per_gate);
     return check_launch("gated_add");
 }
 
-template <typename T>
+template <typename T_>
 __global__ __launch_bounds__(256) void blockwise_forecast_kernel(BlockwiseArgs a) {
+    typedef elem_t<T_> T;
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i * 8 >= a.numel) return;
     const int64_t e = i * 8, r = e / a.D;
@@ -835,7 +848,7 @@ int launch_blockwise_forecast(int dt, const BlockwiseArgs& a, hipStream_t s) {
             return fail(BC_ERR_INVALID_ARG, "blockwise forecast: gate offset %d", a.goff[q]);
     const int64_t n8 = a.numel / 8;
     const unsigned g = (unsigned)((n8 + 255) / 256);
-    if (dt == BC_BF16) blockwise_forecast_kernel<bf16><<<g, 256, 0, s>>>(a);
+    if (dt == BC_BF16) blockwise_forecast_kernel<bf16_tag><<<g, 256, 0, s>>>(a);
     else blockwise_forecast_kernel<float><<<g, 256, 0, s>>>(a);
     return check_launch("blockwise_forecast");
 }
@@ -863,9 +876,10 @@ __device__ __forceinline__ void abs_sums(const u32x4& c, const u32x4& p, float& 
     }
 }
 
-template <typename T>
-__global__ __launch_bounds__(256) void rel_l1_kernel(const T* __restrict__ cur, T* __restrict__ prev, int64_t n,
+template <typename T_>
+__global__ __launch_bounds__(256) void rel_l1_kernel(const elem_t<T_>* __restrict__ cur, elem_t<T_>* __restrict__ prev, int64_t n,
                                                      float* __restrict__ part) {
+    typedef elem_t<T_> T;
     constexpr int E = 16 / (int)sizeof(T);
     const int64_t nc = n / E;
     const u32x4* c4 = reinterpret_cast<const u32x4*>(cur);
@@ -931,7 +945,7 @@ int launch_rel_l1(int dt, const void* cur, void* prev, int64_t n, float* part, d
     const int64_t nc = n / (16 / (int64_t)dtype_size(dt));
     const int nblk = (int)std::min<int64_t>(kRelL1Blocks, std::max<int64_t>(1, (nc + 1023) / 1024));
     if (dt == BC_BF16)
-        rel_l1_kernel<bf16><<<nblk, 256, 0, s>>>(static_cast<const bf16*>(cur), static_cast<bf16*>(prev), n, part);
+        rel_l1_kernel<bf16_tag><<<nblk, 256, 0, s>>>(static_cast<const bf16*>(cur), static_cast<bf16*>(prev), n, part);
     else
         rel_l1_kernel<float><<<nblk, 256, 0, s>>>(static_cast<const float*>(cur), static_cast<float*>(prev), n, part);
     const int rc = check_launch("rel_l1");

@@ -147,3 +147,18 @@ def test_host_logic_under_address_and_ub_sanitizers(tmp_path):
     print(r.stdout)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "failures 0" in r.stdout
+
+
+def test_kernel_symbols_demangle(bclib):
+    """Every kernel symbol of the library demangles with the platform's
+    demangler (c++filt): element types reach kernel templates as tags, never
+    as __bf16, whose mangling (DF16b) older demanglers reject or misread —
+    as profilers' kernel names then do."""
+    out = subprocess.run(["nm", bclib.LIB_PATH], capture_output=True, text=True).stdout
+    names = sorted({l.split()[-1] for l in out.splitlines() if "_kernel" in l and l.split()[-1].startswith("_Z")})
+    assert len(names) > 50
+    assert not [n for n in names if "DF16b" in n]
+    dem = subprocess.run(["c++filt"], input="\n".join(names), capture_output=True, text=True).stdout.splitlines()
+    assert len(dem) == len(names)
+    bad = [(n, d) for n, d in zip(names, dem) if d == n or "_Accum" in d]
+    assert not bad, bad[:3]
