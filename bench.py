@@ -66,6 +66,9 @@ def parse():
                     help="launch only the roofline kernels at the workloads' shapes, for hardware-counter passes")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run one 1 GiB device copy through the library (counter calibration)")
+    ap.add_argument("--launch-log", default=None, help="--kernels-only: write the tag of every launch here")
+    ap.add_argument("--summarize-counters", default=None,
+                    help="write profiles/<tag>_counters.json from the rocprofv3 --pmc passes in this directory")
     return ap.parse_args()
 
 
@@ -171,6 +174,7 @@ def group_launches(records, cfg):
 
 
 def roofline_of(g, tag=None, src=None):
+    """Roofline record of a kernel group; traffic from its counter summary."""
     avg_s = g["avg_us"] / 1e6
     achieved = g["work"] / avg_s / 1e12
     r = {"bound": "mfma", "kernel": g["kernel"], "class": g["class"], "shape": g["shape"],
@@ -187,10 +191,12 @@ def roofline_of(g, tag=None, src=None):
 
 
 def counter_tag(cfg, g):
-    if g["class"] == "attention":
-        return f"attention_{cfg.name}", "attention"
-    short = {"gemm_down": "fc2", "gemm_gelu": "fc1", "gemm_bias": "qkv", "gemm_gated": "proj"}[g["class"]]
-    return f"gemm_{short}_{cfg.name}", "gemm"
+    """The counter-summary tag of a profiled kernel group (matched by its
+    algorithmic FLOPs among the counter program's kernels), or None."""
+    for k in kernel_tags(cfg):
+        if abs(k["flops"] - g["work"]) <= 1e-9 * g["work"]:
+            return k["tag"], k["tag"].split("_")[0]
+    return None, None
 
 
 # ---------------------------------------------------------------------------
@@ -277,10 +283,8 @@ def measure(bc, torch, cfg, steps, warmup, extras=False, adaptive_ell=0.13):
             e["frac_of_hbm_peak"] = round(e["gbs"] / PEAK_HBM_GBS, 4)
         classes[name] = e
     groups = [g for g in group_launches(records, cfg) if g["class"] in MFMA_CLASSES]
-    top = groups[0]
-    tag, src = counter_tag(cfg, top)
-    res["roofline"] = roofline_of(top, tag, src)
-    res["roofline_others"] = [roofline_of(g) for g in groups[1:6]]
+    res["roofline"] = roofline_of(groups[0], *counter_tag(cfg, groups[0]))
+    res["roofline_others"] = [roofline_of(g, *counter_tag(cfg, g)) for g in groups[1:6]]
     res["kernel_classes"] = classes
     res["profiled_run_ms"] = round(float(sum(float(ms.sum()) for ms, _ in records.values())), 3)
 
@@ -582,14 +586,37 @@ def cpu_baseline_image(cfg, nsteps=9):
 # counter program
 # ---------------------------------------------------------------------------
 
+def kernel_tags(cfg):
+    """Counter tags, shapes and algorithmic bytes / FLOPs of the kernels the
+    counter program launches for a workload (in launch order per block)."""
+    B, T, D, F, H, hd = cfg.batch, cfg.tokens, cfg.hidden, cfg.mlp, cfg.heads, cfg.head_dim
+    bf = 2
+    def gemm(tag, M, N, K, gated):
+        # A and W read once, output written once (+ the fp32 residual read for
+        # the gated epilogue: res read and out written as fp32)
+        byt = (M * K + N * K) * bf + (M * N * 8 if gated else M * N * bf)
+        return {"tag": f"gemm_{tag}_{cfg.name}", "shape": [M, N, K], "flops": 2.0 * M * N * K, "bytes": byt}
+    def att(L):
+        return {"tag": f"attention_{cfg.name}", "shape": [B, H, L, hd], "flops": 4.0 * B * H * L * L * hd,
+                "bytes": 4 * B * L * H * hd * bf}
+    if cfg.kind == "mmdit":
+        L = T + cfg.txt_tokens
+        return [gemm("single_in", B * L, 3 * D + F, D, False), att(L), gemm("single_out", B * L, D, D + F, True)]
+    M = B * T
+    return [gemm("qkv", M, 3 * D, D, False), att(T), gemm("proj", M, D, D, True), gemm("fc1", M, F, D, False),
+            gemm("fc2", M, D, F, True)]
+
+
 def kernels_only(args):
     """The roofline kernels at the workloads' shapes, launched through the C
     ABI without the sampling loop: the program the rocprofv3 counter passes
     run on.  Per workload, `steps` rounds over as many distinct weight sets as
-    the model has blocks (so weights arrive from HBM, as in the loop):
-    DiT-XL/2 QKV, out-projection, MLP up and down projections and
-    self-attention; the video model's joint attention and single-stream
-    projections; then the K = 3 bf16 forecast."""
+    the model has blocks (so weights arrive from HBM, as in the loop): for
+    DiT-XL/2 the QKV, out-projection, MLP up and down projections and
+    self-attention; for the video model the single-stream block's projections
+    and the joint attention over 14 566 tokens.  Then the K = 3 bf16 forecast
+    and, with --calib-copy, one 1 GiB copy of known size.  With --launch-log
+    the tag of every library launch is written there, in launch order."""
     import torch
 
     import synth
@@ -597,6 +624,7 @@ def kernels_only(args):
     dev = "cuda:0"
     g = torch.Generator(device=dev)
     g.manual_seed(synth.SEED)
+    log_tags = []
 
     def rnd(*shape, dt=torch.bfloat16, scale=0.02):
         t = torch.empty(shape, dtype=torch.float32, device=dev)
@@ -605,6 +633,7 @@ def kernels_only(args):
 
     for name in args.workload.split(","):
         cfg = synth.CONFIGS[name]
+        tags = [k["tag"] for k in kernel_tags(cfg)]
         B, T, D, F, H, hd = cfg.batch, cfg.tokens, cfg.hidden, cfg.mlp, cfg.heads, cfg.head_dim
         if cfg.kind == "mmdit":
             L = T + cfg.txt_tokens
@@ -623,6 +652,7 @@ def kernels_only(args):
                     bc.linear(h, w1[i], b1, y, bc.EPI_BIAS_GELU)
                     bc.attention(q, k, v, o)
                     bc.linear(z, w2[i], b2, xs, bc.EPI_GATE_RES, res=xs, gate=gate, rows_per_gate=L)
+                    log_tags += tags
             torch.cuda.synchronize()
             del w1, w2, h, y, z, xs, q, k, v, o
         else:
@@ -647,6 +677,7 @@ def kernels_only(args):
                     bc.linear(a, wo[i], bo, x, bc.EPI_GATE_RES, res=x, gate=gate, rows_per_gate=T)
                     bc.linear(h, w1[i], b1, hm, bc.EPI_BIAS_GELU)
                     bc.linear(hm, w2[i], b2, x, bc.EPI_GATE_RES, res=x, gate=gate, rows_per_gate=T)
+                    log_tags += tags
             torch.cuda.synchronize()
             del wq, wo, w1, w2, h, qkv, a, hm, x, q, k, v, o
         torch.cuda.empty_cache()
@@ -661,6 +692,7 @@ def kernels_only(args):
     w = bc.bary_weights(s, t)
     for _ in range(args.steps):
         bc.bary_extrapolate(ring, w, out)
+        log_tags.append("forecast_k3_bf16")
     torch.cuda.synchronize()
     del storage, out, ring
     if args.calib_copy:
@@ -669,8 +701,92 @@ def kernels_only(args):
         store = torch.empty((1, nn), dtype=torch.bfloat16, device=dev)
         ring = bc.CacheRing(1, store)
         ring.push(src, 0.0)
+        log_tags.append("calib_copy_1gib")
         torch.cuda.synchronize()
-    print(json.dumps({"kernels_only": args.workload, "rounds": args.steps}), flush=True)
+    if args.launch_log:
+        with open(args.launch_log, "w") as f:
+            json.dump(log_tags, f)
+    print(json.dumps({"kernels_only": args.workload, "rounds": args.steps, "launches": len(log_tags)}), flush=True)
+
+
+def summarize_counters(args):
+    """Per-kernel summaries of rocprofv3 --pmc passes over the counter program
+    (--kernels-only): each directory under args.summarize_counters holds one
+    pass's run_counter_collection.csv; launches.json the program's launch log.
+    HBM bytes: FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by
+    the ratio of known bytes to the counter's reading on the 1 GiB copy.
+    Writes profiles/<tag>_counters.json."""
+    import csv
+    import glob
+    import statistics
+
+    import synth
+    root = args.summarize_counters
+    tags = json.load(open(os.path.join(root, "launches.json")))
+    per = {}   # counter -> list per library dispatch (in order)
+    for path in sorted(glob.glob(os.path.join(root, "*", "run_counter_collection.csv"))):
+        rows = list(csv.DictReader(open(path)))
+        vals, names = {}, {}
+        for r in rows:
+            d = int(r["Dispatch_Id"])
+            names[d] = r["Kernel_Name"]
+            vals.setdefault(d, {}).setdefault(r["Counter_Name"], 0.0)
+            vals[d][r["Counter_Name"]] += float(r["Counter_Value"])
+        lib = [d for d in sorted(names) if names[d].startswith(("void bc::", "bc::"))]
+        if len(lib) != len(tags):
+            raise SystemExit(f"{path}: {len(lib)} library dispatches, launch log has {len(tags)}")
+        for d, tag in zip(lib, tags):
+            for c, v in vals[d].items():
+                per.setdefault(tag, {}).setdefault(c, []).append(v)
+            per[tag].setdefault("_kernel", set()).add(names[d])
+    calib = per.get("calib_copy_1gib")
+    if not calib:
+        raise SystemExit("no calibration copy in the launch log")
+    nbytes = float(1 << 30)
+    f_fetch = nbytes / (calib["FETCH_SIZE"][0] * 1024.0)
+    f_write = nbytes / (calib["WRITE_SIZE"][0] * 1024.0)
+    known = {}
+    for name in args.workload.split(","):
+        for k in kernel_tags(synth.CONFIGS[name]):
+            known[k["tag"]] = k
+    n = synth.FORECAST_SHAPE[0] * synth.FORECAST_SHAPE[1] * synth.FORECAST_SHAPE[2]
+    known["forecast_k3_bf16"] = {"tag": "forecast_k3_bf16", "shape": list(synth.FORECAST_SHAPE), "bytes": 4 * n * 2}
+    src_for = {"attention": KERNEL_SOURCES["attention"], "gemm": KERNEL_SOURCES["gemm"],
+               "forecast": KERNEL_SOURCES["forecast"]}
+    written = []
+    for tag, c in per.items():
+        if tag == "calib_copy_1gib":
+            continue
+        med = {k: statistics.median(v) for k, v in c.items() if k != "_kernel"}
+        info = known[tag]
+        rec = {"tag": tag, "kernel": sorted(c["_kernel"]), "shape": info["shape"], "dispatches": len(c.get("FETCH_SIZE", [])),
+               "source_hash": source_hash(*src_for[tag.split("_")[0]]),
+               "command": "rocprofv3 --pmc <counters> -d <dir>/<pass> -o run --output-format csv -- python3 bench.py "
+                          f"--kernels-only --workload {args.workload} --steps {args.steps} --calib-copy "
+                          "--launch-log <dir>/launches.json  (passes: FETCH_SIZE; WRITE_SIZE; SQ counters)",
+               "calibration": {"copy_bytes": int(nbytes), "fetch_factor": round(f_fetch, 4),
+                               "write_factor": round(f_write, 4)},
+               "counters_median_per_dispatch": {k: round(v, 1) for k, v in med.items()}}
+        if "FETCH_SIZE" in med and "WRITE_SIZE" in med:
+            rec["hbm_fetch_bytes"] = int(med["FETCH_SIZE"] * 1024 * f_fetch)
+            rec["hbm_write_bytes"] = int(med["WRITE_SIZE"] * 1024 * f_write)
+            rec["hbm_bytes_per_launch"] = rec["hbm_fetch_bytes"] + rec["hbm_write_bytes"]
+            rec["algorithmic_bytes"] = int(info["bytes"])
+            rec["traffic_over_algorithmic"] = round(rec["hbm_bytes_per_launch"] / info["bytes"], 3)
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in med and "GRBM_GUI_ACTIVE" in med:
+            # GRBM_GUI_ACTIVE is reported per XCD (8 instances summed), MFMA busy per SIMD (1024 summed)
+            rec["mfma_busy_frac"] = round(med["SQ_VALU_MFMA_BUSY_CYCLES"] / 1024 / (med["GRBM_GUI_ACTIVE"] / 8), 4)
+            if "SQ_VALU_MFMA_COEXEC_CYCLES" in med:
+                rec["mfma_valu_coexec_frac"] = round(med["SQ_VALU_MFMA_COEXEC_CYCLES"] / 1024 / (med["GRBM_GUI_ACTIVE"] / 8), 4)
+            if "SQ_LDS_BANK_CONFLICT" in med and "SQ_LDS_IDX_ACTIVE" in med:
+                rec["lds_bank_conflict_over_active"] = round(med["SQ_LDS_BANK_CONFLICT"] / max(med["SQ_LDS_IDX_ACTIVE"], 1), 4)
+        if "flops" in info:
+            rec["flops_per_launch"] = info["flops"]
+        out = os.path.join(ROOT, "profiles", f"{tag}_counters.json")
+        with open(out, "w") as f:
+            json.dump(rec, f, indent=1)
+        written.append(out)
+    print(json.dumps({"written": written}))
 
 
 # ---------------------------------------------------------------------------
@@ -683,6 +799,9 @@ def main():
         sys.exit(2)
     if args.kernels_only:
         kernels_only(args)
+        return
+    if args.summarize_counters:
+        summarize_counters(args)
         return
     import torch
 
