@@ -67,6 +67,8 @@ def parse():
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run one 1 GiB device copy through the library (counter calibration)")
     ap.add_argument("--launch-log", default=None, help="--kernels-only: write the tag of every launch here")
+    ap.add_argument("--summarize-trace", default=None,
+                    help="STATS_CSV,LINE_JSON: write profiles/bench_kernel_trace.md from a kernel-trace run")
     ap.add_argument("--summarize-counters", default=None,
                     help="write profiles/<tag>_counters.json from the rocprofv3 --pmc passes in this directory")
     return ap.parse_args()
@@ -789,6 +791,37 @@ def summarize_counters(args):
     print(json.dumps({"written": written}))
 
 
+def summarize_trace(args):
+    """profiles/bench_kernel_trace.md from a rocprofv3 --kernel-trace --stats
+    run of the default bench command (run_kernel_stats.csv) and the JSON line
+    that run printed."""
+    import csv
+    stats_path, line_path = args.summarize_trace.split(",")
+    rows = list(csv.DictReader(open(stats_path)))
+    rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    line = json.load(open(line_path))
+    total = sum(float(r["TotalDurationNs"]) for r in rows)
+    out = ["# Kernel trace of the default benchmark command", "",
+           "Command (from a shell in `/tmp`, `TMPDIR=/tmp`):", "",
+           "    rocprofv3 --kernel-trace --stats -d <dir> -o run --output-format csv -- "
+           "python3 bench.py --gpus 1 --steps 20 --warmup 5", "",
+           "The run covers everything the command does: the video workload (5 warm-up, 20 timed and one "
+           "event-timed sampling runs, then one all-full-mask run), the DiT-XL/2 and PixArt legs, the forecast sweep, "
+           "the push copy.  Per-call averages are the figures to compare with the JSON line's per-launch averages "
+           "(which come from HIP events in the same process).", "",
+           f"JSON line of this traced run: value {line['value']} samples/s, {line['ms_per_step']} ms per sampling run; "
+           f"roofline kernel `{line['roofline']['kernel']}` avg {line['roofline']['avg_us']} us "
+           f"-> {line['roofline']['achieved']} TFLOP/s = {line['roofline']['frac']} of {line['roofline']['peak']}.", "",
+           "| kernel | calls | total ms | avg us | share |", "|---|---|---|---|---|"]
+    for r in rows[:30]:
+        out.append(f"| `{r['Name'][:150]}` | {r['Calls']} | {float(r['TotalDurationNs']) / 1e6:.1f} | "
+                   f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['TotalDurationNs']) / total:.1%} |")
+    path = os.path.join(ROOT, "profiles", "bench_kernel_trace.md")
+    with open(path, "w") as f:
+        f.write("\n".join(out) + "\n")
+    print(path)
+
+
 # ---------------------------------------------------------------------------
 
 def main():
@@ -802,6 +835,9 @@ def main():
         return
     if args.summarize_counters:
         summarize_counters(args)
+        return
+    if args.summarize_trace:
+        summarize_trace(args)
         return
     import torch
 
