@@ -69,6 +69,11 @@ def parse():
     ap.add_argument("--launch-log", default=None, help="--kernels-only: write the tag of every launch here")
     ap.add_argument("--summarize-trace", default=None,
                     help="STATS_CSV,LINE_JSON: write profiles/bench_kernel_trace.md from a kernel-trace run")
+    ap.add_argument("--loop-counters", action="store_true",
+                    help="run the workload's sampling loop --steps times and the 1 GiB calibration copy, nothing "
+                         "else (the program of the whole-loop rocprofv3 --pmc passes)")
+    ap.add_argument("--summarize-loop-counters", default=None,
+                    help="write profiles/sampling_loop_<workload>_counters.md from the --pmc passes in this directory")
     ap.add_argument("--summarize-counters", default=None,
                     help="write profiles/<tag>_counters.json from the rocprofv3 --pmc passes in this directory")
     return ap.parse_args()
@@ -791,6 +796,118 @@ def summarize_counters(args):
     print(json.dumps({"written": written}))
 
 
+def loop_counters(args):
+    """The whole sampling loop of --workload, --steps runs back to back, then
+    one 1 GiB copy through the library's push path (counter calibration):
+    what the whole-loop counter passes profile."""
+    import torch
+
+    import synth
+    from paper_2608_28670_amd import loader
+    bc = ensure_library()
+    dev = "cuda:0"
+    cfg = synth.CONFIGS[args.workload]
+    dm = loader.DeviceModel(cfg, None, dev_params=device_params(cfg, torch, dev))
+    mask = bc.make_mask(cfg.steps, cfg.interval)
+    labels = synth.labels(cfg) if cfg.n_classes else None
+    text = synth.text(cfg) if cfg.kind != "dit" else None
+    x = torch.from_numpy(synth.latents(cfg)).to(dev)
+    tl = torch.from_numpy(labels).to(dev) if labels is not None else None
+    tt = torch.from_numpy(text).to(dev).to(loader.torch_dtype(cfg)) if text is not None else None
+    for r in range(args.steps):
+        dm.sample(x, mask, labels=tl, text=tt)
+        torch.cuda.synchronize()
+        log(f"[{cfg.name}] sampling run {r + 1} of {args.steps} done")
+    del dm
+    torch.cuda.empty_cache()
+    nn = 1 << 29
+    src = torch.ones(nn, dtype=torch.bfloat16, device=dev)
+    store = torch.empty((1, nn), dtype=torch.bfloat16, device=dev)
+    ring = bc.CacheRing(1, store)
+    ring.push(src, 0.0)
+    torch.cuda.synchronize()
+    print(json.dumps({"loop_counters": args.workload, "runs": args.steps, "full_steps": int(mask.sum())}), flush=True)
+
+
+def summarize_loop_counters(args):
+    """profiles/sampling_loop_<workload>_counters.md from rocprofv3 --pmc
+    passes over `bench.py --loop-counters` (one run_counter_collection.csv per
+    pass directory under args.summarize_loop_counters): per kernel, the
+    dispatches of one sampling run, HBM bytes per dispatch (FETCH_SIZE and
+    WRITE_SIZE scaled by the calibration copy, the last library dispatch) and
+    MFMA-busy / VALU-active fractions of the dispatch's cycles."""
+    import csv
+    import glob
+    import statistics
+    root = args.summarize_loop_counters
+    per = {}      # kernel -> counter -> [values per dispatch]
+    calib = {}
+    passes = []
+    for path in sorted(glob.glob(os.path.join(root, "*", "run_counter_collection.csv"))):
+        vals, names = {}, {}
+        for r in csv.DictReader(open(path)):
+            d = int(r["Dispatch_Id"])
+            names[d] = r["Kernel_Name"]
+            vals.setdefault(d, {}).setdefault(r["Counter_Name"], 0.0)
+            vals[d][r["Counter_Name"]] += float(r["Counter_Value"])
+        lib = [d for d in sorted(names) if names[d].startswith(("void bc::", "bc::"))]
+        passes.append(os.path.basename(os.path.dirname(path)) + ": " + ", ".join(sorted(vals[lib[0]])))
+        last = lib[-1]
+        for c, v in vals[last].items():
+            calib[c] = v
+        for d in lib[:-1]:
+            for c, v in vals[d].items():
+                per.setdefault(names[d], {}).setdefault(c, []).append(v)
+    nbytes = float(1 << 30)
+    f_fetch = nbytes / (calib["FETCH_SIZE"] * 1024.0) if "FETCH_SIZE" in calib else None
+    f_write = nbytes / (calib["WRITE_SIZE"] * 1024.0) if "WRITE_SIZE" in calib else None
+    runs = args.steps
+    rows = []
+    for name, c in per.items():
+        n = max(len(v) for v in c.values())
+        med = {k: statistics.median(v) for k, v in c.items()}
+        tot = {k: sum(v) for k, v in c.items()}
+        r = {"name": name, "per_run": n / runs}
+        if f_fetch and "FETCH_SIZE" in med:
+            r["fetch_mb"] = med["FETCH_SIZE"] * 1024 * f_fetch / 1e6
+        if f_write and "WRITE_SIZE" in med:
+            r["write_mb"] = med["WRITE_SIZE"] * 1024 * f_write / 1e6
+        if "GRBM_GUI_ACTIVE" in tot:
+            cyc = tot["GRBM_GUI_ACTIVE"] / 8          # per XCD, summed over the 8
+            r["cycles_per_run"] = cyc / runs
+            if "SQ_VALU_MFMA_BUSY_CYCLES" in tot:
+                r["mfma_busy"] = tot["SQ_VALU_MFMA_BUSY_CYCLES"] / 1024 / cyc
+            if "SQ_ACTIVE_INST_VALU" in tot:
+                r["valu_active"] = tot["SQ_ACTIVE_INST_VALU"] * 4 / 1024 / cyc
+        rows.append(r)
+    rows.sort(key=lambda r: -r.get("cycles_per_run", 0.0))
+    total_cyc = sum(r.get("cycles_per_run", 0.0) for r in rows)
+    out = [f"# Hardware counters over the whole sampling loop: {args.workload}", "",
+           "Commands (from a shell in `/tmp`, `TMPDIR=/tmp`), one pass per counter set:", "",
+           f"    rocprofv3 --pmc <counters> -d <dir>/<pass> -o run --output-format csv -- "
+           f"python3 bench.py --loop-counters --workload {args.workload} --steps {runs}",
+           f"    python3 bench.py --summarize-loop-counters <dir> --workload {args.workload} --steps {runs}", "",
+           "Passes: " + "; ".join(passes) + ".", "",
+           "Counter runs serialise the dispatches, so cycles are each dispatch's own duration "
+           "(GRBM_GUI_ACTIVE, summed over the 8 XCDs and divided by 8). HBM bytes: FETCH_SIZE and WRITE_SIZE "
+           "(KiB per dispatch, medians) times the factor that makes the 1 GiB calibration copy read its known "
+           f"size (fetch x{f_fetch:.4f}, write x{f_write:.4f})." if f_fetch and f_write else "",
+           "MFMA busy: SQ_VALU_MFMA_BUSY_CYCLES over the 1024 SIMDs' cycles; VALU active: SQ_ACTIVE_INST_VALU "
+           "(counted per 4 cycles) over the same.", "",
+           "| kernel | dispatches per run | share of cycles | fetch MB | write MB | MFMA busy | VALU active |",
+           "|---|---|---|---|---|---|---|"]
+    def f(r, k, fmt):
+        return format(r[k], fmt) if k in r else "-"
+    for r in rows[:40]:
+        share = r.get("cycles_per_run", 0.0) / total_cyc if total_cyc else 0.0
+        out.append(f"| `{r['name'][:140]}` | {r['per_run']:.0f} | {share:.1%} | {f(r, 'fetch_mb', '.1f')} | "
+                   f"{f(r, 'write_mb', '.1f')} | {f(r, 'mfma_busy', '.1%')} | {f(r, 'valu_active', '.1%')} |")
+    path = os.path.join(ROOT, "profiles", f"sampling_loop_{args.workload}_counters.md")
+    with open(path, "w") as fh:
+        fh.write("\n".join(out) + "\n")
+    print(path)
+
+
 def summarize_trace(args):
     """profiles/bench_kernel_trace.md from a rocprofv3 --kernel-trace --stats
     run of the default bench command (run_kernel_stats.csv) and the JSON line
@@ -835,6 +952,12 @@ def main():
         return
     if args.summarize_counters:
         summarize_counters(args)
+        return
+    if args.loop_counters:
+        loop_counters(args)
+        return
+    if args.summarize_loop_counters:
+        summarize_loop_counters(args)
         return
     if args.summarize_trace:
         summarize_trace(args)

@@ -64,8 +64,7 @@ __global__ __launch_bounds__(kAttnThreads) void attention_kernel(AttnArgs a) {
     // head) share one L2 and its keys and values are fetched once per XCD.
     const int nqt = (Tq + QT - 1) / QT;
     const int nwg = gridDim.x;
-    int pid = blockIdx.x;
-    if ((nwg & 7) == 0) pid = (pid & 7) * (nwg >> 3) + (pid >> 3);
+    const int pid = xcd_contiguous(blockIdx.x, nwg);
     const int qt = pid % nqt;
     const int h = (pid / nqt) % a.H;
     const int b = pid / (nqt * a.H);
@@ -360,8 +359,7 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
     const int Tq = a.Tq0 + a.Tq1, Tk = a.Tk0 + a.Tk1;
     const int nqt = (Tq + QT - 1) / QT;
     const int nwg = gridDim.x;
-    int pid = blockIdx.x;
-    if ((nwg & 7) == 0) pid = (pid & 7) * (nwg >> 3) + (pid >> 3);
+    const int pid = xcd_contiguous(blockIdx.x, nwg);
     const int qt = pid % nqt;
     const int h = (pid / nqt) % a.H;
     const int b = pid / (nqt * a.H);

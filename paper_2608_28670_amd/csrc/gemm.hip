@@ -117,8 +117,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(GemmArgs g
     const int tiles_m = (g.M + BM - 1) / BM;
     const int tiles_n = (g.N + BN - 1) / BN;
     const int nwg = gridDim.x;
-    int pid = blockIdx.x;
-    if ((nwg & 7) == 0) pid = (pid & 7) * (nwg >> 3) + (pid >> 3);
+    const int pid = xcd_contiguous(blockIdx.x, nwg);
     constexpr int GROUP_M = 8;
     const int group = GROUP_M * tiles_n;
     const int first_m = (pid / group) * GROUP_M;
@@ -262,8 +261,7 @@ __device__ __forceinline__ void gemm_dma_body(GemmArgs g, const GemmSeg* sg) {
     const int tiles_m = (g.M + BM - 1) / BM;
     const int tiles_n = (g.N + BN - 1) / BN;
     const int nwg = gridDim.x;
-    int pid = blockIdx.x;
-    if ((nwg & 7) == 0) pid = (pid & 7) * (nwg >> 3) + (pid >> 3);
+    const int pid = xcd_contiguous(blockIdx.x, nwg);
     constexpr int GROUP_M = 8;
     const int group = GROUP_M * tiles_n;
     const int first_m = (pid / group) * GROUP_M;
@@ -548,8 +546,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KG) void gemm_wide_kernel(
     const int tiles_m = (g.M + BM - 1) / BM;
     const int tiles_n = (g.N + BN - 1) / BN;
     const int nwg = gridDim.x;
-    int pid = blockIdx.x;
-    if ((nwg & 7) == 0) pid = (pid & 7) * (nwg >> 3) + (pid >> 3);
+    const int pid = xcd_contiguous(blockIdx.x, nwg);
     const int tile = pid;
     constexpr int GROUP_M = 8;
     const int group = GROUP_M * tiles_n;

@@ -47,6 +47,17 @@ __device__ __forceinline__ void unpack(const u32x4& u, float* f, const float*) {
     f[2] = __uint_as_float(u.z); f[3] = __uint_as_float(u.w);
 }
 
+// Workgroup id -> tile id with each XCD holding a contiguous range of tiles.
+// The dispatcher deals workgroups round-robin to the 8 XCDs (workgroup i to
+// XCD i % 8), so XCD x receives nwg / 8 workgroups, plus one more when
+// x < nwg % 8; numbering those consecutively keeps neighbouring tiles, which
+// share operands, in one XCD's L2.  A bijection on [0, nwg) for any nwg.
+__device__ __forceinline__ int xcd_contiguous(int bid, int nwg) {
+    const int q = nwg >> 3, r = nwg & 7;
+    const int x = bid & 7, i = bid >> 3;
+    return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
+}
+
 template <typename T> struct ElemsPer16B { static constexpr int v = 16 / (int)sizeof(T); };
 
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + __expf(-x)); }
