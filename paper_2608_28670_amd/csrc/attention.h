@@ -20,8 +20,14 @@ struct AttnArgs {
     void *o0, *o1;
     int64_t ldo;
     int B, H, d;
+    // 1: q was written already multiplied by attn_q_scale(d) (its producer
+    // rounded q * scale once), so scores leave the MFMA in log2 units.
+    int q_scaled;
     float scale_log2;   // set by the launcher
 };
+
+// Softmax scale in log2 units: log2(e) / sqrt(head_dim).
+inline float attn_q_scale(int head_dim) { return 1.4426950408889634f / sqrtf((float)head_dim); }
 
 bool attention_supported(int head_dim);
 int launch_attention(int dtype, AttnArgs a, hipStream_t s);

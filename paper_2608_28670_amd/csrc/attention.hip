@@ -339,7 +339,7 @@ __device__ __forceinline__ float group_sum(float v) {
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
-template <int HD, int QG, int NWV, int NB, bool STREAM>
+template <int HD, int QG, int NWV, int NB, bool STREAM, bool QS>
 __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
     typedef AttnShape<bf16, HD> S;
     typedef KvLayout<HD> LY;
@@ -471,21 +471,60 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
     float m_run[QG];
 #pragma unroll
     for (int g = 0; g < QG; ++g) {
-        m_run[g] = -INFINITY;
+        m_run[g] = QS ? 0.f : -INFINITY;     // the pre-scaled streaming tile's reference starts at 0
         osum[g] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int i = 0; i < S::DV / 16; ++i) o[g][i] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
 
 
-    // Scores, online softmax and the P V update of one 64-key tile at k0.
+    // O^T += V^T P^T for one tile's probabilities (and the row sums, see above).
+    auto pv = [&](const bf16* V, f32x4 (&s)[QG][4]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            bf16x8 pf[QG];
+#pragma unroll
+            for (int g = 0; g < QG; ++g)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    pf[g][r] = (bf16)s[g][2 * u][r];
+                    pf[g][4 + r] = (bf16)s[g][2 * u + 1][r];
+                }
+            const int kb0 = 32 * u + 4 * grp + (ql >> 2);      // this lane's source key, first half
+            const int dsub = 4 * (ql & 3);
+#pragma unroll
+            for (int i = 0; i < S::DV / 16; ++i) {
+                const int d0 = 16 * i + dsub;
+                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) s16x4*)(V + LY::at(kb0, d0)));
+                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) s16x4*)(V + LY::at(kb0 + 16, d0)));
+                bf16x8 vf = __builtin_bit_cast(bf16x8, u32x4{__builtin_bit_cast(u32x2, lo).x, __builtin_bit_cast(u32x2, lo).y,
+                                                            __builtin_bit_cast(u32x2, hi).x, __builtin_bit_cast(u32x2, hi).y});
+                // Padding rows d >= HD of the last block take ones: their
+                // output rows become the row sums of P (as rounded for the MFMA).
+                if (PADSUM && i == S::DV / 16 - 1 && (lane & 15) >= HD - 16 * i)
+                    vf = __builtin_bit_cast(bf16x8, u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
+#pragma unroll
+                for (int g = 0; g < QG; ++g) o[g][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[g], o[g][i], 0, 0, 0);
+            }
+            if constexpr (!PADSUM) {
+                const bf16x8 ones = __builtin_bit_cast(bf16x8, u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
+#pragma unroll
+                for (int g = 0; g < QG; ++g) osum[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[g], osum[g], 0, 0, 0);
+            }
+        }
+    };
+
+    // Scores, online softmax and the P V update of one 64-key tile at k0, for
+    // queries not pre-scaled (scores times c in one FMA with the max).
     // Keys past Tk occur in the last tile only.  Two ways to mask them:
-    //   * branch (the streaming loop of the STREAM instantiations): after the MFMAs, their scores are set
-    //     to -inf under a branch taken once per workgroup, so the other tiles
-    //     spend no instructions on the mask;
-    //   * select (otherwise): their score accumulators
-    //     start at -inf, one select per score slot shared by the query groups,
-    //     which keeps the tile one basic block for the scheduler.
+    //   * branch (the streaming loop of the STREAM instantiations): after the
+    //     MFMAs, their scores are set to -inf under a branch taken once per
+    //     workgroup, so the other tiles spend no instructions on the mask;
+    //   * select (otherwise): their score accumulators start at -inf, one
+    //     select per score slot shared by the query groups, which keeps the
+    //     tile one basic block for the scheduler.
     auto tile = [&](int k0, const bf16* K, const bf16* V, auto branch_mask) __attribute__((always_inline)) {
         constexpr bool BRANCH = decltype(branch_mask)::value;
         f32x4 init[4];
@@ -549,40 +588,83 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
                 }
         }
 
+        pv(V, s);
+    };
+
+    // Streaming tile for pre-scaled queries (QS: q already carries the factor
+    // c = log2(e) / sqrt(d)), so the MFMA yields scores in log2 units.  Each
+    // group's score accumulators start at -m (m: the group's reference max),
+    // so the MFMA output is already s c - m and p = 2^(output): no per-score
+    // FMA.  The reference moves (by the tile's excess, with O and the row
+    // sums rescaled) on the first tile and whenever some lane's tile max
+    // exceeds it by more than 8, which keeps p < 2^8.  Keys past Tk occur only
+    // in the last tile; their scores are set to -inf under a branch.  The row
+    // max takes 8 three-input maxima for the 16 scores of a lane.
+    f32x4 negm[QG];
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            bf16x8 pf[QG];
+    for (int g = 0; g < QG; ++g) negm[g] = f32x4{0.f, 0.f, 0.f, 0.f};
+    auto tile_stream = [&](int k0, const bf16* K, const bf16* V, bool first) __attribute__((always_inline)) {
+        f32x4 s[QG][4];
 #pragma unroll
-            for (int g = 0; g < QG; ++g)
+        for (int j = 0; j < 4; ++j) {
+            const int krow = 16 * j + ql;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    pf[g][r] = (bf16)s[g][2 * u][r];
-                    pf[g][4 + r] = (bf16)s[g][2 * u + 1][r];
-                }
-            const int kb0 = 32 * u + 4 * grp + (ql >> 2);      // this lane's source key, first half
-            const int dsub = 4 * (ql & 3);
+            for (int c = 0; c < S::n32x; ++c) {
+                const bf16x8 kf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(K + LY::at(krow, 32 * c + grp * 8)));
 #pragma unroll
-            for (int i = 0; i < S::DV / 16; ++i) {
-                const int d0 = 16 * i + dsub;
-                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (__attribute__((address_space(3))) s16x4*)(V + LY::at(kb0, d0)));
-                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (__attribute__((address_space(3))) s16x4*)(V + LY::at(kb0 + 16, d0)));
-                bf16x8 vf = __builtin_bit_cast(bf16x8, u32x4{__builtin_bit_cast(u32x2, lo).x, __builtin_bit_cast(u32x2, lo).y,
-                                                            __builtin_bit_cast(u32x2, hi).x, __builtin_bit_cast(u32x2, hi).y});
-                // Padding rows d >= HD of the last block take ones: their
-                // output rows become the row sums of P (as rounded for the MFMA).
-                if (PADSUM && i == S::DV / 16 - 1 && (lane & 15) >= HD - 16 * i)
-                    vf = __builtin_bit_cast(bf16x8, u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
-#pragma unroll
-                for (int g = 0; g < QG; ++g) o[g][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[g], o[g][i], 0, 0, 0);
-            }
-            if constexpr (!PADSUM) {
-                const bf16x8 ones = __builtin_bit_cast(bf16x8, u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
-#pragma unroll
-                for (int g = 0; g < QG; ++g) osum[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[g], osum[g], 0, 0, 0);
+                for (int g = 0; g < QG; ++g)
+                    s[g][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[g][c], c == 0 ? negm[g] : s[g][j], 0, 0, 0);
             }
         }
+        if (k0 + kKTile > Tk) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    if (k0 + 16 * j + 4 * grp + r >= Tk) {
+#pragma unroll
+                        for (int g = 0; g < QG; ++g) s[g][j][r] = -INFINITY;
+                    }
+        }
+        float mloc[QG];
+#pragma unroll
+        for (int g = 0; g < QG; ++g) {
+            const f32x4* v = s[g];
+            float m1 = vmax(vmax(v[0][0], v[0][1]), v[0][2]);
+            float m2 = vmax(vmax(v[0][3], v[1][0]), v[1][1]);
+            float m3 = vmax(vmax(v[1][2], v[1][3]), v[2][0]);
+            float m4 = vmax(vmax(v[2][1], v[2][2]), v[2][3]);
+            float m5 = vmax(vmax(v[3][0], v[3][1]), v[3][2]);
+            float m6 = vmax(vmax(m1, m2), v[3][3]);
+            float m7 = vmax(vmax(m3, m4), m5);
+            mloc[g] = group_max(vmax(m6, m7));
+        }
+        bool any_up = first;
+#pragma unroll
+        for (int g = 0; g < QG; ++g) any_up = any_up || mloc[g] > 8.0f;
+        if (__any(any_up)) {
+#pragma unroll
+            for (int g = 0; g < QG; ++g) {
+                const float shift = first ? mloc[g] : vmax(mloc[g], 0.f);
+                m_run[g] += shift;
+                negm[g] = f32x4{-m_run[g], -m_run[g], -m_run[g], -m_run[g]};
+                if (!first) {
+                    const float alpha = __builtin_amdgcn_exp2f(-shift);
+                    if constexpr (!PADSUM) osum[g] *= alpha;
+#pragma unroll
+                    for (int i = 0; i < S::DV / 16; ++i) o[g][i] *= alpha;
+                }
+#pragma unroll
+                for (int j = 0; j < 4; ++j) s[g][j] -= shift;
+            }
+        }
+#pragma unroll
+        for (int g = 0; g < QG; ++g)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) s[g][j][r] = __builtin_amdgcn_exp2f(s[g][j][r]);
+        pv(V, s);
     };
 
     if (resident) {
@@ -595,7 +677,8 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
             __builtin_amdgcn_s_waitcnt((0 & 15) | (7 << 4) | (15 << 8));   // vmcnt(0): this wave's loads of tile t
             __syncthreads();
             if (t + 1 < ntiles) issue((t + 1) * kKTile, buf ^ 1);
-            tile(t * kKTile, sK[buf], sV[buf], std::integral_constant<bool, STREAM>{});
+            if constexpr (STREAM && QS) tile_stream(t * kKTile, sK[buf], sV[buf], t == 0);
+            else tile(t * kKTile, sK[buf], sV[buf], std::integral_constant<bool, STREAM>{});
         }
     }
 
@@ -625,20 +708,20 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
     }
 }
 
-template <int QG, int NWV, int NB, bool STREAM = true>
+template <int QG, int NWV, int NB, bool STREAM = true, bool QS = false>
 static int run_attention_dma(const AttnArgs& a, int hd, hipStream_t s) {
     const int Tq = a.Tq0 + a.Tq1;
     const int64_t nwg = (int64_t)((Tq + 16 * QG * NWV - 1) / (16 * QG * NWV)) * a.H * a.B;
     if (nwg > 0x7fffffff) return fail(BC_ERR_UNSUPPORTED, "attention grid too large");
     dim3 grid((unsigned)nwg), block(64 * NWV);
     switch (hd) {
-#define BC_ATT_CASE(HD) case HD: launch_k(attention_dma_kernel<HD, QG, NWV, NB, STREAM>, grid, block, s, a); break;
+#define BC_ATT_CASE(HD) case HD: launch_k(attention_dma_kernel<HD, QG, NWV, NB, STREAM, QS>, grid, block, s, a); break;
         BC_ATT_CASE(32) BC_ATT_CASE(64) BC_ATT_CASE(72)
 #undef BC_ATT_CASE
         case 128:
             // 64 queries per wave at d = 128 would spill: only up to 32.
             if constexpr (QG <= 2) {
-                launch_k(attention_dma_kernel<128, QG, NWV, NB, STREAM>, grid, block, s, a);
+                launch_k(attention_dma_kernel<128, QG, NWV, NB, STREAM, QS>, grid, block, s, a);
                 break;
             } else {
                 return fail(BC_ERR_UNSUPPORTED, "head_dim 128 with %d query groups per wave", QG);
@@ -675,7 +758,8 @@ int launch_attention(int dtype, AttnArgs a, hipStream_t s) {
     if ((a.ldk | a.ldv) % 8 || kv % 16 || (dtype == BC_BF16 && (a.ldq % 8 || qa % 16)))
         return fail(BC_ERR_UNSUPPORTED, "attention rows must be 16-byte aligned");
     if (dtype == BC_F32 && a.d > 64) return fail(BC_ERR_UNSUPPORTED, "fp32 attention supports head_dim <= 64");
-    a.scale_log2 = 1.4426950408889634f / sqrtf((float)a.d);
+    // Pre-scaled queries (q_scaled) already carry the factor log2(e) / sqrt(d).
+    a.scale_log2 = a.q_scaled ? 1.0f : attn_q_scale(a.d);
     prof_begin(PROF_ATTENTION, s, 4.0 * a.B * a.H * (double)(a.Tq0 + a.Tq1) * (double)(a.Tk0 + a.Tk1) * a.d);
     // The direct-to-LDS kernel needs 16-byte aligned Q/K/V rows (checked above).
     // Up to 256 keys: 8 waves of 16 queries with every key tile resident in
@@ -692,9 +776,12 @@ int launch_attention(int dtype, AttnArgs a, hipStream_t s) {
         const int64_t bh = (int64_t)a.B * a.H;
         const int64_t n512 = (Tq + 511) / 512 * bh, n256 = (Tq + 255) / 256 * bh;
         if (Tk <= 4 * kKTile) rc = run_attention_dma<1, 8, 4, false>(a, a.d, s);
-        else if (a.d <= 72 && n512 >= 256) rc = run_attention_dma<4, 8, 2>(a, a.d, s);
-        else if (n256 >= 128) rc = run_attention_dma<2, 8, 2>(a, a.d, s);
-        else rc = run_attention_dma<1, 8, 2>(a, a.d, s);
+        else if (a.d <= 72 && n512 >= 256)
+            rc = a.q_scaled ? run_attention_dma<4, 8, 2, true, true>(a, a.d, s) : run_attention_dma<4, 8, 2>(a, a.d, s);
+        else if (n256 >= 128)
+            rc = a.q_scaled ? run_attention_dma<2, 8, 2, true, true>(a, a.d, s) : run_attention_dma<2, 8, 2>(a, a.d, s);
+        else
+            rc = a.q_scaled ? run_attention_dma<1, 8, 2, true, true>(a, a.d, s) : run_attention_dma<1, 8, 2>(a, a.d, s);
     } else {
         rc = run_attention<float, 1>(a, a.d, s);
     }

@@ -6,7 +6,8 @@
 namespace bc {
 
 // Epilogue of y = A W^T.  Column c of row r gets v = acc + bias[c]; then
-//   BIAS kind: v = GELU(v) if c >= gelu_from; stored to out[r*ldo + c] (fp32
+//   BIAS kind: v = q_scale * v if c < q_scale_to (attention queries written
+//     pre-scaled); v = GELU(v) if c >= gelu_from; stored to out[r*ldo + c] (fp32
 //     if out_f32, else the operand dtype) if c < split, else (operand dtype)
 //     to out2[r*ldo2 + c - split + off2];
 //   GATE_RES kind: v = res[r*ldr + c] + gate[(r / rows_per_gate)*ldg + c] * v
@@ -21,6 +22,8 @@ struct GemmEpi {
     void* out2;
     int64_t ldo2;
     int split, off2, gelu_from;
+    int q_scale_to;
+    float q_scale;
     const float* res;
     int64_t ldr;
     const float* gate;

@@ -77,6 +77,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& g, const f32x4 (&acc)[T
                         else st(static_cast<T*>(e.out) + o, v);
                     }
                 } else {
+                    if (col < e.q_scale_to) v *= e.q_scale;
                     if (col >= e.gelu_from) v = gelu_tanh(v);
                     if (col >= e.split) st(static_cast<T*>(e.out2) + (int64_t)row * e.ldo2 + (col - e.split + e.off2), v);
                     else if (e.out_f32) static_cast<float*>(e.out)[(int64_t)row * e.ldo + col] = v;
@@ -466,6 +467,10 @@ __device__ __forceinline__ void epilogue_t(const GemmArgs& g, const f32x4 (&acc)
             float v[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) v[r] = acc[i][j][r] + bv[r];
+            if (col < e.q_scale_to) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] *= e.q_scale;
+            }
             if (col >= e.gelu_from) {
 #pragma unroll
                 for (int r = 0; r < 4; ++r) v[r] = gelu_tanh(v[r]);
@@ -791,12 +796,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KG) void gemm_wide_kernel(
                     for (int r = 0; r < 4; ++r) bv[r] = (float)b4[r];
                 }
                 const bool act = col >= e.gelu_from;
+                const float qs = col < e.q_scale_to ? e.q_scale : 1.f;
 #pragma unroll
                 for (int i = 0; i < TM; ++i) {
                     bf16x4 q;
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
-                        float v = acc[i][j][r] + bv[r];
+                        float v = (acc[i][j][r] + bv[r]) * qs;
                         if (act) v = gelu_tanh(v);
                         q[r] = (bf16)v;
                     }
@@ -863,6 +869,7 @@ static bool wide_ok(const GemmArgs& g, int epi) {
     // GELU boundaries and the bf16 row strides and offsets are multiples of 8.
     if (g.N % 8 || e.ldo % 8) return false;
     if (e.gelu_from < g.N && e.gelu_from % 8) return false;
+    if (e.q_scale_to > 0 && e.q_scale_to % 8) return false;
     if (e.split < g.N && (e.split % 8 || e.off2 % 8 || e.ldo2 % 8 || !al(e.out2))) return false;
     return true;
 }
@@ -975,6 +982,7 @@ GemmArgs gemm_args(const void* A, int64_t lda, const void* W, int64_t ldw, int M
     e.out = nullptr; e.ldo = N; e.out_f32 = 0;
     e.out2 = nullptr; e.ldo2 = 0; e.split = N; e.off2 = 0;
     e.gelu_from = N;
+    e.q_scale_to = 0; e.q_scale = 1.f;
     e.res = nullptr; e.ldr = N;
     e.gate = nullptr; e.ldg = N; e.rows_per_gate = 1;
     e.seg = M > 0 ? M : 1; e.keep = e.seg;

@@ -95,6 +95,21 @@ static int plain(int dt, const void* A, int64_t lda, const void* W, const void* 
 
 #define BC_TRY(x) do { const int _rc = (x); if (_rc != BC_OK) return _rc; } while (0)
 
+// Projection whose first q_cols output columns are attention queries: they
+// leave the epilogue multiplied by the softmax scale log2(e) / sqrt(head_dim),
+// rounded once, and the attention takes them as pre-scaled (q_cols = 0: no
+// queries, or their scale is applied after a norm that follows).
+static int qproj(int dt, const void* A, int64_t lda, const void* W, const void* bias, int M, int N, int K, void* out,
+                 int q_cols, int head_dim, hipStream_t s) {
+    GemmArgs g = gemm_args(A, lda, W, K, M, N, K);
+    g.e.bias = bias;
+    g.e.out = out;
+    g.e.ldo = N;
+    g.e.q_scale_to = q_cols;
+    g.e.q_scale = attn_q_scale(head_dim);
+    return launch_gemm(dt, BC_EPI_BIAS, g, s);
+}
+
 // One DiT or PixArt block on x [B*T, D] (fp32).  mod: [B, >= 6D] fp32 rows
 // ld_mod apart, ordered (shift1, scale1, gate1, shift2, scale2, gate2).
 // sites (blockwise mode): the block's module outputs before their gates
@@ -107,9 +122,10 @@ static int dit_block(const bc_block_desc& d, const bc_block_weights& w, float* x
     const int M = d.B * T;
     const bc_stream_weights& sw = w.img;
     BC_TRY(launch_ln_mod(BC_F32, x, M, D, mod, mod + D, ld_mod, T, dt, bb.h, s));
-    BC_TRY(plain(dt, bb.h, D, sw.w_qkv, sw.b_qkv, M, 3 * D, D, bb.qkv, false, s));
+    BC_TRY(qproj(dt, bb.h, D, sw.w_qkv, sw.b_qkv, M, 3 * D, D, bb.qkv, D, d.head_dim, s));
     AttnArgs a = {};
     const size_t esz = dtype_size(dt);
+    a.q_scaled = 1;
     a.q0 = a.q1 = bb.qkv; a.Tq0 = T; a.ldq = 3 * D;
     a.k0 = a.k1 = static_cast<char*>(bb.qkv) + D * esz; a.Tk0 = T; a.ldk = 3 * D;
     a.v0 = a.v1 = static_cast<char*>(bb.qkv) + 2 * D * esz; a.ldv = 3 * D;
@@ -125,8 +141,9 @@ static int dit_block(const bc_block_desc& d, const bc_block_weights& w, float* x
     if (d.kind == BC_BLOCK_PIXART) {
         // Cross-attention to the text context: no norm, no gate.
         BC_TRY(launch_convert(BC_F32, x, dt, bb.h, (int64_t)M * D, s));
-        BC_TRY(plain(dt, bb.h, D, w.wx_q, w.bx_q, M, D, D, bb.qkv, false, s));
+        BC_TRY(qproj(dt, bb.h, D, w.wx_q, w.bx_q, M, D, D, bb.qkv, D, d.head_dim, s));
         AttnArgs c = {};
+        c.q_scaled = 1;
         c.q0 = c.q1 = bb.qkv; c.Tq0 = T; c.ldq = D;
         c.k0 = c.k1 = ctx_kv; c.Tk0 = d.T_ctx; c.ldk = 2 * D;
         c.v0 = c.v1 = static_cast<const char*>(ctx_kv) + D * esz; c.ldv = 2 * D;
@@ -161,15 +178,19 @@ static int dual_block(const bc_block_desc& d, const bc_block_weights& w, float* 
     char* qkv_t = qkv_i + (int64_t)Mi * 3 * D * esz;
     char* at_i = static_cast<char*>(bb.attn);
     char* at_t = at_i + (int64_t)Mi * D * esz;
+    // Queries leave pre-scaled: from the QKV epilogue, or after their RMSNorm.
+    const float qs = attn_q_scale(d.head_dim);
+    const bool qn_i = w.img.q_norm != nullptr, qn_t = w.txt.q_norm != nullptr;
     BC_TRY(launch_ln_mod(BC_F32, x, Mi, D, mi, mi + D, ld_mod, T, dt, bb.h, s));
-    BC_TRY(plain(dt, bb.h, D, w.img.w_qkv, w.img.b_qkv, Mi, 3 * D, D, qkv_i, false, s));
+    BC_TRY(qproj(dt, bb.h, D, w.img.w_qkv, w.img.b_qkv, Mi, 3 * D, D, qkv_i, qn_i ? 0 : D, d.head_dim, s));
     BC_TRY(launch_qk_norm_rope(dt, qkv_i, Mi, 3 * D, D, d.heads, d.head_dim, w.img.q_norm, w.img.k_norm, T, T,
-                               d.rope_f, d.rope_h, d.rope_w, d.rope_theta, s));
+                               d.rope_f, d.rope_h, d.rope_w, d.rope_theta, qn_i ? qs : 1.f, s));
     BC_TRY(launch_ln_mod(BC_F32, xt, Mt, D, mt, mt + D, ld_mod, Tt, dt, bb.h, s));
-    BC_TRY(plain(dt, bb.h, D, w.txt.w_qkv, w.txt.b_qkv, Mt, 3 * D, D, qkv_t, false, s));
+    BC_TRY(qproj(dt, bb.h, D, w.txt.w_qkv, w.txt.b_qkv, Mt, 3 * D, D, qkv_t, qn_t ? 0 : D, d.head_dim, s));
     BC_TRY(launch_qk_norm_rope(dt, qkv_t, Mt, 3 * D, D, d.heads, d.head_dim, w.txt.q_norm, w.txt.k_norm, Tt, 0, 0, 0,
-                               0, 0.0, s));
+                               0, 0.0, qn_t ? qs : 1.f, s));
     AttnArgs a = {};
+    a.q_scaled = 1;
     a.q0 = qkv_i; a.q1 = qkv_t; a.Tq0 = T; a.Tq1 = Tt; a.ldq = 3 * D;
     a.k0 = qkv_i + D * esz; a.k1 = qkv_t + D * esz; a.Tk0 = T; a.Tk1 = Tt; a.ldk = 3 * D;
     a.v0 = qkv_i + 2 * D * esz; a.v1 = qkv_t + 2 * D * esz; a.ldv = 3 * D;
@@ -204,10 +225,15 @@ static int single_block(const bc_block_desc& d, const bc_block_weights& w, float
     g.e.ldo2 = D + F;
     g.e.off2 = D;
     g.e.gelu_from = 3 * D;
+    // Queries leave pre-scaled: from this epilogue, or after their RMSNorm.
+    const bool qn = w.img.q_norm != nullptr;
+    g.e.q_scale_to = qn ? 0 : D;
+    g.e.q_scale = attn_q_scale(d.head_dim);
     BC_TRY(launch_gemm(dt, BC_EPI_BIAS, g, s));
     BC_TRY(launch_qk_norm_rope(dt, bb.qkv, M, 3 * D, D, d.heads, d.head_dim, w.img.q_norm, w.img.k_norm, L, d.T,
-                               d.rope_f, d.rope_h, d.rope_w, d.rope_theta, s));
+                               d.rope_f, d.rope_h, d.rope_w, d.rope_theta, qn ? attn_q_scale(d.head_dim) : 1.f, s));
     AttnArgs a = {};
+    a.q_scaled = 1;
     a.q0 = a.q1 = bb.qkv; a.Tq0 = L; a.ldq = 3 * D;
     a.k0 = a.k1 = static_cast<char*>(bb.qkv) + D * esz; a.Tk0 = L; a.ldk = 3 * D;
     a.v0 = a.v1 = static_cast<char*>(bb.qkv) + 2 * D * esz; a.ldv = 3 * D;

@@ -107,11 +107,12 @@ __device__ __forceinline__ void sampler_update(const SamplerCoef& k, float* x, f
 // buffer (rows of ld elements: q at columns [0, D), k at [D, 2D)): per head,
 // RMSNorm with the scales wq / wk ([head_dim], or NULL for none; eps 1e-6,
 // fp32), then for the first n_img rows of every rows_per_sample the 3D rotary
-// embedding over a gf x gh x gw token grid (theta <= 0: none).  head_dim
-// <= 128, even; with the rotation a multiple of 32.
+// embedding over a gf x gh x gw token grid (theta <= 0: none); the queries
+// are then multiplied by q_scale (the attention's pre-scaled queries; 1:
+// none).  head_dim <= 128, even; with the rotation a multiple of 32.
 int launch_qk_norm_rope(int dt, void* qkv, int64_t rows, int64_t ld, int D, int heads, int head_dim, const void* wq,
                         const void* wk, int rows_per_sample, int n_img, int gf, int gh, int gw, double theta,
-                        hipStream_t s);
+                        float q_scale, hipStream_t s);
 
 // Blockwise mode.  x [rows, D] fp32 (rows of rows_per_gate tokens per sample):
 //   gated add:  x += gate[r / rows_per_gate] (.) site   (gate rows ldg floats

@@ -579,7 +579,7 @@ template <typename T_>
 __global__ __launch_bounds__(256) void qk_norm_rope_kernel(elem_t<T_>* __restrict__ qkv, int64_t rows, int64_t ldr, int D,
                                                            int heads, int hd, const elem_t<T_>* __restrict__ wq,
                                                            const elem_t<T_>* __restrict__ wk, int L, int n_img, int gf,
-                                                           int gh, int gw, float log2_theta) {
+                                                           int gh, int gw, float log2_theta, float q_scale) {
     typedef elem_t<T_> T;
     const int64_t wid = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 6;
     const int lane = threadIdx.x & 63;
@@ -623,8 +623,9 @@ __global__ __launch_bounds__(256) void qk_norm_rope_kernel(elem_t<T_>* __restric
         x1 = y1;
     }
     if (act) {
-        p[2 * lane] = (T)x0;
-        p[2 * lane + 1] = (T)x1;
+        const float os = qk ? 1.f : q_scale;
+        p[2 * lane] = (T)(x0 * os);
+        p[2 * lane + 1] = (T)(x1 * os);
     }
 }
 
@@ -638,7 +639,7 @@ template <int CPH, typename B_>
 __global__ __launch_bounds__(256) void qk_norm_rope_row_kernel(elem_t<B_>* __restrict__ qkv, int64_t rows, int64_t ldr,
                                                                int D, const elem_t<B_>* __restrict__ wq,
                                                                const elem_t<B_>* __restrict__ wk, int L, int n_img, int gf,
-                                                               int gh, int gw, float log2_theta) {
+                                                               int gh, int gw, float log2_theta, float q_scale) {
     constexpr int HD = 8 * CPH;
     const int64_t wid = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 6;
     const int lane = threadIdx.x & 63;
@@ -700,10 +701,11 @@ __global__ __launch_bounds__(256) void qk_norm_rope_row_kernel(elem_t<B_>* __res
             }
         }
         if (act) {
+            const float os = qk ? 1.f : q_scale;
             u32x4 o;
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
-                const bf16 lo = (bf16)v[2 * k], hi = (bf16)v[2 * k + 1];
+                const bf16 lo = (bf16)(v[2 * k] * os), hi = (bf16)(v[2 * k + 1] * os);
                 o[k] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
             }
             *reinterpret_cast<u32x4*>(p + (int64_t)c * 8) = o;
@@ -713,9 +715,9 @@ __global__ __launch_bounds__(256) void qk_norm_rope_row_kernel(elem_t<B_>* __res
 
 int launch_qk_norm_rope(int dt, void* qkv, int64_t rows, int64_t ld, int D, int heads, int head_dim, const void* wq,
                         const void* wk, int rows_per_sample, int n_img, int gf, int gh, int gw, double theta,
-                        hipStream_t s) {
+                        float q_scale, hipStream_t s) {
     const bool rope = theta > 0.0 && n_img > 0;
-    if (!wq && !wk && !rope) return BC_OK;
+    if (!wq && !wk && !rope && q_scale == 1.f) return BC_OK;
     if (head_dim < 2 || head_dim > 128 || head_dim % 2 || heads * head_dim != D || rows_per_sample < 1 ||
         (rope && (head_dim % 32 || (int64_t)gf * gh * gw != n_img)))
         return fail(BC_ERR_INVALID_ARG, "qk_norm_rope: head_dim %d, grid %d x %d x %d for %d tokens", head_dim, gf, gh,
@@ -730,20 +732,20 @@ int launch_qk_norm_rope(int dt, void* qkv, int64_t rows, int64_t ld, int D, int 
         const bf16 *a = static_cast<const bf16*>(wq), *b = static_cast<const bf16*>(wk);
         const int ni = rope ? n_img : 0;
         if (head_dim == 128)
-            qk_norm_rope_row_kernel<16, bf16_tag><<<gr, 256, 0, s>>>(q, rows, ld, D, a, b, rows_per_sample, ni, gf, gh, gw, l2t);
+            qk_norm_rope_row_kernel<16, bf16_tag><<<gr, 256, 0, s>>>(q, rows, ld, D, a, b, rows_per_sample, ni, gf, gh, gw, l2t, q_scale);
         else
-            qk_norm_rope_row_kernel<8, bf16_tag><<<gr, 256, 0, s>>>(q, rows, ld, D, a, b, rows_per_sample, ni, gf, gh, gw, l2t);
+            qk_norm_rope_row_kernel<8, bf16_tag><<<gr, 256, 0, s>>>(q, rows, ld, D, a, b, rows_per_sample, ni, gf, gh, gw, l2t, q_scale);
         return check_launch("qk_norm_rope_row");
     }
     const unsigned g = (unsigned)((waves + 3) / 4);
     if (dt == BC_BF16)
         qk_norm_rope_kernel<bf16_tag><<<g, 256, 0, s>>>(static_cast<bf16*>(qkv), rows, ld, D, heads, head_dim,
                                                     static_cast<const bf16*>(wq), static_cast<const bf16*>(wk),
-                                                    rows_per_sample, rope ? n_img : 0, gf, gh, gw, l2t);
+                                                    rows_per_sample, rope ? n_img : 0, gf, gh, gw, l2t, q_scale);
     else
         qk_norm_rope_kernel<float><<<g, 256, 0, s>>>(static_cast<float*>(qkv), rows, ld, D, heads, head_dim,
                                                      static_cast<const float*>(wq), static_cast<const float*>(wk),
-                                                     rows_per_sample, rope ? n_img : 0, gf, gh, gw, l2t);
+                                                     rows_per_sample, rope ? n_img : 0, gf, gh, gw, l2t, q_scale);
     return check_launch("qk_norm_rope");
 }
 
