@@ -603,14 +603,58 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
     f32x4 negm[QG];
 #pragma unroll
     for (int g = 0; g < QG; ++g) negm[g] = f32x4{0.f, 0.f, 0.f, 0.f};
-    auto tile_stream = [&](int k0, const bf16* K, const bf16* V, bool first) __attribute__((always_inline)) {
+    // Operand addresses: per-lane byte offsets within a tile, worked out once.
+    // A row's swizzle depends only on the row mod 16, so the fragments 16 and
+    // 32 rows further on sit at constant distances, and with the buffer fixed
+    // at compile time every read is a lane offset plus an immediate.
+    typedef __attribute__((address_space(3))) const char lds_char;
+    uint32_t kofs[S::n32x], vofs[S::DV / 16];
+#pragma unroll
+    for (int c = 0; c < S::n32x; ++c) kofs[c] = 2u * (uint32_t)LY::at(ql, 32 * c + grp * 8);
+#pragma unroll
+    for (int i = 0; i < S::DV / 16; ++i) vofs[i] = 2u * (uint32_t)LY::at(4 * grp + (ql >> 2), 16 * i + 4 * (ql & 3));
+    constexpr uint32_t ROWB = 2u * HD;    // bytes per tile row
+    auto pv_fixed = [&](lds_char* Vb, f32x4 (&s)[QG][4]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            bf16x8 pf[QG];
+#pragma unroll
+            for (int g = 0; g < QG; ++g)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    pf[g][r] = (bf16)s[g][2 * u][r];
+                    pf[g][4 + r] = (bf16)s[g][2 * u + 1][r];
+                }
+#pragma unroll
+            for (int i = 0; i < S::DV / 16; ++i) {
+                lds_char* p = Vb + vofs[i] + 32u * u * ROWB;
+                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p);
+                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p + 16 * ROWB));
+                bf16x8 vf = __builtin_bit_cast(bf16x8, u32x4{__builtin_bit_cast(u32x2, lo).x, __builtin_bit_cast(u32x2, lo).y,
+                                                            __builtin_bit_cast(u32x2, hi).x, __builtin_bit_cast(u32x2, hi).y});
+                if (PADSUM && i == S::DV / 16 - 1 && (lane & 15) >= HD - 16 * i)
+                    vf = __builtin_bit_cast(bf16x8, u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
+#pragma unroll
+                for (int g = 0; g < QG; ++g) o[g][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[g], o[g][i], 0, 0, 0);
+            }
+            if constexpr (!PADSUM) {
+                const bf16x8 ones = __builtin_bit_cast(bf16x8, u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
+#pragma unroll
+                for (int g = 0; g < QG; ++g) osum[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[g], osum[g], 0, 0, 0);
+            }
+        }
+    };
+    auto tile_stream = [&](int k0, auto bufc, bool first) __attribute__((always_inline)) {
+        constexpr int BUF = decltype(bufc)::value;
+        lds_char* Kb = (lds_char*)&sK[BUF][0];
+        lds_char* Vb = (lds_char*)&sV[BUF][0];
         f32x4 s[QG][4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int krow = 16 * j + ql;
 #pragma unroll
             for (int c = 0; c < S::n32x; ++c) {
-                const bf16x8 kf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(K + LY::at(krow, 32 * c + grp * 8)));
+                const bf16x8 kf = __builtin_bit_cast(
+                    bf16x8, *(__attribute__((address_space(3))) const u32x4*)(Kb + kofs[c] + 16u * j * ROWB));
 #pragma unroll
                 for (int g = 0; g < QG; ++g)
                     s[g][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[g][c], c == 0 ? negm[g] : s[g][j], 0, 0, 0);
@@ -664,21 +708,33 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
             for (int j = 0; j < 4; ++j)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) s[g][j][r] = __builtin_amdgcn_exp2f(s[g][j][r]);
-        pv(V, s);
+        pv_fixed(Vb, s);
     };
 
     if (resident) {
         __builtin_amdgcn_s_waitcnt((0 & 15) | (7 << 4) | (15 << 8));   // vmcnt(0): this wave's loads
         __syncthreads();
         for (int t = 0; t < ntiles; ++t) tile(t * kKTile, sK[t], sV[t], std::false_type{});
+    } else if constexpr (STREAM && QS) {
+        // Unrolled by two so that each step's buffer is a compile-time constant.
+        auto step = [&](int t, auto bufc) __attribute__((always_inline)) {
+            constexpr int BUF = decltype(bufc)::value;
+            __builtin_amdgcn_s_waitcnt((0 & 15) | (7 << 4) | (15 << 8));   // vmcnt(0): this wave's loads of tile t
+            __syncthreads();
+            if (t + 1 < ntiles) issue((t + 1) * kKTile, BUF ^ 1);
+            tile_stream(t * kKTile, bufc, t == 0);
+        };
+        for (int t = 0; t < ntiles; t += 2) {
+            step(t, std::integral_constant<int, 0>{});
+            if (t + 1 < ntiles) step(t + 1, std::integral_constant<int, 1>{});
+        }
     } else {
         for (int t = 0; t < ntiles; ++t) {
             const int buf = t & 1;
             __builtin_amdgcn_s_waitcnt((0 & 15) | (7 << 4) | (15 << 8));   // vmcnt(0): this wave's loads of tile t
             __syncthreads();
             if (t + 1 < ntiles) issue((t + 1) * kKTile, buf ^ 1);
-            if constexpr (STREAM && QS) tile_stream(t * kKTile, sK[buf], sV[buf], t == 0);
-            else tile(t * kKTile, sK[buf], sV[buf], std::integral_constant<bool, STREAM>{});
+            tile(t * kKTile, sK[buf], sV[buf], std::integral_constant<bool, STREAM>{});
         }
     }
 
