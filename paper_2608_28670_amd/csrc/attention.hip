@@ -681,15 +681,18 @@ __global__ __launch_bounds__(64 * NWV) void attention_dma_kernel(AttnArgs a) {
             float m5 = vmax(vmax(v[3][0], v[3][1]), v[3][2]);
             float m6 = vmax(vmax(m1, m2), v[3][3]);
             float m7 = vmax(vmax(m3, m4), m5);
-            mloc[g] = group_max(vmax(m6, m7));
+            mloc[g] = vmax(m6, m7);     // this lane's 16 scores; the query's max needs its 4 lanes
         }
-        bool any_up = first;
+        // The test needs no cross-lane max: some lane over the threshold is
+        // enough, and only the (rare) rescale reduces over a query's lanes.
+        float lane_top = mloc[0];
 #pragma unroll
-        for (int g = 0; g < QG; ++g) any_up = any_up || mloc[g] > 8.0f;
-        if (__any(any_up)) {
+        for (int g = 1; g < QG; ++g) lane_top = vmax(lane_top, mloc[g]);
+        if (__any(first || lane_top > 8.0f)) {
 #pragma unroll
             for (int g = 0; g < QG; ++g) {
-                const float shift = first ? mloc[g] : vmax(mloc[g], 0.f);
+                const float qmax = group_max(mloc[g]);
+                const float shift = first ? qmax : vmax(qmax, 0.f);
                 m_run[g] += shift;
                 negm[g] = f32x4{-m_run[g], -m_run[g], -m_run[g], -m_run[g]};
                 if (!first) {
