@@ -180,20 +180,71 @@ def group_launches(records, cfg):
     return groups
 
 
-def roofline_of(g, tag=None, src=None):
-    """Roofline record of a kernel group; traffic from its counter summary."""
+# kernel-name prefix of a profiled class's launches (the gated epilogue is template argument 2)
+CLASS_KERNEL = {"attention": "void bc::attention_dma_kernel<", "gemm_gated": "void bc::gemm_wide_kernel<2,",
+                "gemm_down": "void bc::gemm_wide_kernel<2,", "gemm_gelu": "void bc::gemm_wide_kernel<0,",
+                "gemm_bias": "void bc::gemm_wide_kernel<0,"}
+
+
+def loop_traffic(workload, g, src):
+    """HBM bytes per launch of a kernel group from the whole-loop counter
+    summary of this workload: the one (kernel, grid) group of the class's
+    kernel with as many dispatches per run as the group has launches, if the
+    kernel source is unchanged since the counters were taken; else None."""
+    path = os.path.join(ROOT, "profiles", f"sampling_loop_{workload}_counters.json")
+    if not os.path.exists(path) or g["class"] not in CLASS_KERNEL:
+        return None
+    with open(path) as f:
+        c = json.load(f)
+    if c.get("source_hashes", {}).get(src) != source_hash(*KERNEL_SOURCES[src]):
+        return None
+    hits = [r for r in c["groups"] if r["kernel"].startswith(CLASS_KERNEL[g["class"]])
+            and abs(r["dispatches_per_run"] - g["launches"]) < 0.5 and "hbm_bytes" in r
+            and grid_fits(r["kernel"], r["grid_threads"], g)]
+    return hits[0]["hbm_bytes"] if len(hits) == 1 else None
+
+
+def grid_fits(kernel, grid_threads, g):
+    """Whether a dispatch grid is the one the kernel's template arguments give
+    for the group's shape (GEMM [M, N, K]: one workgroup per BM x BN tile;
+    attention [B, H, Tq, Tk, d]: one per 16 QG NWV queries of a head)."""
+    import re
+    m = re.search(r"<([^>]*)>", kernel)
+    if not m or not g.get("shape"):
+        return False
+    args = [a.strip() for a in m.group(1).split(",")]
+    if "attention" in kernel:
+        qg, nwv = int(args[1]), int(args[2])
+        B, H, Tq = g["shape"][0], g["shape"][1], g["shape"][2]
+        qt = 16 * qg * nwv
+        return grid_threads == -(-Tq // qt) * H * B * 64 * nwv
+    bm, bn, wm, wn, kg = int(args[1]), int(args[2]), int(args[3]), int(args[4]), int(args[7])
+    M, N = g["shape"][0], g["shape"][1]
+    return grid_threads == -(-M // bm) * -(-N // bn) * 64 * wm * wn * kg
+
+
+def roofline_of(g, tag=None, src=None, workload=None):
+    """Roofline record of a kernel group; traffic from the whole-loop counter
+    summary, else from the counter program's summary."""
     avg_s = g["avg_us"] / 1e6
     achieved = g["work"] / avg_s / 1e12
     r = {"bound": "mfma", "kernel": g["kernel"], "class": g["class"], "shape": g["shape"],
          "flops_per_launch": g["work"], "avg_us": round(g["avg_us"], 2), "launches": g["launches"],
          "ms_per_run": round(g["ms_per_run"], 3), "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
          "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4)}
-    if tag is not None:
+    r["traffic"] = None
+    if src is None:
+        src = "attention" if g["class"] == "attention" else "gemm" if g["class"].startswith("gemm") else None
+    if src is not None:
         h = source_hash(*KERNEL_SOURCES[src])
-        r["traffic"] = counters_traffic(tag, h)
         r["source_hash"] = h
-    else:
-        r["traffic"] = None
+        lt = loop_traffic(workload, g, src) if workload else None
+        if lt is not None:
+            r["traffic"], r["traffic_from"] = lt, "sampling loop (profiles/sampling_loop_%s_counters.json)" % workload
+        elif tag is not None:
+            ct = counters_traffic(tag, h)
+            if ct is not None:
+                r["traffic"], r["traffic_from"] = ct, "counter program (profiles/%s_counters.json)" % tag
     return r
 
 
@@ -290,8 +341,8 @@ def measure(bc, torch, cfg, steps, warmup, extras=False, adaptive_ell=0.13):
             e["frac_of_hbm_peak"] = round(e["gbs"] / PEAK_HBM_GBS, 4)
         classes[name] = e
     groups = [g for g in group_launches(records, cfg) if g["class"] in MFMA_CLASSES]
-    res["roofline"] = roofline_of(groups[0], *counter_tag(cfg, groups[0]))
-    res["roofline_others"] = [roofline_of(g, *counter_tag(cfg, g)) for g in groups[1:6]]
+    res["roofline"] = roofline_of(groups[0], *counter_tag(cfg, groups[0]), workload=cfg.name)
+    res["roofline_others"] = [roofline_of(g, *counter_tag(cfg, g), workload=cfg.name) for g in groups[1:6]]
     res["kernel_classes"] = classes
     res["profiled_run_ms"] = round(float(sum(float(ms.sum()) for ms, _ in records.values())), 3)
 
@@ -830,30 +881,30 @@ def loop_counters(args):
 
 
 def summarize_loop_counters(args):
-    """profiles/sampling_loop_<workload>_counters.md from rocprofv3 --pmc
-    passes over `bench.py --loop-counters` (one run_counter_collection.csv per
-    pass directory under args.summarize_loop_counters): per kernel, the
-    dispatches of one sampling run, HBM bytes per dispatch (FETCH_SIZE and
-    WRITE_SIZE scaled by the calibration copy, the last library dispatch) and
-    MFMA-busy / VALU-active fractions of the dispatch's cycles."""
+    """profiles/sampling_loop_<workload>_counters.{md,json} from rocprofv3
+    --pmc passes over `bench.py --loop-counters` (one run_counter_collection.csv
+    per pass directory under args.summarize_loop_counters): per kernel and grid
+    size, the dispatches of one sampling run, HBM bytes per dispatch
+    (FETCH_SIZE and WRITE_SIZE scaled by the calibration copy, the last library
+    dispatch) and MFMA-busy / VALU-active fractions of the dispatch's cycles.
+    The JSON is what the roofline's `traffic` is read from."""
     import csv
     import glob
     import statistics
     root = args.summarize_loop_counters
-    per = {}      # kernel -> counter -> [values per dispatch]
+    per = {}      # (kernel, grid) -> counter -> [values per dispatch]
     calib = {}
     passes = []
     for path in sorted(glob.glob(os.path.join(root, "*", "run_counter_collection.csv"))):
         vals, names = {}, {}
         for r in csv.DictReader(open(path)):
             d = int(r["Dispatch_Id"])
-            names[d] = r["Kernel_Name"]
+            names[d] = (r["Kernel_Name"], int(r["Grid_Size"]))
             vals.setdefault(d, {}).setdefault(r["Counter_Name"], 0.0)
             vals[d][r["Counter_Name"]] += float(r["Counter_Value"])
-        lib = [d for d in sorted(names) if names[d].startswith(("void bc::", "bc::"))]
+        lib = [d for d in sorted(names) if names[d][0].startswith(("void bc::", "bc::"))]
         passes.append(os.path.basename(os.path.dirname(path)) + ": " + ", ".join(sorted(vals[lib[0]])))
-        last = lib[-1]
-        for c, v in vals[last].items():
+        for c, v in vals[lib[-1]].items():
             calib[c] = v
         for d in lib[:-1]:
             for c, v in vals[d].items():
@@ -863,29 +914,39 @@ def summarize_loop_counters(args):
     f_write = nbytes / (calib["WRITE_SIZE"] * 1024.0) if "WRITE_SIZE" in calib else None
     runs = args.steps
     rows = []
-    for name, c in per.items():
+    for (name, grid), c in per.items():
         n = max(len(v) for v in c.values())
         med = {k: statistics.median(v) for k, v in c.items()}
         tot = {k: sum(v) for k, v in c.items()}
-        r = {"name": name, "per_run": n / runs}
+        r = {"kernel": name, "grid_threads": grid, "dispatches_per_run": n / runs}
         if f_fetch and "FETCH_SIZE" in med:
-            r["fetch_mb"] = med["FETCH_SIZE"] * 1024 * f_fetch / 1e6
+            r["fetch_bytes"] = int(med["FETCH_SIZE"] * 1024 * f_fetch)
         if f_write and "WRITE_SIZE" in med:
-            r["write_mb"] = med["WRITE_SIZE"] * 1024 * f_write / 1e6
+            r["write_bytes"] = int(med["WRITE_SIZE"] * 1024 * f_write)
+        if "fetch_bytes" in r and "write_bytes" in r:
+            r["hbm_bytes"] = r["fetch_bytes"] + r["write_bytes"]
         if "GRBM_GUI_ACTIVE" in tot:
             cyc = tot["GRBM_GUI_ACTIVE"] / 8          # per XCD, summed over the 8
             r["cycles_per_run"] = cyc / runs
             if "SQ_VALU_MFMA_BUSY_CYCLES" in tot:
-                r["mfma_busy"] = tot["SQ_VALU_MFMA_BUSY_CYCLES"] / 1024 / cyc
+                r["mfma_busy"] = round(tot["SQ_VALU_MFMA_BUSY_CYCLES"] / 1024 / cyc, 4)
             if "SQ_ACTIVE_INST_VALU" in tot:
-                r["valu_active"] = tot["SQ_ACTIVE_INST_VALU"] * 4 / 1024 / cyc
+                r["valu_active"] = round(tot["SQ_ACTIVE_INST_VALU"] * 4 / 1024 / cyc, 4)
         rows.append(r)
     rows.sort(key=lambda r: -r.get("cycles_per_run", 0.0))
     total_cyc = sum(r.get("cycles_per_run", 0.0) for r in rows)
+    cmd = (f"rocprofv3 --pmc <counters> -d <dir>/<pass> -o run --output-format csv -- "
+           f"python3 bench.py --loop-counters --workload {args.workload} --steps {runs}")
+    rec = {"workload": args.workload, "runs": runs, "command": cmd, "passes": passes,
+           "source_hashes": {k: source_hash(*v) for k, v in KERNEL_SOURCES.items()},
+           "calibration": {"copy_bytes": int(nbytes), "fetch_factor": round(f_fetch, 4) if f_fetch else None,
+                           "write_factor": round(f_write, 4) if f_write else None},
+           "groups": rows}
+    with open(os.path.join(ROOT, "profiles", f"sampling_loop_{args.workload}_counters.json"), "w") as fh:
+        json.dump(rec, fh, indent=1)
     out = [f"# Hardware counters over the whole sampling loop: {args.workload}", "",
            "Commands (from a shell in `/tmp`, `TMPDIR=/tmp`), one pass per counter set:", "",
-           f"    rocprofv3 --pmc <counters> -d <dir>/<pass> -o run --output-format csv -- "
-           f"python3 bench.py --loop-counters --workload {args.workload} --steps {runs}",
+           "    " + cmd,
            f"    python3 bench.py --summarize-loop-counters <dir> --workload {args.workload} --steps {runs}", "",
            "Passes: " + "; ".join(passes) + ".", "",
            "Counter runs serialise the dispatches, so cycles are each dispatch's own duration "
@@ -893,15 +954,17 @@ def summarize_loop_counters(args):
            "(KiB per dispatch, medians) times the factor that makes the 1 GiB calibration copy read its known "
            f"size (fetch x{f_fetch:.4f}, write x{f_write:.4f})." if f_fetch and f_write else "",
            "MFMA busy: SQ_VALU_MFMA_BUSY_CYCLES over the 1024 SIMDs' cycles; VALU active: SQ_ACTIVE_INST_VALU "
-           "(counted per 4 cycles) over the same.", "",
-           "| kernel | dispatches per run | share of cycles | fetch MB | write MB | MFMA busy | VALU active |",
-           "|---|---|---|---|---|---|---|"]
-    def f(r, k, fmt):
-        return format(r[k], fmt) if k in r else "-"
+           "(counted per 4 cycles) over the same. One row per kernel and grid size.", "",
+           "| kernel | grid (threads) | dispatches per run | share of cycles | fetch MB | write MB | MFMA busy | VALU active |",
+           "|---|---|---|---|---|---|---|---|"]
+
+    def f(r, k, fmt, scale=1.0):
+        return format(r[k] * scale, fmt) if k in r else "-"
     for r in rows[:40]:
         share = r.get("cycles_per_run", 0.0) / total_cyc if total_cyc else 0.0
-        out.append(f"| `{r['name'][:140]}` | {r['per_run']:.0f} | {share:.1%} | {f(r, 'fetch_mb', '.1f')} | "
-                   f"{f(r, 'write_mb', '.1f')} | {f(r, 'mfma_busy', '.1%')} | {f(r, 'valu_active', '.1%')} |")
+        out.append(f"| `{r['kernel'][:140]}` | {r['grid_threads']} | {r['dispatches_per_run']:.0f} | {share:.1%} | "
+                   f"{f(r, 'fetch_bytes', '.1f', 1e-6)} | {f(r, 'write_bytes', '.1f', 1e-6)} | "
+                   f"{f(r, 'mfma_busy', '.1%')} | {f(r, 'valu_active', '.1%')} |")
     path = os.path.join(ROOT, "profiles", f"sampling_loop_{args.workload}_counters.md")
     with open(path, "w") as fh:
         fh.write("\n".join(out) + "\n")
