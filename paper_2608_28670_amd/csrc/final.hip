@@ -6,9 +6,9 @@
 // in each wave, lane l holds token l % 16 and the 16-byte feature chunks
 // 4 s + l / 16 of the wave's chunk steps s, which is exactly the A-operand layout of
 // v_mfma_f32_16x16x32_bf16, so the normalised row feeds the MFMA without
-// leaving registers.  A workgroup's D / 128 waves split the row's D (four
-// chunk steps each) and meet in LDS for the row statistics and the sum of
-// their partial outputs.  The HBM traffic is the K cached features plus the
+// leaving registers.  A workgroup's waves split the row's D (four chunk steps
+// each, twelve at D = 3072) and meet in LDS for the row statistics and the sum
+// of their partial outputs.  The HBM traffic is the K cached features plus the
 // latents; the feature, the LayerNorm output and the model output never touch
 // memory.
 #include "ops.h"
@@ -26,57 +26,74 @@ __device__ __forceinline__ float group4_sum(float v) {
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
-// CH = D / 32 chunk steps of a row, four per wave over CH / 4 waves; NT =
-// NO / 16 output tiles; KK = number of cached features.
-template <int CH, int NT, int KK>
-__global__ __launch_bounds__(16 * CH) void final_step_kernel(FinalStepArgs a) {
-    constexpr int CW = 4;                               // chunk steps of a wave
+// CH = D / 32 chunk steps of a row, CW per wave over CH / CW waves (CW = 4;
+// 12 for D = 3072: 8 waves, two per SIMD); NT = NO / 16 output tiles; KK =
+// number of cached features.  With CW > 4 the modulation vectors
+// and weight fragments are loaded per chunk step in the linear, after the
+// statistics, instead of with the features (they would not fit the
+// registers next to them).  Rows past the last token (B T not a multiple of
+// 16) read the last row and update nothing.
+template <int CH, int NT, int KK, int CW>
+__global__ __launch_bounds__(64 * (CH / CW)) void final_step_kernel(FinalStepArgs a) {
     constexpr int NWV = CH / CW;                        // waves per workgroup
-    static_assert(NWV * CW == CH, "D / 32 must be a multiple of 4");
+    constexpr bool LATE = CW > 4;                       // modulation and weights loaded in the linear
+    static_assert(NWV * CW == CH, "D / 32 must be a multiple of the chunk steps per wave");
     __shared__ float s_stat[NWV][16];
     __shared__ f32x4 s_out[NWV][NT][64];
     const int lane = threadIdx.x & 63, grp = lane >> 4, wave = threadIdx.x >> 6;
-    const int64_t row0 = (int64_t)blockIdx.x * 16;      // rows is a multiple of 16
-    const int64_t row = row0 + (lane & 15);
+    const int64_t rows = (int64_t)a.B * a.T;
+    const int64_t row0 = (int64_t)blockIdx.x * 16;
+    const int64_t row = min(row0 + (lane & 15), rows - 1);
     const int D = CH * 32;
     const int sbeg = wave * CW;
 
     // 1. This wave's feature chunks of the row, all K sources loaded at once,
     // combined in fp32 and rounded to bf16.
-    u32x4 raw[KK][CW];
+    // (Up to four chunk steps of all K sources are in flight at a time.)
+    constexpr int CB = CW < 4 ? CW : 4;
+    u32x4 raw[KK][CB];
+    auto load_raw = [&](int s0) __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < KK; ++j)
+        for (int j = 0; j < KK; ++j)
 #pragma unroll
-        for (int s = 0; s < CW; ++s)
-            raw[j][s] = *reinterpret_cast<const u32x4*>(static_cast<const bf16*>(a.src[j]) + row * D + 32 * (sbeg + s) + 8 * grp);
+            for (int s = 0; s < CB; ++s)
+                raw[j][s] = *reinterpret_cast<const u32x4*>(static_cast<const bf16*>(a.src[j]) + row * D +
+                                                            32 * (sbeg + s0 + s) + 8 * grp);
+    };
+    load_raw(0);
     // The modulation vectors and the weight fragments do not depend on the
     // statistics: load them now, with the features.
     const int b = (int)(row / a.T);
     const float* shift = a.fmod + (int64_t)b * 2 * D;
     const float* scale = shift + D;
     const bf16* W = static_cast<const bf16*>(a.W);
-    f32x4 shv4[CW][2], scv4[CW][2];
-    bf16x8 wf[CW][NT];
-#pragma unroll
-    for (int s = 0; s < CW; ++s) {
+    constexpr int CP = LATE ? 1 : CW;                   // chunk steps whose operands are preloaded
+    f32x4 shv4[CP][2], scv4[CP][2];
+    bf16x8 wf[CP][NT];
+    auto load_ops = [&](int s, int slot) __attribute__((always_inline)) {
         const int d0 = 32 * (sbeg + s) + 8 * grp;
-        shv4[s][0] = *reinterpret_cast<const f32x4*>(shift + d0);
-        shv4[s][1] = *reinterpret_cast<const f32x4*>(shift + d0 + 4);
-        scv4[s][0] = *reinterpret_cast<const f32x4*>(scale + d0);
-        scv4[s][1] = *reinterpret_cast<const f32x4*>(scale + d0 + 4);
+        shv4[slot][0] = *reinterpret_cast<const f32x4*>(shift + d0);
+        shv4[slot][1] = *reinterpret_cast<const f32x4*>(shift + d0 + 4);
+        scv4[slot][0] = *reinterpret_cast<const f32x4*>(scale + d0);
+        scv4[slot][1] = *reinterpret_cast<const f32x4*>(scale + d0 + 4);
 #pragma unroll
         for (int t = 0; t < NT; ++t)
-            wf[s][t] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(W + (int64_t)(16 * t + (lane & 15)) * D + d0));
+            wf[slot][t] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(W + (int64_t)(16 * t + (lane & 15)) * D + d0));
+    };
+    if constexpr (!LATE) {
+#pragma unroll
+        for (int s = 0; s < CW; ++s) load_ops(s, s);
     }
     u32x4 h[CW];
     float sum = 0.f;
 #pragma unroll
     for (int s = 0; s < CW; ++s) {
+        if (s > 0 && s % CB == 0) load_raw(s);
         float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int j = 0; j < KK; ++j) {
             float f[8];
-            unpack(raw[j][s], f, static_cast<const bf16*>(nullptr));
+            unpack(raw[j][s % CB], f, static_cast<const bf16*>(nullptr));
 #pragma unroll
             for (int e = 0; e < 8; ++e) acc[e] += a.w[j] * f[e];
         }
@@ -123,12 +140,14 @@ __global__ __launch_bounds__(16 * CH) void final_step_kernel(FinalStepArgs a) {
     for (int t = 0; t < NT; ++t) out[t] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < CW; ++s) {
+        const int q4 = LATE ? 0 : s;
+        if constexpr (LATE) load_ops(s, 0);
         float f[8];
         unpack(h[s], f, static_cast<const bf16*>(nullptr));
-        const float shv[8] = {shv4[s][0][0], shv4[s][0][1], shv4[s][0][2], shv4[s][0][3],
-                              shv4[s][1][0], shv4[s][1][1], shv4[s][1][2], shv4[s][1][3]};
-        const float scv[8] = {scv4[s][0][0], scv4[s][0][1], scv4[s][0][2], scv4[s][0][3],
-                              scv4[s][1][0], scv4[s][1][1], scv4[s][1][2], scv4[s][1][3]};
+        const float shv[8] = {shv4[q4][0][0], shv4[q4][0][1], shv4[q4][0][2], shv4[q4][0][3],
+                              shv4[q4][1][0], shv4[q4][1][1], shv4[q4][1][2], shv4[q4][1][3]};
+        const float scv[8] = {scv4[q4][0][0], scv4[q4][0][1], scv4[q4][0][2], scv4[q4][0][3],
+                              scv4[q4][1][0], scv4[q4][1][1], scv4[q4][1][2], scv4[q4][1][3]};
         uint32_t wd[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -138,7 +157,7 @@ __global__ __launch_bounds__(16 * CH) void final_step_kernel(FinalStepArgs a) {
         }
         const bf16x8 af = __builtin_bit_cast(bf16x8, u32x4{wd[0], wd[1], wd[2], wd[3]});
 #pragma unroll
-        for (int t = 0; t < NT; ++t) out[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, wf[s][t], out[t], 0, 0, 0);
+        for (int t = 0; t < NT; ++t) out[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, wf[q4][t], out[t], 0, 0, 0);
     }
 #pragma unroll
     for (int t = 0; t < NT; ++t) s_out[wave][t][lane] = out[t];
@@ -167,6 +186,7 @@ __global__ __launch_bounds__(16 * CH) void final_step_kernel(FinalStepArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int64_t tr = row0 + 4 * grp + r;
+            if (tr >= rows) continue;
             const int bb = (int)(tr / a.T), tok = (int)(tr % a.T);
             const int f = tok / (hp * wp), ty = (tok / wp) % hp, tx = tok % wp;
             const int64_t i = ((int64_t)bb * ls.C + c) * S + ((int64_t)f * ls.H + ty * p + py) * ls.W + tx * p + px;
@@ -177,12 +197,13 @@ __global__ __launch_bounds__(16 * CH) void final_step_kernel(FinalStepArgs a) {
 
 }  // namespace
 
-// Instantiated (D / 32, NO / 16): D 1152 (DiT-XL/2, PixArt) and 1280, 128 and
-// 256 (small models), with 16 to 64 outputs per token; 1 to 4 cached features.
-#define BC_FINAL_VARIANTS(X) X(36, 2) X(36, 4) X(40, 2) X(40, 4) X(4, 1) X(4, 2) X(8, 1) X(8, 2) X(8, 4)
+// Instantiated (D / 32, NO / 16): D 1152 (DiT-XL/2, PixArt), 3072 (the video
+// model) and 1280, 128 and 256 (small models), with 16 to 64 outputs per
+// token; 1 to 4 cached features.
+#define BC_FINAL_VARIANTS(X) X(36, 2) X(36, 4) X(40, 2) X(40, 4) X(96, 4) X(4, 1) X(4, 2) X(8, 1) X(8, 2) X(8, 4)
 
 bool final_step_supported(int dt, int D, int NO, int T) {
-    if (dt != BC_BF16 || D % 32 || NO % 16 || T % 16) return false;
+    if (dt != BC_BF16 || D % 32 || NO % 16 || T < 1) return false;
     const int ch = D / 32, nt = NO / 16;
 #define BC_FS_HAS(CH, NTT) if (ch == CH && nt == NTT) return true;
     BC_FINAL_VARIANTS(BC_FS_HAS)
@@ -192,11 +213,13 @@ bool final_step_supported(int dt, int D, int NO, int T) {
 
 template <int CH, int NT>
 static int launch_fs(const FinalStepArgs& a, dim3 grid, hipStream_t s) {
+    constexpr int CW = CH > 40 ? 12 : 4;
+    const dim3 block(64 * (CH / CW));
     switch (a.K) {
-        case 1: final_step_kernel<CH, NT, 1><<<grid, 16 * CH, 0, s>>>(a); break;
-        case 2: final_step_kernel<CH, NT, 2><<<grid, 16 * CH, 0, s>>>(a); break;
-        case 3: final_step_kernel<CH, NT, 3><<<grid, 16 * CH, 0, s>>>(a); break;
-        case 4: final_step_kernel<CH, NT, 4><<<grid, 16 * CH, 0, s>>>(a); break;
+        case 1: final_step_kernel<CH, NT, 1, CW><<<grid, block, 0, s>>>(a); break;
+        case 2: final_step_kernel<CH, NT, 2, CW><<<grid, block, 0, s>>>(a); break;
+        case 3: final_step_kernel<CH, NT, 3, CW><<<grid, block, 0, s>>>(a); break;
+        case 4: final_step_kernel<CH, NT, 4, CW><<<grid, block, 0, s>>>(a); break;
         default: return fail(BC_ERR_UNSUPPORTED, "fused final step: %d cached features", a.K);
     }
     return check_launch("final step");
@@ -207,7 +230,7 @@ int launch_final_step(const FinalStepArgs& a, hipStream_t s) {
         a.NO != a.ls.p * a.ls.p * a.C_out || a.T != a.ls.tokens())
         return fail(BC_ERR_UNSUPPORTED, "fused final step: D %d, NO %d, T %d, K %d", a.D, a.NO, a.T, a.K);
     const int64_t rows = (int64_t)a.B * a.T;
-    const dim3 grid((unsigned)(rows / 16));
+    const dim3 grid((unsigned)((rows + 15) / 16));
     const int ch = a.D / 32, nt = a.NO / 16;
 #define BC_FS(CH, NTT) if (ch == CH && nt == NTT) return launch_fs<CH, NTT>(a, grid, s);
     BC_FINAL_VARIANTS(BC_FS)
