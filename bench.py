@@ -984,8 +984,9 @@ def summarize_trace(args):
     out = ["# Kernel trace of the default benchmark command", "",
            "Command (from a shell in `/tmp`, `TMPDIR=/tmp`):", "",
            "    rocprofv3 --kernel-trace --stats -d <dir> -o run --output-format csv -- "
-           "python3 bench.py --gpus 1 --steps 20 --warmup 5", "",
-           "The run covers everything the command does: the video workload (5 warm-up, 20 timed and one "
+           f"python3 bench.py --gpus 1 --steps {line['steps']} --warmup {line['warmup']}", "",
+           f"The run covers everything the command does: the video workload ({line['warmup']} warm-up, "
+           f"{line['steps']} timed and one "
            "event-timed sampling runs, then one all-full-mask run), the DiT-XL/2 and PixArt legs, the forecast sweep, "
            "the push copy.  Per-call averages are the figures to compare with the JSON line's per-launch averages "
            "(which come from HIP events in the same process).", "",
