@@ -640,6 +640,91 @@ def cpu_baseline_image(cfg, nsteps=9):
                        f"to {nfull} full + {cfg.steps - nfull} forecast steps; numpy fp64 on {cores} host threads")}
 
 
+def cpu_baseline_tiny(cfg):
+    """The oracle (numpy fp64) running the tiny fp32 workload end to end: the
+    whole batch through the whole schedule (full steps and forecasts)."""
+    import numpy as np
+
+    import synth
+    from oracle import bary, model as om, sampler as osm
+    M = om.Model(cfg, synth.params(cfg))
+    mask = bary.make_mask(cfg.steps, cfg.interval)
+    x = synth.latents(cfg).astype(np.float64)
+    t0 = time.perf_counter()
+    osm.sample(M, x, mask, cfg.K)
+    dt = time.perf_counter() - t0
+    return {"value": round(cfg.batch / dt, 3), "unit": "samples/s", "kind": "oracle", "composed": False,
+            "sample": f"the whole batch of {cfg.batch} through all {cfg.steps} steps ({int(mask.sum())} full), "
+                      f"numpy fp64: {dt:.2f} s"}
+
+
+def cpu_baseline_blocks(cfg):
+    """The oracle (numpy fp32 model) on one sample of an image workload, timed
+    in pieces at the full shape (one block, with PixArt's cross-attention; one
+    forecast step over K features; one final layer + sampler update) and
+    composed to a run: #full x depth blocks + #skipped forecasts + every
+    step's final layer (the per-run caption context and the embeddings are
+    left out)."""
+    import numpy as np
+
+    import synth
+    from oracle import bary, model as om, sampler as osm
+    one = synth.scaled(cfg, depth=1, batch=1)
+    M = om.Model(one, synth.params(one), dtype=np.float32)
+    D, T = cfg.hidden, cfg.tokens
+    x = synth.normal("cpu/bx", (1, T, D))
+    c = synth.normal("cpu/bc", (1, D), 0.5)
+    if cfg.kind == "pixart":
+        t6 = synth.normal("cpu/bt6", (1, 6 * D), 0.5)
+        bcond, fcond, ctx = {"t6": t6}, {"t": c, "t6": t6}, M.context(synth.text(one))
+    else:
+        bcond = fcond = {"c": c}
+        ctx = None
+    t0 = time.perf_counter()
+    M.dit_block(0, x, M.block_mod(0, bcond), ctx)
+    t_blk = time.perf_counter() - t0
+    ring = [synth.normal(f"cpu/bring{j}", (1, T, D)) for j in range(cfg.K)]
+    w = bary.bary_weights([float(10 - 2 * j) for j in range(cfg.K)], 12.0)
+    t0 = time.perf_counter()
+    feat = bary.forecast(ring, w)
+    t_fc = time.perf_counter() - t0
+    smp = osm.Sampler(cfg.sampler, cfg.steps, cfg.in_ch, cfg.flow_shift)
+    lat = synth.latents(one).astype(np.float64)
+    t0 = time.perf_counter()
+    smp.step(0, lat, M.final(feat, fcond))
+    t_fin = time.perf_counter() - t0
+    mask = bary.make_mask(cfg.steps, cfg.interval)
+    nfull = int(mask.sum())
+    per = nfull * cfg.depth * t_blk + (cfg.steps - nfull) * t_fc + cfg.steps * t_fin
+    what = "block with cross-attention" if cfg.kind == "pixart" else "block"
+    return {"value": round(1.0 / per, 6), "unit": "samples/s", "kind": "oracle", "composed": True,
+            "sample": (f"oracle pieces on one sample at the full shape (numpy fp32 model): {what} "
+                       f"{t_blk:.2f} s ({T} tokens, D {D}), forecast K={cfg.K} {t_fc * 1e3:.0f} ms, final layer + "
+                       f"update {t_fin * 1e3:.0f} ms; composed to {nfull} full steps x {cfg.depth} blocks + "
+                       f"{cfg.steps - nfull} forecasts + {cfg.steps} final layers")}
+
+
+def cpu_baseline_forecast():
+    """The oracle's Eq. 13 (fp64 accumulation) on fp32 K = 3 features of the
+    forecast microbenchmark shape, timed on a 1/64 slice of it and scaled to
+    the whole [8, 16384, 3072] tensor."""
+    import synth
+    from oracle import bary
+    K, shape = 3, synth.FORECAST_SHAPE
+    rows = 2048                       # of the 8 x 16384 rows: 1/64 of the tensor
+    feats = synth.forecast_features(K, (1, rows, shape[2]))
+    s, t = synth.forecast_times(K)
+    w = bary.bary_weights(s, t)
+    t0 = time.perf_counter()
+    bary.forecast([feats[j] for j in range(K)], w)
+    scale = shape[0] * shape[1] // rows
+    dt = (time.perf_counter() - t0) * scale
+    n = shape[0] * shape[1] * shape[2]
+    return {"value": round((K * 4 + 4) * n / dt / 1e9, 2), "unit": "GB/s", "kind": "oracle", "composed": True,
+            "sample": f"K = 3 fp32 features [1, {rows}, {shape[2]}] (1/{scale} of [8, 16384, 3072]), scaled "
+                      f"x{scale}: {dt:.2f} s for the whole tensor"}
+
+
 # ---------------------------------------------------------------------------
 # counter program
 # ---------------------------------------------------------------------------
@@ -1046,8 +1131,15 @@ def main():
         legs[name] = leg
     forecast, push = (None, None) if args.no_forecast else forecast_sweep(bc, torch)
     cpu = None
+    others = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline_video(cfg) if cfg.kind == "mmdit" else cpu_baseline_image(cfg)
+        # The other configurations' oracle timings (context for their legs).
+        others = {"tiny": cpu_baseline_tiny(synth.CONFIGS["tiny"]),
+                  "dit_xl2": cpu_baseline_blocks(synth.CONFIGS["dit_xl2"]),
+                  "pixart": cpu_baseline_blocks(synth.CONFIGS["pixart"]),
+                  "forecast_k3_f32": cpu_baseline_forecast()}
+        log("[cpu] other configurations: " + ", ".join(f"{k} {v['value']} {v['unit']}" for k, v in others.items()))
 
     mask = head.pop("mask")
     line = {
@@ -1068,6 +1160,7 @@ def main():
         "forecast": forecast,
         "push_copy": push,
         "cpu_baseline": cpu,
+        "cpu_baselines_other": others,
         "paper_context": PAPER_CONTEXT,
     }
     for k in ("graph_replay", "adaptive", "blockwise"):
