@@ -474,6 +474,13 @@ int bc_linear(int M, int N, int K, const void* A, const void* W, const void* bia
 int bc_attention(int B, int H, int Tq, int Tk, int d, const void* q, const void* k,
                  const void* v, void* out, int dtype, void* ws, size_t ws_bytes, void* stream);
 int bc_attention_workspace_size(int B, int H, int Tq, int Tk, int d, int dtype, size_t* bytes);
+/* As bc_attention with pre-scaled queries, the form the sampling loop's
+ * projections write (the attention of Eq. 4's blocks): q already holds
+ * q log2(e) / sqrt(d), so softmax(Q K^T / sqrt(d)) = normalised 2^(q_stored
+ * k^T), and the kernel exponentiates the MFMA output directly.  bf16 only;
+ * the same shapes, layouts, workspace and errors as bc_attention. */
+int bc_attention_prescaled(int B, int H, int Tq, int Tk, int d, const void* q, const void* k,
+                           const void* v, void* out, int dtype, void* ws, size_t ws_bytes, void* stream);
 
 /* Per-kernel timing with HIP events on the stream each kernel is launched on.
  * While enabled for a kernel class, every launch of that class is bracketed by

@@ -143,6 +143,8 @@ _SIGS = {
                             C.c_int, C.c_void_p, C.c_void_p, C.c_int, C.c_int, C.c_void_p]),
     "bc_attention": (C.c_int, [C.c_int, C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_void_p,
                                C.c_void_p, C.c_void_p, C.c_int, C.c_void_p, C.c_size_t, C.c_void_p]),
+    "bc_attention_prescaled": (C.c_int, [C.c_int, C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_void_p,
+                               C.c_void_p, C.c_void_p, C.c_int, C.c_void_p, C.c_size_t, C.c_void_p]),
     "bc_attention_workspace_size": (C.c_int, [C.c_int, C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
                                               C.POINTER(C.c_size_t)]),
     "bc_profile_enable": (C.c_int, [C.c_int, C.c_int]),
@@ -351,12 +353,14 @@ def attention_workspace_size(B, H, Tq, Tk, d, dtype) -> int:
     return n.value
 
 
-def attention(q, k, v, out, ws=None, stream=None):
+def attention(q, k, v, out, ws=None, stream=None, prescaled=False):
+    """prescaled: q already holds q * log2(e) / sqrt(d) (bc_attention_prescaled)."""
     B, Tq, H, d = q.shape
     Tk = k.shape[1]
-    _check(lib().bc_attention(B, H, Tq, Tk, d, dev_ptr(q), dev_ptr(k), dev_ptr(v), dev_ptr(out),
-                              dtype_code(q), dev_ptr(ws), ws.numel() * ws.element_size() if ws is not None else 0,
-                              stream_handle(stream)))
+    fn = lib().bc_attention_prescaled if prescaled else lib().bc_attention
+    _check(fn(B, H, Tq, Tk, d, dev_ptr(q), dev_ptr(k), dev_ptr(v), dev_ptr(out),
+              dtype_code(q), dev_ptr(ws), ws.numel() * ws.element_size() if ws is not None else 0,
+              stream_handle(stream)))
 
 
 def block_desc(kind, B, T, D, heads, head_dim, mlp, dtype, T_txt=0, T_ctx=0, rope=None) -> BlockDesc:

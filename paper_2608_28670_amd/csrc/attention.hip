@@ -868,20 +868,34 @@ int bc_attention_workspace_size(int B, int H, int Tq, int Tk, int d, int dtype, 
     return BC_OK;
 }
 
-int bc_attention(int B, int H, int Tq, int Tk, int d, const void* q, const void* k, const void* v, void* out,
-                 int dtype, void* ws, size_t ws_bytes, void* stream) {
-    clear_error();
-    (void)ws; (void)ws_bytes;
+static int attention_entry(int B, int H, int Tq, int Tk, int d, const void* q, const void* k, const void* v, void* out,
+                           int dtype, int q_scaled, void* stream) {
     if (!q || !k || !v || !out) return fail(BC_ERR_INVALID_ARG, "NULL pointer");
     if (B < 1 || H < 1 || Tq < 1 || Tk < 1 || d < 1) return fail(BC_ERR_INVALID_ARG, "empty attention");
     if (dtype != BC_F32 && dtype != BC_BF16) return fail(BC_ERR_INVALID_ARG, "dtype %d", dtype);
+    if (q_scaled && dtype != BC_BF16) return fail(BC_ERR_UNSUPPORTED, "pre-scaled queries are bf16 only");
     AttnArgs a = {};
+    a.q_scaled = q_scaled;
     a.q0 = q; a.q1 = q; a.Tq0 = Tq; a.Tq1 = 0; a.ldq = (int64_t)H * d;
     a.k0 = k; a.k1 = k; a.Tk0 = Tk; a.Tk1 = 0; a.ldk = (int64_t)H * d;
     a.v0 = v; a.v1 = v; a.ldv = (int64_t)H * d;
     a.o0 = out; a.o1 = out; a.ldo = (int64_t)H * d;
     a.B = B; a.H = H; a.d = d;
     return launch_attention(dtype, a, static_cast<hipStream_t>(stream));
+}
+
+int bc_attention(int B, int H, int Tq, int Tk, int d, const void* q, const void* k, const void* v, void* out,
+                 int dtype, void* ws, size_t ws_bytes, void* stream) {
+    clear_error();
+    (void)ws; (void)ws_bytes;
+    return attention_entry(B, H, Tq, Tk, d, q, k, v, out, dtype, 0, stream);
+}
+
+int bc_attention_prescaled(int B, int H, int Tq, int Tk, int d, const void* q, const void* k, const void* v,
+                           void* out, int dtype, void* ws, size_t ws_bytes, void* stream) {
+    clear_error();
+    (void)ws; (void)ws_bytes;
+    return attention_entry(B, H, Tq, Tk, d, q, k, v, out, dtype, 1, stream);
 }
 
 }  // extern "C"

@@ -89,6 +89,37 @@ def test_attention(bclib, dt, B, H, Tq, Tk, d):
     assert err <= (1e-2 if dt == "bf16" else 1e-5), err
 
 
+# Pre-scaled queries (the form the blocks' projections write): every key-loop
+# variant, i.e. the resident loop, and the streaming loop with 16, 32 (4-wave
+# workgroups at d = 128, 8-wave otherwise) and 64 queries per wave.
+@pytest.mark.parametrize("B,H,Tq,Tk,d", [
+    (16, 16, 256, 256, 72), (1, 2, 100, 37, 128), (1, 2, 1100, 700, 72), (1, 2, 520, 333, 128),
+    (2, 1, 600, 1030, 32), (4, 16, 300, 300, 72), (4, 32, 300, 333, 128), (8, 32, 300, 300, 72),
+    (8, 32, 300, 270, 64), (1, 1, 1, 1, 72)])
+def test_attention_prescaled(bclib, B, H, Tq, Tk, d):
+    q = _inputs(f"q{Tq}{d}", (B, Tq, H, d), "bf16")
+    k = _inputs(f"k{Tk}{d}", (B, Tk, H, d), "bf16")
+    v = _inputs(f"v{Tk}{d}", (B, Tk, H, d), "bf16")
+    # the producer's rounding: q * log2(e) / sqrt(d) in fp32, rounded to bf16
+    c = np.float32(1.4426950408889634) / np.sqrt(np.float32(d))
+    qs = synth.bf16_round((q.astype(np.float32) * c).astype(np.float32))
+    # softmax(q k^T / sqrt(d)) with the queries the stored values stand for
+    qeff = qs.astype(np.float64) / float(c)
+    exp = om.attention(*(a.astype(np.float64).transpose(0, 2, 1, 3) for a in (qeff, k, v))).transpose(0, 2, 1, 3)
+    out = torch.empty((B, Tq, H, d), dtype=torch.bfloat16, device=DEV)
+    bclib.attention(_dev(qs, "bf16"), _dev(k, "bf16"), _dev(v, "bf16"), out, prescaled=True)
+    torch.cuda.synchronize()
+    err = rel_l2(out.float().cpu().numpy().astype(np.float64), exp)
+    assert err <= 1e-2, err
+
+
+def test_attention_prescaled_rejects_fp32(bclib):
+    z = torch.zeros((1, 4, 1, 32), dtype=torch.float32, device=DEV)
+    with pytest.raises(bclib.BCError) as e:
+        bclib.attention(z, z, z, torch.empty_like(z), prescaled=True)
+    assert e.value.code == bclib.ERR_UNSUPPORTED
+
+
 def test_attention_rejects_unsupported_head_dim(bclib):
     z = torch.zeros((1, 4, 1, 40), dtype=torch.bfloat16, device=DEV)
     with pytest.raises(bclib.BCError) as e:
