@@ -481,8 +481,20 @@ __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV ==
     }
 
 
-    // O^T += V^T P^T for one tile's probabilities (and the row sums, see above).
-    auto pv = [&](const bf16* V, f32x4 (&s)[QG][4]) __attribute__((always_inline)) {
+    // Operand addresses: per-lane byte offsets within a tile, worked out once.
+    // A row's swizzle depends only on the row mod 16, so the fragments 16 and
+    // 32 rows further on sit at constant distances, and with the buffer fixed
+    // at compile time every read is a lane offset plus an immediate.
+    typedef __attribute__((address_space(3))) const char lds_char;
+    uint32_t kofs[S::n32x], vofs[S::DV / 16];
+#pragma unroll
+    for (int c = 0; c < S::n32x; ++c) kofs[c] = 2u * (uint32_t)LY::at(ql, 32 * c + grp * 8);
+#pragma unroll
+    for (int i = 0; i < S::DV / 16; ++i) vofs[i] = 2u * (uint32_t)LY::at(4 * grp + (ql >> 2), 16 * i + 4 * (ql & 3));
+    constexpr uint32_t ROWB = 2u * HD;    // bytes per tile row
+    // O^T += V^T P^T for one tile's probabilities (and the row sums, see
+    // above) from the V tile at Vb.
+    auto pv = [&](lds_char* Vb, f32x4 (&s)[QG][4]) __attribute__((always_inline)) {
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
             bf16x8 pf[QG];
@@ -493,15 +505,11 @@ __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV ==
                     pf[g][r] = (bf16)s[g][2 * u][r];
                     pf[g][4 + r] = (bf16)s[g][2 * u + 1][r];
                 }
-            const int kb0 = 32 * u + 4 * grp + (ql >> 2);      // this lane's source key, first half
-            const int dsub = 4 * (ql & 3);
 #pragma unroll
             for (int i = 0; i < S::DV / 16; ++i) {
-                const int d0 = 16 * i + dsub;
-                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (__attribute__((address_space(3))) s16x4*)(V + LY::at(kb0, d0)));
-                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (__attribute__((address_space(3))) s16x4*)(V + LY::at(kb0 + 16, d0)));
+                lds_char* p = Vb + vofs[i] + 32u * u * ROWB;
+                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p);
+                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p + 16 * ROWB));
                 bf16x8 vf = __builtin_bit_cast(bf16x8, u32x4{__builtin_bit_cast(u32x2, lo).x, __builtin_bit_cast(u32x2, lo).y,
                                                             __builtin_bit_cast(u32x2, hi).x, __builtin_bit_cast(u32x2, hi).y});
                 // Padding rows d >= HD of the last block take ones: their
@@ -591,7 +599,7 @@ __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV ==
                 }
         }
 
-        pv(V, s);
+        pv((lds_char*)V, s);
     };
 
     // Streaming tile for pre-scaled queries (QS: q already carries the factor
@@ -606,47 +614,6 @@ __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV ==
     f32x4 negm[QG];
 #pragma unroll
     for (int g = 0; g < QG; ++g) negm[g] = f32x4{0.f, 0.f, 0.f, 0.f};
-    // Operand addresses: per-lane byte offsets within a tile, worked out once.
-    // A row's swizzle depends only on the row mod 16, so the fragments 16 and
-    // 32 rows further on sit at constant distances, and with the buffer fixed
-    // at compile time every read is a lane offset plus an immediate.
-    typedef __attribute__((address_space(3))) const char lds_char;
-    uint32_t kofs[S::n32x], vofs[S::DV / 16];
-#pragma unroll
-    for (int c = 0; c < S::n32x; ++c) kofs[c] = 2u * (uint32_t)LY::at(ql, 32 * c + grp * 8);
-#pragma unroll
-    for (int i = 0; i < S::DV / 16; ++i) vofs[i] = 2u * (uint32_t)LY::at(4 * grp + (ql >> 2), 16 * i + 4 * (ql & 3));
-    constexpr uint32_t ROWB = 2u * HD;    // bytes per tile row
-    auto pv_fixed = [&](lds_char* Vb, f32x4 (&s)[QG][4]) __attribute__((always_inline)) {
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            bf16x8 pf[QG];
-#pragma unroll
-            for (int g = 0; g < QG; ++g)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    pf[g][r] = (bf16)s[g][2 * u][r];
-                    pf[g][4 + r] = (bf16)s[g][2 * u + 1][r];
-                }
-#pragma unroll
-            for (int i = 0; i < S::DV / 16; ++i) {
-                lds_char* p = Vb + vofs[i] + 32u * u * ROWB;
-                const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)p);
-                const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p + 16 * ROWB));
-                bf16x8 vf = __builtin_bit_cast(bf16x8, u32x4{__builtin_bit_cast(u32x2, lo).x, __builtin_bit_cast(u32x2, lo).y,
-                                                            __builtin_bit_cast(u32x2, hi).x, __builtin_bit_cast(u32x2, hi).y});
-                if (PADSUM && i == S::DV / 16 - 1 && (lane & 15) >= HD - 16 * i)
-                    vf = __builtin_bit_cast(bf16x8, u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
-#pragma unroll
-                for (int g = 0; g < QG; ++g) o[g][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[g], o[g][i], 0, 0, 0);
-            }
-            if constexpr (!PADSUM) {
-                const bf16x8 ones = __builtin_bit_cast(bf16x8, u32x4{0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u});
-#pragma unroll
-                for (int g = 0; g < QG; ++g) osum[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[g], osum[g], 0, 0, 0);
-            }
-        }
-    };
     auto tile_stream = [&](int k0, auto bufc, bool first) __attribute__((always_inline)) {
         constexpr int BUF = decltype(bufc)::value;
         lds_char* Kb = (lds_char*)&sK[BUF][0];
@@ -714,7 +681,7 @@ __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV ==
             for (int j = 0; j < 4; ++j)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) s[g][j][r] = __builtin_amdgcn_exp2f(s[g][j][r]);
-        pv_fixed(Vb, s);
+        pv(Vb, s);
     };
 
     if (resident) {
