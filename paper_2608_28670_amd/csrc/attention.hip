@@ -472,6 +472,7 @@ __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV ==
 
     f32x4 o[QG][S::DV / 16], osum[QG];
     float m_run[QG];
+    const bool o8 = (a.ldo & 3) == 0 && ((reinterpret_cast<uintptr_t>(a.o0) | reinterpret_cast<uintptr_t>(a.o1)) & 7) == 0;
 #pragma unroll
     for (int g = 0; g < QG; ++g) {
         m_run[g] = QS ? 0.f : -INFINITY;     // the pre-scaled streaming tile's reference starts at 0
@@ -726,13 +727,22 @@ __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV ==
         const float inv = 1.f / lsum;
         if (myq[g] < Tq) {
             bf16* orow = const_cast<bf16*>(seg_row<bf16>(a.o0, a.o1, a.Tq0, a.Tq1, a.ldo, b, myq[g])) + col0;
+            // A lane holds four consecutive d of each 16-row block: one 8-byte
+            // store each where the output rows are 8-byte aligned.
 #pragma unroll
-            for (int i = 0; i < S::DV / 16; ++i)
+            for (int i = 0; i < S::DV / 16; ++i) {
+                const int d = 16 * i + 4 * grp;     // HD % 4 == 0: all four in or all out
+                if (d >= HD) continue;
+                if (o8) {
+                    bf16x4 w;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int d = 16 * i + 4 * grp + r;
-                    if (d < HD) st(orow + d, o[g][i][r] * inv);
+                    for (int r = 0; r < 4; ++r) w[r] = (bf16)(o[g][i][r] * inv);
+                    *reinterpret_cast<bf16x4*>(orow + d) = w;
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) st(orow + d + r, o[g][i][r] * inv);
                 }
+            }
         }
     }
 }

@@ -113,6 +113,24 @@ def test_attention_prescaled(bclib, B, H, Tq, Tk, d):
     assert err <= 1e-2, err
 
 
+# Output rows that are not 8-byte aligned take the per-element stores.
+@pytest.mark.parametrize("B,H,Tq,Tk,d", [(2, 3, 200, 200, 72), (1, 2, 520, 333, 128)])
+def test_attention_unaligned_output(bclib, B, H, Tq, Tk, d):
+    q = _inputs(f"q{Tq}{d}", (B, Tq, H, d), "bf16")
+    k = _inputs(f"k{Tk}{d}", (B, Tk, H, d), "bf16")
+    v = _inputs(f"v{Tk}{d}", (B, Tk, H, d), "bf16")
+    exp = om.attention(*(a.astype(np.float64).transpose(0, 2, 1, 3) for a in (q, k, v))).transpose(0, 2, 1, 3)
+    n = B * Tq * H * d
+    buf = torch.zeros(n + 2, dtype=torch.bfloat16, device=DEV)
+    out = buf[2:].view(B, Tq, H, d)     # 4 bytes past an aligned start
+    assert out.data_ptr() % 8 == 4
+    bclib.attention(_dev(q, "bf16"), _dev(k, "bf16"), _dev(v, "bf16"), out)
+    torch.cuda.synchronize()
+    err = rel_l2(out.float().cpu().numpy().astype(np.float64), exp)
+    assert err <= 1e-2, err
+    assert float(buf[:2].abs().sum()) == 0.0     # nothing written before the output
+
+
 def test_attention_prescaled_rejects_fp32(bclib):
     z = torch.zeros((1, 4, 1, 32), dtype=torch.float32, device=DEV)
     with pytest.raises(bclib.BCError) as e:
