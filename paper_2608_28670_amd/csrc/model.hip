@@ -900,11 +900,28 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
         return BC_OK;
     };
 
-    // The fused final step needs 16-byte aligned ring slots and weights (checked
+    // The fused final step needs 16-byte aligned features (ring slots, or the
+    // blockwise sampler's fp32 stream in the workspace) and weights (checked
     // here once) and an instantiated (D, p*p*C_out).
-    const bool fused_final = !guided && !bw && final_step_supported(dt, D, d.patch * d.patch * d.out_ch, T) &&
-                             reinterpret_cast<uintptr_t>(ring->storage) % 16 == 0 && (ring->numel * esz) % 16 == 0 &&
-                             reinterpret_cast<uintptr_t>(mw.final_w) % 16 == 0;
+    const bool fused_final = final_step_supported(dt, D, d.patch * d.patch * d.out_ch, T) && (D <= 1280 || !(guided || bw)) &&
+                             reinterpret_cast<uintptr_t>(mw.final_w) % 16 == 0 &&
+                             (bw ? reinterpret_cast<uintptr_t>(w.x) % 16 == 0
+                                 : reinterpret_cast<uintptr_t>(ring->storage) % 16 == 0 && (ring->numel * esz) % 16 == 0);
+    auto final_args = [&](const SamplerCoef& sc, const float* fmod) {
+        FinalStepArgs fa;
+        std::memset(&fa, 0, sizeof fa);
+        fa.guided = guided ? 1 : 0;
+        fa.cfg = cfg;
+        fa.B = B; fa.T = T; fa.D = D; fa.NO = d.patch * d.patch * d.out_ch; fa.C_out = d.out_ch;
+        fa.fmod = fmod;
+        fa.W = mw.final_w;
+        fa.bias = mw.final_b;
+        fa.sc = sc;
+        fa.x = latents;
+        fa.prev = w.prev;
+        fa.ls = ls;
+        return fa;
+    };
 
     int full_index = 0;
     double acc = 0.0;   // adaptive: changes summed since the last full step
@@ -991,6 +1008,16 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
                 BC_TRY(launch_blockwise_forecast(dt, a, s));
             }
             const SamplerCoef sc = sampler_coef(sampler, k, S, tau.data(), ab, &h_prev, d.flow_shift);
+            if (fused_final) {
+                // The stream itself is the feature: final layer and update in one pass.
+                FinalStepArgs fa = final_args(sc, fmod);
+                fa.src_f32 = 1;
+                fa.K = 1;
+                fa.src[0] = w.x;
+                fa.w[0] = 1.f;
+                BC_TRY(launch_final_step(fa, s));
+                continue;
+            }
             BC_TRY(launch_ln_mod(BC_F32, w.x, (int64_t)Bm * T, D, fmod, fmod + D, 2 * D, T, dt, w.bb.h, s));
             GemmArgs fg = gemm_args(w.bb.h, D, mw.final_w, D, Bm * T, NO, D);
             fg.e.bias = mw.final_b;
@@ -1050,7 +1077,7 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
         if (fused_final && (st.is_full || st.count <= kFinalMaxK)) {
             // Stepwise feature (the new slot, or the forecast from the ring), final
             // layer and sampler update in one pass over the tokens.
-            FinalStepArgs fa;
+            FinalStepArgs fa = final_args(sc, fmod);
             if (st.is_full) {
                 fa.K = 1;
                 fa.src[0] = feat;
@@ -1062,14 +1089,6 @@ static int sample_run(const bc_model* m, int B, int sampler, int S, const uint8_
                     fa.w[j] = (float)st.w[j];
                 }
             }
-            fa.B = B; fa.T = T; fa.D = D; fa.NO = NO; fa.C_out = d.out_ch;
-            fa.fmod = fmod;
-            fa.W = mw.final_w;
-            fa.bias = mw.final_b;
-            fa.sc = sc;
-            fa.x = latents;
-            fa.prev = w.prev;
-            fa.ls = ls;
             BC_TRY(launch_final_step(fa, s));
             continue;
         }

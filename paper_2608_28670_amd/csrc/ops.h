@@ -159,6 +159,9 @@ struct FinalStepArgs {
     const void* src[8];
     float w[8];
     int K;
+    int src_f32;          // one fp32 feature (K = 1) instead of K bf16 ones
+    int guided;           // features and modulation hold 2B samples, the second half unconditional
+    float cfg;            // guidance scale (guided)
     int B, T, D, NO, C_out;
     const float* fmod;
     const void* W;

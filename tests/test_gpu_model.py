@@ -426,15 +426,17 @@ def test_sample_cfg_tiny_conditional_fp32(bclib):
     assert ring.numel == 2 * 2 * cfg.tokens * cfg.hidden
 
 
-def test_sample_cfg_dit_xl2_reduced_depth(bclib):
-    cfg = synth.scaled(synth.CONFIGS["dit_xl2"], depth=2, batch=2)
+# bf16: the fused final step combines the two halves (K = 2, 3, 4 cached features).
+@pytest.mark.parametrize("K", [2, 3, 4])
+def test_sample_cfg_dit_xl2_reduced_depth(bclib, K):
+    cfg = synth.scaled(synth.CONFIGS["dit_xl2"], depth=2, batch=2, K=K)
     P = synth.params(cfg)
     mask = bary.make_mask(cfg.steps, cfg.interval)
     labels = synth.labels(cfg, batch=2)
     xT, got, _ = _run_cfg(cfg, P, 2, mask, labels, 1.5)
     exp = osm.sample(om.Model(cfg, P), xT.astype(np.float64), mask, cfg.K, labels=labels, cfg_scale=1.5)
     err = rel_l2(got, exp)
-    print(f"dit_xl2 depth 2, cfg 1.5: rel-L2 {err:.2e}")
+    print(f"dit_xl2 depth 2, K {K}, cfg 1.5: rel-L2 {err:.2e}")
     assert err <= 2e-2
 
 
