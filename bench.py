@@ -149,12 +149,15 @@ def kernel_shapes(cfg):
             att("cross-attention", T, cfg.ctx_tokens)
     else:
         Tt = cfg.txt_tokens
+        L = T + Tt
         for s, M in (("image", B * T), ("text", B * Tt)):
             gemm("gemm_bias", f"dual-stream {s} QKV projection", M, 3 * D, D)
-            gemm("gemm_gated", f"dual-stream {s} output projection + gated residual", M, D, D)
-            gemm("gemm_gelu", f"dual-stream {s} MLP up projection + GELU", M, F, D)
-            gemm("gemm_down", f"dual-stream {s} MLP down projection + gated residual", M, D, F)
-        L = T + Tt
+        # The other dual-stream GEMMs run the image and text streams in one
+        # launch (the text tiles fill the image grid's last round): one group
+        # with the work of B (T + Tt) rows.
+        gemm("gemm_gated", "dual-stream output projection + gated residual (image and text)", B * L, D, D)
+        gemm("gemm_gelu", "dual-stream MLP up projection + GELU (image and text)", B * L, F, D)
+        gemm("gemm_down", "dual-stream MLP down projection + gated residual (image and text)", B * L, D, F)
         gemm("gemm_gelu", "single-stream [qkv | mlp] projection + GELU", B * L, 3 * D + F, D)
         gemm("gemm_down", "single-stream output projection + gated residual", B * L, D, D + F)
         att("joint attention (dual- and single-stream)", L, L)
@@ -181,9 +184,11 @@ def group_launches(records, cfg):
 
 
 # kernel-name prefix of a profiled class's launches (the gated epilogue is template argument 2)
-CLASS_KERNEL = {"attention": "void bc::attention_dma_kernel<", "gemm_gated": "void bc::gemm_wide_kernel<2,",
-                "gemm_down": "void bc::gemm_wide_kernel<2,", "gemm_gelu": "void bc::gemm_wide_kernel<0,",
-                "gemm_bias": "void bc::gemm_wide_kernel<0,"}
+CLASS_KERNEL = {"attention": ("void bc::attention_dma_kernel<",),
+                "gemm_gated": ("void bc::gemm_wide_kernel<2,", "void bc::gemm_wide_pair_kernel<2,"),
+                "gemm_down": ("void bc::gemm_wide_kernel<2,", "void bc::gemm_wide_pair_kernel<2,"),
+                "gemm_gelu": ("void bc::gemm_wide_kernel<0,", "void bc::gemm_wide_pair_kernel<0,"),
+                "gemm_bias": ("void bc::gemm_wide_kernel<0,", "void bc::gemm_wide_pair_kernel<0,")}
 
 
 def loop_traffic(workload, g, src):

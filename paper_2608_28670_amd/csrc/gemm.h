@@ -54,6 +54,11 @@ struct GemmSeg {
 GemmArgs gemm_args(const void* A, int64_t lda, const void* W, int64_t ldw, int M, int N, int K);
 // epi: BC_EPI_BIAS (covers GELU via gelu_from) or BC_EPI_GATE_RES.
 int launch_gemm(int dtype, int epi, const GemmArgs& g, hipStream_t s);
+// Two GEMMs with the same epilogue kind in one launch when the second one's
+// tiles fit the idle part of the first one's last round (the dual-stream
+// blocks' text-stream projections beside the image-stream ones); otherwise
+// two launches.
+int launch_gemm_pair(int dtype, int epi, const GemmArgs& g0, const GemmArgs& g1, hipStream_t s);
 // Bias epilogue over nseg column segments (g.N is ignored; g.e.out / ldo
 // describe the whole [M, nseg*Nseg] output).
 int launch_gemm_grouped(int dtype, const GemmArgs& g, const GemmSeg& sg, int nseg, hipStream_t s);

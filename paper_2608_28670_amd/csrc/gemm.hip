@@ -511,8 +511,8 @@ template <int Q, int L = 0, int LMAX = 3> __device__ __forceinline__ void wait_g
     }
 }
 
-template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int BK, int KG, int PIPE = 0>
-__global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KG) void gemm_wide_kernel(GemmArgs g) {
+template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int BK, int KG, int PIPE>
+__device__ __forceinline__ void gemm_wide_body(GemmArgs g, int tile) {
     typedef bf16 T;
     typedef Mma<bf16> MM;
     constexpr int NWG = WAVES_M * WAVES_N;                // waves per K group
@@ -550,9 +550,6 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KG) void gemm_wide_kernel(
 
     const int tiles_m = (g.M + BM - 1) / BM;
     const int tiles_n = (g.N + BN - 1) / BN;
-    const int nwg = gridDim.x;
-    const int pid = xcd_contiguous(blockIdx.x, nwg);
-    const int tile = pid;
     constexpr int GROUP_M = 8;
     const int group = GROUP_M * tiles_n;
     const int first_m = (tile / group) * GROUP_M;
@@ -828,6 +825,24 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KG) void gemm_wide_kernel(
     epilogue_t<EPI, TM, TN>(g, acc, bm + wm * WM, bn + j0 * 16, lane, jn, pf);
 }
 
+template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int BK, int KG, int PIPE = 0>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KG) void gemm_wide_kernel(GemmArgs g) {
+    gemm_wide_body<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, BK, KG, PIPE>(g, xcd_contiguous(blockIdx.x, gridDim.x));
+}
+
+// Two GEMMs in one grid: workgroups [0, tiles0) take the first (in the
+// XCD-contiguous order over its own tiles), the rest the second, whose
+// workgroups come last and are dealt round-robin to the XCDs, so its tiles
+// fill the first one's last round.
+template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES, int BK, int KG, int PIPE = 0>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N * KG) void gemm_wide_pair_kernel(GemmArgs g0, GemmArgs g1,
+                                                                                     int tiles0) {
+    const int b = blockIdx.x;
+    const bool second = b >= tiles0;
+    gemm_wide_body<EPI, BM, BN, WAVES_M, WAVES_N, STAGES, BK, KG, PIPE>(second ? g1 : g0,
+                                                                        second ? b - tiles0 : xcd_contiguous(b, tiles0));
+}
+
 template <int EPI, int BM, int BN, int WAVES_M, int WAVES_N, int STAGES = 2, int BK = 64, int KG = 1, int PIPE = 0>
 static void launch_wide(const GemmArgs& g, hipStream_t s) {
     const unsigned tiles = (unsigned)(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN));
@@ -971,6 +986,37 @@ int launch_gemm(int dtype, int epi, const GemmArgs& g, hipStream_t s) {
     }
     prof_end(cls, s);
     return rc;
+}
+
+// The first GEMM's tile choice must be 256 x 256 (as run_gemm picks it) and
+// the second one's tiles must fit the idle part of the first one's last
+// round; otherwise two launches.
+int launch_gemm_pair(int dtype, int epi, const GemmArgs& g0, const GemmArgs& g1, hipStream_t s) {
+    if (g1.M <= 0 || g1.N <= 0) return launch_gemm(dtype, epi, g0, s);
+    if (g0.M <= 0 || g0.N <= 0) return launch_gemm(dtype, epi, g1, s);
+    auto wide = [&](const GemmArgs& g) {
+        return dtype == BC_BF16 && g.K > 0 && g.K % 64 == 0 && g.lda % 8 == 0 && g.ldw % 8 == 0 &&
+               (reinterpret_cast<uintptr_t>(g.A) | reinterpret_cast<uintptr_t>(g.W)) % 16 == 0 && wide_ok(g, epi);
+    };
+    const int64_t t0 = (int64_t)((g0.M + 255) / 256) * ((g0.N + 255) / 256);
+    const int64_t t1 = (int64_t)((g1.M + 255) / 256) * ((g1.N + 255) / 256);
+    const int64_t t288 = (int64_t)((g0.M + 255) / 256) * ((g0.N + 287) / 288);
+    const int64_t idle = (t0 + 255) / 256 * 256 - t0;
+    const bool big = t288 >= 256 && g0.N % 288 != 0 && g0.N % 256 == 0;
+    if (!(wide(g0) && wide(g1) && big && t1 <= idle && t0 + t1 <= 0x7fffffff)) {
+        const int rc = launch_gemm(dtype, epi, g0, s);
+        return rc != BC_OK ? rc : launch_gemm(dtype, epi, g1, s);
+    }
+    const int cls = epi == BC_EPI_GATE_RES ? (g0.K > g0.N ? PROF_GEMM_DOWN : PROF_GEMM_GATE)
+                    : g0.e.gelu_from < g0.N ? PROF_GEMM_GELU : PROF_GEMM_BIAS;
+    prof_begin(cls, s, 2.0 * g0.M * (double)g0.N * g0.K + 2.0 * g1.M * (double)g1.N * g1.K);
+    const dim3 grid((unsigned)(t0 + t1)), block(1024);
+    if (epi == BC_EPI_GATE_RES)
+        launch_k(gemm_wide_pair_kernel<BC_EPI_GATE_RES, 256, 256, 4, 4, 2, 64, 1, 0>, grid, block, s, g0, g1, (int)t0);
+    else
+        launch_k(gemm_wide_pair_kernel<BC_EPI_BIAS, 256, 256, 4, 4, 2, 64, 1, 0>, grid, block, s, g0, g1, (int)t0);
+    prof_end(cls, s);
+    return check_launch("gemm pair");
 }
 
 GemmArgs gemm_args(const void* A, int64_t lda, const void* W, int64_t ldw, int M, int N, int K) {

@@ -61,8 +61,8 @@ struct BlockOut {
     int seg = 0, keep = 0;
 };
 
-static int gated(int dt, const void* A, int64_t lda, const void* W, const void* bias, int M, int N, int K, float* x,
-                 const float* gate, int64_t ldg, int rows_per_gate, const BlockOut* out, hipStream_t s) {
+static GemmArgs gated_args(const void* A, int64_t lda, const void* W, const void* bias, int M, int N, int K, float* x,
+                           const float* gate, int64_t ldg, int rows_per_gate, const BlockOut* out = nullptr) {
     GemmArgs g = gemm_args(A, lda, W, K, M, N, K);
     g.e.bias = bias;
     g.e.res = x;
@@ -80,17 +80,27 @@ static int gated(int dt, const void* A, int64_t lda, const void* W, const void* 
         g.e.out_f32 = 1;
     }
     g.e.ldo = N;
-    return launch_gemm(dt, BC_EPI_GATE_RES, g, s);
+    return g;
 }
 
-static int plain(int dt, const void* A, int64_t lda, const void* W, const void* bias, int M, int N, int K, void* out,
-                 bool gelu, hipStream_t s) {
+static int gated(int dt, const void* A, int64_t lda, const void* W, const void* bias, int M, int N, int K, float* x,
+                 const float* gate, int64_t ldg, int rows_per_gate, const BlockOut* out, hipStream_t s) {
+    return launch_gemm(dt, BC_EPI_GATE_RES, gated_args(A, lda, W, bias, M, N, K, x, gate, ldg, rows_per_gate, out), s);
+}
+
+static GemmArgs plain_args(const void* A, int64_t lda, const void* W, const void* bias, int M, int N, int K, void* out,
+                           bool gelu) {
     GemmArgs g = gemm_args(A, lda, W, K, M, N, K);
     g.e.bias = bias;
     g.e.out = out;
     g.e.ldo = N;
     if (gelu) g.e.gelu_from = 0;
-    return launch_gemm(dt, BC_EPI_BIAS, g, s);
+    return g;
+}
+
+static int plain(int dt, const void* A, int64_t lda, const void* W, const void* bias, int M, int N, int K, void* out,
+                 bool gelu, hipStream_t s) {
+    return launch_gemm(dt, BC_EPI_BIAS, plain_args(A, lda, W, bias, M, N, K, out, gelu), s);
 }
 
 #define BC_TRY(x) do { const int _rc = (x); if (_rc != BC_OK) return _rc; } while (0)
@@ -197,14 +207,23 @@ static int dual_block(const bc_block_desc& d, const bc_block_weights& w, float* 
     a.o0 = at_i; a.o1 = at_t; a.ldo = D;
     a.B = d.B; a.H = d.heads; a.d = d.head_dim;
     BC_TRY(launch_attention(dt, a, s));
-    BC_TRY(gated(dt, at_i, D, w.img.w_o, w.img.b_o, Mi, D, D, x, mi + 2 * D, ld_mod, T, nullptr, s));
-    BC_TRY(gated(dt, at_t, D, w.txt.w_o, w.txt.b_o, Mt, D, D, xt, mt + 2 * D, ld_mod, Tt, nullptr, s));
-    BC_TRY(launch_ln_mod(BC_F32, x, Mi, D, mi + 3 * D, mi + 4 * D, ld_mod, T, dt, bb.h, s));
-    BC_TRY(plain(dt, bb.h, D, w.img.w_fc1, w.img.b_fc1, Mi, F, D, bb.mlp, true, s));
-    BC_TRY(gated(dt, bb.mlp, F, w.img.w_fc2, w.img.b_fc2, Mi, D, F, x, mi + 5 * D, ld_mod, T, nullptr, s));
-    BC_TRY(launch_ln_mod(BC_F32, xt, Mt, D, mt + 3 * D, mt + 4 * D, ld_mod, Tt, dt, bb.h, s));
-    BC_TRY(plain(dt, bb.h, D, w.txt.w_fc1, w.txt.b_fc1, Mt, F, D, bb.mlp, true, s));
-    return gated(dt, bb.mlp, F, w.txt.w_fc2, w.txt.b_fc2, Mt, D, F, xt, mt + 5 * D, ld_mod, Tt, nullptr, s);
+    // The output projections and the MLP: each text-stream GEMM shares a launch
+    // with its image-stream counterpart (its tiles fill the image grid's last
+    // round); the LayerNorm outputs and MLP hiddens hold image rows, then text rows.
+    BC_TRY(launch_gemm_pair(dt, BC_EPI_GATE_RES,
+                            gated_args(at_i, D, w.img.w_o, w.img.b_o, Mi, D, D, x, mi + 2 * D, ld_mod, T),
+                            gated_args(at_t, D, w.txt.w_o, w.txt.b_o, Mt, D, D, xt, mt + 2 * D, ld_mod, Tt), s));
+    char* h_i = static_cast<char*>(bb.h);
+    char* h_t = h_i + (int64_t)Mi * D * esz;
+    char* f_i = static_cast<char*>(bb.mlp);
+    char* f_t = f_i + (int64_t)Mi * F * esz;
+    BC_TRY(launch_ln_mod(BC_F32, x, Mi, D, mi + 3 * D, mi + 4 * D, ld_mod, T, dt, h_i, s));
+    BC_TRY(launch_ln_mod(BC_F32, xt, Mt, D, mt + 3 * D, mt + 4 * D, ld_mod, Tt, dt, h_t, s));
+    BC_TRY(launch_gemm_pair(dt, BC_EPI_BIAS, plain_args(h_i, D, w.img.w_fc1, w.img.b_fc1, Mi, F, D, f_i, true),
+                            plain_args(h_t, D, w.txt.w_fc1, w.txt.b_fc1, Mt, F, D, f_t, true), s));
+    return launch_gemm_pair(dt, BC_EPI_GATE_RES,
+                            gated_args(f_i, F, w.img.w_fc2, w.img.b_fc2, Mi, D, F, x, mi + 5 * D, ld_mod, T),
+                            gated_args(f_t, F, w.txt.w_fc2, w.txt.b_fc2, Mt, D, F, xt, mt + 5 * D, ld_mod, Tt), s);
 }
 
 // Single-stream block on x [B*(T+Tt), D]: mod (shift, scale, gate) [B, >= 3D].
