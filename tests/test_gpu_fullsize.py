@@ -105,6 +105,24 @@ def test_dual_block_video_real_width(bclib, video):
     _check("dual block text rows", gt[:, rt], xt[:, rt], et)
 
 
+def test_dual_block_video_real_width_ragged_text(bclib, video):
+    """77 text tokens: the text stream's projections, which share launches with
+    the image stream's, run one ragged row tile."""
+    cfg0, P = video
+    cfg = synth.scaled(cfg0, txt_tokens=77)
+    M = om.Model(cfg, P, dtype=np.float32)
+    x = synth.normal("vblk/x", (1, cfg.tokens, cfg.hidden))
+    xt = synth.normal("vblk/xt77", (1, cfg.txt_tokens, cfg.hidden))
+    c = synth.normal("vblk/c", (1, cfg.hidden), 0.5)
+    print("dual block 3072 x 24x128, 14310 + 77 tokens: GPU", flush=True)
+    gi, gt = _video_block(bclib, cfg, P, bclib.BLOCK_DUAL, x, c, x_txt=xt)
+    ri, rt = _rows(cfg.tokens, 32, 5), _rows(cfg.txt_tokens, 16, 6)
+    print("dual block, 77 text tokens: oracle on sampled rows", flush=True)
+    ei, et = M.dual_block(0, x, xt, {"c": c}, rows=(ri, rt))
+    _check("dual block (77 text tokens) image rows", gi[:, ri], x[:, ri], ei)
+    _check("dual block (77 text tokens) text rows", gt[:, rt], xt[:, rt], et)
+
+
 def test_single_block_video_real_width(bclib, video):
     cfg, P = video
     M = om.Model(cfg, P, dtype=np.float32)
