@@ -385,6 +385,25 @@ def test_sample_dit_xl2_full_size_sampled(bclib):
         assert err <= 2e-2
 
 
+def test_sample_pixart_full_tokens_batch4_sampled(bclib):
+    """The PixArt workload's batch of 4 at its full token shape in the
+    sampling loop (16 384 rows: the block GEMMs take their multi-round tiles,
+    and the attention its 512-query workgroups), full schedule, depth 2;
+    samples 0 and 3 recomputed alone by the oracle in fp32."""
+    cfg = synth.scaled(synth.CONFIGS["pixart"], depth=2, batch=4)
+    assert cfg.tokens == 4096 and cfg.batch == 4
+    P = synth.params(cfg)
+    mask = bary.make_mask(cfg.steps, cfg.interval)
+    text = synth.text(cfg, batch=4)
+    xT, got, ring = _run_sample(bclib, cfg, P, 4, mask, text=text)
+    _check_ring(ring, mask, cfg.K)
+    for b in (0, 3):
+        exp = _oracle_sample(cfg, P, xT[b:b + 1], mask, text=text[b:b + 1], dtype=np.float32)
+        err = rel_l2(got[b:b + 1], exp)
+        print(f"pixart batch 4 full tokens, sample {b}: final latents rel-L2 {err:.2e}")
+        assert err <= 2e-2
+
+
 def test_sample_rejects_bad_inputs(bclib):
     cfg = synth.CONFIGS["tiny"]
     P = synth.params(cfg)
