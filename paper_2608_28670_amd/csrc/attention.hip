@@ -801,8 +801,13 @@ int launch_attention(int dtype, AttnArgs a, hipStream_t s) {
     a.scale_log2 = a.q_scaled ? 1.0f : attn_q_scale(a.d);
     prof_begin(PROF_ATTENTION, s, 4.0 * a.B * a.H * (double)(a.Tq0 + a.Tq1) * (double)(a.Tk0 + a.Tk1) * a.d);
     // The direct-to-LDS kernel needs 16-byte aligned Q/K/V rows (checked above).
-    // Up to 256 keys: 8 waves of 16 queries with every key tile resident in
-    // LDS (one load, no barriers in the key loop); longer sequences: waves
+    // Up to 256 keys: 8 waves with every key tile resident in LDS (one load,
+    // no barriers in the key loop), 32 queries each when that still leaves two
+    // rounds of 256-query workgroups (PixArt's cross-attention to 120 keys at
+    // batch 4: 35.1 -> 28.7 us in a probe, 59.6 -> 58.5 ms of attention per
+    // sampling run), else 16 (DiT-XL/2's self-attention, one round of
+    // 256-query workgroups: 15.2 -> 14.0 us in a probe, but not faster in the
+    // sampling loop); longer sequences: waves
     // over a double buffer, 64 queries each for d <= 72 (every K/V fragment
     // read from LDS feeds four MFMAs; 8 waves) and 32 for d = 128 (64 would
     // not fit the registers; pre-scaled queries in 4-wave workgroups, two per
@@ -815,7 +820,8 @@ int launch_attention(int dtype, AttnArgs a, hipStream_t s) {
         // they still give the grid a full round of workgroups.
         const int64_t bh = (int64_t)a.B * a.H;
         const int64_t n512 = (Tq + 511) / 512 * bh, n256 = (Tq + 255) / 256 * bh;
-        if (Tk <= 4 * kKTile) rc = run_attention_dma<1, 8, 4, false>(a, a.d, s);
+        if (Tk <= 4 * kKTile && n256 >= 512) rc = run_attention_dma<2, 8, 4, false>(a, a.d, s);
+        else if (Tk <= 4 * kKTile) rc = run_attention_dma<1, 8, 4, false>(a, a.d, s);
         else if (a.d <= 72 && n512 >= 256)
             rc = a.q_scaled ? run_attention_dma<4, 8, 2, true, true>(a, a.d, s) : run_attention_dma<4, 8, 2>(a, a.d, s);
         else if (n256 >= 128 && a.d == 128 && a.q_scaled)

@@ -76,6 +76,8 @@ def test_linear_rejects_bad_k(bclib):
     ("bf16", 1, 2, 1100, 700, 72), ("bf16", 2, 1, 600, 1030, 32), ("bf16", 1, 2, 520, 333, 128),
     # enough (sample, head) pairs for the 256- and 512-query workgroups
     ("bf16", 8, 32, 300, 300, 72), ("bf16", 8, 32, 300, 270, 64), ("bf16", 4, 32, 300, 333, 128),
+    # resident key tiles with 32 queries per wave (short key sequences, large grids)
+    ("bf16", 8, 32, 300, 120, 72), ("bf16", 8, 32, 300, 200, 128), ("bf16", 8, 32, 260, 256, 32),
     ("f32", 2, 4, 64, 64, 32), ("f32", 1, 2, 77, 131, 64)])
 def test_attention(bclib, dt, B, H, Tq, Tk, d):
     q = _inputs(f"q{Tq}{d}", (B, Tq, H, d), dt)
@@ -96,7 +98,8 @@ def test_attention(bclib, dt, B, H, Tq, Tk, d):
 @pytest.mark.parametrize("B,H,Tq,Tk,d", [
     (16, 16, 256, 256, 72), (1, 2, 100, 37, 128), (1, 2, 1100, 700, 72), (1, 2, 520, 333, 128),
     (2, 1, 600, 1030, 32), (4, 16, 300, 300, 72), (4, 32, 300, 333, 128), (4, 32, 300, 310, 128),
-    (8, 32, 300, 300, 72), (8, 32, 300, 270, 64), (1, 1, 1, 1, 72)])
+    (8, 32, 300, 300, 72), (8, 32, 300, 270, 64), (8, 32, 300, 120, 72), (8, 32, 300, 200, 128),
+    (1, 1, 1, 1, 72)])
 def test_attention_prescaled(bclib, B, H, Tq, Tk, d):
     q = _inputs(f"q{Tq}{d}", (B, Tq, H, d), "bf16")
     k = _inputs(f"k{Tk}{d}", (B, Tk, H, d), "bf16")
