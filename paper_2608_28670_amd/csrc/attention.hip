@@ -387,14 +387,17 @@ __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV ==
     // This wave's instructions and its lane's (row, chunk) in each are fixed:
     // worked out once, so a tile's issue only offsets the key.
     constexpr int NJ = (LY::CPR + NWV - 1) / NWV;
-    int irow[NJ], icol[NJ];
-#pragma unroll
-    for (int q = 0; q < NJ; ++q) {
+    // (row, global column) of this lane's chunk in instruction q, recomputed
+    // where needed rather than held in registers.
+    auto irow = [&](int q) { return (64 * (wave + NWV * q) + lane) / LY::CPR; };
+    auto icol = [&](int q) {
         const int c = 64 * (wave + NWV * q) + lane;
         const int row = c / LY::CPR, slot = c % LY::CPR;
-        irow[q] = row;
-        icol[q] = col0 + 8 * (LY::SWZ ? slot ^ ((row / LY::RPB) % LY::CPR) : slot);
-    }
+        return col0 + 8 * (LY::SWZ ? slot ^ ((row / LY::RPB) % LY::CPR) : slot);
+    };
+    // With four query groups per wave the value offsets are derived from the
+    // key offsets (one register per instruction fewer).
+    constexpr bool VFROMK = QG >= 4;
     // STREAM (the instantiations for long key sequences, whose tiles stream
     // through the buffers): a tile that lies wholly inside one key segment
     // is addressed from one row pointer, common to the workgroup, plus each
@@ -402,12 +405,12 @@ __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV ==
     // that crosses the segment boundary or runs past the last key, and every
     // tile of the other instantiations, take the per-row path.
     const bool off32 = STREAM && (int64_t)kKTile * (a.ldk > a.ldv ? a.ldk : a.ldv) < ((int64_t)1 << 31);
-    int koff[NJ], voff[NJ];
+    int koff[NJ], voff[VFROMK ? 1 : NJ];
     if constexpr (STREAM) {
 #pragma unroll
         for (int q = 0; q < NJ; ++q) {
-            koff[q] = (int)(irow[q] * a.ldk + icol[q]);     // used only when off32
-            voff[q] = (int)(irow[q] * a.ldv + icol[q]);
+            koff[q] = (int)(irow(q) * a.ldk + icol(q));     // used only when off32
+            if constexpr (!VFROMK) voff[q] = (int)(irow(q) * a.ldv + icol(q));
         }
     }
     auto issue_rows = [&](int k0, int buf) {
@@ -415,9 +418,10 @@ __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV ==
         for (int q = 0; q < NJ; ++q) {
             const int j = wave + NWV * q;
             if (j >= LY::CPR) break;
-            const int key = min(k0 + irow[q], Tk - 1);
-            const bf16* kr = seg_row<bf16>(a.k0, a.k1, a.Tk0, a.Tk1, a.ldk, b, key) + icol[q];
-            const bf16* vr = seg_row<bf16>(a.v0, a.v1, a.Tk0, a.Tk1, a.ldv, b, key) + icol[q];
+            const int key = min(k0 + irow(q), Tk - 1);
+            const int ic = icol(q);
+            const bf16* kr = seg_row<bf16>(a.k0, a.k1, a.Tk0, a.Tk1, a.ldk, b, key) + ic;
+            const bf16* vr = seg_row<bf16>(a.v0, a.v1, a.Tk0, a.Tk1, a.ldv, b, key) + ic;
             dma16a(kr, &sK[buf][64 * j * 8]);
             dma16a(vr, &sV[buf][64 * j * 8]);
         }
@@ -441,7 +445,7 @@ __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV ==
                 const int j = wave + NWV * q;
                 if (j >= LY::CPR) break;
                 dma16a(kb + koff[q], &sK[buf][64 * j * 8]);
-                dma16a(vb + voff[q], &sV[buf][64 * j * 8]);
+                dma16a(vb + (VFROMK ? koff[q] + irow(q) * (int)(a.ldv - a.ldk) : voff[VFROMK ? 0 : q]), &sV[buf][64 * j * 8]);
             }
         } else {
             issue_rows(k0, buf);
