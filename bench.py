@@ -138,11 +138,16 @@ def kernel_shapes(cfg):
 
     if cfg.kind in ("dit", "pixart"):
         M = B * T
-        gemm("gemm_bias", "QKV projection", M, 3 * D, D)
+        if cfg.dtype == "bf16" and T <= 256 and hd in (32, 64, 72) and D % 64 == 0:
+            # one kernel per (sample, head): the QKV projection into LDS, then the attention
+            out.append(("attention", "QKV projection + self-attention (one kernel per sample and head)",
+                        [B, H, T, T, hd], 2.0 * M * 3 * D * D + 4.0 * B * H * T * T * hd))
+        else:
+            gemm("gemm_bias", "QKV projection", M, 3 * D, D)
+            att("self-attention", T, T)
         gemm("gemm_gated", "attention output projection + gated residual", M, D, D)
         gemm("gemm_gelu", "MLP up projection + GELU", M, F, D)
         gemm("gemm_down", "MLP down projection + gated residual", M, D, F)
-        att("self-attention", T, T)
         if cfg.kind == "pixart":
             gemm("gemm_bias", "cross-attention query projection", M, D, D)
             gemm("gemm_bias", "cross-attention output projection", M, D, D)

@@ -339,11 +339,139 @@ __device__ __forceinline__ float group_sum(float v) {
     return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+// The QKV projection of one (sample, head) for the fused kernel below: the
+// sample's T <= 256 rows of x times the head's q, k and v rows of W_qkv (3 HD
+// of them, padded to whole 16-row MFMA blocks with repeats of the last), plus
+// the bias, with the q columns times q_scale, rounded to bf16 -- the same
+// operands, k order, MFMA and roundings as the separate QKV GEMM, so the
+// results are the same bits.  Operands stream through LDS in 64-wide k-steps
+// (two stages, 128-byte rows with the GEMM's XOR swizzle) via direct-to-LDS
+// loads; 8 waves as 4 x 2 hold 64-row x (TN 16)-column accumulator blocks.
+// The results go to LDS in the attention's layouts: Q row-major [256, HD],
+// K and V as the four 64-key tiles.  Rows past T repeat row T - 1 (finite;
+// their keys are masked and their queries not stored).
+template <int HD, int TILE>
+__device__ __forceinline__ void qkv_head_to_lds(const AttnArgs& a, int b, int h, bf16* smem, bf16 (*sK)[TILE],
+                                                bf16 (*sV)[TILE], bf16* sQ) {
+    typedef KvLayout<HD> LY;
+    constexpr int BM = 256, BK = 64, NW = 8, WAVES_N = 2;
+    constexpr int NWP = (3 * HD + 15) / 16 * 16;          // weight rows, padded
+    constexpr int NBLK = NWP / 16, TN = NBLK / WAVES_N, TM = BM / (NW / WAVES_N) / 16;
+    static_assert(NBLK % WAVES_N == 0, "column blocks per wave");
+    constexpr int ROWS = BM + NWP, STAGE = ROWS * BK;      // a stage: the x rows, then the weight rows
+    constexpr int NOCT = ROWS / 8, QMAX = (NOCT + NW - 1) / NW;
+    static_assert(ROWS % 8 == 0, "rows per load");
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int T = a.Tk0, D = a.dmodel;
+    const bf16* x = static_cast<const bf16*>(a.x);
+    const bf16* W = static_cast<const bf16*>(a.w_qkv);
+    // Load o = wave + NW q of a stage fills rows 8 o .. 8 o + 7; lane L the
+    // 16-byte slot L % 8 of row 8 o + L / 8, fetching the chunk the swizzle
+    // puts there.
+    const bf16* src[QMAX];
+#pragma unroll
+    for (int q = 0; q < QMAX; ++q) {
+        const int o = min(wave + NW * q, NOCT - 1);
+        const int r = 8 * o + lane / 8, chunk = (lane % 8) ^ ((r >> 1) & 7);
+        const bf16* row;
+        if (r < BM) {
+            row = x + ((int64_t)b * T + min(r, T - 1)) * a.ldx;
+        } else {
+            const int rr = min(r - BM, 3 * HD - 1), sec = rr / HD;
+            row = W + ((int64_t)sec * D + h * HD + (rr - sec * HD)) * D;
+        }
+        src[q] = row + chunk * 8;
+    }
+    auto issue = [&](int kt, int buf) {
+#pragma unroll
+        for (int q = 0; q < QMAX; ++q) {
+            const int o = wave + NW * q;
+            if (NOCT % NW == 0 || o < NOCT) dma16a(src[q] + kt * BK, smem + buf * STAGE + o * 8 * BK);
+        }
+    };
+    f32x4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int nk = D / BK;
+    const int frow = lane & 15, grp = lane >> 4;
+    issue(0, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+        __builtin_amdgcn_s_waitcnt((0 & 15) | (7 << 4) | (15 << 8));   // vmcnt(0): stage kt has landed
+        __syncthreads();
+        if (kt + 1 < nk) issue(kt + 1, (kt + 1) & 1);
+        const bf16* st = smem + (kt & 1) * STAGE;
+#pragma unroll
+        for (int kk = 0; kk < BK / 32; ++kk) {
+            const int c = kk * 4 + grp;
+            bf16x8 af[TM], bfr[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                const int r = wm * 64 + i * 16 + frow;
+                af[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(st + r * BK + (c ^ ((r >> 1) & 7)) * 8));
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                const int r = BM + (wn * TN + j) * 16 + frow;
+                bfr[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(st + r * BK + (c ^ ((r >> 1) & 7)) * 8));
+            }
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);
+        }
+    }
+    __syncthreads();   // every wave is done with the stages, which Q, K and V now overwrite
+    // A lane holds four consecutive columns of one row per block.
+    const bf16* bias = static_cast<const bf16*>(a.b_qkv);
+    const float qs = a.proj_q_scale;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int col = (wn * TN + j) * 16 + 4 * grp;
+        if (col >= 3 * HD) continue;
+        const int sec = col / HD, e = col - sec * HD;   // HD % 4 == 0: the four columns share a section
+        float bv[4] = {0.f, 0.f, 0.f, 0.f};
+        if (bias) {
+            const bf16x4 b4 = *reinterpret_cast<const bf16x4*>(bias + (int64_t)sec * D + h * HD + e);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) bv[r] = (float)b4[r];
+        }
+        const float sc = sec == 0 ? qs : 1.f;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const int row = wm * 64 + i * 16 + frow;
+            bf16x4 q;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) q[r] = (bf16)((acc[i][j][r] + bv[r]) * sc);
+            bf16* dst = sec == 0 ? sQ + row * HD + e
+                                 : (sec == 1 ? sK[row / 64] : sV[row / 64]) + LY::at(row % 64, e);
+            *reinterpret_cast<bf16x4*>(dst) = q;
+        }
+    }
+    // The slack past each tile's last row is read (for d >= HD operand rows,
+    // whose outputs are discarded): keep it finite.
+    if (tid < 32) {
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb) {
+            sK[nb][kKTile * HD + tid] = (bf16)0.f;
+            sV[nb][kKTile * HD + tid] = (bf16)0.f;
+        }
+    }
+    __syncthreads();
+}
+
 // Four-wave workgroups are held to two waves per SIMD (256 registers), so two
 // workgroups share a CU and their barriers do not line up.
-template <int HD, int QG, int NWV, int NB, bool STREAM, bool QS>
+// QKV: the block's QKV projection for this (sample, head) runs first, into
+// LDS (qkv_head_to_lds), and the attention reads Q, K and V from there: one
+// workgroup per (sample, head) of up to 256 tokens.
+template <int HD, int QG, int NWV, int NB, bool STREAM, bool QS, bool QKV = false>
 __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV == 4 ? 2 : 1))) void attention_dma_kernel(
     AttnArgs a) {
+    static_assert(!QKV || (!STREAM && QS && QG == 2 && NWV == 8 && NB == 4 && HD <= 72), "fused QKV shape");
     typedef AttnShape<bf16, HD> S;
     typedef KvLayout<HD> LY;
     constexpr int QT = 16 * QG * NWV;
@@ -354,8 +482,18 @@ __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV ==
     // rows of the last output block carry them (the deferred rescale of O
     // covers them); otherwise one more 16-row block of ones, osum.
     constexpr bool PADSUM = HD % 16 != 0;
-    __shared__ __attribute__((aligned(1024))) bf16 sK[NB][TILE];
-    __shared__ __attribute__((aligned(1024))) bf16 sV[NB][TILE];
+    // QKV: one buffer holds the projection's stages, then K, V and Q.
+    constexpr int QKV_ELEMS = QKV ? (2 * (256 + (3 * HD + 15) / 16 * 16) * 64 > 2 * NB * TILE + 256 * HD
+                                         ? 2 * (256 + (3 * HD + 15) / 16 * 16) * 64
+                                         : 2 * NB * TILE + 256 * HD)
+                                  : 8;
+    __shared__ __attribute__((aligned(1024))) bf16 sK_[QKV ? 8 : NB * TILE];
+    __shared__ __attribute__((aligned(1024))) bf16 sV_[QKV ? 8 : NB * TILE];
+    __shared__ __attribute__((aligned(1024))) bf16 sX_[QKV_ELEMS];
+    typedef bf16 TileArr[TILE];
+    TileArr* sK = reinterpret_cast<TileArr*>(QKV ? sX_ : sK_);
+    TileArr* sV = reinterpret_cast<TileArr*>(QKV ? sX_ + NB * TILE : sV_);
+    bf16* sQ = sX_ + 2 * NB * TILE;     // QKV only
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -370,8 +508,10 @@ __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV ==
     const int ql = lane & 15, grp = lane >> 4;
 
     // The slack past the last row is read (for d >= HD operand rows, whose
-    // outputs are discarded) but never loaded: keep it finite.
-    if (tid < 32) {
+    // outputs are discarded) but never loaded: keep it finite.  (QKV: written
+    // after the projection, whose stages share the buffer.)
+    if constexpr (QKV) qkv_head_to_lds<HD, TILE>(a, b, h, sX_, sK, sV, sQ);
+    else if (tid < 32) {
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
             sK[nb][kKTile * HD + tid] = (bf16)0.f;
@@ -454,7 +594,9 @@ __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV ==
     const int ntiles = (Tk + kKTile - 1) / kKTile;
     const bool resident = ntiles <= NB;
     // K/V loads go out first so that their latency overlaps the Q loads.
-    if (resident) {
+    if constexpr (QKV) {
+        // (K and V are in LDS already.)
+    } else if (resident) {
         for (int t = 0; t < ntiles; ++t) issue_rows(t * kKTile, t);
     } else {
         issue(0, 0);
@@ -465,7 +607,8 @@ __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(NWV ==
 #pragma unroll
     for (int g = 0; g < QG; ++g) {
         myq[g] = qt * QT + wave * 16 * QG + 16 * g + ql;
-        const bf16* qrow = myq[g] < Tq ? seg_row<bf16>(a.q0, a.q1, a.Tq0, a.Tq1, a.ldq, b, myq[g]) + col0 : nullptr;
+        const bf16* qrow = QKV ? sQ + myq[g] * HD
+                         : myq[g] < Tq ? seg_row<bf16>(a.q0, a.q1, a.Tq0, a.Tq1, a.ldq, b, myq[g]) + col0 : nullptr;
 #pragma unroll
         for (int c = 0; c < S::n32x; ++c) {
             const int d = 32 * c + grp * 8;       // HD % 8 == 0: a chunk is wholly in or out
@@ -839,6 +982,34 @@ int launch_attention(int dtype, AttnArgs a, hipStream_t s) {
     }
     prof_end(PROF_ATTENTION, s);
     return rc;
+}
+
+bool qkv_attention_supported(int dtype, int T, int head_dim, int dmodel) {
+    return dtype == BC_BF16 && T >= 1 && T <= 4 * kKTile && (head_dim == 32 || head_dim == 64 || head_dim == 72) &&
+           dmodel >= 64 && dmodel % 64 == 0;
+}
+
+int launch_qkv_attention(int dtype, AttnArgs a, hipStream_t s) {
+    auto al = [](const void* p, int n) { return reinterpret_cast<uintptr_t>(p) % n == 0; };
+    if (!qkv_attention_supported(dtype, a.Tk0, a.d, a.dmodel) || a.Tq0 != a.Tk0 || a.Tq1 || a.Tk1 || a.H * a.d != a.dmodel)
+        return fail(BC_ERR_UNSUPPORTED, "fused QKV attention: T=%d, d=%d, D=%d, H=%d", a.Tk0, a.d, a.dmodel, a.H);
+    if (!a.x || !a.w_qkv || !a.o0 || !al(a.x, 16) || !al(a.w_qkv, 16) || a.ldx % 8 || !al(a.b_qkv, 8))
+        return fail(BC_ERR_UNSUPPORTED, "fused QKV attention: 16-byte aligned x and weights, 8-byte aligned bias");
+    if (a.B < 1 || a.H < 1) return BC_OK;
+    a.o1 = a.o0;
+    a.q_scaled = 1;
+    a.scale_log2 = 1.0f;
+    a.proj_q_scale = attn_q_scale(a.d);
+    const double T = a.Tk0;
+    prof_begin(PROF_ATTENTION, s, 2.0 * a.B * T * 3.0 * a.dmodel * a.dmodel + 4.0 * a.B * a.H * T * T * a.d);
+    const dim3 grid((unsigned)(a.B * a.H)), block(512);
+    switch (a.d) {
+        case 32: launch_k(attention_dma_kernel<32, 2, 8, 4, false, true, true>, grid, block, s, a); break;
+        case 64: launch_k(attention_dma_kernel<64, 2, 8, 4, false, true, true>, grid, block, s, a); break;
+        default: launch_k(attention_dma_kernel<72, 2, 8, 4, false, true, true>, grid, block, s, a); break;
+    }
+    prof_end(PROF_ATTENTION, s);
+    return check_launch("qkv attention");
 }
 
 }  // namespace bc

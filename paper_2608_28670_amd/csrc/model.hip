@@ -132,16 +132,26 @@ static int dit_block(const bc_block_desc& d, const bc_block_weights& w, float* x
     const int M = d.B * T;
     const bc_stream_weights& sw = w.img;
     BC_TRY(launch_ln_mod(BC_F32, x, M, D, mod, mod + D, ld_mod, T, dt, bb.h, s));
-    BC_TRY(qproj(dt, bb.h, D, sw.w_qkv, sw.b_qkv, M, 3 * D, D, bb.qkv, D, d.head_dim, s));
     AttnArgs a = {};
     const size_t esz = dtype_size(dt);
     a.q_scaled = 1;
-    a.q0 = a.q1 = bb.qkv; a.Tq0 = T; a.ldq = 3 * D;
-    a.k0 = a.k1 = static_cast<char*>(bb.qkv) + D * esz; a.Tk0 = T; a.ldk = 3 * D;
-    a.v0 = a.v1 = static_cast<char*>(bb.qkv) + 2 * D * esz; a.ldv = 3 * D;
     a.o0 = a.o1 = bb.attn; a.ldo = D;
     a.B = d.B; a.H = d.heads; a.d = d.head_dim;
-    BC_TRY(launch_attention(dt, a, s));
+    auto al = [](const void* p, int n) { return reinterpret_cast<uintptr_t>(p) % n == 0; };
+    if (qkv_attention_supported(dt, T, d.head_dim, D) && d.heads * d.head_dim == D && al(sw.w_qkv, 16) &&
+        al(sw.b_qkv, 8)) {
+        // Short sequences (DiT-XL/2's 256 tokens): the QKV projection and the
+        // self-attention of a (sample, head) in one workgroup, Q, K and V in LDS.
+        a.Tq0 = a.Tk0 = T;
+        a.x = bb.h; a.ldx = D; a.w_qkv = sw.w_qkv; a.b_qkv = sw.b_qkv; a.dmodel = D;
+        BC_TRY(launch_qkv_attention(dt, a, s));
+    } else {
+        BC_TRY(qproj(dt, bb.h, D, sw.w_qkv, sw.b_qkv, M, 3 * D, D, bb.qkv, D, d.head_dim, s));
+        a.q0 = a.q1 = bb.qkv; a.Tq0 = T; a.ldq = 3 * D;
+        a.k0 = a.k1 = static_cast<char*>(bb.qkv) + D * esz; a.Tk0 = T; a.ldk = 3 * D;
+        a.v0 = a.v1 = static_cast<char*>(bb.qkv) + 2 * D * esz; a.ldv = 3 * D;
+        BC_TRY(launch_attention(dt, a, s));
+    }
     if (sites) {
         BC_TRY(plain(dt, bb.attn, D, sw.w_o, sw.b_o, M, D, D, sites[0], false, s));
         BC_TRY(launch_gated_add(dt, sites[0], M, D, x, mod + 2 * D, ld_mod, T, s));
