@@ -124,8 +124,10 @@ def log(msg):
 # ---------------------------------------------------------------------------
 
 def kernel_shapes(cfg):
-    """(class, name, shape, work) of every block kernel of one full step; work
-    = algorithmic FLOPs per launch, which with the class identifies a launch."""
+    """(class, name, shape, work) of every block kernel of one full step and
+    of the conditioning GEMMs that run once per run or per chunk of full
+    steps; work = algorithmic FLOPs per launch, which with the class
+    identifies a launch."""
     B, D, F, T = cfg.batch, cfg.hidden, cfg.mlp, cfg.tokens
     H, hd = cfg.heads, cfg.head_dim
     out = []
@@ -166,6 +168,24 @@ def kernel_shapes(cfg):
         gemm("gemm_gelu", "single-stream [qkv | mlp] projection + GELU", B * L, 3 * D + F, D)
         gemm("gemm_down", "single-stream output projection + gated residual", B * L, D, D + F)
         att("joint attention (dual- and single-stream)", L, L)
+    # Once per run (or per chunk of full steps): the conditioning GEMMs.
+    S = cfg.steps
+    nf = sum(1 for k in range(S) if k % cfg.interval == 0 or k == S - 1)
+    chunk = max(1, min(S, 256 // B, 64))
+    for f0 in range(0, nf, chunk):
+        Mc = min(chunk, nf - f0) * B
+        if cfg.kind == "dit":
+            gemm("gemm_bias", "adaLN modulation of a chunk of full steps (all blocks, one grouped launch)",
+                 Mc, cfg.depth * 6 * D, D)
+        elif cfg.kind == "pixart":
+            gemm("gemm_bias", "t6 projection of a chunk of full steps", Mc, 6 * D, D)
+        else:
+            gemm("gemm_bias", "dual-stream adaLN modulation of a chunk of full steps (grouped)",
+                 Mc, 2 * cfg.depth * 6 * D, D)
+            gemm("gemm_bias", "single-stream adaLN modulation of a chunk of full steps (grouped)",
+                 Mc, cfg.depth_single * 3 * D, D)
+    if cfg.kind != "pixart":
+        gemm("gemm_bias", "final-layer modulation of every step", S * B, 2 * D, D)
     return out
 
 

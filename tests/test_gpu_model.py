@@ -69,6 +69,25 @@ def test_dit_block(bclib, name, B, latent):
         assert upd < 1e-4
 
 
+# Samples of at most 256 tokens take the fused QKV projection + attention
+# (one workgroup per sample and head): head dims 72, 64 and 32, a ragged last
+# key tile (196 and 110 tokens), a full one (256) and a single token.
+@pytest.mark.parametrize("hidden,heads,hd,latent,B", [
+    (1152, 16, 72, (4, 28, 28), 2), (512, 8, 64, (4, 20, 22), 3), (256, 8, 32, (4, 32, 32), 2),
+    (1152, 16, 72, (4, 2, 2), 2)], ids=["d72_T196", "d64_T110", "d32_T256", "d72_T1"])
+def test_dit_block_fused_qkv_attention(bclib, hidden, heads, hd, latent, B):
+    cfg = synth.scaled(synth.CONFIGS["dit_xl2"], depth=1, hidden=hidden, heads=heads, head_dim=hd,
+                       mlp=4 * hidden, latent=latent)
+    assert cfg.tokens <= 256
+    P = synth.params(cfg)
+    M = om.Model(cfg, P)
+    x = synth.normal("blk/x", (B, cfg.tokens, cfg.hidden))
+    c = synth.normal("blk/c", (B, cfg.hidden), 0.5)
+    exp = M.dit_block(0, x.astype(np.float64), M.block_mod(0, {"c": c.astype(np.float64)}))
+    got, _ = _block_call(bclib, cfg, P, bclib.BLOCK_DIT, x, c)
+    _check_block(got, x, exp, 2e-2)
+
+
 def test_pixart_block(bclib):
     cfg = synth.scaled(synth.CONFIGS["pixart"], depth=1, latent=(4, 32, 32), batch=2)
     P = synth.params(cfg)
