@@ -44,8 +44,9 @@ int launch_attention(int dtype, AttnArgs a, hipStream_t s);
 // A block's QKV projection and its self-attention in one launch, one
 // workgroup per (sample, head) holding the head's Q, K and V in LDS: for bf16,
 // up to 256 tokens per sample, head dims 32, 64 and 72, dmodel a multiple of
-// 64 (= H d).  Writes only the attention output (a.o0, rows ldo apart), the
-// same bits as the QKV GEMM followed by launch_attention.
+// 64 (= H d).  Writes only the attention output (a.o0, rows ldo apart): the
+// same arithmetic, in the same order, as the QKV GEMM with single-group
+// tiles followed by launch_attention.
 bool qkv_attention_supported(int dtype, int T, int head_dim, int dmodel);
 int launch_qkv_attention(int dtype, AttnArgs a, hipStream_t s);
 

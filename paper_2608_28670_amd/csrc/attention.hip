@@ -343,8 +343,9 @@ __device__ __forceinline__ float group_sum(float v) {
 // sample's T <= 256 rows of x times the head's q, k and v rows of W_qkv (3 HD
 // of them, padded to whole 16-row MFMA blocks with repeats of the last), plus
 // the bias, with the q columns times q_scale, rounded to bf16 -- the same
-// operands, k order, MFMA and roundings as the separate QKV GEMM, so the
-// results are the same bits.  Operands stream through LDS in 64-wide k-steps
+// operands, k order, MFMA and roundings as the separate QKV GEMM when its
+// tiles keep K in one wave group (DiT-XL/2's 4096 rows), so there the same
+// bits (split-K tiles at small M sum in another order).  Operands stream through LDS in 64-wide k-steps
 // (two stages, 128-byte rows with the GEMM's XOR swizzle) via direct-to-LDS
 // loads; 8 waves as 4 x 2 hold 64-row x (TN 16)-column accumulator blocks.
 // The results go to LDS in the attention's layouts: Q row-major [256, HD],
