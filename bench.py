@@ -280,9 +280,10 @@ def roofline_of(g, tag=None, src=None, workload=None):
 
 def counter_tag(cfg, g):
     """The counter-summary tag of a profiled kernel group (matched by its
-    algorithmic FLOPs among the counter program's kernels), or None."""
+    class and algorithmic FLOPs among the counter program's kernels: DiT-XL/2's
+    MLP up and down projections have the same FLOPs), or None."""
     for k in kernel_tags(cfg):
-        if abs(k["flops"] - g["work"]) <= 1e-9 * g["work"]:
+        if k["class"] == g["class"] and abs(k["flops"] - g["work"]) <= 1e-9 * g["work"]:
             return k["tag"], k["tag"].split("_")[0]
     return None, None
 
@@ -764,20 +765,22 @@ def kernel_tags(cfg):
     counter program launches for a workload (in launch order per block)."""
     B, T, D, F, H, hd = cfg.batch, cfg.tokens, cfg.hidden, cfg.mlp, cfg.heads, cfg.head_dim
     bf = 2
-    def gemm(tag, M, N, K, gated):
+    def gemm(tag, cls, M, N, K, gated):
         # A and W read once, output written once (+ the fp32 residual read for
         # the gated epilogue: res read and out written as fp32)
         byt = (M * K + N * K) * bf + (M * N * 8 if gated else M * N * bf)
-        return {"tag": f"gemm_{tag}_{cfg.name}", "shape": [M, N, K], "flops": 2.0 * M * N * K, "bytes": byt}
+        return {"tag": f"gemm_{tag}_{cfg.name}", "class": cls, "shape": [M, N, K], "flops": 2.0 * M * N * K,
+                "bytes": byt}
     def att(L):
-        return {"tag": f"attention_{cfg.name}", "shape": [B, H, L, hd], "flops": 4.0 * B * H * L * L * hd,
-                "bytes": 4 * B * L * H * hd * bf}
+        return {"tag": f"attention_{cfg.name}", "class": "attention", "shape": [B, H, L, hd],
+                "flops": 4.0 * B * H * L * L * hd, "bytes": 4 * B * L * H * hd * bf}
     if cfg.kind == "mmdit":
         L = T + cfg.txt_tokens
-        return [gemm("single_in", B * L, 3 * D + F, D, False), att(L), gemm("single_out", B * L, D, D + F, True)]
+        return [gemm("single_in", "gemm_gelu", B * L, 3 * D + F, D, False), att(L),
+                gemm("single_out", "gemm_down", B * L, D, D + F, True)]
     M = B * T
-    return [gemm("qkv", M, 3 * D, D, False), att(T), gemm("proj", M, D, D, True), gemm("fc1", M, F, D, False),
-            gemm("fc2", M, D, F, True)]
+    return [gemm("qkv", "gemm_bias", M, 3 * D, D, False), att(T), gemm("proj", "gemm_gated", M, D, D, True),
+            gemm("fc1", "gemm_gelu", M, F, D, False), gemm("fc2", "gemm_down", M, D, F, True)]
 
 
 def kernels_only(args):
