@@ -245,8 +245,12 @@ def grid_fits(kernel, grid_threads, g):
     args = [a.strip() for a in m.group(1).split(",")]
     if "attention" in kernel:
         qg, nwv = int(args[1]), int(args[2])
-        B, H, Tq = g["shape"][0], g["shape"][1], g["shape"][2]
+        B, H, Tq, Tk = g["shape"][0], g["shape"][1], g["shape"][2], g["shape"][3]
         qt = 16 * qg * nwv
+        # the streaming key loop (template argument 4) serves more than 256 keys
+        # (PixArt's self- and cross-attention share B, H and Tq)
+        if (args[4] == "true") != (Tk > 256):
+            return False
         return grid_threads == -(-Tq // qt) * H * B * 64 * nwv
     bm, bn, wm, wn, kg = int(args[1]), int(args[2]), int(args[3]), int(args[4]), int(args[7])
     M, N = g["shape"][0], g["shape"][1]
