@@ -71,10 +71,12 @@ def test_dit_block(bclib, name, B, latent):
 
 # Samples of at most 256 tokens take the fused QKV projection + attention
 # (one workgroup per sample and head): head dims 72, 64 and 32, a ragged last
-# key tile (196 and 110 tokens), a full one (256) and a single token.
+# key tile (196 and 110 tokens), a full one (256), a single token, and 33
+# samples (528 workgroups: more than one round over the CUs).
 @pytest.mark.parametrize("hidden,heads,hd,latent,B", [
     (1152, 16, 72, (4, 28, 28), 2), (512, 8, 64, (4, 20, 22), 3), (256, 8, 32, (4, 32, 32), 2),
-    (1152, 16, 72, (4, 2, 2), 2)], ids=["d72_T196", "d64_T110", "d32_T256", "d72_T1"])
+    (1152, 16, 72, (4, 2, 2), 2), (1152, 16, 72, (4, 28, 28), 33)],
+    ids=["d72_T196", "d64_T110", "d32_T256", "d72_T1", "d72_T196_B33"])
 def test_dit_block_fused_qkv_attention(bclib, hidden, heads, hd, latent, B):
     cfg = synth.scaled(synth.CONFIGS["dit_xl2"], depth=1, hidden=hidden, heads=heads, head_dim=hd,
                        mlp=4 * hidden, latent=latent)
