@@ -147,13 +147,16 @@ def kernel_shapes(cfg):
         else:
             gemm("gemm_bias", "QKV projection", M, 3 * D, D)
             att("self-attention", T, T)
-        gemm("gemm_gated", "attention output projection + gated residual", M, D, D)
+        if cfg.kind == "pixart":
+            # The cross-attention's output projection is a residual GEMM of the
+            # same shape as the attention output projection: one group.
+            gemm("gemm_gated", "attention and cross-attention output projections + residual", M, D, D)
+            gemm("gemm_bias", "cross-attention query projection", M, D, D)
+            att("cross-attention", T, cfg.ctx_tokens)
+        else:
+            gemm("gemm_gated", "attention output projection + gated residual", M, D, D)
         gemm("gemm_gelu", "MLP up projection + GELU", M, F, D)
         gemm("gemm_down", "MLP down projection + gated residual", M, D, F)
-        if cfg.kind == "pixart":
-            gemm("gemm_bias", "cross-attention query projection", M, D, D)
-            gemm("gemm_bias", "cross-attention output projection", M, D, D)
-            att("cross-attention", T, cfg.ctx_tokens)
     else:
         Tt = cfg.txt_tokens
         L = T + Tt
